@@ -1,0 +1,400 @@
+"""CPU oracle for the Action-Subspace-Protected (ASP) linear layer.
+
+TEST INFRASTRUCTURE ONLY.  Only the test-suite, the smoke check and the
+benchmark's CPU-baseline leg may import this module.  It shares no code with
+the GPU library and never imports it.
+
+It is a plain, slow, step-by-step restatement of what the paper
+"Q-WAM: 4-Bit Quantization of World Action Models with Action-Subspace
+Protection" computes for one quantized linear layer, written with numpy in
+float64 / int64 (float32 where the method's rounding points are float32).
+Library primitives used as single steps: matmul (float64; exact whenever every
+operand and partial sum is an integer below 2**53), svd / eigh, frexp, rint.
+
+Paper references used below
+  Eq. 2   symmetric b-bit group quantizer (Sec. 3, "Post-Training Quantization")
+  Eq. 3   smoothing + rotation pair, W~^T x~ = W^T x (Sec. 3)
+  Eq. 7   eigen-decomposition of the (rotated) Gramian (Sec. 4.2)
+  Eq. 8   split of x~ into V(V^T x~) + x~_perp (Sec. 4.2, "Splitting the layer")
+  Eq. 9   ASP layer: (V^T W~)^T (V^T x~) + Q4(W~_perp)^T Q4(x~_perp) (Sec. 4.2)
+  Prop. "Optimal protected subspace" (App. A.3, Ky Fan maximum principle)
+  App. B.1 "Quantization settings and kernels": symmetric round-to-nearest,
+      one scale per group of consecutive input channels, codes in [-8, 7],
+      activation scale = group absmax / 7 per token, smoothing factor
+      s_j = max|X_j|^a / max|W_:,j|^(1-a) with a = 0.5, divide the activation by
+      s and multiply the weight by s; the fused kernels differ from the
+      reference rule only in floating-point accumulation order.
+
+Readings taken where the paper is silent (all are listed in the design notes):
+  * group = 64 along K; scales are float32; rounding is half-to-even;
+    scale = fl32(absmax / 7), codes = clamp(rint(fl32(v * fl32(1/scale))), -8, 7);
+    a group whose absmax is below 7 * 2**-126 gets scale 0 and all codes 0.
+  * the activation is smoothed by multiplying with fl32(1/lambda) (the
+    reciprocal is formed once, at weight-pack time) and the 4-bit path
+    quantizes x~ itself (not the deflated x~_perp of Eq. 9); no Hadamard
+    rotation.  In exact arithmetic both give x~ W~ (Eq. 9 and R^T V = 0).
+  * packing: byte j of a row holds k = 2j in its low nibble and k = 2j+1 in
+    its high nibble, two's complement.
+  * the 16-bit branch is bf16: L1 = bf16(V), L2 = bf16(L1^T W~),
+    R = fl32(W~ - L1 L2), t = bf16(sum_k bf16(x~_k) L1[k, j]) with an exact sum.
+  * output reference y = sum_g sx sw P + t L2 (+ bias), float64, not rounded.
+
+Layouts: x [M][K]; w, R [N][K] (row = output channel, i.e. the paper's W
+transposed); codes [rows][K] int8; scales [rows][G] float32 (G = K / 64);
+packed [rows][K/2] uint8; L1 [K][r]; L2 [r][N]; t [M][r]; P [M][N][G].
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+GROUP = 64
+QMAX = 7          # 2**(4-1) - 1  (Eq. 2 with b = 4)
+CODE_MIN, CODE_MAX = -8, 7
+ALPHA = 0.5       # smoothing strength (App. B.1)
+RIDGE = 1e-3      # the stand-in Gramian is A A^T / K + RIDGE * I
+
+# ----------------------------------------------------------------------------
+# bf16 helpers (round to nearest, ties to even)
+# ----------------------------------------------------------------------------
+
+
+def bf16_bits_to_f64(bits: np.ndarray) -> np.ndarray:
+    """Value of bf16 bit patterns, as float64 (exact)."""
+    b = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
+    return b.view(np.float32).astype(np.float64)
+
+
+def round_to_bf16(v: np.ndarray) -> np.ndarray:
+    """Round float32/float64 values to the nearest bf16 value, ties to even.
+
+    Written from the definition: bf16 keeps 8 significant bits; the quantum of
+    a normal value with exponent e (v = f * 2**e, 0.5 <= |f| < 1) is 2**(e-8);
+    below 2**-126 the quantum is fixed at 2**-133.  Returns float64 values.
+    """
+    v = np.asarray(v, dtype=np.float64)
+    _, e = np.frexp(v)
+    e = np.maximum(e, -125)            # |v| < 2**-126  ->  subnormal quantum 2**-133
+    q = np.ldexp(np.ones_like(v), e - 8)
+    out = np.rint(v / q) * q           # v / q exact (power of two), rint ties to even
+    return out
+
+
+def f64_to_bf16_bits(v: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns of round_to_bf16(v)."""
+    r = round_to_bf16(v).astype(np.float32)    # exact: r is representable in bf16
+    return (r.view(np.uint32) >> np.uint32(16)).astype(np.uint16)
+
+
+# ----------------------------------------------------------------------------
+# Offline construction of one ASP layer (Sec. 3, Sec. 4.2, App. B.1)
+# ----------------------------------------------------------------------------
+
+
+def smoothing_factors(x: np.ndarray, w: np.ndarray, alpha: float = ALPHA) -> np.ndarray:
+    """Per-input-channel smoothing factor (App. B.1, Eq. 13).
+
+    s_k = max_m |X[m, k]|**alpha / max_n |W[n, k]|**(1 - alpha), computed in
+    float64 and stored as float32.  A channel whose activation or weight
+    maximum is zero gets factor 1 (the formula is undefined there).
+    x: float [M][K] activation values; w: float [N][K] weight values.
+    """
+    xmax = np.max(np.abs(np.asarray(x, dtype=np.float64)), axis=0)
+    wmax = np.max(np.abs(np.asarray(w, dtype=np.float64)), axis=0)
+    ok = (xmax > 0) & (wmax > 0)
+    s = np.ones_like(xmax)
+    s[ok] = xmax[ok] ** alpha / wmax[ok] ** (1.0 - alpha)
+    return s.astype(np.float32)
+
+
+def gramian(a: np.ndarray) -> np.ndarray:
+    """The SPD stand-in for the layer's Gramian: G = A A^T / K + RIDGE * I."""
+    a = np.asarray(a, dtype=np.float64)
+    K = a.shape[0]
+    return a @ a.T / K + RIDGE * np.eye(K)
+
+
+def _fix_signs(V: np.ndarray) -> np.ndarray:
+    """Eigenvectors are defined up to sign: make the largest-|entry| of each column positive."""
+    V = V.copy()
+    idx = np.argmax(np.abs(V), axis=0)
+    sgn = np.sign(V[idx, np.arange(V.shape[1])])
+    sgn[sgn == 0] = 1.0
+    return V * sgn[None, :]
+
+
+def protected_basis_eigh(G: np.ndarray, r: int):
+    """Top-r eigenvectors of a symmetric PSD G (Eq. 7), by the definition.
+
+    Returns (V [K][r] with orthonormal columns, eigenvalues of G sorted
+    descending).  The span of V is the layer's action subspace (Sec. 4.2).
+    """
+    evals, evecs = np.linalg.eigh(np.asarray(G, dtype=np.float64))
+    order = np.argsort(evals)[::-1]
+    evals = evals[order]
+    V = _fix_signs(evecs[:, order[:r]])
+    return V, evals
+
+
+def protected_basis_from_factor(a: np.ndarray, r: int) -> np.ndarray:
+    """Top-r eigenvectors of G = A A^T / K + RIDGE * I without forming G.
+
+    The eigenvectors of A A^T are the left singular vectors of A (eigenvalue
+    sigma**2 / K + RIDGE, so the order is the singular-value order); the ridge
+    shifts eigenvalues, not eigenvectors.  Requires r < number of columns of A
+    so that the top-r space is separated from the flat ridge part.
+    """
+    U, S, _ = np.linalg.svd(np.asarray(a, dtype=np.float64), full_matrices=False)
+    assert r < a.shape[1], "rank must be below the Gramian factor's width"
+    return _fix_signs(U[:, :r])
+
+
+def build_layer(x_bits: np.ndarray, w_bits: np.ndarray, V: np.ndarray):
+    """Deployed ASP factors of one layer from bf16 x [M][K], bf16 w [N][K] and
+    a protected basis V [K][r] (float64, orthonormal columns).
+
+    Steps (Sec. 3 Eq. 3, Sec. 4.2 Eq. 9, App. B.1):
+      lambda = smoothing factors (float32)
+      W~[n, k] = lambda_k * W[n, k]                       (float64)
+      L1 = bf16(V)                                        [K][r]
+      L2 = bf16(L1^T W~)     (the paper's V^T W~)         [r][N]
+      R  = fl32(W~ - L1 L2)  (the paper's W~_perp, here built against the
+                               rounded factors, so W~ = R + L1 L2 up to fl32)
+    Returns a dict of numpy arrays: lam (f32 [K]), L1 (bf16 bits [K][r]),
+    L2 (bf16 bits [r][N]), R (f32 [N][K]).
+    """
+    x = bf16_bits_to_f64(x_bits)
+    w = bf16_bits_to_f64(w_bits)
+    lam = smoothing_factors(x, w)
+    wt = w * lam.astype(np.float64)[None, :]                  # [N][K]
+    L1 = f64_to_bf16_bits(V)                                  # [K][r]
+    L1f = bf16_bits_to_f64(L1)
+    L2 = f64_to_bf16_bits(L1f.T @ wt.T)                       # [r][N]
+    L2f = bf16_bits_to_f64(L2)
+    R = (wt - (L1f @ L2f).T).astype(np.float32)               # [N][K]
+    return {"lam": lam, "L1": L1, "L2": L2, "R": R}
+
+
+def build_layer_exact(x: np.ndarray, w: np.ndarray, V: np.ndarray):
+    """Exact-mode factors (float64 throughout, nothing rounded).
+
+    lam (float64, by the formula), V, VtW = V^T W~ [r][N], R = (I - V V^T) W~
+    stored [N][K] (Sec. 4.2: W~_perp).
+    """
+    x = np.asarray(x, dtype=np.float64)
+    w = np.asarray(w, dtype=np.float64)
+    xmax = np.max(np.abs(x), axis=0)
+    wmax = np.max(np.abs(w), axis=0)
+    ok = (xmax > 0) & (wmax > 0)
+    lam = np.ones_like(xmax)
+    lam[ok] = xmax[ok] ** ALPHA / wmax[ok] ** (1.0 - ALPHA)
+    wt = w * lam[None, :]
+    VtW = V.T @ wt.T                                          # [r][N]
+    R = wt - (V @ VtW).T                                      # [N][K]
+    return {"lam": lam, "V": V, "VtW": VtW, "R": R}
+
+
+# ----------------------------------------------------------------------------
+# The quantizer (Eq. 2) and packing
+# ----------------------------------------------------------------------------
+
+
+def quantize_groups(v: np.ndarray, group: int = GROUP, dtype=np.float32):
+    """Symmetric 4-bit group quantizer of Eq. 2, one scale per `group`
+    consecutive entries of each row.
+
+    In precision `dtype` (float32 for the deployed layer):
+      a = max |v| over the group                   (exact)
+      a < 7 * 2**-126  ->  scale 0, codes 0        (guards 0 * inf)
+      scale = fl(a / 7)
+      inv   = fl(1 / scale)
+      code  = clamp(rint(fl(v * inv)), -8, 7)      (rint: ties to even)
+    Returns codes int8 [rows][K] and scales `dtype` [rows][K/group].
+    """
+    v = np.asarray(v, dtype=dtype)
+    rows, K = v.shape
+    assert K % group == 0
+    G = K // group
+    vg = v.reshape(rows, G, group)
+    a = np.max(np.abs(vg), axis=2)
+    small = a < dtype(QMAX * 2.0 ** -126)
+    scale = (a / dtype(QMAX)).astype(dtype)
+    scale[small] = 0
+    inv = np.zeros_like(scale)
+    inv[~small] = dtype(1) / scale[~small]
+    prod = (vg * inv[:, :, None]).astype(dtype)
+    codes = np.clip(np.rint(prod), CODE_MIN, CODE_MAX).astype(np.int8)
+    codes[small] = 0
+    return codes.reshape(rows, K), scale
+
+
+def dequantize_groups(codes: np.ndarray, scales: np.ndarray, group: int = GROUP) -> np.ndarray:
+    """Q_b(X) = scale * code (Eq. 2), float64."""
+    rows, K = codes.shape
+    c = codes.astype(np.float64).reshape(rows, K // group, group)
+    return (c * np.asarray(scales, dtype=np.float64)[:, :, None]).reshape(rows, K)
+
+
+def pack_nibbles(codes: np.ndarray) -> np.ndarray:
+    """Two 4-bit two's-complement codes per byte: even k low nibble, odd k high."""
+    c = np.asarray(codes, dtype=np.int16)
+    lo = c[:, 0::2] & 0xF
+    hi = c[:, 1::2] & 0xF
+    return (lo | (hi << 4)).astype(np.uint8)
+
+
+def unpack_nibbles(packed: np.ndarray) -> np.ndarray:
+    """Inverse of pack_nibbles (sign-extends each nibble)."""
+    p = np.asarray(packed, dtype=np.int16)
+    lo = p & 0xF
+    hi = (p >> 4) & 0xF
+    lo = np.where(lo >= 8, lo - 16, lo)
+    hi = np.where(hi >= 8, hi - 16, hi)
+    out = np.empty((p.shape[0], 2 * p.shape[1]), dtype=np.int8)
+    out[:, 0::2] = lo
+    out[:, 1::2] = hi
+    return out
+
+
+# ----------------------------------------------------------------------------
+# The hot path, deployed mode
+# ----------------------------------------------------------------------------
+
+
+def inverse_smoothing(lam: np.ndarray) -> np.ndarray:
+    """fl32(1 / lambda): the reciprocal formed once when the weights are packed."""
+    lam = np.asarray(lam, dtype=np.float32)
+    return (np.float32(1) / lam).astype(np.float32)
+
+
+def pack_weights(R: np.ndarray, lam: np.ndarray):
+    """Offline weight pack (weights are quantized once, Sec. 3 / App. B.1).
+
+    R: float32 [N][K] residual weight.  Returns (packed codes uint8 [N][K/2],
+    scales float32 [N][G], inverse smoothing float32 [K], codes int8 [N][K]).
+    """
+    codes, scales = quantize_groups(np.asarray(R, dtype=np.float32))
+    return pack_nibbles(codes), scales, inverse_smoothing(lam), codes
+
+
+def smooth_activations(x_bits: np.ndarray, inv_lam: np.ndarray) -> np.ndarray:
+    """x~ = fl32(x * fl32(1/lambda)) per channel (Eq. 3 without rotation)."""
+    x = bf16_bits_to_f64(x_bits).astype(np.float32)
+    return (x * np.asarray(inv_lam, dtype=np.float32)[None, :]).astype(np.float32)
+
+
+def down_projection(xt: np.ndarray, L1_bits: np.ndarray) -> np.ndarray:
+    """t = bf16( sum_k bf16(x~_k) * L1[k, j] ), the sum taken exactly (float64).
+
+    The paper's V^T x~ (Eq. 8 / Eq. 9) in the 16-bit branch.  Returns bf16 bits [M][r].
+    Every product of two bf16 values is exact in float64; the float64 sum of at
+    most 2**14 such terms is within ~1e-12 relative of the exact sum.
+    """
+    xb = round_to_bf16(xt)
+    s = xb @ bf16_bits_to_f64(L1_bits)
+    return f64_to_bf16_bits(s)
+
+
+def quantize_activations(x_bits: np.ndarray, inv_lam: np.ndarray, L1_bits: np.ndarray):
+    """The activation side of one layer call: smoothing, per-token group
+    quantization (Eq. 2, absmax/7 per token, App. B.1), nibble packing and the
+    rank-r down-projection.  Returns (packed uint8 [M][K/2], scales f32 [M][G],
+    t bf16 bits [M][r], codes int8 [M][K], x~ float32 [M][K])."""
+    xt = smooth_activations(x_bits, inv_lam)
+    codes, scales = quantize_groups(xt)
+    t = down_projection(xt, L1_bits)
+    return pack_nibbles(codes), scales, t, codes, xt
+
+
+def group_partials(qx: np.ndarray, qw: np.ndarray, group: int = GROUP) -> np.ndarray:
+    """P[m, n, g] = sum_{k in group g} qx[m, k] * qw[n, k] (the integer GEMM of
+    Sec. 3, one partial per group because each group has its own scales).
+
+    qx int8 [M][K], qw int8 [N][K] -> int64 [M][N][G].  Each group's product is
+    a float64 matmul of integer values |v| <= 8 over 64 terms: every partial sum
+    is an integer of magnitude <= 4096, so the float64 result is exact.
+    """
+    M, K = qx.shape
+    N = qw.shape[0]
+    G = K // group
+    P = np.empty((M, N, G), dtype=np.int64)
+    for g in range(G):
+        sl = slice(g * group, (g + 1) * group)
+        P[:, :, g] = np.rint(qx[:, sl].astype(np.float64) @ qw[:, sl].astype(np.float64).T).astype(np.int64)
+    return P
+
+
+def asp_output(sx: np.ndarray, sw: np.ndarray, P: np.ndarray, t_bits: np.ndarray,
+               L2_bits: np.ndarray, bias_bits=None) -> np.ndarray:
+    """y = sum_g sx[m, g] sw[n, g] P[m, n, g] + t L2 (+ bias), float64, unrounded.
+
+    The dequantized 4-bit product Q4(R)^T Q4(x~) (Eq. 2 per group) plus the
+    16-bit branch (V^T W~)^T (V^T x~) of Eq. 9, plus the bias.
+    sx [M][G], sw [N][G] float32; P [M][N][G]; t [M][r], L2 [r][N] bf16 bits.
+    """
+    sx64 = np.asarray(sx, dtype=np.float64)
+    sw64 = np.asarray(sw, dtype=np.float64)
+    y = np.einsum("mg,ng,mng->mn", sx64, sw64, P.astype(np.float64))
+    y = y + bf16_bits_to_f64(t_bits) @ bf16_bits_to_f64(L2_bits)
+    if bias_bits is not None:
+        y = y + bf16_bits_to_f64(bias_bits)[None, :]
+    return y
+
+
+def asp_output_bruteforce(qx, sx, qw, sw, t_bits, L2_bits, bias_bits=None) -> np.ndarray:
+    """Same output computed the other way: dequantize both operands, multiply."""
+    xd = dequantize_groups(qx, sx)
+    wd = dequantize_groups(qw, sw)
+    y = xd @ wd.T + bf16_bits_to_f64(t_bits) @ bf16_bits_to_f64(L2_bits)
+    if bias_bits is not None:
+        y = y + bf16_bits_to_f64(bias_bits)[None, :]
+    return y
+
+
+def asp_linear(x_bits, layer, bias_bits=None, rows=None):
+    """Whole deployed layer for the tokens `rows` (all if None).
+
+    layer: dict from build_layer (lam, L1, L2, R).  Returns a dict with every
+    intermediate: wq, sw, inv_lam, qw, xq, sx, t, qx, P, y.
+    """
+    wq, sw, inv_lam, qw = pack_weights(layer["R"], layer["lam"])
+    xb = x_bits if rows is None else x_bits[rows]
+    xq, sx, t, qx, _ = quantize_activations(xb, inv_lam, layer["L1"])
+    P = group_partials(qx, qw)
+    y = asp_output(sx, sw, P, t, layer["L2"], bias_bits)
+    return {"wq": wq, "sw": sw, "inv_lam": inv_lam, "qw": qw, "xq": xq, "sx": sx,
+            "t": t, "qx": qx, "P": P, "y": y}
+
+
+def asp_output_rows(xq_rows, sx_rows, t_rows, wq, sw, L2_bits, bias_bits=None):
+    """Reference output for a few tokens, straight from their packed codes and
+    scales (no full [M][N][G] tensor): used to check sampled rows of large layers."""
+    qx = unpack_nibbles(xq_rows)
+    qw = unpack_nibbles(wq)
+    P = group_partials(qx, qw)
+    return asp_output(sx_rows, sw, P, t_rows, L2_bits, bias_bits), P
+
+
+# ----------------------------------------------------------------------------
+# Exact mode: same steps, float64 factors, nothing rounded outside the quantizer
+# ----------------------------------------------------------------------------
+
+
+def asp_linear_exact(x: np.ndarray, layer_exact) -> np.ndarray:
+    """y = Q4(x~) Q4(R)^T + (x~ V)(V^T W~), all float64 (Eq. 9 with the 4-bit
+    path applied to x~; the quantizer itself run in float64)."""
+    x = np.asarray(x, dtype=np.float64)
+    xt = x / layer_exact["lam"][None, :]
+    qx, sx = quantize_groups(xt, dtype=np.float64)
+    qw, sw = quantize_groups(layer_exact["R"], dtype=np.float64)
+    y4 = dequantize_groups(qx, sx) @ dequantize_groups(qw, sw).T
+    return y4 + (xt @ layer_exact["V"]) @ layer_exact["VtW"]
+
+
+def bits_per_weight(K: int, N: int, r: int, group: int = GROUP, scale_bits: int = 32,
+                    branch_bits: int = 16, smooth_bits: int = 32) -> float:
+    """Effective bits per weight of one packed ASP layer: 4-bit codes, one scale
+    per group, the two bf16 branch factors (r(K + N) values) and the per-channel
+    smoothing reciprocal, divided by the K*N weights it replaces."""
+    total = 4 * K * N + scale_bits * (K // group) * N + branch_bits * r * (K + N) + smooth_bits * K
+    return total / (K * N)
