@@ -1,0 +1,170 @@
+/*
+ * qwam.h -- C ABI of the Action-Subspace-Protected (ASP) W4A4 linear layer
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * One ASP layer computes (row-vector convention, x is [M][K], y is [M][N])
+ *
+ *     y = Q4(x / lambda) . Q4(R)^T  +  ((x / lambda) . L1) . L2  (+ bias)
+ *
+ * following "Q-WAM: 4-Bit Quantization of World Action Models with
+ * Action-Subspace Protection":
+ *   - Q4 is the symmetric 4-bit group quantizer of Eq. 2 (Sec. 3), one float32
+ *     scale per group of 64 consecutive input channels: scale = absmax / 7,
+ *     code = clamp(round_half_even(v * (1 / scale)), -8, 7).  Weights are
+ *     quantized once offline, activations per token at run time (Sec. 3,
+ *     App. B.1).
+ *   - lambda is the per-channel smoothing factor of Eq. 3 / App. B.1 (the
+ *     activation is divided by it, the weight multiplied by it).
+ *   - L1 = bf16(V) and L2 = bf16(V^T W~) are the factors of the 16-bit branch
+ *     (V^T W~)^T (V^T x~) of Eq. 9, V being the top-r eigenvectors of the
+ *     layer's Gramian (Eq. 7); R = W~ - L1 L2 is the deflated weight W~_perp.
+ *   - The deployed layer is two kernels (App. B.1): one smooths, projects and
+ *     quantizes the activation (qwam_quantize_act), the other multiplies the
+ *     packed 4-bit operands and adds the branch and the bias in its epilogue
+ *     (qwam_asp_linear).
+ *
+ * Conventions for every call
+ *   - All array pointers are DEVICE pointers owned by the caller (the library
+ *     never allocates and never frees).  The qwam_layer struct itself is a HOST
+ *     struct read during the call only.
+ *   - bf16 arrays are passed as uint16_t bit patterns.
+ *   - Every call is asynchronous: it validates its arguments on the host,
+ *     enqueues its kernel(s) on `stream` (a hipStream_t; NULL = the null
+ *     stream) and returns.  Results are visible once the stream is
+ *     synchronised.  The library never synchronises.
+ *   - Every vector-loaded array must be 16-byte aligned (QWAM_ERR_MISALIGNED).
+ *   - Arguments are checked before any HIP call is made and device memory is
+ *     never dereferenced on the host; a failing check returns its status and
+ *     enqueues nothing.  qwam_last_error() then returns a message
+ *     (thread-local, valid until the thread's next call).
+ *   - No exception or abort crosses the ABI.  Calls are reentrant; distinct
+ *     streams may run calls concurrently on disjoint outputs.
+ *   - Inputs must be finite (no NaN / Inf); other inputs give unspecified
+ *     codes.
+ *
+ * Layouts (row-major, G = K / 64)
+ *   x    bf16    [M][K]      activations (row = token)
+ *   R    float   [N][K]      residual weight, row = output channel
+ *   smooth float [K]         lambda
+ *   wq   uint8   [N][K/2]    packed weight codes: byte j of a row holds the
+ *                            code of k = 2j in its low nibble and k = 2j+1 in
+ *                            its high nibble, 4-bit two's complement
+ *   ws   float   [G][N]      weight scales, group-major
+ *   inv_smooth float [K]     fl32(1 / lambda)
+ *   xq   uint8   [M][K/2]    packed activation codes (same nibble order)
+ *   xs   float   [G][M]      activation scales, group-major
+ *   L1t  bf16    [r][K]      L1 transposed: row j is the j-th protected direction
+ *   L2t  bf16    [N][r]      L2 transposed: row n holds (V^T W~)[:, n]
+ *   t    bf16    [M][r]      t = bf16(sum_k bf16(x~_k) L1[k, j]), float32 accumulation
+ *   bias bf16    [N]         optional
+ *   y    bf16    [M][N]      output, round to nearest even from float32
+ *
+ * Shape limits: group == 64; K % 64 == 0, 64 <= K <= 65536; N % 16 == 0,
+ * 16 <= N <= 1048576; r in {16, 32, 48, 64}; 1 <= M <= 1048576.
+ */
+#ifndef QWAM_H
+#define QWAM_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define QWAM_ABI_VERSION 1
+#define QWAM_GROUP 64
+
+typedef enum {
+    QWAM_OK = 0,
+    QWAM_ERR_INVALID_ARG = 1,   /* null pointer, bad shape or group size            */
+    QWAM_ERR_UNSUPPORTED = 2,   /* well-formed but outside the supported limits     */
+    QWAM_ERR_MISALIGNED = 3,    /* a vector-loaded array is not 16-byte aligned     */
+    QWAM_ERR_NO_DEVICE = 4,     /* no HIP device is visible                         */
+    QWAM_ERR_HIP = 5            /* the HIP runtime reported an error at launch      */
+} qwam_status;
+
+/* One packed ASP layer: a plain struct of caller-owned device pointers. */
+typedef struct qwam_layer {
+    int32_t K;                  /* input channels (multiple of 64)                  */
+    int32_t N;                  /* output channels (multiple of 16)                 */
+    int32_t r;                  /* rank of the protected subspace (16/32/48/64)     */
+    int32_t group;              /* must be 64                                        */
+    const uint8_t *wq;          /* [N][K/2]  packed residual codes                   */
+    const float *ws;            /* [K/64][N] residual group scales                   */
+    const float *inv_smooth;    /* [K]       fl32(1/lambda)                          */
+    const uint16_t *L1t;        /* [r][K]    bf16                                    */
+    const uint16_t *L2t;        /* [N][r]    bf16                                    */
+    const uint16_t *bias;       /* [N]       bf16, or NULL for no bias               */
+} qwam_layer;
+
+/*
+ * Offline weight pack (weights are quantized once, Sec. 3; the exported codes
+ * of App. B.1).  Quantizes each group of 64 consecutive entries of each row of
+ * R with the quantizer of Eq. 2 (scale = fl32(absmax / 7); a group with absmax
+ * below 7 * 2^-126 gets scale 0 and codes 0), packs the codes and writes
+ * inv_smooth[k] = fl32(1 / smooth[k]).
+ *   R          in   float [N][K]
+ *   smooth     in   float [K], every entry finite and nonzero
+ *   wq         out  uint8 [N][K/2]
+ *   ws         out  float [K/64][N]
+ *   inv_smooth out  float [K]
+ */
+qwam_status qwam_pack_weights(int32_t K, int32_t N, int32_t group,
+                              const float *R, const float *smooth,
+                              uint8_t *wq, float *ws, float *inv_smooth,
+                              void *stream);
+
+/*
+ * Activation side of one layer call (the first kernel of App. B.1): for every
+ * token, x~ = fl32(x * inv_smooth) (Eq. 3, the smoothing divide done as a
+ * multiply by the packed reciprocal), per-token group quantization of x~
+ * (Eq. 2, absmax / 7 per token and group), nibble packing, and the rank-r
+ * down-projection t = V^T x~ of Eq. 9 (bf16 inputs, float32 accumulation,
+ * bf16 result), in one pass over x.
+ *   L   in   layer (reads K, r, group, inv_smooth, L1t)
+ *   x   in   bf16 [M][K]
+ *   xq  out  uint8 [M][K/2]
+ *   xs  out  float [K/64][M]
+ *   t   out  bf16 [M][r]
+ */
+qwam_status qwam_quantize_act(const qwam_layer *L, int32_t M, const uint16_t *x,
+                              uint8_t *xq, float *xs, uint16_t *t, void *stream);
+
+/*
+ * The ASP GEMM (the second kernel of App. B.1): the integer partial sum of
+ * every group, P[m, n, g] = sum_{k in g} qx[m, k] qw[n, k] (exact, int32,
+ * INT8 matrix cores), scaled by xs[g][m] * ws[g][n] and accumulated over the
+ * groups in float32, plus the branch t . L2 and the bias, rounded to bf16:
+ *     y[m, n] = bf16( sum_g xs ws P + sum_j t[m, j] L2t[n, j] + bias[n] )
+ *   L   in   packed layer
+ *   xq, xs, t  in  outputs of qwam_quantize_act for the same M
+ *   y   out  bf16 [M][N]
+ */
+qwam_status qwam_asp_linear(const qwam_layer *L, int32_t M, const uint8_t *xq,
+                            const float *xs, const uint16_t *t, uint16_t *y,
+                            void *stream);
+
+/*
+ * Test access to the exact integer group partials of qwam_asp_linear's
+ * integer GEMM (same unpack and matrix-core path).
+ *   L   in   packed layer (reads K, N, group, wq)
+ *   xq  in   uint8 [M][K/2]
+ *   P   out  int32 [M][N][K/64]
+ */
+qwam_status qwam_debug_group_partials(const qwam_layer *L, int32_t M, const uint8_t *xq,
+                                      int32_t *P, void *stream);
+
+/* Message describing the calling thread's last non-OK status ("" if none). */
+const char *qwam_last_error(void);
+
+/* Static name of a status code. */
+const char *qwam_status_string(qwam_status s);
+
+/* QWAM_ABI_VERSION of the loaded library. */
+int32_t qwam_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QWAM_H */

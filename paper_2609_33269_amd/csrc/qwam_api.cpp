@@ -1,0 +1,169 @@
+// C ABI of libqwam: argument validation and dispatch to the HIP kernels.
+// Every check runs on the host before any HIP call; device memory is never
+// dereferenced here.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdint>
+#include <cstdio>
+
+#include "../../include/qwam.h"
+#include "qwam_internal.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+qwam_status fail(qwam_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+qwam_status ok() {
+  g_err[0] = '\0';
+  return QWAM_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+#define QWAM_REQUIRE_PTR(p)                                                              \
+  do {                                                                                   \
+    if ((p) == nullptr) return fail(QWAM_ERR_INVALID_ARG, "%s: %s is NULL", fn, #p);     \
+    if (!aligned16(p)) return fail(QWAM_ERR_MISALIGNED, "%s: %s is not 16-byte aligned", fn, #p); \
+  } while (0)
+
+constexpr int32_t kMaxK = 65536;
+constexpr int32_t kMaxN = 1 << 20;
+constexpr int32_t kMaxM = 1 << 20;
+
+qwam_status check_kn(const char* fn, int32_t K, int32_t N, int32_t group) {
+  if (group != QWAM_GROUP) return fail(QWAM_ERR_INVALID_ARG, "%s: group must be 64 (got %d)", fn, group);
+  if (K <= 0 || K % QWAM_GROUP != 0) return fail(QWAM_ERR_INVALID_ARG, "%s: K must be a positive multiple of 64 (got %d)", fn, K);
+  if (N <= 0 || N % 16 != 0) return fail(QWAM_ERR_INVALID_ARG, "%s: N must be a positive multiple of 16 (got %d)", fn, N);
+  if (K > kMaxK) return fail(QWAM_ERR_UNSUPPORTED, "%s: K = %d exceeds %d", fn, K, kMaxK);
+  if (N > kMaxN) return fail(QWAM_ERR_UNSUPPORTED, "%s: N = %d exceeds %d", fn, N, kMaxN);
+  return QWAM_OK;
+}
+
+qwam_status check_layer(const char* fn, const qwam_layer* L, bool need_branch) {
+  if (L == nullptr) return fail(QWAM_ERR_INVALID_ARG, "%s: layer is NULL", fn);
+  qwam_status s = check_kn(fn, L->K, L->N, L->group);
+  if (s != QWAM_OK) return s;
+  if (need_branch && !(L->r == 16 || L->r == 32 || L->r == 48 || L->r == 64))
+    return fail(QWAM_ERR_UNSUPPORTED, "%s: rank r must be 16, 32, 48 or 64 (got %d)", fn, L->r);
+  return QWAM_OK;
+}
+
+qwam_status check_m(const char* fn, int32_t M) {
+  if (M <= 0) return fail(QWAM_ERR_INVALID_ARG, "%s: M must be >= 1 (got %d)", fn, M);
+  if (M > kMaxM) return fail(QWAM_ERR_UNSUPPORTED, "%s: M = %d exceeds %d", fn, M, kMaxM);
+  return QWAM_OK;
+}
+
+qwam_status check_device(const char* fn) {
+  int n = 0;
+  const hipError_t e = hipGetDeviceCount(&n);
+  if (e != hipSuccess || n <= 0) {
+    (void)hipGetLastError();
+    return fail(QWAM_ERR_NO_DEVICE, "%s: no HIP device visible", fn);
+  }
+  return QWAM_OK;
+}
+
+qwam_status launched(const char* fn, hipError_t e) {
+  if (e != hipSuccess) return fail(QWAM_ERR_HIP, "%s: kernel launch failed: %s", fn, hipGetErrorString(e));
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+qwam_status qwam_pack_weights(int32_t K, int32_t N, int32_t group, const float* R, const float* smooth,
+                              uint8_t* wq, float* ws, float* inv_smooth, void* stream) {
+  const char* fn = "qwam_pack_weights";
+  qwam_status s = check_kn(fn, K, N, group);
+  if (s != QWAM_OK) return s;
+  QWAM_REQUIRE_PTR(R);
+  QWAM_REQUIRE_PTR(smooth);
+  QWAM_REQUIRE_PTR(wq);
+  QWAM_REQUIRE_PTR(ws);
+  QWAM_REQUIRE_PTR(inv_smooth);
+  if ((s = check_device(fn)) != QWAM_OK) return s;
+  return launched(fn, qwam::launch_pack_weights(K, N, R, smooth, wq, ws, inv_smooth,
+                                                static_cast<hipStream_t>(stream)));
+}
+
+qwam_status qwam_quantize_act(const qwam_layer* L, int32_t M, const uint16_t* x, uint8_t* xq, float* xs,
+                              uint16_t* t, void* stream) {
+  const char* fn = "qwam_quantize_act";
+  qwam_status s = check_layer(fn, L, true);
+  if (s != QWAM_OK) return s;
+  if ((s = check_m(fn, M)) != QWAM_OK) return s;
+  QWAM_REQUIRE_PTR(L->inv_smooth);
+  QWAM_REQUIRE_PTR(L->L1t);
+  QWAM_REQUIRE_PTR(x);
+  QWAM_REQUIRE_PTR(xq);
+  QWAM_REQUIRE_PTR(xs);
+  QWAM_REQUIRE_PTR(t);
+  if ((s = check_device(fn)) != QWAM_OK) return s;
+  return launched(fn, qwam::launch_quantize_act(M, L->K, L->r, x, L->inv_smooth, L->L1t, xq, xs, t,
+                                                static_cast<hipStream_t>(stream)));
+}
+
+qwam_status qwam_asp_linear(const qwam_layer* L, int32_t M, const uint8_t* xq, const float* xs,
+                            const uint16_t* t, uint16_t* y, void* stream) {
+  const char* fn = "qwam_asp_linear";
+  qwam_status s = check_layer(fn, L, true);
+  if (s != QWAM_OK) return s;
+  if ((s = check_m(fn, M)) != QWAM_OK) return s;
+  QWAM_REQUIRE_PTR(L->wq);
+  QWAM_REQUIRE_PTR(L->ws);
+  QWAM_REQUIRE_PTR(L->L2t);
+  if (L->bias != nullptr && !aligned16(L->bias))
+    return fail(QWAM_ERR_MISALIGNED, "%s: bias is not 16-byte aligned", fn);
+  QWAM_REQUIRE_PTR(xq);
+  QWAM_REQUIRE_PTR(xs);
+  QWAM_REQUIRE_PTR(t);
+  QWAM_REQUIRE_PTR(y);
+  if ((s = check_device(fn)) != QWAM_OK) return s;
+  return launched(fn, qwam::launch_asp_gemm(M, L->N, L->K, L->r, xq, xs, t, L->wq, L->ws, L->L2t, L->bias, y,
+                                            static_cast<hipStream_t>(stream)));
+}
+
+qwam_status qwam_debug_group_partials(const qwam_layer* L, int32_t M, const uint8_t* xq, int32_t* P,
+                                      void* stream) {
+  const char* fn = "qwam_debug_group_partials";
+  qwam_status s = check_layer(fn, L, false);
+  if (s != QWAM_OK) return s;
+  if ((s = check_m(fn, M)) != QWAM_OK) return s;
+  QWAM_REQUIRE_PTR(L->wq);
+  QWAM_REQUIRE_PTR(xq);
+  QWAM_REQUIRE_PTR(P);
+  if (static_cast<int64_t>(M) * L->N * (L->K / QWAM_GROUP) > (int64_t(1) << 34))
+    return fail(QWAM_ERR_UNSUPPORTED, "%s: M*N*K/64 too large for a partials dump", fn);
+  if ((s = check_device(fn)) != QWAM_OK) return s;
+  return launched(fn, qwam::launch_group_partials(M, L->N, L->K, xq, L->wq, P,
+                                                  static_cast<hipStream_t>(stream)));
+}
+
+const char* qwam_last_error(void) { return g_err; }
+
+const char* qwam_status_string(qwam_status s) {
+  switch (s) {
+    case QWAM_OK: return "QWAM_OK";
+    case QWAM_ERR_INVALID_ARG: return "QWAM_ERR_INVALID_ARG";
+    case QWAM_ERR_UNSUPPORTED: return "QWAM_ERR_UNSUPPORTED";
+    case QWAM_ERR_MISALIGNED: return "QWAM_ERR_MISALIGNED";
+    case QWAM_ERR_NO_DEVICE: return "QWAM_ERR_NO_DEVICE";
+    case QWAM_ERR_HIP: return "QWAM_ERR_HIP";
+  }
+  return "QWAM_ERR_UNKNOWN";
+}
+
+int32_t qwam_abi_version(void) { return QWAM_ABI_VERSION; }
+
+}  // extern "C"

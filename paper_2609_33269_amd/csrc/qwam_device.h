@@ -1,0 +1,68 @@
+// Device-side helpers shared by the ASP kernels (gfx950).
+//
+// The 4-bit group quantizer of Eq. 2 (Sec. 3) as the kernels apply it:
+//   scale = fl32(absmax / 7)            (0 when absmax < 7 * 2^-126)
+//   inv   = fl32(1 / scale)             (0 when scale == 0)
+//   code  = clamp(rint(fl32(v * inv)), -8, 7)   rint = round half to even
+// Division is IEEE correctly rounded (hipcc's default for float '/'); no
+// contraction is allowed anywhere in this file.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#pragma clang fp contract(off)
+
+namespace qwam {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+typedef short v8s __attribute__((ext_vector_type(8)));
+
+constexpr int kGroup = 64;
+
+__device__ __forceinline__ float q4_scale(float amax) {
+  // 7 * 2^-126 = 1.75 * 2^-124
+  return (amax < 0x1.cp-124f) ? 0.0f : amax / 7.0f;
+}
+
+__device__ __forceinline__ float q4_inv(float scale) {
+  return (scale == 0.0f) ? 0.0f : 1.0f / scale;
+}
+
+// Returns the 4-bit two's-complement nibble (0..15) of the code of v.
+__device__ __forceinline__ uint32_t q4_nibble(float v, float inv) {
+  float p = v * inv;
+  p = __builtin_rintf(p);
+  p = __builtin_fminf(__builtin_fmaxf(p, -8.0f), 7.0f);
+  return static_cast<uint32_t>(static_cast<int>(p)) & 0xFu;
+}
+
+// bf16 bits -> float (exact).
+__device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
+  return __uint_as_float(bits16 << 16);
+}
+
+// float -> bf16 bits, round to nearest, ties to even (finite inputs).
+__device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+// Two floats -> packed bf16x2 (lo in bits 0..15), RNE.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return f32_to_bf16_rne(lo) | (f32_to_bf16_rne(hi) << 16);
+}
+
+// Unpack 8 packed 4-bit codes (one dword, low nibble = even k) into two dwords
+// of int8 values 16*code: `even` holds the codes of k = 0,2,4,6 and `odd` those
+// of k = 1,3,5,7, each scaled by 16 (the nibble lands in the high half of its
+// byte, which is 16*code in two's complement).  Products of two such bytes are
+// 256*qx*qw exactly.
+__device__ __forceinline__ void unpack_nibbles_x16(uint32_t w, uint32_t& even, uint32_t& odd) {
+  even = (w << 4) & 0xF0F0F0F0u;
+  odd = w & 0xF0F0F0F0u;
+}
+
+}  // namespace qwam

@@ -1,0 +1,23 @@
+// Host-side launchers of the ASP kernels (internal to libqwam).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace qwam {
+
+hipError_t launch_pack_weights(int K, int N, const float* R, const float* smooth, uint8_t* wq,
+                               float* ws, float* inv_smooth, hipStream_t stream);
+
+hipError_t launch_quantize_act(int M, int K, int r, const uint16_t* x, const float* inv_smooth,
+                               const uint16_t* L1t, uint8_t* xq, float* xs, uint16_t* t,
+                               hipStream_t stream);
+
+hipError_t launch_asp_gemm(int M, int N, int K, int r, const uint8_t* xq, const float* xs,
+                           const uint16_t* t, const uint8_t* wq, const float* ws,
+                           const uint16_t* L2t, const uint16_t* bias, uint16_t* y,
+                           hipStream_t stream);
+
+hipError_t launch_group_partials(int M, int N, int K, const uint8_t* xq, const uint8_t* wq,
+                                 int32_t* P, hipStream_t stream);
+
+}  // namespace qwam

@@ -1,0 +1,198 @@
+"""Python binding of libqwam (ctypes): argument marshalling only.
+
+Every step of the layer runs in the library's HIP kernels; this module checks
+tensor devices, dtypes and shapes, allocates outputs with PyTorch and passes
+raw device pointers plus the current HIP stream across the C ABI.  If the
+library is not built, every call raises: there is no fallback.
+
+Names follow the C ABI (include/qwam.h): pack_weights, quantize_act,
+asp_linear, debug_group_partials.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+import torch
+
+GROUP = 64
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libqwam.so")
+
+STATUS_NAMES = {0: "QWAM_OK", 1: "QWAM_ERR_INVALID_ARG", 2: "QWAM_ERR_UNSUPPORTED",
+                3: "QWAM_ERR_MISALIGNED", 4: "QWAM_ERR_NO_DEVICE", 5: "QWAM_ERR_HIP"}
+
+# every entry point the header declares, with (restype, argtypes)
+_c_void_p, _i32 = ctypes.c_void_p, ctypes.c_int32
+
+
+class QwamLayerC(ctypes.Structure):
+    _fields_ = [("K", ctypes.c_int32), ("N", ctypes.c_int32), ("r", ctypes.c_int32),
+                ("group", ctypes.c_int32), ("wq", ctypes.c_void_p), ("ws", ctypes.c_void_p),
+                ("inv_smooth", ctypes.c_void_p), ("L1t", ctypes.c_void_p),
+                ("L2t", ctypes.c_void_p), ("bias", ctypes.c_void_p)]
+
+
+_LP = ctypes.POINTER(QwamLayerC)
+SIGNATURES = {
+    "qwam_pack_weights": (ctypes.c_int, [_i32, _i32, _i32, _c_void_p, _c_void_p, _c_void_p,
+                                         _c_void_p, _c_void_p, _c_void_p]),
+    "qwam_quantize_act": (ctypes.c_int, [_LP, _i32, _c_void_p, _c_void_p, _c_void_p, _c_void_p,
+                                         _c_void_p]),
+    "qwam_asp_linear": (ctypes.c_int, [_LP, _i32, _c_void_p, _c_void_p, _c_void_p, _c_void_p,
+                                       _c_void_p]),
+    "qwam_debug_group_partials": (ctypes.c_int, [_LP, _i32, _c_void_p, _c_void_p, _c_void_p]),
+    "qwam_last_error": (ctypes.c_char_p, []),
+    "qwam_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "qwam_abi_version": (ctypes.c_int32, []),
+}
+
+_lib = None
+
+
+class QwamError(RuntimeError):
+    def __init__(self, fn: str, status: int, message: str):
+        super().__init__(f"{fn} -> {STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+
+
+def lib() -> ctypes.CDLL:
+    """Load libqwam.so (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2609_33269_amd.build`")
+        handle = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            f = getattr(handle, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = handle
+    return _lib
+
+
+def _check(fn: str, status: int) -> None:
+    if status != 0:
+        raise QwamError(fn, status, lib().qwam_last_error().decode())
+
+
+def _stream_ptr(stream) -> int:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return int(s.cuda_stream)
+
+
+def _req(t: torch.Tensor, name: str, dtype: torch.dtype, shape) -> int:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a GPU tensor (got {t.device})")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype} (got {t.dtype})")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)} (got {tuple(t.shape)})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+@dataclass
+class PackedLayer:
+    """Device tensors of one packed ASP layer (see include/qwam.h for layouts)."""
+    K: int
+    N: int
+    r: int
+    wq: torch.Tensor          # uint8 [N][K/2]
+    ws: torch.Tensor          # float32 [K/64][N]
+    inv_smooth: torch.Tensor  # float32 [K]
+    L1t: torch.Tensor         # bf16 [r][K]
+    L2t: torch.Tensor         # bf16 [N][r]
+    bias: Optional[torch.Tensor] = None   # bf16 [N]
+
+    def c_struct(self) -> QwamLayerC:
+        G = self.K // GROUP
+        c = QwamLayerC()
+        c.K, c.N, c.r, c.group = self.K, self.N, self.r, GROUP
+        c.wq = _req(self.wq, "wq", torch.uint8, (self.N, self.K // 2))
+        c.ws = _req(self.ws, "ws", torch.float32, (G, self.N))
+        c.inv_smooth = _req(self.inv_smooth, "inv_smooth", torch.float32, (self.K,))
+        c.L1t = _req(self.L1t, "L1t", torch.bfloat16, (self.r, self.K))
+        c.L2t = _req(self.L2t, "L2t", torch.bfloat16, (self.N, self.r))
+        c.bias = None if self.bias is None else _req(self.bias, "bias", torch.bfloat16, (self.N,))
+        return c
+
+
+def pack_weights(R: torch.Tensor, smooth: torch.Tensor, stream=None):
+    """qwam_pack_weights: R float32 [N][K], smooth float32 [K] ->
+    (wq uint8 [N][K/2], ws float32 [K/64][N], inv_smooth float32 [K])."""
+    N, K = R.shape
+    dev = R.device
+    wq = torch.empty((N, K // 2), dtype=torch.uint8, device=dev)
+    ws = torch.empty((K // GROUP, N), dtype=torch.float32, device=dev)
+    inv = torch.empty((K,), dtype=torch.float32, device=dev)
+    st = lib().qwam_pack_weights(K, N, GROUP, _req(R, "R", torch.float32, (N, K)),
+                                 _req(smooth, "smooth", torch.float32, (K,)),
+                                 wq.data_ptr(), ws.data_ptr(), inv.data_ptr(), _stream_ptr(stream))
+    _check("qwam_pack_weights", st)
+    return wq, ws, inv
+
+
+def make_layer(R: torch.Tensor, smooth: torch.Tensor, L1: torch.Tensor, L2: torch.Tensor,
+               bias: Optional[torch.Tensor] = None, stream=None) -> PackedLayer:
+    """Pack R and lambda and lay out the branch factors: L1 bf16 [K][r] and
+    L2 bf16 [r][N] are stored transposed (L1t [r][K], L2t [N][r])."""
+    N, K = R.shape
+    r = L1.shape[1]
+    wq, ws, inv = pack_weights(R, smooth, stream)
+    return PackedLayer(K=K, N=N, r=r, wq=wq, ws=ws, inv_smooth=inv,
+                       L1t=L1.t().contiguous(), L2t=L2.t().contiguous(),
+                       bias=None if bias is None else bias.contiguous())
+
+
+def quantize_act(layer: PackedLayer, x: torch.Tensor, stream=None):
+    """qwam_quantize_act: x bf16 [M][K] -> (xq uint8 [M][K/2], xs float32 [K/64][M], t bf16 [M][r])."""
+    M = x.shape[0]
+    dev = x.device
+    xq = torch.empty((M, layer.K // 2), dtype=torch.uint8, device=dev)
+    xs = torch.empty((layer.K // GROUP, M), dtype=torch.float32, device=dev)
+    t = torch.empty((M, layer.r), dtype=torch.bfloat16, device=dev)
+    c = layer.c_struct()
+    st = lib().qwam_quantize_act(ctypes.byref(c), M, _req(x, "x", torch.bfloat16, (M, layer.K)),
+                                 xq.data_ptr(), xs.data_ptr(), t.data_ptr(), _stream_ptr(stream))
+    _check("qwam_quantize_act", st)
+    return xq, xs, t
+
+
+def asp_linear(layer: PackedLayer, xq: torch.Tensor, xs: torch.Tensor, t: torch.Tensor,
+               out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """qwam_asp_linear: -> y bf16 [M][N]."""
+    M = xq.shape[0]
+    G = layer.K // GROUP
+    y = torch.empty((M, layer.N), dtype=torch.bfloat16, device=xq.device) if out is None else out
+    c = layer.c_struct()
+    st = lib().qwam_asp_linear(ctypes.byref(c), M, _req(xq, "xq", torch.uint8, (M, layer.K // 2)),
+                               _req(xs, "xs", torch.float32, (G, M)),
+                               _req(t, "t", torch.bfloat16, (M, layer.r)),
+                               _req(y, "y", torch.bfloat16, (M, layer.N)), _stream_ptr(stream))
+    _check("qwam_asp_linear", st)
+    return y
+
+
+def forward(layer: PackedLayer, x: torch.Tensor, stream=None) -> torch.Tensor:
+    """Both kernels of one layer call: quantize_act then asp_linear."""
+    xq, xs, t = quantize_act(layer, x, stream)
+    return asp_linear(layer, xq, xs, t, stream=stream)
+
+
+def debug_group_partials(layer: PackedLayer, xq: torch.Tensor, stream=None) -> torch.Tensor:
+    """qwam_debug_group_partials: -> P int32 [M][N][K/64] (exact integer partials)."""
+    M = xq.shape[0]
+    G = layer.K // GROUP
+    P = torch.empty((M, layer.N, G), dtype=torch.int32, device=xq.device)
+    c = layer.c_struct()
+    st = lib().qwam_debug_group_partials(ctypes.byref(c), M,
+                                         _req(xq, "xq", torch.uint8, (M, layer.K // 2)),
+                                         P.data_ptr(), _stream_ptr(stream))
+    _check("qwam_debug_group_partials", st)
+    return P

@@ -1,0 +1,93 @@
+"""Shared helpers of the GPU parity tests: move seeded inputs and oracle-built
+layer factors to the GPU, run the library through its C ABI, and compare."""
+
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import torch
+
+from oracle import qwam_oracle as O
+from paper_2609_33269_amd import qwam as Q
+
+U32 = 2.0 ** -24
+
+
+def log(msg: str) -> None:
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def bf16_dev(bits: np.ndarray) -> torch.Tensor:
+    """uint16 bf16 bits (numpy) -> bf16 tensor on cuda:0 (bit-exact)."""
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to("cuda:0")
+
+
+def f32_dev(a: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to("cuda:0")
+
+
+def bits(t: torch.Tensor) -> np.ndarray:
+    """bf16 tensor -> uint16 bits (numpy)."""
+    return t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def oracle_factors(draws, r=None):
+    r = draws.shape.r if r is None else r
+    V = O.protected_basis_from_factor(draws.a, r)
+    return O.build_layer(draws.x, draws.w, V)
+
+
+def gpu_layer(factors, bias_bits=None) -> Q.PackedLayer:
+    """Pack the oracle-built factors with the library (qwam_pack_weights)."""
+    L1 = bf16_dev(factors["L1"])
+    L2 = bf16_dev(factors["L2"])
+    bias = None if bias_bits is None else bf16_dev(bias_bits)
+    return Q.make_layer(f32_dev(factors["R"]), f32_dev(factors["lam"]), L1, L2, bias)
+
+
+def rel_fro(a: np.ndarray, b: np.ndarray) -> float:
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    nb = np.linalg.norm(b)
+    return float(np.linalg.norm(a - b) / (nb if nb > 0 else 1.0))
+
+
+def bf16_ulp(v: np.ndarray) -> np.ndarray:
+    """Spacing of bf16 numbers at |v| (2**-133 below the normal range)."""
+    v = np.abs(np.asarray(v, dtype=np.float64))
+    _, e = np.frexp(v)
+    e = np.maximum(e, -125)
+    return np.ldexp(np.ones_like(v), e - 8)
+
+
+def check_t(t_gpu_bits, t_ref_bits, xt, L1_bits, frac_over_1ulp=1e-3):
+    """t from the GPU (bf16 of a float32 accumulation) against the oracle's
+    bf16 of the exact sum.
+
+    Rigorous per element: |t_gpu - t_ref| <= ulp(t) + K 2^-24 sum_k |bf16(x~_k) L1[k, j]|
+    (rounding of both to bf16 plus the worst-case error of a float32 sum of K
+    terms).  Statistically: at most `frac_over_1ulp` of the elements differ by
+    more than one bf16 ulp (that only happens where the sum nearly cancels).
+    """
+    tg = O.bf16_bits_to_f64(t_gpu_bits)
+    tr = O.bf16_bits_to_f64(t_ref_bits)
+    K = xt.shape[1]
+    absterms = np.abs(O.round_to_bf16(xt)) @ np.abs(O.bf16_bits_to_f64(L1_bits))
+    ulp = np.maximum(bf16_ulp(tr), bf16_ulp(tg))
+    diff = np.abs(tg - tr)
+    bound = ulp + K * U32 * absterms
+    assert (diff <= bound).all(), f"t outside the rounding bound at {np.argwhere(diff > bound)[:5].tolist()}"
+    over = float(np.mean(diff > ulp))
+    assert over <= frac_over_1ulp, f"{over:.2e} of t elements differ by more than 1 bf16 ulp"
+    return over
+
+
+def run_gpu(layer: Q.PackedLayer, x_bits: np.ndarray):
+    """quantize_act + asp_linear on cuda:0; returns device tensors."""
+    x = bf16_dev(x_bits)
+    xq, xs, t = Q.quantize_act(layer, x)
+    y = Q.asp_linear(layer, xq, xs, t)
+    torch.cuda.synchronize()
+    return x, xq, xs, t, y

@@ -1,0 +1,123 @@
+"""The C ABI on the host: the library loads, exports every entry point that
+include/qwam.h declares, and rejects bad arguments with the documented status
+before any HIP call (no device memory is touched: the pointers below are
+fake, never dereferenced)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+import torch
+
+from paper_2609_33269_amd import qwam as Q
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "qwam.h")
+
+OK, INVALID, UNSUPPORTED, MISALIGNED, NO_DEVICE = 0, 1, 2, 3, 4
+FAKE = 0x10000          # 16-byte aligned, never dereferenced
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(Q.LIB_PATH):
+        from paper_2609_33269_amd import build
+        build.build()
+    return Q.lib()
+
+
+def _declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(qwam_[a-z_]+)\s*\(", src)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = _declared_functions()
+    assert set(names) == set(Q.SIGNATURES), "binding and header disagree"
+    for n in names:
+        assert hasattr(lib, n), n
+    assert lib.qwam_abi_version() == 1
+    assert lib.qwam_status_string(3) == b"QWAM_ERR_MISALIGNED"
+
+
+def _layer(K=256, N=256, r=16, group=64, **ptrs):
+    c = Q.QwamLayerC()
+    c.K, c.N, c.r, c.group = K, N, r, group
+    for f in ("wq", "ws", "inv_smooth", "L1t", "L2t"):
+        setattr(c, f, ptrs.get(f, FAKE))
+    c.bias = ptrs.get("bias", None)
+    return c
+
+
+def _act(lib, layer, M=64, x=FAKE, xq=FAKE, xs=FAKE, t=FAKE):
+    return lib.qwam_quantize_act(ctypes.byref(layer), M, x, xq, xs, t, None)
+
+
+def _lin(lib, layer, M=64, xq=FAKE, xs=FAKE, t=FAKE, y=FAKE):
+    return lib.qwam_asp_linear(ctypes.byref(layer), M, xq, xs, t, y, None)
+
+
+@pytest.mark.parametrize("K,N,group,status", [
+    (256, 256, 32, INVALID), (100, 256, 64, INVALID), (0, 256, 64, INVALID), (256, 24, 64, INVALID),
+    (256, 0, 64, INVALID), (-64, 256, 64, INVALID), (131072, 256, 64, UNSUPPORTED),
+    (256, 1 << 21, 64, UNSUPPORTED)])
+def test_pack_rejects_bad_shapes(lib, K, N, group, status):
+    assert lib.qwam_pack_weights(K, N, group, FAKE, FAKE, FAKE, FAKE, FAKE, None) == status
+    assert lib.qwam_last_error().startswith(b"qwam_pack_weights")
+
+
+def test_pack_rejects_null_and_misaligned(lib):
+    args = [FAKE] * 5
+    for i in range(5):
+        a = list(args); a[i] = None
+        assert lib.qwam_pack_weights(256, 256, 64, *a, None) == INVALID
+        a = list(args); a[i] = FAKE + 4
+        assert lib.qwam_pack_weights(256, 256, 64, *a, None) == MISALIGNED
+
+
+def test_layer_calls_reject_bad_arguments(lib):
+    assert lib.qwam_quantize_act(None, 64, FAKE, FAKE, FAKE, FAKE, None) == INVALID
+    for r in (0, 8, 24, 128):
+        assert _act(lib, _layer(r=r)) == UNSUPPORTED
+        assert _lin(lib, _layer(r=r)) == UNSUPPORTED
+    for M, st in ((0, INVALID), (-3, INVALID), (1 << 21, UNSUPPORTED)):
+        assert _act(lib, _layer(), M=M) == st
+        assert _lin(lib, _layer(), M=M) == st
+    assert _act(lib, _layer(group=128)) == INVALID
+    assert _lin(lib, _layer(K=96)) == INVALID
+    for f in ("inv_smooth", "L1t"):
+        assert _act(lib, _layer(**{f: None})) == INVALID
+        assert _act(lib, _layer(**{f: FAKE + 2})) == MISALIGNED
+    for f in ("wq", "ws", "L2t"):
+        assert _lin(lib, _layer(**{f: None})) == INVALID
+        assert _lin(lib, _layer(**{f: FAKE + 8})) == MISALIGNED
+    assert _lin(lib, _layer(bias=FAKE + 2)) == MISALIGNED
+    for kw in ("x", "xq", "xs", "t"):
+        assert _act(lib, _layer(), **{kw: None}) == INVALID
+        assert _act(lib, _layer(), **{kw: FAKE + 1}) == MISALIGNED
+    for kw in ("xq", "xs", "t", "y"):
+        assert _lin(lib, _layer(), **{kw: None}) == INVALID
+    msg = lib.qwam_last_error()
+    assert msg.startswith(b"qwam_asp_linear") and b"y is NULL" in msg
+    # partials: rank is not used, but shapes and pointers are checked
+    assert lib.qwam_debug_group_partials(ctypes.byref(_layer(r=7)), 1, None, FAKE, None) == INVALID
+
+
+@pytest.mark.skipif(torch.cuda.device_count() > 0, reason="a GPU is visible: the no-device path cannot be forced")
+def test_no_device_is_reported_before_any_launch(lib):
+    assert lib.qwam_pack_weights(256, 256, 64, FAKE, FAKE, FAKE, FAKE, FAKE, None) == NO_DEVICE
+    assert _act(lib, _layer()) == NO_DEVICE
+    assert _lin(lib, _layer()) == NO_DEVICE
+    assert lib.qwam_debug_group_partials(ctypes.byref(_layer()), 4, FAKE, FAKE, None) == NO_DEVICE
+    assert b"no HIP device" in lib.qwam_last_error()
+
+
+def test_binding_rejects_host_tensors():
+    layer = Q.PackedLayer(K=64, N=16, r=16, wq=torch.zeros(16, 32, dtype=torch.uint8),
+                          ws=torch.zeros(1, 16), inv_smooth=torch.ones(64),
+                          L1t=torch.zeros(16, 64, dtype=torch.bfloat16),
+                          L2t=torch.zeros(16, 16, dtype=torch.bfloat16))
+    with pytest.raises(ValueError, match="GPU tensor"):
+        layer.c_struct()
