@@ -141,11 +141,12 @@ def protected_basis_from_factor(a: np.ndarray, r: int) -> np.ndarray:
 
     The eigenvectors of A A^T are the left singular vectors of A (eigenvalue
     sigma**2 / K + RIDGE, so the order is the singular-value order); the ridge
-    shifts eigenvalues, not eigenvectors.  Requires r < number of columns of A
-    so that the top-r space is separated from the flat ridge part.
+    shifts eigenvalues, not eigenvectors.  Requires r <= number of columns of A:
+    the first 64 eigenvalues exceed the flat ridge part, so the top-r space is
+    unique.
     """
     U, S, _ = np.linalg.svd(np.asarray(a, dtype=np.float64), full_matrices=False)
-    assert r < a.shape[1], "rank must be below the Gramian factor's width"
+    assert r <= a.shape[1], "rank must not exceed the Gramian factor's width"
     return _fix_signs(U[:, :r])
 
 
