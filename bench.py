@@ -1,0 +1,233 @@
+"""Benchmark of the ASP W4A4 + rank-32 linear layer on one MI355X.
+
+Workload: the video-DiT FFN up-projection, M = 4096 tokens, K = 3072,
+N = 14336, rank r = 32, group 64, bf16 in / out, seeded synthetic inputs
+(activations N(0,1) with 1% of channels scaled by a log-uniform factor in
+[10, 50]; weights N(0, 1/K); factors from the top-32 eigenvectors of a seeded
+SPD Gramian).  One step = one pass of the layer's hot path over one batch:
+the fused activation kernel (smoothing, group-64 INT4 quantization, packing,
+down-projection) and the W4A4 GEMM with the fused bf16 branch.  The weights
+are packed once before timing (they are quantized offline); every input is
+resident in HBM when the timed region starts.
+
+To keep the 256 MB Infinity Cache from serving "HBM" traffic, the steps cycle
+through `--rotate` distinct copies of every input and output buffer.
+
+Prints ONE JSON line (metric, value = effective TOPS = 2 M K N / step time,
+roofline of the dominant kernel, CPU-oracle baseline).
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+M, K, N, R_RANK, GROUP = 4096, 3072, 14336, 32, 64
+G = K // GROUP
+INT8_PEAK_TOPS = 5000.0        # MI355X dense INT8 matrix peak, TOP/s
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+VALU_OPS_PER_OUTPUT_GROUP = 3  # int->float convert, scale product, fused multiply-add
+METRIC = "ASP W4A4+r32 linear: effective TOPS & % int8 MFMA peak at 4096×3072×14336"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_asp_gemm_ffn_up.json")
+GEMM_SRC = os.path.join(ROOT, "paper_2609_33269_amd", "csrc", "qwam_gemm.hip")
+
+
+def algorithmic_bytes():
+    act = M * K * 2 + K * 4 + R_RANK * K * 2 + M * K // 2 + M * G * 4 + M * R_RANK * 2
+    gemm = M * K // 2 + M * G * 4 + M * R_RANK * 2 + N * K // 2 + N * G * 4 + N * R_RANK * 2 + M * N * 2
+    return act, gemm
+
+
+def source_hash(path: str) -> str:
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per GEMM launch from committed rocprofv3 counters, or None if
+    the kernel source changed since they were taken."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("gemm_source_sha256_16") != source_hash(GEMM_SRC):
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(draws, seconds: float = 12.0):
+    """The CPU oracle as it stands, timed on a bounded token sample of the same
+    layer (weights packed beforehand, as on the GPU)."""
+    from oracle import qwam_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:   # pragma: no cover
+        threads = 1
+    V = O.protected_basis_from_factor(draws.a, R_RANK)
+    f = O.build_layer(draws.x, draws.w, V)
+    wq, sw, inv_lam, qw = O.pack_weights(f["R"], f["lam"])
+    chunk = 32
+    done = 0
+    t0 = time.perf_counter()
+    while done + chunk <= M:
+        rows = slice(done, done + chunk)
+        xq, sx, t, qx, _ = O.quantize_activations(draws.x[rows], inv_lam, f["L1"])
+        P = O.group_partials(qx, qw)
+        O.asp_output(sx, sw, P, t, f["L2"])
+        done += chunk
+        if time.perf_counter() - t0 >= seconds:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": 2.0 * done * K * N / dt / 1e12, "unit": "TOPS", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{done} of {M} tokens (chunks of {chunk}) of the {M}x{K}x{N} r{R_RANK} layer, "
+                      f"weights packed beforehand; {dt:.1f} s; value = 2*tokens*K*N/time"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--rotate", type=int, default=24, help="distinct buffer sets cycled through")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the layer is not sharded "
+              f"across GPUs in this build", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_33269_amd import calib, inputs, qwam
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    print(f"[bench] drawing inputs {M}x{K}x{N} r{R_RANK}", file=sys.stderr, flush=True)
+    draws = inputs.video_dit_ffn_up()
+    x0 = torch.from_numpy(draws.x.view(np.int16)).view(torch.bfloat16).to(dev)
+    w0 = torch.from_numpy(draws.w.view(np.int16)).view(torch.bfloat16).to(dev)
+    V = calib.protected_basis(torch.from_numpy(draws.a), R_RANK)
+    f = calib.build_layer(x0, w0, V)
+    layer0 = qwam.make_layer(f["R"], f["lam"], f["L1"], f["L2"])
+    del f, w0
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+    nrot = max(1, args.rotate)
+    layers, xins, outs = [], [], []
+    for i in range(nrot):
+        L = layer0 if i == 0 else qwam.PackedLayer(
+            K=K, N=N, r=R_RANK, wq=layer0.wq.clone(), ws=layer0.ws.clone(),
+            inv_smooth=layer0.inv_smooth.clone(), L1t=layer0.L1t.clone(), L2t=layer0.L2t.clone())
+        layers.append(L)
+        xins.append(x0 if i == 0 else x0.clone())
+        outs.append((torch.empty((M, K // 2), dtype=torch.uint8, device=dev),
+                     torch.empty((G, M), dtype=torch.float32, device=dev),
+                     torch.empty((M, R_RANK), dtype=torch.bfloat16, device=dev),
+                     torch.empty((M, N), dtype=torch.bfloat16, device=dev)))
+    stream = torch.cuda.current_stream()
+
+    def step(i, ev=None):
+        j = i % nrot
+        xq, xs, t, y = outs[j]
+        if ev is not None:
+            ev[0].record(stream)
+        qwam.quantize_act(layers[j], xins[j], out=(xq, xs, t))
+        if ev is not None:
+            ev[1].record(stream)
+        qwam.asp_linear(layers[j], xq, xs, t, out=y)
+        if ev is not None:
+            ev[2].record(stream)
+
+    print(f"[bench] warmup {args.warmup} steps", file=sys.stderr, flush=True)
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for i in range(args.steps):
+        step(args.warmup + i, evs[i])
+    end.record(stream)
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(end)
+    ms_step = total_ms / args.steps
+    k1_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    k2_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    print(f"[bench] {args.steps} steps: {ms_step * 1e3:.1f} us/step, act kernel {k1_ms * 1e3:.1f} us, "
+          f"gemm {k2_ms * 1e3:.1f} us", file=sys.stderr, flush=True)
+
+    int_ops = 2.0 * M * K * N
+    eff_tops = int_ops / (ms_step * 1e-3) / 1e12
+    k2_tops = int_ops / (k2_ms * 1e-3) / 1e12
+    act_bytes, gemm_bytes = algorithmic_bytes()
+    k1_gbs = act_bytes / (k1_ms * 1e-3) / 1e9
+
+    # secondary: the bf16 linear the layer replaces (hipBLASLt through torch), same shape
+    wb = torch.randn((N, K), device=dev, dtype=torch.bfloat16)
+    for _ in range(5):
+        torch.nn.functional.linear(x0, wb)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(20):
+        torch.nn.functional.linear(x0, wb)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    bf16_ms = e0.elapsed_time(e1) / 20
+    del wb
+
+    traffic = measured_traffic()
+    out = {
+        "metric": METRIC,
+        "value": round(eff_tops, 2),
+        "unit": "TOPS",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int8",
+        "data": "synthetic",
+        "config": {"workload": "video_dit_ffn_up", "M": M, "K": K, "N": N, "r": R_RANK, "group": GROUP,
+                   "act": "N(0,1), 1% channels x U_log(10,50)", "weights": "N(0,1/K)",
+                   "rotated_buffer_sets": nrot},
+        "roofline": {"bound": "mfma", "kernel": "asp_gemm_kernel<32>", "achieved": round(k2_tops, 1),
+                     "peak": INT8_PEAK_TOPS, "unit": "TOP/s", "frac": round(k2_tops / INT8_PEAK_TOPS, 4),
+                     "traffic": traffic, "algorithmic_bytes": gemm_bytes},
+        "layer_frac_int8_peak": round(eff_tops / INT8_PEAK_TOPS, 4),
+        "kernels_us": {"quantize_act": round(k1_ms * 1e3, 2), "asp_gemm": round(k2_ms * 1e3, 2)},
+        "quantize_act_roofline": {"bound": "hbm", "achieved": round(k1_gbs, 1), "peak": HBM_PEAK_GBS,
+                                  "unit": "GB/s", "frac": round(k1_gbs / HBM_PEAK_GBS, 4),
+                                  "algorithmic_bytes": act_bytes},
+        # per output and group: 64 int8 MACs on the matrix cores (1024 MAC/clk/SIMD) against
+        # VALU_OPS_PER_OUTPUT_GROUP float32 VALU ops (16 lanes/clk/SIMD): the MFMA share the
+        # VALU issue rate allows if both overlap perfectly
+        "gemm_valu_ceiling_frac": round((64 / 1024) / (VALU_OPS_PER_OUTPUT_GROUP / 16), 4),
+        "bf16_linear_us": round(bf16_ms * 1e3, 2),
+        "speedup_vs_bf16_linear": round(bf16_ms / ms_step, 3),
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on a token sample", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(draws, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

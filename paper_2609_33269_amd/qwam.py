@@ -150,16 +150,23 @@ def make_layer(R: torch.Tensor, smooth: torch.Tensor, L1: torch.Tensor, L2: torc
                        bias=None if bias is None else bias.contiguous())
 
 
-def quantize_act(layer: PackedLayer, x: torch.Tensor, stream=None):
-    """qwam_quantize_act: x bf16 [M][K] -> (xq uint8 [M][K/2], xs float32 [K/64][M], t bf16 [M][r])."""
+def quantize_act(layer: PackedLayer, x: torch.Tensor, stream=None, out=None):
+    """qwam_quantize_act: x bf16 [M][K] -> (xq uint8 [M][K/2], xs float32 [K/64][M], t bf16 [M][r]).
+
+    `out` may give the three output tensors (preallocated, e.g. for a benchmark loop)."""
     M = x.shape[0]
     dev = x.device
-    xq = torch.empty((M, layer.K // 2), dtype=torch.uint8, device=dev)
-    xs = torch.empty((layer.K // GROUP, M), dtype=torch.float32, device=dev)
-    t = torch.empty((M, layer.r), dtype=torch.bfloat16, device=dev)
+    if out is None:
+        xq = torch.empty((M, layer.K // 2), dtype=torch.uint8, device=dev)
+        xs = torch.empty((layer.K // GROUP, M), dtype=torch.float32, device=dev)
+        t = torch.empty((M, layer.r), dtype=torch.bfloat16, device=dev)
+    else:
+        xq, xs, t = out
     c = layer.c_struct()
     st = lib().qwam_quantize_act(ctypes.byref(c), M, _req(x, "x", torch.bfloat16, (M, layer.K)),
-                                 xq.data_ptr(), xs.data_ptr(), t.data_ptr(), _stream_ptr(stream))
+                                 _req(xq, "xq", torch.uint8, (M, layer.K // 2)),
+                                 _req(xs, "xs", torch.float32, (layer.K // GROUP, M)),
+                                 _req(t, "t", torch.bfloat16, (M, layer.r)), _stream_ptr(stream))
     _check("qwam_quantize_act", st)
     return xq, xs, t
 
