@@ -60,7 +60,9 @@
  *   y    bf16    [M][N]      output, round to nearest even from float32
  *
  * Shape limits: group == 64; K % 64 == 0, 64 <= K <= 65536; N % 16 == 0,
- * 16 <= N <= 1048576; r in {16, 32, 48, 64}; 1 <= M <= 1048576.
+ * 16 <= N <= 1048576; r in {16, 32, 48, 64}; 1 <= M <= 1048576; for
+ * qwam_asp_linear also M * K / 64 < 2^29 and N * K / 64 < 2^29
+ * (QWAM_ERR_UNSUPPORTED otherwise).
  */
 #ifndef QWAM_H
 #define QWAM_H

@@ -129,6 +129,10 @@ qwam_status qwam_asp_linear(const qwam_layer* L, int32_t M, const uint8_t* xq, c
   QWAM_REQUIRE_PTR(xs);
   QWAM_REQUIRE_PTR(t);
   QWAM_REQUIRE_PTR(y);
+  // the kernel addresses each scale array with 32-bit byte offsets
+  if (static_cast<int64_t>(M) * (L->K / QWAM_GROUP) >= (int64_t(1) << 29) ||
+      static_cast<int64_t>(L->N) * (L->K / QWAM_GROUP) >= (int64_t(1) << 29))
+    return fail(QWAM_ERR_UNSUPPORTED, "%s: M*K/64 and N*K/64 must be below 2^29", fn);
   if ((s = check_device(fn)) != QWAM_OK) return s;
   return launched(fn, qwam::launch_asp_gemm(M, L->N, L->K, L->r, xq, xs, t, L->wq, L->ws, L->L2t, L->bias, y,
                                             static_cast<hipStream_t>(stream)));

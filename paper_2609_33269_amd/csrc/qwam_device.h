@@ -66,3 +66,29 @@ __device__ __forceinline__ void unpack_nibbles_x16(uint32_t w, uint32_t& even, u
 }
 
 }  // namespace qwam
+
+namespace qwam {
+
+// Raw buffer resource over [base, base + bytes): loads whose byte offset falls
+// outside the range return zero (no fault), so ragged tiles and prefetches past
+// the last group need no branches.  Offsets are 32-bit.
+typedef __amdgpu_buffer_rsrc_t buf_rsrc;
+
+__device__ __forceinline__ buf_rsrc make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, static_cast<int>(bytes),
+                                           0x00020000);
+}
+
+__device__ __forceinline__ uint4 buf_load16(buf_rsrc r, uint32_t off) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+
+__device__ __forceinline__ uint2 buf_load8(buf_rsrc r, uint32_t off) {
+  return __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
+}
+
+__device__ __forceinline__ float buf_load4f(buf_rsrc r, uint32_t off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+}
+
+}  // namespace qwam
