@@ -92,3 +92,35 @@ __device__ __forceinline__ float buf_load4f(buf_rsrc r, uint32_t off) {
 }
 
 }  // namespace qwam
+
+namespace qwam {
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Direct global -> LDS copy of 16 bytes per lane (buffer_load_dwordx4 ... lds):
+// lane i's bytes land at lds_base + 16 * i.  lds_base must be wave-uniform.
+// Out-of-range offsets deposit zeros.  Completion is tracked by vmcnt.
+__device__ __forceinline__ void buf_load16_lds(buf_rsrc r, uint32_t off, void* lds_base) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)lds_base, 16, off, 0, 0, 0);
+}
+
+// Same with 4 bytes per lane (lane i -> lds_base + 4 * i).
+__device__ __forceinline__ void buf_load4_lds(buf_rsrc r, uint32_t off, void* lds_base) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)lds_base, 4, off, 0, 0, 0);
+}
+
+// Workgroup barrier without the implicit full memory fence of __syncthreads()
+// (which would drain every outstanding copy of the LDS ring).  Callers make
+// their own data visible first: wait_vmcnt for their LDS copies, and LDS
+// stores / loads are ordered by the barrier itself.  The "memory" clobber keeps
+// the compiler from moving memory accesses across it.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// s_waitcnt with only the vector-memory counter constrained (vmcnt <= n).
+template <int n>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(n >= 0 && n < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+}  // namespace qwam
