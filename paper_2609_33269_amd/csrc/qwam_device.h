@@ -124,3 +124,18 @@ __device__ __forceinline__ void wait_vmcnt() {
 }
 
 }  // namespace qwam
+
+namespace qwam {
+
+typedef unsigned int v2u_t __attribute__((ext_vector_type(2)));
+
+// Buffer stores: bytes whose offset falls outside the resource are dropped.
+__device__ __forceinline__ void buf_store8(uint2 v, buf_rsrc r, uint32_t off) {
+  __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(v2u_t, v), r, off, 0, 0);
+}
+
+__device__ __forceinline__ void buf_store4f(float v, buf_rsrc r, uint32_t off) {
+  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned int, v), r, off, 0, 0);
+}
+
+}  // namespace qwam

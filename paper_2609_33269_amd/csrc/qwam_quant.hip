@@ -56,52 +56,86 @@ __global__ __launch_bounds__(256) void inverse_smoothing_kernel(const float* __r
 // A-operand layout of v_mfma_f32_16x16x32_bf16 (row = l % 16, the k slots of
 // lane l shared with lane l of the B operand), so the smoothed values feed the
 // down-projection directly from registers: two MFMA steps of 32 channels per
-// group and 16 columns of t.  The per-wave partial t tiles are summed in LDS
-// in wave order (deterministic) and rounded to bf16 once.
+// group and 16 columns of t.  Each wave prefetches the next group (x, 1/lambda,
+// L1t) while it quantizes the current one; x is read with buffer loads and the
+// codes / scales are written with buffer stores, so rows past M need no
+// branches.  The per-wave partial t tiles are summed in LDS in wave order
+// (deterministic) and rounded to bf16 once.
 // ---------------------------------------------------------------------------
 template <int RANK>
-__global__ __launch_bounds__(1024) void quantize_act_kernel(
+struct ActFetch {
+  uint4 xa, xb;                 // 16 bf16 of x
+  v8s l1[RANK / 16][2];         // L1t fragments: 16 channels of 16 columns of t
+};
+
+// Waves per workgroup: 16 (4 per SIMD) up to rank 32, 8 above (more registers
+// for the larger L1t prefetch).
+template <int RANK>
+constexpr int act_waves() { return RANK <= 32 ? 16 : 8; }
+
+template <int RANK, bool INV_LDS>
+__global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_kernel(
     const uint16_t* __restrict__ x, const float* __restrict__ inv_smooth,
     const uint16_t* __restrict__ L1t, uint8_t* __restrict__ xq, float* __restrict__ xs,
     uint16_t* __restrict__ t, int M, int K, int groups_per_wave) {
   constexpr int RB = RANK / 16;
-  extern __shared__ float red[];  // [nwaves][16][RANK]
+  // dynamic LDS: [nwaves][16][RANK] partial t, then (INV_LDS) [nwaves][groups_per_wave * 64] 1/lambda
+  extern __shared__ float red[];
 
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int nwaves = blockDim.x >> 6;
   const int row = lane & 15;
   const int chunk = lane >> 4;
   const int m0 = blockIdx.x * 16;
-  const int m = m0 + row;
-  const bool valid = m < M;
+  const int rows = min(16, M - m0);
   const int G = K / kGroup;
   const int g_begin = wave * groups_per_wave;
   const int g_end = min(G, g_begin + groups_per_wave);
+
+  // the workgroup's 16 rows of x, xq; out-of-range rows read as zero / are dropped
+  const buf_rsrc x_rsrc = make_rsrc(x + static_cast<int64_t>(m0) * K, static_cast<uint32_t>(rows) * K * 2u);
+  const buf_rsrc q_rsrc = make_rsrc(xq + static_cast<int64_t>(m0) * (K / 2), static_cast<uint32_t>(rows) * (K / 2));
+  const uint32_t x_off = static_cast<uint32_t>(row * K + chunk * 16) * 2u;
+  const uint32_t q_off = static_cast<uint32_t>(row * (K / 2) + chunk * 8);
+
+  // the wave's slice of 1/lambda goes to LDS once (a per-group float4 load by
+  // every lane would move 16x more bytes through the address unit than it uses)
+  float* inv_w = red + nwaves * 16 * RANK + wave * groups_per_wave * kGroup;
+  if (INV_LDS && g_begin < g_end) {
+    const int n4 = (g_end - g_begin) * (kGroup / 4);
+    const float4* src = reinterpret_cast<const float4*>(inv_smooth + g_begin * kGroup);
+    for (int i = lane; i < n4; i += 64) reinterpret_cast<float4*>(inv_w)[i] = src[i];
+  }
+
+  auto fetch = [&](int g, ActFetch<RANK>& f) {
+    const uint32_t go = static_cast<uint32_t>(g) * kGroup * 2u;
+    f.xa = buf_load16(x_rsrc, x_off + go);
+    f.xb = buf_load16(x_rsrc, x_off + go + 16u);
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const uint16_t* lp = L1t + static_cast<int64_t>(rb * 16 + row) * K + g * kGroup + chunk * 16;
+      f.l1[rb][0] = *reinterpret_cast<const v8s*>(lp);
+      f.l1[rb][1] = *reinterpret_cast<const v8s*>(lp + 8);
+    }
+  };
 
   v4f acc[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) acc[rb] = v4f{0.f, 0.f, 0.f, 0.f};
 
-  const uint16_t* xrow = x + static_cast<int64_t>(valid ? m : 0) * K;
-
-  for (int g = g_begin; g < g_end; ++g) {
-    const int k0 = g * kGroup + chunk * 16;
-    uint4 xa = make_uint4(0, 0, 0, 0), xb = make_uint4(0, 0, 0, 0);
-    if (valid) {
-      xa = *reinterpret_cast<const uint4*>(xrow + k0);
-      xb = *reinterpret_cast<const uint4*>(xrow + k0 + 8);
-    }
-    const float4* ip = reinterpret_cast<const float4*>(inv_smooth + k0);
+  auto work = [&](int g, const ActFetch<RANK>& f) {
+    const uint32_t xw[8] = {f.xa.x, f.xa.y, f.xa.z, f.xa.w, f.xb.x, f.xb.y, f.xb.z, f.xb.w};
+    const float4* ip = INV_LDS ? reinterpret_cast<const float4*>(inv_w + (g - g_begin) * kGroup + chunk * 16)
+                               : reinterpret_cast<const float4*>(inv_smooth + g * kGroup + chunk * 16);
     const float4 i0 = ip[0], i1 = ip[1], i2 = ip[2], i3 = ip[3];
-    const uint32_t xw[8] = {xa.x, xa.y, xa.z, xa.w, xb.x, xb.y, xb.z, xb.w};
     const float iv[16] = {i0.x, i0.y, i0.z, i0.w, i1.x, i1.y, i1.z, i1.w,
                           i2.x, i2.y, i2.z, i2.w, i3.x, i3.y, i3.z, i3.w};
     float v[16];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      v[2 * j] = bf16_to_f32(xw[j] & 0xFFFFu) * iv[2 * j];
-      v[2 * j + 1] = bf16_to_f32(xw[j] >> 16) * iv[2 * j + 1];
+      v[2 * j] = __uint_as_float(xw[j] << 16) * iv[2 * j];
+      v[2 * j + 1] = __uint_as_float(xw[j] & 0xFFFF0000u) * iv[2 * j + 1];
     }
     float amax = 0.0f;
 #pragma unroll
@@ -110,37 +144,52 @@ __global__ __launch_bounds__(1024) void quantize_act_kernel(
     amax = __builtin_fmaxf(amax, __shfl_xor(amax, 32));
     const float s = q4_scale(amax);
     const float inv = q4_inv(s);
+    // codes: q = clamp(rint(v * inv), -8, 7); a byte holds (q_odd + 8) * 16 + (q_even + 8),
+    // and XOR 0x88 turns that into the two's-complement nibbles (q & 15) | (q_odd & 15) << 4
     uint32_t packed[2];
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       uint32_t wv = 0;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) wv |= q4_nibble(v[8 * h + j], inv) << (4 * j);
-      packed[h] = wv;
+      for (int b = 0; b < 4; ++b) {
+        const float qe = __builtin_fminf(__builtin_fmaxf(__builtin_rintf(v[8 * h + 2 * b] * inv), -8.0f), 7.0f);
+        const float qo = __builtin_fminf(__builtin_fmaxf(__builtin_rintf(v[8 * h + 2 * b + 1] * inv), -8.0f), 7.0f);
+        wv = __builtin_amdgcn_cvt_pk_u8_f32(__builtin_fmaf(qo, 16.0f, qe) + 136.0f, b, wv);
+      }
+      packed[h] = wv ^ 0x88888888u;
     }
-    if (valid) {
-      *reinterpret_cast<uint2*>(xq + static_cast<int64_t>(m) * (K / 2) + g * (kGroup / 2) + chunk * 8) =
-          make_uint2(packed[0], packed[1]);
-      if (chunk == 0) xs[static_cast<int64_t>(g) * M + m] = s;
-    }
+    buf_store8(make_uint2(packed[0], packed[1]), q_rsrc, q_off + static_cast<uint32_t>(g) * (kGroup / 2));
+    // every lane of a row holds the same scale; lanes of row r write it at r
+    if (row < rows) xs[static_cast<int64_t>(g) * M + m0 + row] = s;
 
     // down-projection: A = bf16(x~) of this token, B = L1t rows (columns of t)
-    v8s a_lo, a_hi;
+    typedef __bf16 v8b __attribute__((ext_vector_type(8)));
+    v8b a_lo, a_hi;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      a_lo[j] = static_cast<short>(f32_to_bf16_rne(v[j]));
-      a_hi[j] = static_cast<short>(f32_to_bf16_rne(v[8 + j]));
+      a_lo[j] = static_cast<__bf16>(v[j]);
+      a_hi[j] = static_cast<__bf16>(v[8 + j]);
     }
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
-      const uint16_t* lp = L1t + static_cast<int64_t>(rb * 16 + row) * K + k0;
-      const v8s b_lo = *reinterpret_cast<const v8s*>(lp);
-      const v8s b_hi = *reinterpret_cast<const v8s*>(lp + 8);
-      acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf, a_lo),
-                                                        __builtin_bit_cast(v8bf, b_lo), acc[rb], 0, 0, 0);
-      acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf, a_hi),
-                                                        __builtin_bit_cast(v8bf, b_hi), acc[rb], 0, 0, 0);
+      acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_lo, __builtin_bit_cast(v8bf, f.l1[rb][0]), acc[rb], 0, 0, 0);
+      acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_hi, __builtin_bit_cast(v8bf, f.l1[rb][1]), acc[rb], 0, 0, 0);
     }
+  };
+
+  // software pipeline, two groups per trip so the fetch registers are named statically;
+  // the prefetch past the wave's last group re-reads that group (harmless, in bounds)
+  if (g_begin < g_end) {
+    ActFetch<RANK> fa, fb;
+    fetch(g_begin, fa);
+    int g = g_begin;
+    for (; g + 1 < g_end; g += 2) {
+      fetch(g + 1, fb);
+      work(g, fa);
+      fetch(min(g + 2, g_end - 1), fa);
+      work(g + 1, fb);
+    }
+    if (g < g_end) work(g, fa);
   }
 
   // partial t tiles -> LDS: result row 4*(l/16)+i, column l%16 of block rb
@@ -154,7 +203,7 @@ __global__ __launch_bounds__(1024) void quantize_act_kernel(
     const int i = e / RANK, j = e % RANK;
     float sum = 0.0f;
     for (int w = 0; w < nwaves; ++w) sum += red[(w * 16 + i) * RANK + j];
-    if (m0 + i < M) t[static_cast<int64_t>(m0 + i) * RANK + j] = static_cast<uint16_t>(f32_to_bf16_rne(sum));
+    if (i < rows) t[static_cast<int64_t>(m0 + i) * RANK + j] = static_cast<uint16_t>(f32_to_bf16_rne(sum));
   }
 }
 
@@ -174,27 +223,32 @@ hipError_t launch_quantize_act(int M, int K, int r, const uint16_t* x, const flo
                                const uint16_t* L1t, uint8_t* xq, float* xs, uint16_t* t,
                                hipStream_t stream) {
   const int G = K / kGroup;
-  const int nwaves = G < 16 ? G : 16;
-  const int gpw = (G + nwaves - 1) / nwaves;
-  const dim3 grid((M + 15) / 16), block(64 * nwaves);
-  const size_t lds = static_cast<size_t>(nwaves) * 16 * r * sizeof(float);
+  // 1/lambda is staged in LDS when the slice fits (K <= 16384); larger K reads it from global memory
+  const bool inv_lds = K <= 16384;
+  auto go = [&](auto kernel_lds, auto kernel_global, int max_waves) {
+    const int nwaves = G < max_waves ? G : max_waves;
+    const int gpw = (G + nwaves - 1) / nwaves;
+    const size_t lds = static_cast<size_t>(nwaves) * (16 * r + (inv_lds ? gpw * kGroup : 0)) * sizeof(float);
+    if (lds > 64 * 1024) {   // opt in to more than 64 KB of dynamic LDS
+      const void* fn = inv_lds ? reinterpret_cast<const void*>(kernel_lds) : reinterpret_cast<const void*>(kernel_global);
+      const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+      if (e != hipSuccess) return e;
+    }
+    if (inv_lds)
+      hipLaunchKernelGGL(kernel_lds, dim3((M + 15) / 16), dim3(64 * nwaves), lds, stream, x, inv_smooth, L1t,
+                         xq, xs, t, M, K, gpw);
+    else
+      hipLaunchKernelGGL(kernel_global, dim3((M + 15) / 16), dim3(64 * nwaves), lds, stream, x, inv_smooth, L1t,
+                         xq, xs, t, M, K, gpw);
+    return hipGetLastError();
+  };
   switch (r) {
-    case 16:
-      hipLaunchKernelGGL(quantize_act_kernel<16>, grid, block, lds, stream, x, inv_smooth, L1t, xq, xs, t, M, K, gpw);
-      break;
-    case 32:
-      hipLaunchKernelGGL(quantize_act_kernel<32>, grid, block, lds, stream, x, inv_smooth, L1t, xq, xs, t, M, K, gpw);
-      break;
-    case 48:
-      hipLaunchKernelGGL(quantize_act_kernel<48>, grid, block, lds, stream, x, inv_smooth, L1t, xq, xs, t, M, K, gpw);
-      break;
-    case 64:
-      hipLaunchKernelGGL(quantize_act_kernel<64>, grid, block, lds, stream, x, inv_smooth, L1t, xq, xs, t, M, K, gpw);
-      break;
-    default:
-      return hipErrorInvalidValue;
+    case 16: return go(quantize_act_kernel<16, true>, quantize_act_kernel<16, false>, act_waves<16>());
+    case 32: return go(quantize_act_kernel<32, true>, quantize_act_kernel<32, false>, act_waves<32>());
+    case 48: return go(quantize_act_kernel<48, true>, quantize_act_kernel<48, false>, act_waves<48>());
+    case 64: return go(quantize_act_kernel<64, true>, quantize_act_kernel<64, false>, act_waves<64>());
+    default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
 }
 
 }  // namespace qwam
