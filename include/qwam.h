@@ -46,18 +46,26 @@
  *   x    bf16    [M][K]      activations (row = token)
  *   R    float   [N][K]      residual weight, row = output channel
  *   smooth float [K]         lambda
- *   wq   uint8   [N][K/2]    packed weight codes: byte j of a row holds the
- *                            code of k = 2j in its low nibble and k = 2j+1 in
- *                            its high nibble, 4-bit two's complement
+ *   wq   uint8   [N][K/2]    packed weight codes (code words, below)
  *   ws   float   [G][N]      weight scales, group-major
  *   inv_smooth float [K]     fl32(1 / lambda)
- *   xq   uint8   [M][K/2]    packed activation codes (same nibble order)
+ *   xq   uint8   [M][K/2]    packed activation codes (code words, below)
  *   xs   float   [G][M]      activation scales, group-major
  *   L1t  bf16    [r][K]      L1 transposed: row j is the j-th protected direction
  *   L2t  bf16    [N][r]      L2 transposed: row n holds (V^T W~)[:, n]
  *   t    bf16    [M][r]      t = bf16(sum_k bf16(x~_k) L1[k, j]), float32 accumulation
  *   bias bf16    [N]         optional
  *   y    bf16    [M][N]      output, round to nearest even from float32
+ *
+ * Code words: 4 bits per code, sign-magnitude.  The codes c[k0 .. k0+7] of 8
+ * consecutive channels of a row (k0 a multiple of 8) form one little-endian
+ * 32-bit word (bytes k0/2 .. k0/2+3); byte j of the word holds |c[k0+2j]| in
+ * bits 0-2 and the sign of c[k0+2j] in bit 7, |c[k0+2j+1]| in bits 4-6, and in
+ * bit 3 the sign of c[k0+2j-1] (of c[k0+7] for j = 0).  A sign bit is 1 exactly
+ * for a negative code.  Codes lie in [-7, 7]: with the scale absmax / 7 the
+ * clamp of Eq. 2 never reaches -8.  (Masking a word with 0x87878787, and the
+ * word rotated right by 4 bits with the same mask, yields the codes as FP8
+ * e4m3 bytes of value code * 2^-9, which is how the GEMM consumes them.)
  *
  * Shape limits: group == 64; K % 64 == 0, 64 <= K <= 65536; N % 16 == 0,
  * 16 <= N <= 1048576; r in {16, 32, 48, 64}; 1 <= M <= 1048576; for
@@ -73,7 +81,7 @@
 extern "C" {
 #endif
 
-#define QWAM_ABI_VERSION 1
+#define QWAM_ABI_VERSION 2
 #define QWAM_GROUP 64
 
 typedef enum {
@@ -103,7 +111,8 @@ typedef struct qwam_layer {
  * Offline weight pack (weights are quantized once, Sec. 3; the exported codes
  * of App. B.1).  Quantizes each group of 64 consecutive entries of each row of
  * R with the quantizer of Eq. 2 (scale = fl32(absmax / 7); a group with absmax
- * below 7 * 2^-126 gets scale 0 and codes 0), packs the codes and writes
+ * below 7 * 2^-126 gets scale 0 and codes 0), packs the codes into code words
+ * and writes
  * inv_smooth[k] = fl32(1 / smooth[k]).
  *   R          in   float [N][K]
  *   smooth     in   float [K], every entry finite and nonzero
@@ -120,7 +129,7 @@ qwam_status qwam_pack_weights(int32_t K, int32_t N, int32_t group,
  * Activation side of one layer call (the first kernel of App. B.1): for every
  * token, x~ = fl32(x * inv_smooth) (Eq. 3, the smoothing divide done as a
  * multiply by the packed reciprocal), per-token group quantization of x~
- * (Eq. 2, absmax / 7 per token and group), nibble packing, and the rank-r
+ * (Eq. 2, absmax / 7 per token and group), code-word packing, and the rank-r
  * down-projection t = V^T x~ of Eq. 9 (bf16 inputs, float32 accumulation,
  * bf16 result), in one pass over x.
  *   L   in   layer (reads K, r, group, inv_smooth, L1t)
@@ -134,8 +143,8 @@ qwam_status qwam_quantize_act(const qwam_layer *L, int32_t M, const uint16_t *x,
 
 /*
  * The ASP GEMM (the second kernel of App. B.1): the integer partial sum of
- * every group, P[m, n, g] = sum_{k in g} qx[m, k] qw[n, k] (exact, int32,
- * INT8 matrix cores), scaled by xs[g][m] * ws[g][n] and accumulated over the
+ * every group, P[m, n, g] = sum_{k in g} qx[m, k] qw[n, k] (exact, on the FP8
+ * matrix cores), scaled by xs[g][m] * ws[g][n] and accumulated over the
  * groups in float32, plus the branch t . L2 and the bias, rounded to bf16:
  *     y[m, n] = bf16( sum_g xs ws P + sum_j t[m, j] L2t[n, j] + bias[n] )
  *   L   in   packed layer

@@ -33,8 +33,11 @@ Readings taken where the paper is silent (all are listed in the design notes):
     reciprocal is formed once, at weight-pack time) and the 4-bit path
     quantizes x~ itself (not the deflated x~_perp of Eq. 9); no Hadamard
     rotation.  In exact arithmetic both give x~ W~ (Eq. 9 and R^T V = 0).
-  * packing: byte j of a row holds k = 2j in its low nibble and k = 2j+1 in
-    its high nibble, two's complement.
+  * packing: 4 bits per code, sign-magnitude, eight codes per 32-bit word
+    (pack_codes); the paper fixes the code range, not a byte layout.  This one
+    lets a kernel turn a word into FP8 bytes of value code * 2^-9 with one mask
+    (and a rotate for the odd codes), and needs |code| <= 7, which the
+    quantizer guarantees.
   * the 16-bit branch is bf16: L1 = bf16(V), L2 = bf16(L1^T W~),
     R = fl32(W~ - L1 L2), t = bf16(sum_k bf16(x~_k) L1[k, j]) with an exact sum.
   * output reference y = sum_g sx sw P + t L2 (+ bias), float64, not rounded.
@@ -236,24 +239,47 @@ def dequantize_groups(codes: np.ndarray, scales: np.ndarray, group: int = GROUP)
     return (c * np.asarray(scales, dtype=np.float64)[:, :, None]).reshape(rows, K)
 
 
-def pack_nibbles(codes: np.ndarray) -> np.ndarray:
-    """Two 4-bit two's-complement codes per byte: even k low nibble, odd k high."""
+def pack_codes(codes: np.ndarray) -> np.ndarray:
+    """Packed code words: 4 bits per code, sign-magnitude.
+
+    The codes of channels 8i .. 8i+7 of a row form the little-endian 32-bit
+    word i (bytes 4i .. 4i+3).  Byte j of a word holds the magnitude of the code
+    of channel 8i+2j in bits 0-2 and its sign in bit 7, the magnitude of the
+    code of channel 8i+2j+1 in bits 4-6, and in bit 3 the sign of the code of
+    channel 8i+2j-1 (of channel 8i+7 when j = 0).  The sign bit is 1 exactly
+    for negative codes.  Codes must lie in [-7, 7]: with the scale absmax / 7
+    of Eq. 2 the code -8 is never produced.
+    """
     c = np.asarray(codes, dtype=np.int16)
-    lo = c[:, 0::2] & 0xF
-    hi = c[:, 1::2] & 0xF
-    return (lo | (hi << 4)).astype(np.uint8)
+    rows, K = c.shape
+    if K % 8:
+        raise ValueError("the channel count must be a multiple of 8")
+    if c.size and (c.min() < -7 or c.max() > 7):
+        raise ValueError("packed codes must lie in [-7, 7]")
+    mag = np.abs(c)
+    neg = (c < 0).astype(np.int16)
+    out = np.zeros((rows, K // 2), dtype=np.int16)
+    for j in range(4):
+        even, odd, prev_odd = 2 * j, 2 * j + 1, (2 * j - 1) % 8
+        out[:, j::4] = (mag[:, even::8] | (neg[:, even::8] << 7) |
+                        (mag[:, odd::8] << 4) | (neg[:, prev_odd::8] << 3))
+    return out.astype(np.uint8)
 
 
-def unpack_nibbles(packed: np.ndarray) -> np.ndarray:
-    """Inverse of pack_nibbles (sign-extends each nibble)."""
+def unpack_codes(packed: np.ndarray) -> np.ndarray:
+    """Inverse of pack_codes (a negative zero reads as 0)."""
     p = np.asarray(packed, dtype=np.int16)
-    lo = p & 0xF
-    hi = (p >> 4) & 0xF
-    lo = np.where(lo >= 8, lo - 16, lo)
-    hi = np.where(hi >= 8, hi - 16, hi)
-    out = np.empty((p.shape[0], 2 * p.shape[1]), dtype=np.int8)
-    out[:, 0::2] = lo
-    out[:, 1::2] = hi
+    rows, nbytes = p.shape
+    if nbytes % 4:
+        raise ValueError("packed rows are whole 32-bit words")
+    out = np.empty((rows, 2 * nbytes), dtype=np.int8)
+    for j in range(4):
+        byte = p[:, j::4]
+        next_byte = p[:, (j + 1) % 4::4]
+        e_mag, e_neg = byte & 7, (byte >> 7) & 1
+        o_mag, o_neg = (byte >> 4) & 7, (next_byte >> 3) & 1
+        out[:, 2 * j::8] = np.where(e_neg == 1, -e_mag, e_mag)
+        out[:, 2 * j + 1::8] = np.where(o_neg == 1, -o_mag, o_mag)
     return out
 
 
@@ -275,7 +301,7 @@ def pack_weights(R: np.ndarray, lam: np.ndarray):
     scales float32 [N][G], inverse smoothing float32 [K], codes int8 [N][K]).
     """
     codes, scales = quantize_groups(np.asarray(R, dtype=np.float32))
-    return pack_nibbles(codes), scales, inverse_smoothing(lam), codes
+    return pack_codes(codes), scales, inverse_smoothing(lam), codes
 
 
 def smooth_activations(x_bits: np.ndarray, inv_lam: np.ndarray) -> np.ndarray:
@@ -298,13 +324,13 @@ def down_projection(xt: np.ndarray, L1_bits: np.ndarray) -> np.ndarray:
 
 def quantize_activations(x_bits: np.ndarray, inv_lam: np.ndarray, L1_bits: np.ndarray):
     """The activation side of one layer call: smoothing, per-token group
-    quantization (Eq. 2, absmax/7 per token, App. B.1), nibble packing and the
+    quantization (Eq. 2, absmax/7 per token, App. B.1), code packing and the
     rank-r down-projection.  Returns (packed uint8 [M][K/2], scales f32 [M][G],
     t bf16 bits [M][r], codes int8 [M][K], x~ float32 [M][K])."""
     xt = smooth_activations(x_bits, inv_lam)
     codes, scales = quantize_groups(xt)
     t = down_projection(xt, L1_bits)
-    return pack_nibbles(codes), scales, t, codes, xt
+    return pack_codes(codes), scales, t, codes, xt
 
 
 def group_partials(qx: np.ndarray, qw: np.ndarray, group: int = GROUP) -> np.ndarray:
@@ -370,8 +396,8 @@ def asp_linear(x_bits, layer, bias_bits=None, rows=None):
 def asp_output_rows(xq_rows, sx_rows, t_rows, wq, sw, L2_bits, bias_bits=None):
     """Reference output for a few tokens, straight from their packed codes and
     scales (no full [M][N][G] tensor): used to check sampled rows of large layers."""
-    qx = unpack_nibbles(xq_rows)
-    qw = unpack_nibbles(wq)
+    qx = unpack_codes(xq_rows)
+    qw = unpack_codes(wq)
     P = group_partials(qx, qw)
     return asp_output(sx_rows, sw, P, t_rows, L2_bits, bias_bits), P
 

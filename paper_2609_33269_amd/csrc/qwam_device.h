@@ -55,14 +55,22 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return f32_to_bf16_rne(lo) | (f32_to_bf16_rne(hi) << 16);
 }
 
-// Unpack 8 packed 4-bit codes (one dword, low nibble = even k) into two dwords
-// of int8 values 16*code: `even` holds the codes of k = 0,2,4,6 and `odd` those
-// of k = 1,3,5,7, each scaled by 16 (the nibble lands in the high half of its
-// byte, which is 16*code in two's complement).  Products of two such bytes are
-// 256*qx*qw exactly.
-__device__ __forceinline__ void unpack_nibbles_x16(uint32_t w, uint32_t& even, uint32_t& odd) {
-  even = (w << 4) & 0xF0F0F0F0u;
-  odd = w & 0xF0F0F0F0u;
+// Packed code word, the storage format of every 4-bit code (qwam.h): the codes
+// c[k0..k0+7] of 8 consecutive channels share one little-endian 32-bit word,
+// byte j holding |c[k0+2j]| in bits 0-2 and its sign in bit 7, |c[k0+2j+1]| in
+// bits 4-6, and in bit 3 the sign of the odd code of byte j-1 (of byte 3 for
+// j = 0).  The quantizer never yields -8 (|v * inv| <= 7 (1 + 3u) < 7.5), so
+// three magnitude bits suffice; a zero code has sign 0.  Masking a word with
+// 0x87878787, and the word rotated right by 4 with the same mask, gives the
+// even and the odd codes as FP8 e4m3 bytes of value code * 2^-9.
+//
+// Conversion from 8 two's-complement nibbles t (nibble i = code of k0+i): the
+// negative nibbles are negated (one's complement + 1: carry-free, as the
+// result lies in 1..7) and every sign bit moves 4 places up, circularly.
+__device__ __forceinline__ uint32_t twos_nibbles_to_code_word(uint32_t t) {
+  const uint32_t neg = (t >> 3) & 0x11111111u;   // 1 in the low bit of each negative nibble
+  const uint32_t mag = ((t ^ (neg * 15u)) + neg) & 0x77777777u;
+  return mag | (__builtin_amdgcn_alignbit(t, t, 28) & 0x88888888u);
 }
 
 }  // namespace qwam

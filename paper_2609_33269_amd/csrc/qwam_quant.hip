@@ -11,31 +11,39 @@
 namespace qwam {
 
 // ---------------------------------------------------------------------------
-// Weight pack: 16 lanes per (row, group); each lane owns 4 consecutive floats.
+// Weight pack: 8 lanes per (row, group); each lane owns 8 consecutive floats,
+// i.e. one packed code word.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void pack_weights_kernel(const float* __restrict__ R,
                                                            uint8_t* __restrict__ wq,
                                                            float* __restrict__ ws, int N, int K) {
   const int G = K / kGroup;
-  const int64_t team = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) >> 4;
-  const int sub = threadIdx.x & 15;
+  const int64_t team = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) >> 3;
+  const int sub = threadIdx.x & 7;
   const bool active = team < static_cast<int64_t>(N) * G;
   const int n = active ? static_cast<int>(team / G) : 0;
   const int g = active ? static_cast<int>(team % G) : 0;
 
-  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-  if (active) v = *reinterpret_cast<const float4*>(R + static_cast<int64_t>(n) * K + g * kGroup + sub * 4);
-  float amax = __builtin_fmaxf(__builtin_fmaxf(__builtin_fabsf(v.x), __builtin_fabsf(v.y)),
-                               __builtin_fmaxf(__builtin_fabsf(v.z), __builtin_fabsf(v.w)));
+  float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  if (active) {
+    const float4* src = reinterpret_cast<const float4*>(R + static_cast<int64_t>(n) * K + g * kGroup + sub * 8);
+    const float4 a = src[0], b = src[1];
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+  }
+  float amax = 0.0f;
 #pragma unroll
-  for (int o = 1; o < 16; o <<= 1) amax = __builtin_fmaxf(amax, __shfl_xor(amax, o));
+  for (int i = 0; i < 8; ++i) amax = __builtin_fmaxf(amax, __builtin_fabsf(v[i]));
+#pragma unroll
+  for (int o = 1; o < 8; o <<= 1) amax = __builtin_fmaxf(amax, __shfl_xor(amax, o));
   const float s = q4_scale(amax);
   const float inv = q4_inv(s);
-  const uint32_t c = q4_nibble(v.x, inv) | (q4_nibble(v.y, inv) << 4) | (q4_nibble(v.z, inv) << 8) |
-                     (q4_nibble(v.w, inv) << 12);
+  uint32_t t = 0;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) t |= q4_nibble(v[i], inv) << (4 * i);
   if (active) {
-    *reinterpret_cast<uint16_t*>(wq + static_cast<int64_t>(n) * (K / 2) + g * (kGroup / 2) + sub * 2) =
-        static_cast<uint16_t>(c);
+    *reinterpret_cast<uint32_t*>(wq + static_cast<int64_t>(n) * (K / 2) + g * (kGroup / 2) + sub * 4) =
+        twos_nibbles_to_code_word(t);
     if (sub == 0) ws[static_cast<int64_t>(g) * N + n] = s;
   }
 }
@@ -145,7 +153,8 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_kernel(
     const float s = q4_scale(amax);
     const float inv = q4_inv(s);
     // codes: q = clamp(rint(v * inv), -8, 7); a byte holds (q_odd + 8) * 16 + (q_even + 8),
-    // and XOR 0x88 turns that into the two's-complement nibbles (q & 15) | (q_odd & 15) << 4
+    // XOR 0x88 turns that into the two's-complement nibbles (q & 15) | (q_odd & 15) << 4,
+    // and those become the packed code word
     uint32_t packed[2];
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
@@ -156,7 +165,7 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_kernel(
         const float qo = __builtin_fminf(__builtin_fmaxf(__builtin_rintf(v[8 * h + 2 * b + 1] * inv), -8.0f), 7.0f);
         wv = __builtin_amdgcn_cvt_pk_u8_f32(__builtin_fmaf(qo, 16.0f, qe) + 136.0f, b, wv);
       }
-      packed[h] = wv ^ 0x88888888u;
+      packed[h] = twos_nibbles_to_code_word(wv ^ 0x88888888u);
     }
     buf_store8(make_uint2(packed[0], packed[1]), q_rsrc, q_off + static_cast<uint32_t>(g) * (kGroup / 2));
     // every lane of a row holds the same scale; lanes of row r write it at r
@@ -211,7 +220,7 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_kernel(
 hipError_t launch_pack_weights(int K, int N, const float* R, const float* smooth, uint8_t* wq,
                                float* ws, float* inv_smooth, hipStream_t stream) {
   const int64_t teams = static_cast<int64_t>(N) * (K / kGroup);
-  const int64_t blocks = (teams * 16 + 255) / 256;
+  const int64_t blocks = (teams * 8 + 255) / 256;
   hipLaunchKernelGGL(pack_weights_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, R,
                      wq, ws, N, K);
   hipLaunchKernelGGL(inverse_smoothing_kernel, dim3((K + 255) / 256), dim3(256), 0, stream, smooth,

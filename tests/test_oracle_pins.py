@@ -3,7 +3,7 @@
 None of these re-types the oracle's own formula: each checks a closed form, a
 special case with a hand-derived answer, an identity, an independent library
 routine or a brute-force computation, chosen so that a plausible mistake in the
-oracle (wrong divisor, wrong tie rule, swapped nibbles, dropped branch, wrong
+oracle (wrong divisor, wrong tie rule, misplaced code bits, dropped branch, wrong
 eigen-order, transposed factor, inverted smoothing) fails at least one test.
 """
 
@@ -134,21 +134,75 @@ def test_quantizer_codes_match_exact_rational_rounding():
 # packing
 # --------------------------------------------------------------------------
 
-def test_pack_all_bytes_bijective():
-    allb = np.arange(256, dtype=np.uint8).reshape(1, 256)
-    codes = O.unpack_nibbles(allb)
-    assert codes.min() == -8 and codes.max() == 7
-    assert (O.pack_nibbles(codes) == allb).all()
-    # byte b: low nibble is the even-k code, high nibble the odd-k code
-    for b in (0x00, 0x01, 0x0F, 0x10, 0xF1, 0x78, 0x87, 0xFF):
-        lo, hi = b & 0xF, b >> 4
-        assert codes[0, 2 * b] == (lo - 16 if lo >= 8 else lo)
-        assert codes[0, 2 * b + 1] == (hi - 16 if hi >= 8 else hi)
+def _e4m3_value(byte: int) -> float:
+    """FP8 e4m3 (OCP) decoded from its definition: sign, 4 exponent bits with
+    bias 7, 3 mantissa bits, subnormals at exponent 0."""
+    s = -1.0 if byte & 0x80 else 1.0
+    e = (byte >> 3) & 0xF
+    m = byte & 7
+    if e == 0:
+        return s * m / 8 * 2.0 ** -6
+    return s * (1 + m / 8) * 2.0 ** (e - 7)
 
 
-def test_pack_known_bytes():
-    codes = np.array([[1, -1, -8, 7, 0, 3, -3, 0]], dtype=np.int8)
-    assert O.pack_nibbles(codes).tolist() == [[0xF1, 0x78, 0x30, 0x0D]]
+def test_pack_roundtrip_random_codes():
+    rng = np.random.default_rng(13)
+    codes = rng.integers(-7, 8, size=(17, 256)).astype(np.int8)
+    packed = O.pack_codes(codes)
+    assert packed.shape == (17, 128) and packed.dtype == np.uint8
+    assert (O.unpack_codes(packed) == codes).all()
+    # every code value at every position of a word, alone in its word
+    for pos in range(8):
+        for c in range(-7, 8):
+            one = np.zeros((1, 8), np.int8)
+            one[0, pos] = c
+            assert (O.unpack_codes(O.pack_codes(one)) == one).all()
+
+
+def test_pack_every_word_decodes_in_range():
+    rng = np.random.default_rng(15)
+    words = rng.integers(0, 2 ** 32, size=(1, 4096), dtype=np.uint64).astype(np.uint32)
+    packed = words.view(np.uint8).reshape(1, -1)
+    codes = O.unpack_codes(packed)
+    assert codes.min() >= -7 and codes.max() <= 7
+    again = O.pack_codes(codes)
+    # words without a negative zero are reproduced exactly; one with a
+    # negative zero differs from its canonical form only in sign bits
+    same = (again.reshape(-1, 4) == packed.reshape(-1, 4)).all(axis=1)
+    diff = (again.reshape(-1, 4) ^ packed.reshape(-1, 4))
+    assert ((diff & 0x77) == 0).all()
+    assert same.sum() > 0 and (~same).sum() > 0
+
+
+def test_pack_known_words():
+    # hand-derived from the layout: byte j = |even| | sign(even) << 7 |
+    # |odd| << 4 | sign(odd code of byte j-1) << 3
+    codes = np.array([[1, -1, -7, 7, 0, 3, -3, 0]], dtype=np.int8)
+    assert O.pack_codes(codes).tolist() == [[0x11, 0xFF, 0x30, 0x83]]
+    # the last odd code's sign wraps to bit 3 of the word's first byte
+    codes = np.array([[0, 0, 0, 0, 0, 0, 0, -5]], dtype=np.int8)
+    assert O.pack_codes(codes).tolist() == [[0x08, 0x00, 0x00, 0x50]]
+
+
+def test_pack_rejects_minus_eight():
+    with pytest.raises(ValueError):
+        O.pack_codes(np.array([[-8, 0, 0, 0, 0, 0, 0, 0]], dtype=np.int8))
+
+
+def test_packed_words_are_fp8_codes():
+    """The point of the layout: a word masked with 0x87878787 holds the even
+    codes, and the word rotated right by 4 bits, masked the same way, holds the
+    odd codes, each as an e4m3 byte of value code * 2^-9."""
+    rng = np.random.default_rng(16)
+    codes = rng.integers(-7, 8, size=(1, 64)).astype(np.int8)
+    codes[0, :15] = np.arange(-7, 8)
+    words = O.pack_codes(codes).view("<u4").reshape(-1)
+    for i, w in enumerate(int(x) for x in words):
+        even = w & 0x87878787
+        odd = ((w >> 4) | (w << 28)) & 0xFFFFFFFF & 0x87878787
+        for j in range(4):
+            assert _e4m3_value((even >> (8 * j)) & 0xFF) == codes[0, 8 * i + 2 * j] * 2.0 ** -9
+            assert _e4m3_value((odd >> (8 * j)) & 0xFF) == codes[0, 8 * i + 2 * j + 1] * 2.0 ** -9
 
 
 # --------------------------------------------------------------------------
