@@ -6,7 +6,8 @@ N = 14336, rank r = 32, group 64, bf16 in / out, seeded synthetic inputs
 [10, 50]; weights N(0, 1/K); factors from the top-32 eigenvectors of a seeded
 SPD Gramian).  One step = one pass of the layer's hot path over one batch:
 the fused activation kernel (smoothing, group-64 INT4 quantization, packing,
-down-projection) and the W4A4 GEMM with the fused bf16 branch.  The weights
+down-projection) and the W4A4 GEMM (exact integer group partials on the FP8
+matrix cores) with the fused bf16 branch.  The weights
 are packed once before timing (they are quantized offline); every input is
 resident in HBM when the timed region starts.
 
@@ -15,11 +16,19 @@ through `--rotate` distinct copies of every input and output buffer.
 
 Prints ONE JSON line (metric, value = effective TOPS = 2 M K N / step time,
 roofline of the dominant kernel, CPU-oracle baseline).
+
+Counter support (HBM traffic of the GEMM, scaled by a plain copy of known size):
+  python bench.py --no-cpu-baseline --steps 20 --warmup 2 --copy-probe 256
+      under `rocprofv3 --pmc FETCH_SIZE` and, separately, `--pmc WRITE_SIZE`
+      (the copy probe runs after the timed region);
+  python bench.py --reduce-counters FETCH.csv WRITE.csv
+      turns the two counter-collection CSVs into profiles/traffic_asp_gemm_ffn_up.json.
 """
 
 from __future__ import annotations
 
 import argparse
+import csv
 import hashlib
 import json
 import os
@@ -33,12 +42,14 @@ sys.path.insert(0, ROOT)
 
 M, K, N, R_RANK, GROUP = 4096, 3072, 14336, 32, 64
 G = K // GROUP
-INT8_PEAK_TOPS = 5000.0        # MI355X dense INT8 matrix peak, TOP/s
+MFMA_PEAK = 5000.0             # MI355X dense FP8 (= dense INT8) matrix peak, TFLOP/s (TOP/s)
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
-VALU_OPS_PER_OUTPUT_GROUP = 3  # int->float convert, scale product, fused multiply-add
+VALU_OPS_PER_OUTPUT_GROUP = 2  # scale product, fused multiply-add
 METRIC = "ASP W4A4+r32 linear: effective TOPS & % int8 MFMA peak at 4096×3072×14336"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_asp_gemm_ffn_up.json")
-GEMM_SRC = os.path.join(ROOT, "paper_2609_33269_amd", "csrc", "qwam_gemm.hip")
+GEMM_SRCS = [os.path.join(ROOT, "paper_2609_33269_amd", "csrc", f) for f in ("qwam_gemm.hip", "qwam_device.h")]
+GEMM_KERNEL = "asp_gemm_kernel<32, false>"
+COPY_KERNEL = "neg_kernel"
 
 
 def algorithmic_bytes():
@@ -47,9 +58,12 @@ def algorithmic_bytes():
     return act, gemm
 
 
-def source_hash(path: str) -> str:
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+def source_hash(paths) -> str:
+    h = hashlib.sha256()
+    for path in paths:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def measured_traffic():
@@ -60,9 +74,36 @@ def measured_traffic():
             rec = json.load(f)
     except (OSError, ValueError):
         return None
-    if rec.get("gemm_source_sha256_16") != source_hash(GEMM_SRC):
+    if rec.get("gemm_source_sha256_16") != source_hash(GEMM_SRCS):
         return None
     return rec.get("bytes_per_launch")
+
+
+def _counter_rows(path):
+    """(kernel name, value) of every dispatch in a rocprofv3 counter-collection CSV."""
+    with open(path, newline="") as f:
+        return [(r["Kernel_Name"], float(r["Counter_Value"])) for r in csv.DictReader(f)]
+
+
+def reduce_counters(fetch_csv: str, write_csv: str, copy_mib: int):
+    """HBM bytes per GEMM launch: FETCH_SIZE + WRITE_SIZE (KiB per dispatch),
+    each scaled by the factor that maps the same counter of the copy probe onto
+    its known byte count."""
+    out = {"gemm_source_sha256_16": source_hash(GEMM_SRCS), "copy_bytes": copy_mib << 20}
+    for key, path in (("fetch", fetch_csv), ("write", write_csv)):
+        rows = _counter_rows(path)
+        gemm = [v for k, v in rows if GEMM_KERNEL in k]
+        copy = [v for k, v in rows if COPY_KERNEL in k]
+        if not gemm or not copy:
+            raise SystemExit(f"{path}: no {GEMM_KERNEL} or {COPY_KERNEL} dispatches")
+        g_kib, c_kib = float(np.mean(gemm)), float(np.mean(copy))
+        factor = (copy_mib << 20) / (c_kib * 1024.0)
+        out.update({f"{key}_kib_per_launch": round(g_kib, 1), f"copy_{key}_kib": round(c_kib, 1),
+                    f"{key}_factor": round(factor, 5), f"{key}_launches": len(gemm)})
+    out["bytes_per_launch"] = int(round((out["fetch_kib_per_launch"] * out["fetch_factor"] +
+                                         out["write_kib_per_launch"] * out["write_factor"]) * 1024))
+    out["algorithmic_bytes"] = algorithmic_bytes()[1]
+    return out
 
 
 def cpu_baseline(draws, seconds: float = 12.0):
@@ -103,10 +144,22 @@ def main():
     ap.add_argument("--rotate", type=int, default=24, help="distinct buffer sets cycled through")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="after timing, run a plain float32 copy kernel over MIB MiB five times")
+    ap.add_argument("--reduce-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
+    ap.add_argument("--copy-mib", type=int, default=256, help="copy-probe size the counters were taken with")
     args = ap.parse_args()
+    if args.reduce_counters:
+        rec = reduce_counters(*args.reduce_counters, args.copy_mib)
+        os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
+        with open(TRAFFIC_FILE, "w") as f:
+            json.dump(rec, f, indent=1)
+            f.write("\n")
+        print(json.dumps(rec))
+        return
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the layer is not sharded "
-              f"across GPUs in this build", file=sys.stderr)
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the ASP layer is "
+              f"implemented and measured on a single GPU, with no sharding", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -191,6 +244,15 @@ def main():
     bf16_ms = e0.elapsed_time(e1) / 20
     del wb
 
+    if args.copy_probe > 0:
+        n = (args.copy_probe << 20) // 4
+        src_t = torch.ones(n, device=dev, dtype=torch.float32)
+        dst_t = torch.empty_like(src_t)
+        for _ in range(5):
+            torch.neg(src_t, out=dst_t)      # reads and writes copy_probe MiB each
+        torch.cuda.synchronize()
+        del src_t, dst_t
+
     traffic = measured_traffic()
     out = {
         "metric": METRIC,
@@ -203,20 +265,20 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "int8",
+        "dtype": "int4 codes on fp8-e4m3 MFMA (exact), f32 scale/accumulate, bf16 out",
         "data": "synthetic",
         "config": {"workload": "video_dit_ffn_up", "M": M, "K": K, "N": N, "r": R_RANK, "group": GROUP,
                    "act": "N(0,1), 1% channels x U_log(10,50)", "weights": "N(0,1/K)",
                    "rotated_buffer_sets": nrot},
-        "roofline": {"bound": "mfma", "kernel": "asp_gemm_kernel<32>", "achieved": round(k2_tops, 1),
-                     "peak": INT8_PEAK_TOPS, "unit": "TOP/s", "frac": round(k2_tops / INT8_PEAK_TOPS, 4),
+        "roofline": {"bound": "mfma", "kernel": GEMM_KERNEL, "achieved": round(k2_tops, 1),
+                     "peak": MFMA_PEAK, "unit": "TFLOP/s", "frac": round(k2_tops / MFMA_PEAK, 4),
                      "traffic": traffic, "algorithmic_bytes": gemm_bytes},
-        "layer_frac_int8_peak": round(eff_tops / INT8_PEAK_TOPS, 4),
+        "layer_frac_int8_peak": round(eff_tops / MFMA_PEAK, 4),
         "kernels_us": {"quantize_act": round(k1_ms * 1e3, 2), "asp_gemm": round(k2_ms * 1e3, 2)},
         "quantize_act_roofline": {"bound": "hbm", "achieved": round(k1_gbs, 1), "peak": HBM_PEAK_GBS,
                                   "unit": "GB/s", "frac": round(k1_gbs / HBM_PEAK_GBS, 4),
                                   "algorithmic_bytes": act_bytes},
-        # per output and group: 64 int8 MACs on the matrix cores (1024 MAC/clk/SIMD) against
+        # per output and group: 64 MACs on the matrix cores (1024 MAC/clk/SIMD) against
         # VALU_OPS_PER_OUTPUT_GROUP float32 VALU ops (16 lanes/clk/SIMD): the MFMA share the
         # VALU issue rate allows if both overlap perfectly
         "gemm_valu_ceiling_frac": round((64 / 1024) / (VALU_OPS_PER_OUTPUT_GROUP / 16), 4),
