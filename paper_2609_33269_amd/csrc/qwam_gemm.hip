@@ -42,6 +42,8 @@
 //     as the integer blocks) starts from acc, the bias is added, the
 //     result is rounded to bf16 and stored through LDS so that every lane
 //     writes 16 contiguous bytes.
+#include <utility>
+
 #include "qwam_device.h"
 #include "qwam_internal.h"
 
@@ -90,6 +92,31 @@ __device__ __forceinline__ v8i codes_to_e4m3(const uint4& p) {
 
 // E8M0 scale 2^9 (127 + 9) for both operands: (code * 2^-9 * 2^9) products
 constexpr int kE8M0Code = 127 + 9;
+
+// x of lane 16 * (lane / 16) + V (lane V of this lane's row of 16, DPP
+// row_newbcast) times y, in one instruction.  The DPP source x must not be
+// written by a VALU instruction in the two instructions before (here it always
+// comes straight from an LDS load).
+template <int V>
+__device__ __forceinline__ float row_bcast_mul(float x, float y) {
+  float r;
+  asm("v_mul_f32_dpp %0, %1, %2 row_newbcast:%3 row_mask:0xf bank_mask:0xf bound_ctrl:1"
+      : "=v"(r)
+      : "v"(x), "v"(y), "i"(V));
+  return r;
+}
+
+// acc[v] += p[v] * (sx of result row v of this lane) * sw, v = 0..15, where
+// lane 16 * rho + v holds the activation scale that result register v of the
+// lanes in row rho of 16 needs.  All 16 products first, then the 16 updates, so
+// that no update directly follows the product it reads.
+template <int... V>
+__device__ __forceinline__ void scale_accumulate(std::integer_sequence<int, V...>, v16f& acc, const v16f& p,
+                                                 float sx_lane, float sw) {
+  float s[sizeof...(V)];
+  ((s[V] = row_bcast_mul<V>(sx_lane, sw)), ...);
+  ((acc[V] = __builtin_fmaf(p[V], s[V], acc[V])), ...);
+}
 
 // Tile of workgroup `bid`: XCD-major remap (hardware places workgroup b on XCD
 // b % 8), then bands of BAND tile-rows, columns fastest inside a band-column.
@@ -193,6 +220,10 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
   // swz depends on frow only)
   const int frow_off = frow * ROWB;
   const int fslot = fhalf ^ swz(frow);
+  // activation-scale row of this lane inside a 32-row block: lane 16*rho + v
+  // holds the scale of result register v of lanes in rows rho (v = lane % 16):
+  // row 8*(v/4) + 4*(lane/32) + v%4
+  const int sx_row = 8 * ((lane & 15) >> 2) + 4 * (lane >> 5) + (lane & 3);
 
   // one group q of a stage
   auto group = [&](int g, int q, const Stage& cur) __attribute__((always_inline)) {
@@ -222,14 +253,8 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
         }
       } else {
         const float swv = cur.sw[q][wn * 64 + j * 32 + frow];
-#pragma unroll
-        for (int qq = 0; qq < 4; ++qq) {
-          const float4 sx4 = *reinterpret_cast<const float4*>(&cur.sx[q][wm * 64 + i * 32 + 8 * qq + rsub]);
-          const float sxv[4] = {sx4.x, sx4.y, sx4.z, sx4.w};
-#pragma unroll
-          for (int v = 0; v < 4; ++v)
-            accf[i][j][4 * qq + v] = __builtin_fmaf(p[4 * qq + v], sxv[v] * swv, accf[i][j][4 * qq + v]);
-        }
+        const float sxl = cur.sx[q][wm * 64 + i * 32 + sx_row];
+        scale_accumulate(std::make_integer_sequence<int, 16>{}, accf[i][j], p, sxl, swv);
       }
     };
     // software pipeline: MFMAs of the next block before the epilogue of this one
