@@ -90,6 +90,18 @@ __device__ __forceinline__ v8i codes_to_e4m3(const uint4& p) {
   return r;
 }
 
+// 16-byte LDS read that the compiler keeps in program order (volatile)
+__device__ __forceinline__ uint4 lds_load16_volatile(const uint8_t* p) {
+  typedef unsigned v4u __attribute__((ext_vector_type(4)));
+  typedef const volatile __attribute__((address_space(3))) v4u lds_v4u;
+  const v4u v = *(lds_v4u*)(p);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ float lds_load4_volatile(const float* p) {
+  typedef const volatile __attribute__((address_space(3))) float lds_f;
+  return *(lds_f*)(p);
+}
+
 // E8M0 scale 2^9 (127 + 9) for both operands: (code * 2^-9 * 2^9) products
 constexpr int kE8M0Code = 127 + 9;
 
@@ -225,16 +237,40 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
   // row 8*(v/4) + 4*(lane/32) + v%4
   const int sx_row = 8 * ((lane & 15) >> 2) + 4 * (lane >> 5) + (lane & 3);
 
-  // one group q of a stage
-  auto group = [&](int g, int q, const Stage& cur) __attribute__((always_inline)) {
+  // LDS data of one group: packed A / B fragments and the lane's scales
+  struct GroupData {
+    uint4 a[2], b[2];
+    float sx[2], sw[2];
+  };
+  // Reads group q's data one group ahead of its use.  The loads are volatile
+  // and followed by a compiler-only fence, so they are issued here and not
+  // sunk next to their first use; the wait for them lands at that use.
+  auto load_group = [&](const Stage& cur, int q) __attribute__((always_inline)) {
     const int slot_off = ((2 * q) ^ fslot) * 16;
-    v8i af[2], bf[2];
+    GroupData d;
 #pragma unroll
     for (int i = 0; i < 2; ++i)
-      af[i] = codes_to_e4m3(*reinterpret_cast<const uint4*>(cur.a + (wm * 64 + i * 32) * ROWB + frow_off + slot_off));
+      d.a[i] = lds_load16_volatile(cur.a + (wm * 64 + i * 32) * ROWB + frow_off + slot_off);
 #pragma unroll
     for (int j = 0; j < 2; ++j)
-      bf[j] = codes_to_e4m3(*reinterpret_cast<const uint4*>(cur.b + (wn * 64 + j * 32) * ROWB + frow_off + slot_off));
+      d.b[j] = lds_load16_volatile(cur.b + (wn * 64 + j * 32) * ROWB + frow_off + slot_off);
+    if (!PARTIALS) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i) d.sx[i] = lds_load4_volatile(&cur.sx[q][wm * 64 + i * 32 + sx_row]);
+#pragma unroll
+      for (int j = 0; j < 2; ++j) d.sw[j] = lds_load4_volatile(&cur.sw[q][wn * 64 + j * 32 + frow]);
+    }
+    asm volatile("" ::: "memory");
+    return d;
+  };
+
+  // one group g of a stage, from its LDS data
+  auto group = [&](int g, const GroupData& d) __attribute__((always_inline)) {
+    v8i af[2], bf[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) af[i] = codes_to_e4m3(d.a[i]);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) bf[j] = codes_to_e4m3(d.b[j]);
 
     // the exact integer partial of block (i, j), as float32
     auto mfma_block = [&](int i, int j) __attribute__((always_inline)) {
@@ -252,9 +288,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
           if (m < M && n < N) P[(static_cast<int64_t>(m) * N + n) * G + g] = static_cast<int32_t>(p[v]);
         }
       } else {
-        const float swv = cur.sw[q][wn * 64 + j * 32 + frow];
-        const float sxl = cur.sx[q][wm * 64 + i * 32 + sx_row];
-        scale_accumulate(std::make_integer_sequence<int, 16>{}, accf[i][j], p, sxl, swv);
+        scale_accumulate(std::make_integer_sequence<int, 16>{}, accf[i][j], p, d.sx[i], d.sw[j]);
       }
     };
     // software pipeline: MFMAs of the next block before the epilogue of this one
@@ -274,9 +308,16 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
     wait_vmcnt<0>();                  // this thread's copies of stage s have landed
     lds_barrier();                    // ... and every thread's; stage s-1 is fully consumed
     issue(s + 1, nxt);                // past the last stage: harmless reads, never used
+    GroupData d = load_group(cur, 0);
 #pragma unroll
-    for (int q = 0; q < KC; ++q)
-      if (q < nq) group(s * KC + q, q, cur);
+    for (int q = 0; q < KC; ++q) {
+      if (q < nq) {
+        GroupData next = d;
+        if (q + 1 < nq) next = load_group(cur, q + 1);
+        group(s * KC + q, d);
+        d = next;
+      }
+    }
   };
 
   issue(0, st0);
