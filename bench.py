@@ -23,6 +23,13 @@ Counter support (HBM traffic of the GEMM, scaled by a plain copy of known size):
       (the copy probe runs after the timed region);
   python bench.py --reduce-counters FETCH.csv WRITE.csv
       turns the two counter-collection CSVs into profiles/traffic_asp_gemm_ffn_up.json.
+
+Secondary measurement (not the headline line):
+  python bench.py --small-m
+      the action-expert layers (M in {16, 32, 64}, K = 1024, N in {4096, 1024},
+      r = 16): per-call latency of both kernels and algorithmic HBM GB/s, one
+      JSON line per shape, rotating through enough distinct layers that the
+      weights come from HBM.
 """
 
 from __future__ import annotations
@@ -106,6 +113,86 @@ def reduce_counters(fetch_csv: str, write_csv: str, copy_mib: int):
     return out
 
 
+def small_m_report(args):
+    """Per-call latency and algorithmic HBM bandwidth of the action-expert layers.
+
+    Latency is measured as the paper measures it, on graph replays: one HIP
+    graph holds one call (both kernels) on each of `distinct_layers` packed
+    layers, so every replay streams every layer's weights from HBM (together
+    they exceed the 256 MB Infinity Cache)."""
+    import torch
+    from paper_2609_33269_amd import calib, inputs, qwam
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    def graph_us(fn, n, replays=10):
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            for i in range(n):
+                fn(i)
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for i in range(n):
+                fn(i)
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(replays):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / (replays * n)
+
+    # floor: a graph of one-element kernels
+    one = torch.zeros(1, device=dev)
+    floor_us = graph_us(lambda i: one.add_(1.0), 512)
+
+    Ka, ra, Ga = 1024, 16, 1024 // GROUP
+    for (Ms, Ns) in inputs.ACTION_EXPERT_SHAPES:
+        d = inputs.action_expert(Ms, Ns)
+        x0 = torch.from_numpy(d.x.view(np.int16)).view(torch.bfloat16).to(dev)
+        w0 = torch.from_numpy(d.w.view(np.int16)).view(torch.bfloat16).to(dev)
+        f = calib.build_layer(x0, w0, calib.protected_basis(torch.from_numpy(d.a), ra))
+        L0 = qwam.make_layer(f["R"], f["lam"], f["L1"], f["L2"])
+        del f, w0
+        wbytes = Ns * Ka // 2 + Ns * Ga * 4 + Ns * ra * 2 + Ka * 4 + ra * Ka * 2
+        nrot = int(min(1024, max(2, (768 << 20) // wbytes)))        # > the 256 MB Infinity Cache
+        layers = [L0] + [qwam.PackedLayer(K=Ka, N=Ns, r=ra, wq=L0.wq.clone(), ws=L0.ws.clone(),
+                                          inv_smooth=L0.inv_smooth.clone(), L1t=L0.L1t.clone(),
+                                          L2t=L0.L2t.clone()) for _ in range(nrot - 1)]
+        xq = torch.empty((Ms, Ka // 2), dtype=torch.uint8, device=dev)
+        xs = torch.empty((Ga, Ms), dtype=torch.float32, device=dev)
+        t = torch.empty((Ms, ra), dtype=torch.bfloat16, device=dev)
+        y = torch.empty((Ms, Ns), dtype=torch.bfloat16, device=dev)
+
+        def call(i):
+            L = layers[i]
+            qwam.quantize_act(L, x0, out=(xq, xs, t))
+            qwam.asp_linear(L, xq, xs, t, out=y)
+
+        us = graph_us(call, nrot)
+        us1 = graph_us(lambda i: qwam.quantize_act(layers[i], x0, out=(xq, xs, t)), nrot)
+        us2 = graph_us(lambda i: qwam.asp_linear(layers[i], xq, xs, t, out=y), nrot)
+        b1 = Ms * Ka * 2 + Ka * 4 + ra * Ka * 2 + Ms * Ka // 2 + Ms * Ga * 4 + Ms * ra * 2
+        b2 = (Ms * Ka // 2 + Ms * Ga * 4 + Ms * ra * 2 + Ns * Ka // 2 + Ns * Ga * 4 + Ns * ra * 2
+              + Ms * Ns * 2)
+        print(json.dumps({
+            "workload": "action_expert", "M": Ms, "K": Ka, "N": Ns, "r": ra,
+            "us_per_call": round(us, 2), "us_quantize_act": round(us1, 2), "us_asp_gemm": round(us2, 2),
+            "algorithmic_bytes": b1 + b2, "GBs": round((b1 + b2) / (us * 1e-6) / 1e9, 1),
+            "gemm_GBs": round(b2 / (us2 * 1e-6) / 1e9, 1),
+            "hbm_frac": round((b1 + b2) / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+            "graph_kernel_floor_us": round(floor_us, 2), "distinct_layers": nrot,
+            "timing": "HIP graph replay", "data": "synthetic"}), flush=True)
+        del layers, L0, x0
+        torch.cuda.empty_cache()
+
+
 def cpu_baseline(draws, seconds: float = 12.0):
     """The CPU oracle as it stands, timed on a bounded token sample of the same
     layer (weights packed beforehand, as on the GPU)."""
@@ -148,6 +235,7 @@ def main():
                     help="after timing, run a plain float32 copy kernel over MIB MiB five times")
     ap.add_argument("--reduce-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
     ap.add_argument("--copy-mib", type=int, default=256, help="copy-probe size the counters were taken with")
+    ap.add_argument("--small-m", action="store_true", help="report the action-expert layers instead")
     args = ap.parse_args()
     if args.reduce_counters:
         rec = reduce_counters(*args.reduce_counters, args.copy_mib)
@@ -161,6 +249,10 @@ def main():
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the ASP layer is "
               f"implemented and measured on a single GPU, with no sharding", file=sys.stderr)
         sys.exit(2)
+
+    if args.small_m:
+        small_m_report(args)
+        return
 
     import torch
     from paper_2609_33269_amd import calib, inputs, qwam

@@ -3,6 +3,7 @@
 // dereferenced here.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cstdarg>
 #include <cstdint>
 #include <cstdio>
@@ -63,13 +64,21 @@ qwam_status check_m(const char* fn, int32_t M) {
   return QWAM_OK;
 }
 
+// The device count is queried once per process (a query per call would add
+// host time to every launch, which small layers notice).
 qwam_status check_device(const char* fn) {
-  int n = 0;
-  const hipError_t e = hipGetDeviceCount(&n);
-  if (e != hipSuccess || n <= 0) {
-    (void)hipGetLastError();
-    return fail(QWAM_ERR_NO_DEVICE, "%s: no HIP device visible", fn);
+  static std::atomic<int> visible{-1};
+  int n = visible.load(std::memory_order_relaxed);
+  if (n < 0) {
+    int c = 0;
+    if (hipGetDeviceCount(&c) != hipSuccess) {
+      (void)hipGetLastError();
+      c = 0;
+    }
+    visible.store(c, std::memory_order_relaxed);
+    n = c;
   }
+  if (n <= 0) return fail(QWAM_ERR_NO_DEVICE, "%s: no HIP device visible", fn);
   return QWAM_OK;
 }
 
