@@ -178,6 +178,13 @@ def small_m_report(args):
         us = graph_us(call, nrot)
         us1 = graph_us(lambda i: qwam.quantize_act(layers[i], x0, out=(xq, xs, t)), nrot)
         us2 = graph_us(lambda i: qwam.asp_linear(layers[i], xq, xs, t, out=y), nrot)
+        # the bf16 linear it replaces (hipBLASLt through torch), same graph method,
+        # as many distinct bf16 weights as fit the same rotation bytes
+        nb = int(min(nrot, max(2, (768 << 20) // (Ns * Ka * 2))))
+        wbf = [torch.randn((Ns, Ka), device=dev, dtype=torch.bfloat16) for _ in range(nb)]
+        ybf = torch.empty((Ms, Ns), device=dev, dtype=torch.bfloat16)
+        us_bf16 = graph_us(lambda i: torch.matmul(x0, wbf[i].t(), out=ybf), nb)
+        del wbf
         b1 = Ms * Ka * 2 + Ka * 4 + ra * Ka * 2 + Ms * Ka // 2 + Ms * Ga * 4 + Ms * ra * 2
         b2 = (Ms * Ka // 2 + Ms * Ga * 4 + Ms * ra * 2 + Ns * Ka // 2 + Ns * Ga * 4 + Ns * ra * 2
               + Ms * Ns * 2)
@@ -187,6 +194,7 @@ def small_m_report(args):
             "algorithmic_bytes": b1 + b2, "GBs": round((b1 + b2) / (us * 1e-6) / 1e9, 1),
             "gemm_GBs": round(b2 / (us2 * 1e-6) / 1e9, 1),
             "hbm_frac": round((b1 + b2) / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+            "bf16_linear_us": round(us_bf16, 2), "speedup_vs_bf16_linear": round(us_bf16 / us, 3),
             "graph_kernel_floor_us": round(floor_us, 2), "distinct_layers": nrot,
             "timing": "HIP graph replay", "data": "synthetic"}), flush=True)
         del layers, L0, x0

@@ -42,16 +42,13 @@
 //     as the integer blocks) starts from acc, the bias is added, the
 //     result is rounded to bf16 and stored through LDS so that every lane
 //     writes 16 contiguous bytes.
-#include <utility>
-
 #include "qwam_device.h"
 #include "qwam_internal.h"
+#include "qwam_mfma.h"
 
 namespace qwam {
 
 namespace {
-
-typedef float v16f __attribute__((ext_vector_type(16)));
 
 constexpr int BM = 128;
 constexpr int BN = 128;
@@ -74,22 +71,6 @@ static_assert(4 * 64 * LDY * 2 <= sizeof(Stage), "the output staging of all four
 // chunk slot permutation of a row inside a stage
 __device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
-typedef int v8i __attribute__((ext_vector_type(8)));
-
-// 32 packed codes (16 bytes of one row) -> one FP8 MFMA operand of 32 e4m3
-// bytes, ordered [even k of w0, odd k of w0, even k of w1, ...] (the same
-// permutation for A and B, so the dot product is unchanged).
-__device__ __forceinline__ v8i codes_to_e4m3(const uint4& p) {
-  const uint32_t w[4] = {p.x, p.y, p.z, p.w};
-  v8i r;
-#pragma unroll
-  for (int d = 0; d < 4; ++d) {
-    r[2 * d] = static_cast<int>(w[d] & 0x87878787u);
-    r[2 * d + 1] = static_cast<int>(__builtin_amdgcn_alignbit(w[d], w[d], 4) & 0x87878787u);
-  }
-  return r;
-}
-
 // 16-byte LDS read that the compiler keeps in program order (volatile)
 __device__ __forceinline__ uint4 lds_load16_volatile(const uint8_t* p) {
   typedef unsigned v4u __attribute__((ext_vector_type(4)));
@@ -100,34 +81,6 @@ __device__ __forceinline__ uint4 lds_load16_volatile(const uint8_t* p) {
 __device__ __forceinline__ float lds_load4_volatile(const float* p) {
   typedef const volatile __attribute__((address_space(3))) float lds_f;
   return *(lds_f*)(p);
-}
-
-// E8M0 scale 2^9 (127 + 9) for both operands: (code * 2^-9 * 2^9) products
-constexpr int kE8M0Code = 127 + 9;
-
-// x of lane 16 * (lane / 16) + V (lane V of this lane's row of 16, DPP
-// row_newbcast) times y, in one instruction.  The DPP source x must not be
-// written by a VALU instruction in the two instructions before (here it always
-// comes straight from an LDS load).
-template <int V>
-__device__ __forceinline__ float row_bcast_mul(float x, float y) {
-  float r;
-  asm("v_mul_f32_dpp %0, %1, %2 row_newbcast:%3 row_mask:0xf bank_mask:0xf bound_ctrl:1"
-      : "=v"(r)
-      : "v"(x), "v"(y), "i"(V));
-  return r;
-}
-
-// acc[v] += p[v] * (sx of result row v of this lane) * sw, v = 0..15, where
-// lane 16 * rho + v holds the activation scale that result register v of the
-// lanes in row rho of 16 needs.  All 16 products first, then the 16 updates, so
-// that no update directly follows the product it reads.
-template <int... V>
-__device__ __forceinline__ void scale_accumulate(std::integer_sequence<int, V...>, v16f& acc, const v16f& p,
-                                                 float sx_lane, float sw) {
-  float s[sizeof...(V)];
-  ((s[V] = row_bcast_mul<V>(sx_lane, sw)), ...);
-  ((acc[V] = __builtin_fmaf(p[V], s[V], acc[V])), ...);
 }
 
 // Tile of workgroup `bid`: XCD-major remap (hardware places workgroup b on XCD
@@ -403,6 +356,7 @@ hipError_t launch_asp_gemm(int M, int N, int K, int r, const uint8_t* xq, const 
                            const uint16_t* t, const uint8_t* wq, const float* ws,
                            const uint16_t* L2t, const uint16_t* bias, uint16_t* y,
                            hipStream_t stream) {
+  if (M <= kSmallM) return launch_asp_gemm_small(M, N, K, r, xq, xs, t, wq, ws, L2t, bias, y, stream);
   const dim3 grid(gemm_tiles(M, N)), block(NT);
   switch (r) {
     case 16:
@@ -425,6 +379,7 @@ hipError_t launch_asp_gemm(int M, int N, int K, int r, const uint8_t* xq, const 
 
 hipError_t launch_group_partials(int M, int N, int K, const uint8_t* xq, const uint8_t* wq,
                                  int32_t* P, hipStream_t stream) {
+  if (M <= kSmallM) return launch_group_partials_small(M, N, K, xq, wq, P, stream);
   hipLaunchKernelGGL((asp_gemm_kernel<32, true>), dim3(gemm_tiles(M, N)), dim3(NT), 0, stream, xq, nullptr,
                      nullptr, wq, nullptr, nullptr, nullptr, nullptr, P, M, N, K);
   return hipGetLastError();

@@ -20,4 +20,15 @@ hipError_t launch_asp_gemm(int M, int N, int K, int r, const uint8_t* xq, const 
 hipError_t launch_group_partials(int M, int N, int K, const uint8_t* xq, const uint8_t* wq,
                                  int32_t* P, hipStream_t stream);
 
+// the few-token GEMM (one wave per 32 x 32 block), used for M <= kSmallM
+constexpr int kSmallM = 64;
+
+hipError_t launch_asp_gemm_small(int M, int N, int K, int r, const uint8_t* xq, const float* xs,
+                                 const uint16_t* t, const uint8_t* wq, const float* ws,
+                                 const uint16_t* L2t, const uint16_t* bias, uint16_t* y,
+                                 hipStream_t stream);
+
+hipError_t launch_group_partials_small(int M, int N, int K, const uint8_t* xq, const uint8_t* wq,
+                                       int32_t* P, hipStream_t stream);
+
 }  // namespace qwam
