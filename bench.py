@@ -30,6 +30,11 @@ Secondary measurement (not the headline line):
       r = 16): per-call latency of both kernels and algorithmic HBM GB/s, one
       JSON line per shape, rotating through enough distinct layers that the
       weights come from HBM.
+  python bench.py --denoise-step
+      one denoising step of a 30-block transformer (hidden 3072, FFN 14336,
+      8192 tokens; per block QKV, out-projection, FFN up, FFN down, r = 32),
+      every layer with its own weights and a fresh activation: aggregate
+      effective TOPS, one JSON line.
 """
 
 from __future__ import annotations
@@ -201,6 +206,85 @@ def small_m_report(args):
         torch.cuda.empty_cache()
 
 
+def denoise_step_report(args):
+    """Aggregate throughput of the 120 ASP layers of one denoising step.
+
+    The weights and activations of 120 full-size layers are drawn on the GPU
+    (seeded torch generators) from the same recipes as the seeded inputs
+    module: W ~ N(0, 1/K); x ~ N(0, 1) with 1% of channels scaled by a
+    log-uniform factor in [10, 50]; the FFN down-projection gets bf16(GELU(z)),
+    z ~ N(0, 1).  Each layer is calibrated (smoothing, top-32 eigenvectors of a
+    seeded stand-in Gramian, L1 / L2, R) and packed by the library, as offline.
+    """
+    import math
+    import torch
+    from paper_2609_33269_amd import calib, inputs, qwam
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    Ms, rr = 8192, 32
+    layers, acts, flops = [], [], 0
+    t0 = time.perf_counter()
+    for b in range(inputs.DENOISE_BLOCKS):
+        for which, (name, Ks, Ns) in enumerate(inputs.DENOISE_BLOCK):
+            gen = torch.Generator(device=dev)
+            gen.manual_seed(4_000_000 + 4 * b + which)
+            w = (torch.randn((Ns, Ks), generator=gen, device=dev) / math.sqrt(Ks)).to(torch.bfloat16)
+            z = torch.randn((Ms, Ks), generator=gen, device=dev)
+            if name == "ffn_down":
+                x = torch.nn.functional.gelu(z).to(torch.bfloat16)
+            else:
+                n_out = max(1, Ks // 100)
+                cols = torch.randperm(Ks, generator=gen, device=dev)[:n_out]
+                fac = torch.exp(torch.empty(n_out, device=dev).uniform_(math.log(10.0), math.log(50.0),
+                                                                         generator=gen))
+                z[:, cols] *= fac
+                x = z.to(torch.bfloat16)
+            del z
+            a = torch.randn((Ks, 64), generator=gen, device=dev, dtype=torch.float64)
+            f = calib.build_layer(x, w, calib.protected_basis(a, rr))
+            layers.append(qwam.make_layer(f["R"], f["lam"], f["L1"], f["L2"]))
+            acts.append(x)
+            flops += 2.0 * Ms * Ks * Ns
+            del f, w, a
+    torch.cuda.synchronize()
+    setup_s = time.perf_counter() - t0
+    print(f"[bench] {len(layers)} layers drawn, calibrated and packed in {setup_s:.1f} s", file=sys.stderr,
+          flush=True)
+
+    bufs = {}
+    for L in layers:
+        if (L.K, L.N) not in bufs:
+            bufs[(L.K, L.N)] = (torch.empty((Ms, L.K // 2), dtype=torch.uint8, device=dev),
+                                torch.empty((L.K // GROUP, Ms), dtype=torch.float32, device=dev),
+                                torch.empty((Ms, rr), dtype=torch.bfloat16, device=dev),
+                                torch.empty((Ms, L.N), dtype=torch.bfloat16, device=dev))
+
+    def step():
+        for L, x in zip(layers, acts):
+            xq, xs, t, y = bufs[(L.K, L.N)]
+            qwam.quantize_act(L, x, out=(xq, xs, t))
+            qwam.asp_linear(L, xq, xs, t, out=y)
+
+    stream = torch.cuda.current_stream()
+    step()
+    torch.cuda.synchronize()
+    steps = max(1, min(args.steps, 5))
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    print(json.dumps({
+        "workload": "denoise_step", "blocks": inputs.DENOISE_BLOCKS, "layers": len(layers), "M": Ms, "r": rr,
+        "layer_shapes": [[n, k, nn] for n, k, nn in inputs.DENOISE_BLOCK],
+        "ms_per_step": round(ms, 3), "effective_TOPS": round(flops / (ms * 1e-3) / 1e12, 1),
+        "frac_of_5P_peak": round(flops / (ms * 1e-3) / 1e12 / MFMA_PEAK, 4), "steps": steps,
+        "dense_equivalent_ops": flops, "data": "synthetic, drawn on the GPU"}), flush=True)
+
+
 def cpu_baseline(draws, seconds: float = 12.0):
     """The CPU oracle as it stands, timed on a bounded token sample of the same
     layer (weights packed beforehand, as on the GPU)."""
@@ -244,6 +328,7 @@ def main():
     ap.add_argument("--reduce-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
     ap.add_argument("--copy-mib", type=int, default=256, help="copy-probe size the counters were taken with")
     ap.add_argument("--small-m", action="store_true", help="report the action-expert layers instead")
+    ap.add_argument("--denoise-step", action="store_true", help="report one 120-layer denoising step instead")
     args = ap.parse_args()
     if args.reduce_counters:
         rec = reduce_counters(*args.reduce_counters, args.copy_mib)
@@ -260,6 +345,9 @@ def main():
 
     if args.small_m:
         small_m_report(args)
+        return
+    if args.denoise_step:
+        denoise_step_report(args)
         return
 
     import torch
