@@ -244,13 +244,14 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
         scale_accumulate(std::make_integer_sequence<int, 16>{}, accf[i][j], p, d.sx[i], d.sw[j]);
       }
     };
-    // software pipeline: MFMAs of the next block before the epilogue of this one
+    // software pipeline: three MFMAs in flight before the first update, so
+    // that no update waits for the block it reads
     const v16f p00 = mfma_block(0, 0);
     const v16f p01 = mfma_block(0, 1);
-    consume(0, 0, p00);
     const v16f p10 = mfma_block(1, 0);
-    consume(0, 1, p01);
+    consume(0, 0, p00);
     const v16f p11 = mfma_block(1, 1);
+    consume(0, 1, p01);
     consume(1, 0, p10);
     consume(1, 1, p11);
   };
