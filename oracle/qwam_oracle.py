@@ -30,9 +30,14 @@ Readings taken where the paper is silent (all are listed in the design notes):
     scale = fl32(absmax / 7), codes = clamp(rint(fl32(v * fl32(1/scale))), -8, 7);
     a group whose absmax is below 7 * 2**-126 gets scale 0 and all codes 0.
   * the activation is smoothed by multiplying with fl32(1/lambda) (the
-    reciprocal is formed once, at weight-pack time) and the 4-bit path
-    quantizes x~ itself (not the deflated x~_perp of Eq. 9); no Hadamard
-    rotation.  In exact arithmetic both give x~ W~ (Eq. 9 and R^T V = 0).
+    reciprocal is formed once, at weight-pack time); no Hadamard rotation.
+  * the 4-bit path quantizes either x~ itself (the default) or, in the
+    deflated variant, x~_perp of Eq. 8 / Eq. 9; in exact arithmetic both give
+    x~ W~_perp (Eq. 9 and R^T V = 0).  Deflation subtracts the bf16 branch's
+    own rank-r part, t_j * L1[:, j], from x~ one direction at a time, j in
+    ascending order, each step rounded to float32 (deflate_activations); each
+    product of two bf16 values is exact in float32, so every step is one
+    correctly rounded subtraction.
   * packing: 4 bits per code, sign-magnitude, eight codes per 32-bit word
     (pack_codes); the paper fixes the code range, not a byte layout.  This one
     lets a kernel turn a word into FP8 bytes of value code * 2^-9 with one mask
@@ -333,6 +338,41 @@ def quantize_activations(x_bits: np.ndarray, inv_lam: np.ndarray, L1_bits: np.nd
     return pack_codes(codes), scales, t, codes, xt
 
 
+def deflate_activations(xt: np.ndarray, t_bits: np.ndarray, L1_bits: np.ndarray) -> np.ndarray:
+    """x~_perp = x~ - V (V^T x~) (Eq. 8), deployed with the branch's factors.
+
+    V^T x~ is the rounded t of the 16-bit branch and V is L1 = bf16(V), so the
+    4-bit path loses exactly the part the branch adds back.  The r directions
+    are removed one at a time, j = 0 .. r-1:
+        cur <- fl32(cur - t[:, j] * L1[:, j]),   cur starting at x~,
+    each product of two bf16 values being exact in float32 (16 significant
+    bits).  xt float32 [M][K]; t bf16 bits [M][r]; L1 bf16 bits [K][r].
+    Returns float32 [M][K].
+    """
+    cur = np.array(xt, dtype=np.float32, copy=True)
+    t = bf16_bits_to_f64(t_bits)
+    L1 = bf16_bits_to_f64(L1_bits)
+    for j in range(t.shape[1]):
+        prod64 = t[:, j:j + 1] * L1[None, :, j]            # exact in float64
+        prod = prod64.astype(np.float32)
+        if not np.array_equal(prod.astype(np.float64), prod64):
+            raise ValueError("a branch product is not exact in float32 (underflow or overflow)")
+        cur = (cur - prod).astype(np.float32)              # one float32 rounding per step
+    return cur
+
+
+def quantize_activations_deflated(x_bits: np.ndarray, inv_lam: np.ndarray, L1_bits: np.ndarray):
+    """The activation side with the paper's deflation (Eq. 8 / Eq. 9): t is
+    computed from x~ as in quantize_activations, then x~_perp (deflate_activations)
+    is quantized per token and group.  Returns (packed uint8 [M][K/2], scales
+    f32 [M][G], t bf16 bits [M][r], codes int8 [M][K], x~_perp float32 [M][K])."""
+    xt = smooth_activations(x_bits, inv_lam)
+    t = down_projection(xt, L1_bits)
+    xp = deflate_activations(xt, t, L1_bits)
+    codes, scales = quantize_groups(xp)
+    return pack_codes(codes), scales, t, codes, xp
+
+
 def group_partials(qx: np.ndarray, qw: np.ndarray, group: int = GROUP) -> np.ndarray:
     """P[m, n, g] = sum_{k in group g} qx[m, k] * qw[n, k] (the integer GEMM of
     Sec. 3, one partial per group because each group has its own scales).
@@ -378,15 +418,17 @@ def asp_output_bruteforce(qx, sx, qw, sw, t_bits, L2_bits, bias_bits=None) -> np
     return y
 
 
-def asp_linear(x_bits, layer, bias_bits=None, rows=None):
-    """Whole deployed layer for the tokens `rows` (all if None).
+def asp_linear(x_bits, layer, bias_bits=None, rows=None, deflate=False):
+    """Whole deployed layer for the tokens `rows` (all if None); with
+    `deflate` the 4-bit path quantizes x~_perp (Eq. 9) instead of x~.
 
     layer: dict from build_layer (lam, L1, L2, R).  Returns a dict with every
     intermediate: wq, sw, inv_lam, qw, xq, sx, t, qx, P, y.
     """
     wq, sw, inv_lam, qw = pack_weights(layer["R"], layer["lam"])
     xb = x_bits if rows is None else x_bits[rows]
-    xq, sx, t, qx, _ = quantize_activations(xb, inv_lam, layer["L1"])
+    quant = quantize_activations_deflated if deflate else quantize_activations
+    xq, sx, t, qx, _ = quant(xb, inv_lam, layer["L1"])
     P = group_partials(qx, qw)
     y = asp_output(sx, sw, P, t, layer["L2"], bias_bits)
     return {"wq": wq, "sw": sw, "inv_lam": inv_lam, "qw": qw, "xq": xq, "sx": sx,
@@ -407,12 +449,15 @@ def asp_output_rows(xq_rows, sx_rows, t_rows, wq, sw, L2_bits, bias_bits=None):
 # ----------------------------------------------------------------------------
 
 
-def asp_linear_exact(x: np.ndarray, layer_exact) -> np.ndarray:
+def asp_linear_exact(x: np.ndarray, layer_exact, deflate=False) -> np.ndarray:
     """y = Q4(x~) Q4(R)^T + (x~ V)(V^T W~), all float64 (Eq. 9 with the 4-bit
-    path applied to x~; the quantizer itself run in float64)."""
+    path applied to x~, or with `deflate` to x~_perp = x~ - (x~ V) V^T; the
+    quantizer itself run in float64)."""
     x = np.asarray(x, dtype=np.float64)
     xt = x / layer_exact["lam"][None, :]
-    qx, sx = quantize_groups(xt, dtype=np.float64)
+    V = layer_exact["V"]
+    x4 = xt - (xt @ V) @ V.T if deflate else xt
+    qx, sx = quantize_groups(x4, dtype=np.float64)
     qw, sw = quantize_groups(layer_exact["R"], dtype=np.float64)
     y4 = dequantize_groups(qx, sx) @ dequantize_groups(qw, sw).T
     return y4 + (xt @ layer_exact["V"]) @ layer_exact["VtW"]

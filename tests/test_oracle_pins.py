@@ -425,3 +425,125 @@ def test_bits_per_weight():
     assert O.bits_per_weight(4096, 4096, 0, smooth_bits=0) == 4.5
     b = O.bits_per_weight(3072, 14336, 32)
     assert 4.70 < b < 4.72 and 3.39 < 16 / b < 3.41
+
+
+# --------------------------------------------------------------------------
+# activation deflation x~_perp = x~ - V (V^T x~) (Eq. 8 / Eq. 9)
+# --------------------------------------------------------------------------
+
+def _bits_of(values):
+    return O.f64_to_bf16_bits(np.asarray(values, dtype=np.float64))
+
+
+def test_deflation_steps_round_one_at_a_time():
+    """Hand-derived: from x~ = 1, removing two products of 2^-25 one at a time
+    gives 1 - 2^-25 -> 1 (a tie, rounded to even) and again 1, whereas
+    subtracting their sum 2^-24 would give 1 - 2^-24.  Products of 2^-24 are
+    exact steps: 1 - 2^-24, then 1 - 2^-23."""
+    K, r = 64, 4
+    xt = np.ones((2, K), dtype=np.float32)
+    L1 = np.zeros((K, r))
+    L1[:, 0] = L1[:, 1] = 2.0 ** -12
+    t = np.zeros((2, r))
+    t[0, :2] = 2.0 ** -13            # products 2^-25
+    t[1, :2] = 2.0 ** -12            # products 2^-24
+    out = O.deflate_activations(xt, _bits_of(t), _bits_of(L1))
+    assert out.dtype == np.float32
+    assert (out[0] == np.float32(1.0)).all()
+    assert (out[1] == np.float32(1.0 - 2.0 ** -23)).all()
+
+
+def test_deflation_on_coordinate_axes_closed_form():
+    """V = coordinate axes e_i (exact in bf16): t_j = bf16(x~_i) and the
+    deflated activation keeps every other channel and leaves, on channel i,
+    x~_i - bf16(x~_i), the bits bf16 rounding drops (exact in float32)."""
+    d = I.custom(M=9, K=192, N=32, r=16, seed=31, n_outliers=2)
+    rng = np.random.default_rng(31)
+    K, r = 192, 16
+    axes = rng.choice(K, size=r, replace=False)
+    V = np.zeros((K, r))
+    V[axes, np.arange(r)] = 1.0
+    L = O.build_layer(d.x, d.w, V)
+    inv = O.inverse_smoothing(L["lam"])
+    xq, sx, t, codes, xp = O.quantize_activations_deflated(d.x, inv, L["L1"])
+    xt = O.smooth_activations(d.x, inv).astype(np.float64)
+    # t_j = bf16(x~ at channel axes[j]); a one-term sum is rounded once
+    assert (O.bf16_bits_to_f64(t) == O.round_to_bf16(xt[:, axes])).all()
+    expect = xt.copy()
+    expect[:, axes] = xt[:, axes] - O.round_to_bf16(xt[:, axes])
+    assert (xp.astype(np.float64) == expect).all()
+    # and the codes / scales are those of the quantizer applied to that array
+    c2, s2 = O.quantize_groups(expect.astype(np.float32))
+    assert (codes == c2).all() and (sx == s2).all()
+    assert (O.unpack_codes(xq) == codes).all()
+
+
+def test_deflation_within_sequential_rounding_bound():
+    """Deployed x~_perp against the exact value of the same formula
+    (float64, exact products): each of the r steps adds at most half an ulp of
+    float32, so |error| <= r * 2^-24 * (|x~| + sum_j |t_j L1_j|)."""
+    d = I.custom(M=12, K=256, N=32, r=32, seed=32, n_outliers=3)
+    V = O.protected_basis_from_factor(d.a, 32)
+    L = O.build_layer(d.x, d.w, V)
+    inv = O.inverse_smoothing(L["lam"])
+    xt = O.smooth_activations(d.x, inv)
+    t = O.down_projection(xt, L["L1"])
+    xp = O.deflate_activations(xt, t, L["L1"]).astype(np.float64)
+    tf, L1f = O.bf16_bits_to_f64(t), O.bf16_bits_to_f64(L["L1"])
+    exact = xt.astype(np.float64) - tf @ L1f.T
+    bound = 32 * 2.0 ** -24 * (np.abs(xt) + np.abs(tf) @ np.abs(L1f).T)
+    assert (np.abs(xp - exact) <= bound).all()
+    # a dropped direction would be far outside the bound
+    assert (np.abs(tf[:, -1:] * L1f[None, :, -1]) > bound).mean() > 0.5
+
+
+def test_deflation_exact_mode_identities():
+    """Exact arithmetic (Sec. 4.2): x~_perp is orthogonal to V, projecting is
+    idempotent, and x~_perp W~_perp = x~ W~_perp, so without quantization the
+    deflated layer is x W."""
+    rng = np.random.default_rng(33)
+    x = rng.standard_normal((6, 128))
+    w = rng.standard_normal((24, 128))
+    V, _ = np.linalg.qr(rng.standard_normal((128, 16)))
+    Lx = O.build_layer_exact(x, w, V)
+    xt = x / Lx["lam"][None, :]
+    xp = xt - (xt @ V) @ V.T
+    assert np.abs(xp @ V).max() < 1e-12 * np.abs(xt).max() * 128
+    assert np.allclose(xp @ Lx["R"].T, xt @ Lx["R"].T, rtol=0, atol=1e-10 * np.abs(xt @ Lx["R"].T).max())
+    y = (xt @ V) @ Lx["VtW"] + xp @ Lx["R"].T
+    assert np.allclose(y, x @ w.T, rtol=0, atol=1e-10 * np.abs(x @ w.T).max())
+
+
+def test_deflation_shrinks_scales_when_the_action_part_dominates():
+    """Activations that live mostly in the protected subspace (large t, small
+    orthogonal remainder): deflation removes the large part before the 4-bit
+    quantizer, so the group scales shrink and the layer gets closer to x W
+    (the motivation of Eq. 8 / Eq. 9)."""
+    rng = np.random.default_rng(34)
+    M, K, N, r = 16, 256, 48, 16
+    V, _ = np.linalg.qr(rng.standard_normal((K, r)))
+    x = 40.0 * rng.standard_normal((M, r)) @ V.T + 0.5 * rng.standard_normal((M, K))
+    w = rng.standard_normal((N, K)) / np.sqrt(K)
+    xb, wb = O.f64_to_bf16_bits(x), O.f64_to_bf16_bits(w)
+    L = O.build_layer(xb, wb, V)
+    plain = O.asp_linear(xb, L)
+    defl = O.asp_linear(xb, L, deflate=True)
+    assert (defl["t"] == plain["t"]).all()
+    assert np.median(defl["sx"]) < 0.5 * np.median(plain["sx"])
+    ref = O.bf16_bits_to_f64(xb) @ O.bf16_bits_to_f64(wb).T
+    e_plain = np.linalg.norm(plain["y"] - ref) / np.linalg.norm(ref)
+    e_defl = np.linalg.norm(defl["y"] - ref) / np.linalg.norm(ref)
+    assert e_defl < 0.5 * e_plain
+    # exact mode agrees in direction
+    Lx = O.build_layer_exact(O.bf16_bits_to_f64(xb), O.bf16_bits_to_f64(wb), V)
+    ye_plain = O.asp_linear_exact(O.bf16_bits_to_f64(xb), Lx)
+    ye_defl = O.asp_linear_exact(O.bf16_bits_to_f64(xb), Lx, deflate=True)
+    assert np.linalg.norm(ye_defl - ref) < np.linalg.norm(ye_plain - ref)
+
+
+def test_deflation_rejects_inexact_products():
+    xt = np.ones((1, 64), dtype=np.float32)
+    t = np.zeros((1, 16)); t[0, 0] = 2.0 ** -100
+    L1 = np.zeros((64, 16)); L1[:, 0] = 2.0 ** -100
+    with pytest.raises(ValueError):
+        O.deflate_activations(xt, _bits_of(t), _bits_of(L1))
