@@ -81,7 +81,7 @@
 extern "C" {
 #endif
 
-#define QWAM_ABI_VERSION 2
+#define QWAM_ABI_VERSION 3
 #define QWAM_GROUP 64
 
 typedef enum {
@@ -140,6 +140,24 @@ qwam_status qwam_pack_weights(int32_t K, int32_t N, int32_t group,
  */
 qwam_status qwam_quantize_act(const qwam_layer *L, int32_t M, const uint16_t *x,
                               uint8_t *xq, float *xs, uint16_t *t, void *stream);
+
+/*
+ * Activation side with the paper's deflation (Eq. 8 / Eq. 9): as
+ * qwam_quantize_act, but the 4-bit path quantizes x~_perp = x~ - L1 t instead
+ * of x~, so that the part of the activation the 16-bit branch carries is not
+ * quantized twice.  Per token:
+ *   x~      = fl32(x * inv_smooth)
+ *   t       = bf16(sum_k bf16(x~_k) L1[k, j]) -- here rounded once from a
+ *             float64 accumulation, i.e. the bf16 of the exact sum except
+ *             within ~1e-13 relative of a rounding boundary
+ *   x~_perp = x~, then for j = 0 .. r-1 in order:
+ *             x~_perp <- fl32(x~_perp - t_j L1[:, j])   (exact products)
+ *   xq, xs  = group quantization (Eq. 2) and code words of x~_perp
+ * The outputs feed qwam_asp_linear unchanged: y = Q4(x~_perp) Q4(R)^T + t L2.
+ * Arguments, layouts, ownership and errors as for qwam_quantize_act.
+ */
+qwam_status qwam_quantize_act_deflated(const qwam_layer *L, int32_t M, const uint16_t *x,
+                                       uint8_t *xq, float *xs, uint16_t *t, void *stream);
 
 /*
  * The ASP GEMM (the second kernel of App. B.1): the integer partial sum of

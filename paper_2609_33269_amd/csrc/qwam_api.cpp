@@ -106,9 +106,15 @@ qwam_status qwam_pack_weights(int32_t K, int32_t N, int32_t group, const float* 
                                                 static_cast<hipStream_t>(stream)));
 }
 
-qwam_status qwam_quantize_act(const qwam_layer* L, int32_t M, const uint16_t* x, uint8_t* xq, float* xs,
-                              uint16_t* t, void* stream) {
-  const char* fn = "qwam_quantize_act";
+}  // extern "C"
+
+namespace {
+
+typedef hipError_t (*act_launcher)(int, int, int, const uint16_t*, const float*, const uint16_t*, uint8_t*,
+                                   float*, uint16_t*, hipStream_t);
+
+qwam_status quantize_act_common(const char* fn, act_launcher launch, const qwam_layer* L, int32_t M,
+                                const uint16_t* x, uint8_t* xq, float* xs, uint16_t* t, void* stream) {
   qwam_status s = check_layer(fn, L, true);
   if (s != QWAM_OK) return s;
   if ((s = check_m(fn, M)) != QWAM_OK) return s;
@@ -119,8 +125,22 @@ qwam_status qwam_quantize_act(const qwam_layer* L, int32_t M, const uint16_t* x,
   QWAM_REQUIRE_PTR(xs);
   QWAM_REQUIRE_PTR(t);
   if ((s = check_device(fn)) != QWAM_OK) return s;
-  return launched(fn, qwam::launch_quantize_act(M, L->K, L->r, x, L->inv_smooth, L->L1t, xq, xs, t,
-                                                static_cast<hipStream_t>(stream)));
+  return launched(fn, launch(M, L->K, L->r, x, L->inv_smooth, L->L1t, xq, xs, t, static_cast<hipStream_t>(stream)));
+}
+
+}  // namespace
+
+extern "C" {
+
+qwam_status qwam_quantize_act(const qwam_layer* L, int32_t M, const uint16_t* x, uint8_t* xq, float* xs,
+                              uint16_t* t, void* stream) {
+  return quantize_act_common("qwam_quantize_act", qwam::launch_quantize_act, L, M, x, xq, xs, t, stream);
+}
+
+qwam_status qwam_quantize_act_deflated(const qwam_layer* L, int32_t M, const uint16_t* x, uint8_t* xq,
+                                       float* xs, uint16_t* t, void* stream) {
+  return quantize_act_common("qwam_quantize_act_deflated", qwam::launch_quantize_act_deflated, L, M, x, xq, xs,
+                             t, stream);
 }
 
 qwam_status qwam_asp_linear(const qwam_layer* L, int32_t M, const uint8_t* xq, const float* xs,

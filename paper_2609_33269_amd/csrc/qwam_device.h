@@ -50,6 +50,21 @@ __device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
   return u >> 16;
 }
 
+// double -> bf16 bits, round to nearest, ties to even, in one rounding (finite
+// inputs): the double is first rounded to float by round-to-odd (truncate, and
+// set the last bit when inexact), which keeps enough bits for the second
+// rounding to bf16 to be the correctly rounded result.
+__device__ __forceinline__ uint32_t f64_to_bf16_rne(double d) {
+  const float f = static_cast<float>(d);
+  uint32_t u = __float_as_uint(f);
+  const double back = static_cast<double>(f);
+  if (back != d) {
+    if (__builtin_fabs(back) > __builtin_fabs(d)) u -= 1u;   // rounded away from zero: step back
+    u |= 1u;
+  }
+  return f32_to_bf16_rne(__uint_as_float(u));
+}
+
 // Two floats -> packed bf16x2 (lo in bits 0..15), RNE.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return f32_to_bf16_rne(lo) | (f32_to_bf16_rne(hi) << 16);

@@ -12,6 +12,11 @@ hipError_t launch_quantize_act(int M, int K, int r, const uint16_t* x, const flo
                                const uint16_t* L1t, uint8_t* xq, float* xs, uint16_t* t,
                                hipStream_t stream);
 
+// the 4-bit path quantizes the deflated activation x~ - L1 t (Eq. 8 / Eq. 9)
+hipError_t launch_quantize_act_deflated(int M, int K, int r, const uint16_t* x, const float* inv_smooth,
+                                        const uint16_t* L1t, uint8_t* xq, float* xs, uint16_t* t,
+                                        hipStream_t stream);
+
 hipError_t launch_asp_gemm(int M, int N, int K, int r, const uint8_t* xq, const float* xs,
                            const uint16_t* t, const uint8_t* wq, const float* ws,
                            const uint16_t* L2t, const uint16_t* bias, uint16_t* y,

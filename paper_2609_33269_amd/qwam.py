@@ -6,7 +6,7 @@ raw device pointers plus the current HIP stream across the C ABI.  If the
 library is not built, every call raises: there is no fallback.
 
 Names follow the C ABI (include/qwam.h): pack_weights, quantize_act,
-asp_linear, debug_group_partials.
+quantize_act_deflated, asp_linear, debug_group_partials.
 """
 
 from __future__ import annotations
@@ -41,6 +41,8 @@ SIGNATURES = {
                                          _c_void_p, _c_void_p, _c_void_p]),
     "qwam_quantize_act": (ctypes.c_int, [_LP, _i32, _c_void_p, _c_void_p, _c_void_p, _c_void_p,
                                          _c_void_p]),
+    "qwam_quantize_act_deflated": (ctypes.c_int, [_LP, _i32, _c_void_p, _c_void_p, _c_void_p,
+                                                  _c_void_p, _c_void_p]),
     "qwam_asp_linear": (ctypes.c_int, [_LP, _i32, _c_void_p, _c_void_p, _c_void_p, _c_void_p,
                                        _c_void_p]),
     "qwam_debug_group_partials": (ctypes.c_int, [_LP, _i32, _c_void_p, _c_void_p, _c_void_p]),
@@ -154,6 +156,16 @@ def quantize_act(layer: PackedLayer, x: torch.Tensor, stream=None, out=None):
     """qwam_quantize_act: x bf16 [M][K] -> (xq uint8 [M][K/2], xs float32 [K/64][M], t bf16 [M][r]).
 
     `out` may give the three output tensors (preallocated, e.g. for a benchmark loop)."""
+    return _quantize(lib().qwam_quantize_act, "qwam_quantize_act", layer, x, stream, out)
+
+
+def quantize_act_deflated(layer: PackedLayer, x: torch.Tensor, stream=None, out=None):
+    """qwam_quantize_act_deflated: as quantize_act, but the codes are those of
+    the deflated activation x~ - L1 t (Eq. 8 / Eq. 9)."""
+    return _quantize(lib().qwam_quantize_act_deflated, "qwam_quantize_act_deflated", layer, x, stream, out)
+
+
+def _quantize(fn, name: str, layer: PackedLayer, x: torch.Tensor, stream, out):
     M = x.shape[0]
     dev = x.device
     if out is None:
@@ -163,11 +175,11 @@ def quantize_act(layer: PackedLayer, x: torch.Tensor, stream=None, out=None):
     else:
         xq, xs, t = out
     c = layer.c_struct()
-    st = lib().qwam_quantize_act(ctypes.byref(c), M, _req(x, "x", torch.bfloat16, (M, layer.K)),
-                                 _req(xq, "xq", torch.uint8, (M, layer.K // 2)),
-                                 _req(xs, "xs", torch.float32, (layer.K // GROUP, M)),
-                                 _req(t, "t", torch.bfloat16, (M, layer.r)), _stream_ptr(stream))
-    _check("qwam_quantize_act", st)
+    st = fn(ctypes.byref(c), M, _req(x, "x", torch.bfloat16, (M, layer.K)),
+            _req(xq, "xq", torch.uint8, (M, layer.K // 2)),
+            _req(xs, "xs", torch.float32, (layer.K // GROUP, M)),
+            _req(t, "t", torch.bfloat16, (M, layer.r)), _stream_ptr(stream))
+    _check(name, st)
     return xq, xs, t
 
 
@@ -186,9 +198,10 @@ def asp_linear(layer: PackedLayer, xq: torch.Tensor, xs: torch.Tensor, t: torch.
     return y
 
 
-def forward(layer: PackedLayer, x: torch.Tensor, stream=None) -> torch.Tensor:
-    """Both kernels of one layer call: quantize_act then asp_linear."""
-    xq, xs, t = quantize_act(layer, x, stream)
+def forward(layer: PackedLayer, x: torch.Tensor, stream=None, deflate: bool = False) -> torch.Tensor:
+    """Both kernels of one layer call: quantize_act (or quantize_act_deflated)
+    then asp_linear."""
+    xq, xs, t = (quantize_act_deflated if deflate else quantize_act)(layer, x, stream)
     return asp_linear(layer, xq, xs, t, stream=stream)
 
 

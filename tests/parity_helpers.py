@@ -84,10 +84,11 @@ def check_t(t_gpu_bits, t_ref_bits, xt, L1_bits, frac_over_1ulp=1e-3):
     return over
 
 
-def run_gpu(layer: Q.PackedLayer, x_bits: np.ndarray):
-    """quantize_act + asp_linear on cuda:0; returns device tensors."""
+def run_gpu(layer: Q.PackedLayer, x_bits: np.ndarray, deflate: bool = False):
+    """quantize_act (or quantize_act_deflated) + asp_linear on cuda:0; returns
+    device tensors."""
     x = bf16_dev(x_bits)
-    xq, xs, t = Q.quantize_act(layer, x)
+    xq, xs, t = (Q.quantize_act_deflated if deflate else Q.quantize_act)(layer, x)
     y = Q.asp_linear(layer, xq, xs, t)
     torch.cuda.synchronize()
     return x, xq, xs, t, y

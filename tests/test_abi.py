@@ -38,7 +38,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == set(Q.SIGNATURES), "binding and header disagree"
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.qwam_abi_version() == 2
+    assert lib.qwam_abi_version() == 3
     assert lib.qwam_status_string(3) == b"QWAM_ERR_MISALIGNED"
 
 
@@ -51,8 +51,9 @@ def _layer(K=256, N=256, r=16, group=64, **ptrs):
     return c
 
 
-def _act(lib, layer, M=64, x=FAKE, xq=FAKE, xs=FAKE, t=FAKE):
-    return lib.qwam_quantize_act(ctypes.byref(layer), M, x, xq, xs, t, None)
+def _act(lib, layer, M=64, x=FAKE, xq=FAKE, xs=FAKE, t=FAKE, deflated=False):
+    fn = lib.qwam_quantize_act_deflated if deflated else lib.qwam_quantize_act
+    return fn(ctypes.byref(layer), M, x, xq, xs, t, None)
 
 
 def _lin(lib, layer, M=64, xq=FAKE, xs=FAKE, t=FAKE, y=FAKE):
@@ -101,6 +102,14 @@ def test_layer_calls_reject_bad_arguments(lib):
         assert _lin(lib, _layer(), **{kw: None}) == INVALID
     msg = lib.qwam_last_error()
     assert msg.startswith(b"qwam_asp_linear") and b"y is NULL" in msg
+    # the deflated activation call validates exactly like the plain one
+    assert lib.qwam_quantize_act_deflated(None, 64, FAKE, FAKE, FAKE, FAKE, None) == INVALID
+    for r in (0, 24):
+        assert _act(lib, _layer(r=r), deflated=True) == UNSUPPORTED
+    assert _act(lib, _layer(), M=0, deflated=True) == INVALID
+    assert _act(lib, _layer(**{"L1t": FAKE + 2}), deflated=True) == MISALIGNED
+    assert _act(lib, _layer(), t=None, deflated=True) == INVALID
+    assert lib.qwam_last_error().startswith(b"qwam_quantize_act_deflated")
     # partials: rank is not used, but shapes and pointers are checked
     assert lib.qwam_debug_group_partials(ctypes.byref(_layer(r=7)), 1, None, FAKE, None) == INVALID
 
@@ -109,6 +118,7 @@ def test_layer_calls_reject_bad_arguments(lib):
 def test_no_device_is_reported_before_any_launch(lib):
     assert lib.qwam_pack_weights(256, 256, 64, FAKE, FAKE, FAKE, FAKE, FAKE, None) == NO_DEVICE
     assert _act(lib, _layer()) == NO_DEVICE
+    assert _act(lib, _layer(), deflated=True) == NO_DEVICE
     assert _lin(lib, _layer()) == NO_DEVICE
     assert lib.qwam_debug_group_partials(ctypes.byref(_layer()), 4, FAKE, FAKE, None) == NO_DEVICE
     assert b"no HIP device" in lib.qwam_last_error()
