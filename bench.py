@@ -25,6 +25,11 @@ Counter support (HBM traffic of the GEMM, scaled by a plain copy of known size):
       turns the two counter-collection CSVs into profiles/traffic_asp_gemm_ffn_up.json.
 
 Secondary measurement (not the headline line):
+  python bench.py --deflated
+      the same layer and line format with the paper's activation deflation
+      (Eq. 8 / Eq. 9: the 4-bit path quantizes x~ - L1 t), i.e. with
+      qwam_quantize_act_deflated as the activation kernel; its roofline is the
+      FP64 + FP32 matrix-core work of t and of the r rank-1 updates.
   python bench.py --small-m
       the action-expert layers (M in {16, 32, 64}, K = 1024, N in {4096, 1024},
       r = 16): per-call latency of both kernels and algorithmic HBM GB/s, one
@@ -55,6 +60,8 @@ sys.path.insert(0, ROOT)
 M, K, N, R_RANK, GROUP = 4096, 3072, 14336, 32, 64
 G = K // GROUP
 MFMA_PEAK = 5000.0             # MI355X dense FP8 (= dense INT8) matrix peak, TFLOP/s (TOP/s)
+FP64_MFMA_PEAK = 78.6          # MI355X dense FP64 matrix peak, TFLOP/s
+FP32_MFMA_PEAK = 157.3         # MI355X dense FP32 matrix peak, TFLOP/s
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 VALU_OPS_PER_OUTPUT_GROUP = 2  # scale product, fused multiply-add
 METRIC = "ASP W4A4+r32 linear: effective TOPS & % int8 MFMA peak at 4096×3072×14336"
@@ -285,7 +292,21 @@ def denoise_step_report(args):
         "dense_equivalent_ops": flops, "data": "synthetic, drawn on the GPU"}), flush=True)
 
 
-def cpu_baseline(draws, seconds: float = 12.0):
+def deflated_act_roofline(k1_ms: float):
+    """Matrix-core work of the deflated activation kernel: t in double
+    (2 M K r flops at the FP64 peak) and the r rank-1 updates in float
+    (2 M K r flops at the FP32 peak).  `peak` is the rate at which both
+    together would take their ideal time."""
+    flops = 2.0 * M * K * R_RANK
+    ideal_s = flops / (FP64_MFMA_PEAK * 1e12) + flops / (FP32_MFMA_PEAK * 1e12)
+    peak = 2.0 * flops / ideal_s / 1e12
+    achieved = 2.0 * flops / (k1_ms * 1e-3) / 1e12
+    return {"bound": "mfma (fp64 t + fp32 rank-1 updates)", "achieved": round(achieved, 2),
+            "peak": round(peak, 2), "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
+            "ideal_us": round(ideal_s * 1e6, 2), "flops": 2.0 * flops}
+
+
+def cpu_baseline(draws, seconds: float = 12.0, deflate: bool = False):
     """The CPU oracle as it stands, timed on a bounded token sample of the same
     layer (weights packed beforehand, as on the GPU)."""
     from oracle import qwam_oracle as O
@@ -302,7 +323,8 @@ def cpu_baseline(draws, seconds: float = 12.0):
     t0 = time.perf_counter()
     while done + chunk <= M:
         rows = slice(done, done + chunk)
-        xq, sx, t, qx, _ = O.quantize_activations(draws.x[rows], inv_lam, f["L1"])
+        quant = O.quantize_activations_deflated if deflate else O.quantize_activations
+        xq, sx, t, qx, _ = quant(draws.x[rows], inv_lam, f["L1"])
         P = O.group_partials(qx, qw)
         O.asp_output(sx, sw, P, t, f["L2"])
         done += chunk
@@ -311,7 +333,8 @@ def cpu_baseline(draws, seconds: float = 12.0):
     dt = time.perf_counter() - t0
     return {"value": 2.0 * done * K * N / dt / 1e12, "unit": "TOPS", "cores": int(threads),
             "kind": "oracle",
-            "sample": f"{done} of {M} tokens (chunks of {chunk}) of the {M}x{K}x{N} r{R_RANK} layer, "
+            "sample": f"{done} of {M} tokens (chunks of {chunk}) of the {M}x{K}x{N} r{R_RANK} layer"
+                      f"{' with deflation' if deflate else ''}, "
                       f"weights packed beforehand; {dt:.1f} s; value = 2*tokens*K*N/time"}
 
 
@@ -327,6 +350,8 @@ def main():
                     help="after timing, run a plain float32 copy kernel over MIB MiB five times")
     ap.add_argument("--reduce-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
     ap.add_argument("--copy-mib", type=int, default=256, help="copy-probe size the counters were taken with")
+    ap.add_argument("--deflated", action="store_true",
+                    help="the same layer with the deflated activation kernel (Eq. 8 / Eq. 9)")
     ap.add_argument("--small-m", action="store_true", help="report the action-expert layers instead")
     ap.add_argument("--denoise-step", action="store_true", help="report one 120-layer denoising step instead")
     args = ap.parse_args()
@@ -379,13 +404,14 @@ def main():
                      torch.empty((M, R_RANK), dtype=torch.bfloat16, device=dev),
                      torch.empty((M, N), dtype=torch.bfloat16, device=dev)))
     stream = torch.cuda.current_stream()
+    act_fn = qwam.quantize_act_deflated if args.deflated else qwam.quantize_act
 
     def step(i, ev=None):
         j = i % nrot
         xq, xs, t, y = outs[j]
         if ev is not None:
             ev[0].record(stream)
-        qwam.quantize_act(layers[j], xins[j], out=(xq, xs, t))
+        act_fn(layers[j], xins[j], out=(xq, xs, t))
         if ev is not None:
             ev[1].record(stream)
         qwam.asp_linear(layers[j], xq, xs, t, out=y)
@@ -455,14 +481,15 @@ def main():
         "vs_baseline": None,
         "dtype": "int4 codes on fp8-e4m3 MFMA (exact), f32 scale/accumulate, bf16 out",
         "data": "synthetic",
-        "config": {"workload": "video_dit_ffn_up", "M": M, "K": K, "N": N, "r": R_RANK, "group": GROUP,
+        "config": {"workload": "video_dit_ffn_up_deflated" if args.deflated else "video_dit_ffn_up", "M": M, "K": K, "N": N, "r": R_RANK, "group": GROUP,
                    "act": "N(0,1), 1% channels x U_log(10,50)", "weights": "N(0,1/K)",
                    "rotated_buffer_sets": nrot},
         "roofline": {"bound": "mfma", "kernel": GEMM_KERNEL, "achieved": round(k2_tops, 1),
                      "peak": MFMA_PEAK, "unit": "TFLOP/s", "frac": round(k2_tops / MFMA_PEAK, 4),
                      "traffic": traffic, "algorithmic_bytes": gemm_bytes},
         "layer_frac_int8_peak": round(eff_tops / MFMA_PEAK, 4),
-        "kernels_us": {"quantize_act": round(k1_ms * 1e3, 2), "asp_gemm": round(k2_ms * 1e3, 2)},
+        "kernels_us": {("quantize_act_deflated" if args.deflated else "quantize_act"): round(k1_ms * 1e3, 2),
+                       "asp_gemm": round(k2_ms * 1e3, 2)},
         "quantize_act_roofline": {"bound": "hbm", "achieved": round(k1_gbs, 1), "peak": HBM_PEAK_GBS,
                                   "unit": "GB/s", "frac": round(k1_gbs / HBM_PEAK_GBS, 4),
                                   "algorithmic_bytes": act_bytes},
@@ -473,9 +500,11 @@ def main():
         "bf16_linear_us": round(bf16_ms * 1e3, 2),
         "speedup_vs_bf16_linear": round(bf16_ms / ms_step, 3),
     }
+    if args.deflated:
+        out["quantize_act_deflated_roofline"] = deflated_act_roofline(k1_ms)
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a token sample", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(draws, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(draws, args.cpu_seconds, deflate=args.deflated)
     print(json.dumps(out), flush=True)
 
 
