@@ -30,7 +30,14 @@ Readings taken where the paper is silent (all are listed in the design notes):
     scale = fl32(absmax / 7), codes = clamp(rint(fl32(v * fl32(1/scale))), -8, 7);
     a group whose absmax is below 7 * 2**-126 gets scale 0 and all codes 0.
   * the activation is smoothed by multiplying with fl32(1/lambda) (the
-    reciprocal is formed once, at weight-pack time); no Hadamard rotation.
+    reciprocal is formed once, at weight-pack time).
+  * the block Hadamard rotation of Eq. 3 is optional (App. B.1 applies it;
+    the default path of this layer does not).  Block B = the largest power of
+    two dividing K, at most 1024 (App. B.1); the weight side is rotated
+    offline in float64; the activation side runs the fast Walsh-Hadamard
+    transform in float32, one rounding per butterfly, stages on element bit
+    0, 1, .., log2(B)-1 in that order, then multiplies by fl32(1/sqrt(B))
+    (exact when B is a power of 4, e.g. 1024) (rotate_activations).
   * the 4-bit path quantizes either x~ itself (the default) or, in the
     deflated variant, x~_perp of Eq. 8 / Eq. 9; in exact arithmetic both give
     x~ W~_perp (Eq. 9 and R^T V = 0).  Deflation subtracts the bf16 branch's
@@ -158,37 +165,71 @@ def protected_basis_from_factor(a: np.ndarray, r: int) -> np.ndarray:
     return _fix_signs(U[:, :r])
 
 
-def build_layer(x_bits: np.ndarray, w_bits: np.ndarray, V: np.ndarray):
+def hadamard_block(K: int) -> int:
+    """Block size of the rotation: the largest power of two dividing K, at most
+    1024 (App. B.1)."""
+    if K <= 0:
+        raise ValueError("K must be positive")
+    return min(K & -K, 1024)
+
+
+def sylvester_hadamard(B: int) -> np.ndarray:
+    """The +-1 Hadamard matrix of order B (a power of two) by Sylvester's
+    doubling H_2n = [[H, H], [H, -H]]; symmetric, H H = B I."""
+    H = np.ones((1, 1))
+    while H.shape[0] < B:
+        H = np.block([[H, H], [H, -H]])
+    if H.shape[0] != B:
+        raise ValueError("B must be a power of two")
+    return H
+
+
+def rotate_exact(v: np.ndarray, B: int) -> np.ndarray:
+    """Row vectors times the orthonormal block Hadamard matrix diag(H_B, ..)/sqrt(B),
+    float64 (Eq. 3's H; H is symmetric, so x H = (H x^T)^T)."""
+    v = np.asarray(v, dtype=np.float64)
+    rows, K = v.shape
+    H = sylvester_hadamard(B) / np.sqrt(B)
+    return (v.reshape(rows, K // B, B) @ H).reshape(rows, K)
+
+
+def build_layer(x_bits: np.ndarray, w_bits: np.ndarray, V: np.ndarray, hadamard: bool = False):
     """Deployed ASP factors of one layer from bf16 x [M][K], bf16 w [N][K] and
     a protected basis V [K][r] (float64, orthonormal columns).
 
     Steps (Sec. 3 Eq. 3, Sec. 4.2 Eq. 9, App. B.1):
       lambda = smoothing factors (float32)
       W~[n, k] = lambda_k * W[n, k]                       (float64)
+      with `hadamard`: W~ = W~ H (row n rotated blockwise, Eq. 3), and V is
+      a basis of the rotated coordinates
       L1 = bf16(V)                                        [K][r]
       L2 = bf16(L1^T W~)     (the paper's V^T W~)         [r][N]
       R  = fl32(W~ - L1 L2)  (the paper's W~_perp, here built against the
                                rounded factors, so W~ = R + L1 L2 up to fl32)
     Returns a dict of numpy arrays: lam (f32 [K]), L1 (bf16 bits [K][r]),
-    L2 (bf16 bits [r][N]), R (f32 [N][K]).
+    L2 (bf16 bits [r][N]), R (f32 [N][K]), and hadamard (the block size B, or
+    0 without rotation).
     """
     x = bf16_bits_to_f64(x_bits)
     w = bf16_bits_to_f64(w_bits)
     lam = smoothing_factors(x, w)
     wt = w * lam.astype(np.float64)[None, :]                  # [N][K]
+    B = hadamard_block(wt.shape[1]) if hadamard else 0
+    if B:
+        wt = rotate_exact(wt, B)
     L1 = f64_to_bf16_bits(V)                                  # [K][r]
     L1f = bf16_bits_to_f64(L1)
     L2 = f64_to_bf16_bits(L1f.T @ wt.T)                       # [r][N]
     L2f = bf16_bits_to_f64(L2)
     R = (wt - (L1f @ L2f).T).astype(np.float32)               # [N][K]
-    return {"lam": lam, "L1": L1, "L2": L2, "R": R}
+    return {"lam": lam, "L1": L1, "L2": L2, "R": R, "hadamard": B}
 
 
-def build_layer_exact(x: np.ndarray, w: np.ndarray, V: np.ndarray):
+def build_layer_exact(x: np.ndarray, w: np.ndarray, V: np.ndarray, hadamard: bool = False):
     """Exact-mode factors (float64 throughout, nothing rounded).
 
     lam (float64, by the formula), V, VtW = V^T W~ [r][N], R = (I - V V^T) W~
-    stored [N][K] (Sec. 4.2: W~_perp).
+    stored [N][K] (Sec. 4.2: W~_perp); with `hadamard`, W~ is rotated (Eq. 3).
     """
     x = np.asarray(x, dtype=np.float64)
     w = np.asarray(w, dtype=np.float64)
@@ -198,9 +239,12 @@ def build_layer_exact(x: np.ndarray, w: np.ndarray, V: np.ndarray):
     lam = np.ones_like(xmax)
     lam[ok] = xmax[ok] ** ALPHA / wmax[ok] ** (1.0 - ALPHA)
     wt = w * lam[None, :]
+    B = hadamard_block(wt.shape[1]) if hadamard else 0
+    if B:
+        wt = rotate_exact(wt, B)
     VtW = V.T @ wt.T                                          # [r][N]
     R = wt - (V @ VtW).T                                      # [N][K]
-    return {"lam": lam, "V": V, "VtW": VtW, "R": R}
+    return {"lam": lam, "V": V, "VtW": VtW, "R": R, "hadamard": B}
 
 
 # ----------------------------------------------------------------------------
@@ -315,6 +359,38 @@ def smooth_activations(x_bits: np.ndarray, inv_lam: np.ndarray) -> np.ndarray:
     return (x * np.asarray(inv_lam, dtype=np.float32)[None, :]).astype(np.float32)
 
 
+def fwht_f32(v: np.ndarray, B: int) -> np.ndarray:
+    """Fast Walsh-Hadamard transform of every block of B consecutive channels
+    of every row, in float32 (unnormalized: the result is v H_B blockwise).
+
+    Stage s = 0, 1, .., log2(B)-1 pairs the elements whose indices differ in
+    bit s only; the one with the bit clear becomes fl32(a + b), the other
+    fl32(a - b) (a: bit clear, b: bit set).  One rounding per butterfly."""
+    v = np.array(v, dtype=np.float32, copy=True)
+    rows, K = v.shape
+    if B & (B - 1) or K % B:
+        raise ValueError("B must be a power of two dividing K")
+    x = v.reshape(rows, K // B, B)
+    h = 1
+    while h < B:
+        y = x.reshape(rows, K // B, B // (2 * h), 2, h)
+        a, b = y[:, :, :, 0, :], y[:, :, :, 1, :]
+        x = np.stack([(a + b).astype(np.float32), (a - b).astype(np.float32)], axis=3).reshape(rows, K // B, B)
+        h *= 2
+    return x.reshape(rows, K)
+
+
+def hadamard_scale(B: int) -> np.float32:
+    """fl32(1/sqrt(B)), the normalization of the rotation (exact for B = 4^k)."""
+    return np.float32(1.0 / np.sqrt(np.float64(B)))
+
+
+def rotate_activations(xt: np.ndarray, B: int) -> np.ndarray:
+    """The online rotation of the smoothed activation (Eq. 3): the float32
+    fast Walsh-Hadamard transform, then one float32 multiply by fl32(1/sqrt(B))."""
+    return (fwht_f32(xt, B) * hadamard_scale(B)).astype(np.float32)
+
+
 def down_projection(xt: np.ndarray, L1_bits: np.ndarray) -> np.ndarray:
     """t = bf16( sum_k bf16(x~_k) * L1[k, j] ), the sum taken exactly (float64).
 
@@ -327,12 +403,19 @@ def down_projection(xt: np.ndarray, L1_bits: np.ndarray) -> np.ndarray:
     return f64_to_bf16_bits(s)
 
 
-def quantize_activations(x_bits: np.ndarray, inv_lam: np.ndarray, L1_bits: np.ndarray):
-    """The activation side of one layer call: smoothing, per-token group
-    quantization (Eq. 2, absmax/7 per token, App. B.1), code packing and the
-    rank-r down-projection.  Returns (packed uint8 [M][K/2], scales f32 [M][G],
-    t bf16 bits [M][r], codes int8 [M][K], x~ float32 [M][K])."""
+def transformed_activations(x_bits: np.ndarray, inv_lam: np.ndarray, hadamard: int = 0) -> np.ndarray:
+    """x~ of Eq. 3: smoothed, and rotated when `hadamard` (the block size) is set."""
     xt = smooth_activations(x_bits, inv_lam)
+    return rotate_activations(xt, hadamard) if hadamard else xt
+
+
+def quantize_activations(x_bits: np.ndarray, inv_lam: np.ndarray, L1_bits: np.ndarray, hadamard: int = 0):
+    """The activation side of one layer call: smoothing (and the rotation, if
+    `hadamard` is the block size), per-token group quantization (Eq. 2,
+    absmax/7 per token, App. B.1), code packing and the rank-r
+    down-projection.  Returns (packed uint8 [M][K/2], scales f32 [M][G],
+    t bf16 bits [M][r], codes int8 [M][K], x~ float32 [M][K])."""
+    xt = transformed_activations(x_bits, inv_lam, hadamard)
     codes, scales = quantize_groups(xt)
     t = down_projection(xt, L1_bits)
     return pack_codes(codes), scales, t, codes, xt
@@ -361,12 +444,13 @@ def deflate_activations(xt: np.ndarray, t_bits: np.ndarray, L1_bits: np.ndarray)
     return cur
 
 
-def quantize_activations_deflated(x_bits: np.ndarray, inv_lam: np.ndarray, L1_bits: np.ndarray):
+def quantize_activations_deflated(x_bits: np.ndarray, inv_lam: np.ndarray, L1_bits: np.ndarray,
+                                  hadamard: int = 0):
     """The activation side with the paper's deflation (Eq. 8 / Eq. 9): t is
     computed from x~ as in quantize_activations, then x~_perp (deflate_activations)
     is quantized per token and group.  Returns (packed uint8 [M][K/2], scales
     f32 [M][G], t bf16 bits [M][r], codes int8 [M][K], x~_perp float32 [M][K])."""
-    xt = smooth_activations(x_bits, inv_lam)
+    xt = transformed_activations(x_bits, inv_lam, hadamard)
     t = down_projection(xt, L1_bits)
     xp = deflate_activations(xt, t, L1_bits)
     codes, scales = quantize_groups(xp)
@@ -428,7 +512,7 @@ def asp_linear(x_bits, layer, bias_bits=None, rows=None, deflate=False):
     wq, sw, inv_lam, qw = pack_weights(layer["R"], layer["lam"])
     xb = x_bits if rows is None else x_bits[rows]
     quant = quantize_activations_deflated if deflate else quantize_activations
-    xq, sx, t, qx, _ = quant(xb, inv_lam, layer["L1"])
+    xq, sx, t, qx, _ = quant(xb, inv_lam, layer["L1"], layer.get("hadamard", 0))
     P = group_partials(qx, qw)
     y = asp_output(sx, sw, P, t, layer["L2"], bias_bits)
     return {"wq": wq, "sw": sw, "inv_lam": inv_lam, "qw": qw, "xq": xq, "sx": sx,
@@ -455,6 +539,8 @@ def asp_linear_exact(x: np.ndarray, layer_exact, deflate=False) -> np.ndarray:
     quantizer itself run in float64)."""
     x = np.asarray(x, dtype=np.float64)
     xt = x / layer_exact["lam"][None, :]
+    if layer_exact.get("hadamard", 0):
+        xt = rotate_exact(xt, layer_exact["hadamard"])
     V = layer_exact["V"]
     x4 = xt - (xt @ V) @ V.T if deflate else xt
     qx, sx = quantize_groups(x4, dtype=np.float64)

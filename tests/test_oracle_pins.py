@@ -547,3 +547,112 @@ def test_deflation_rejects_inexact_products():
     L1 = np.zeros((64, 16)); L1[:, 0] = 2.0 ** -100
     with pytest.raises(ValueError):
         O.deflate_activations(xt, _bits_of(t), _bits_of(L1))
+
+
+# --------------------------------------------------------------------------
+# block Hadamard rotation (Eq. 3; block size and online transform, App. B.1)
+# --------------------------------------------------------------------------
+
+def test_hadamard_block_sizes():
+    """Largest power of two dividing K, capped at 1024."""
+    cases = {3072: 1024, 14336: 1024, 1024: 1024, 65536: 1024, 4096: 1024, 192: 64, 320: 64,
+             640: 128, 16448: 64, 256: 256, 64: 64, 1536: 512}
+    for K, B in cases.items():
+        assert O.hadamard_block(K) == B, K
+
+
+def test_fwht_stage_order_hand_case():
+    """[1, 2^-24, 2^-24, 2^-24] with B = 4, stages on bit 0 then bit 1:
+    bit 0 gives (1 + 2^-24 -> 1 by ties-to-even, 1 - 2^-24, 2^-23, 0); bit 1
+    gives (1 + 2^-23, 1 - 2^-24, 1 - 2^-23, 1 - 2^-24).  The opposite stage
+    order would give (1 + 2^-23, 1 - 2^-23, 1 - 2^-24, 1 - 2^-24)."""
+    x = np.array([[1.0, 2.0 ** -24, 2.0 ** -24, 2.0 ** -24]], dtype=np.float32)
+    out = O.fwht_f32(x, 4)
+    expect = np.array([[1 + 2.0 ** -23, 1 - 2.0 ** -24, 1 - 2.0 ** -23, 1 - 2.0 ** -24]])
+    assert out.dtype == np.float32 and (out.astype(np.float64) == expect).all()
+
+
+def test_fwht_matches_hadamard_matrix():
+    """Against scipy's Hadamard matrix (Sylvester order): exact on small
+    integers (every partial sum is an integer below 2^24), and within the
+    per-stage rounding bound log2(B) * 2^-24 * sum|x| on random data; the
+    transform applied twice is B times the input (H H = B I)."""
+    import scipy.linalg
+    rng = np.random.default_rng(51)
+    for B in (64, 256, 1024):
+        H = scipy.linalg.hadamard(B).astype(np.float64)
+        xi = rng.integers(-1000, 1000, size=(3, 2 * B)).astype(np.float32)
+        out = O.fwht_f32(xi, B).astype(np.float64)
+        ref = (xi.astype(np.float64).reshape(3, 2, B) @ H).reshape(3, 2 * B)
+        assert (out == ref).all()
+        assert (O.fwht_f32(O.fwht_f32(xi, B), B) == B * xi).all()
+        xr = rng.standard_normal((4, B)).astype(np.float32)
+        ref = xr.astype(np.float64) @ H
+        bound = np.log2(B) * 2.0 ** -24 * np.abs(xr.astype(np.float64)).sum(axis=1, keepdims=True)
+        assert (np.abs(O.fwht_f32(xr, B) - ref) <= bound).all()
+    # the exact float64 rotation is orthonormal
+    v = rng.standard_normal((5, 3072))
+    rv = O.rotate_exact(v, 1024)
+    assert np.allclose(np.linalg.norm(rv, axis=1), np.linalg.norm(v, axis=1), rtol=1e-13)
+
+
+def test_rotation_of_a_one_hot_channel():
+    """e_k rotated with B = 1024 is row k of H / 32: every entry +-2^-5
+    exactly, with sign (-1)^popcount(j & k)."""
+    K, B = 2048, 1024
+    for k in (0, 5, 1023, 1500):
+        x = np.zeros((1, K), dtype=np.float32)
+        x[0, k] = 1.0
+        out = O.rotate_activations(x, B)[0].astype(np.float64)
+        blk = k // B
+        j = np.arange(B)
+        signs = np.array([(-1) ** bin(int(v) & (k % B)).count("1") for v in j], dtype=np.float64)
+        assert (out[blk * B:(blk + 1) * B] == signs / 32.0).all()
+        assert not np.delete(out, np.arange(blk * B, (blk + 1) * B)).any()
+    assert O.hadamard_scale(1024) == np.float32(1 / 32) and O.hadamard_scale(256) == np.float32(1 / 16)
+
+
+def test_rotated_exact_split_is_identity():
+    """Eq. 3 with Eq. 9, exact arithmetic: smoothing and rotation cancel
+    between the two operands, so the rotated split without quantization is x W;
+    deflating changes nothing there either."""
+    rng = np.random.default_rng(52)
+    x = rng.standard_normal((5, 2048))
+    x[:, 7] *= 40.0
+    w = rng.standard_normal((24, 2048)) / 45.0
+    V, _ = np.linalg.qr(rng.standard_normal((2048, 16)))
+    Lx = O.build_layer_exact(x, w, V, hadamard=True)
+    assert Lx["hadamard"] == 1024
+    xt = O.rotate_exact(x / Lx["lam"][None, :], 1024)
+    y = (xt @ V) @ Lx["VtW"] + xt @ Lx["R"].T
+    assert np.allclose(y, x @ w.T, rtol=0, atol=1e-10 * np.abs(x @ w.T).max())
+    xp = xt - (xt @ V) @ V.T
+    y2 = (xt @ V) @ Lx["VtW"] + xp @ Lx["R"].T
+    assert np.allclose(y2, x @ w.T, rtol=0, atol=1e-10 * np.abs(x @ w.T).max())
+
+
+def test_rotation_spreads_outliers_and_helps_4bit():
+    """A few large channels dominate the group maxima; the rotation spreads
+    them over the block, so the groups' scales even out and the 4-bit path
+    (R alone, no branch) gets closer to its exact product."""
+    d = I.custom(M=32, K=1024, N=64, r=16, seed=53, n_outliers=4)
+    V = O.protected_basis_from_factor(d.a, 16)
+    plain = O.build_layer(d.x, d.w, V)
+    rot = O.build_layer(d.x, d.w, V, hadamard=True)
+    errs = []
+    for L in (plain, rot):
+        inv = O.inverse_smoothing(L["lam"])
+        xq, sx, t, qx, xt = O.quantize_activations(d.x, inv, L["L1"], L["hadamard"])
+        y4 = O.dequantize_groups(qx, sx) @ L["R"].astype(np.float64).T
+        ref = xt.astype(np.float64) @ L["R"].astype(np.float64).T
+        errs.append(np.linalg.norm(y4 - ref) / np.linalg.norm(ref))
+        if L is rot:
+            spread = sx.max(axis=1) / sx.min(axis=1)
+        else:
+            spread0 = sx.max(axis=1) / sx.min(axis=1)
+    assert np.median(spread) < np.median(spread0)
+    assert errs[1] < errs[0]
+    # the deployed rotated layer still follows the output formula
+    out = O.asp_linear(d.x, rot)
+    yb = O.asp_output_bruteforce(out["qx"], out["sx"], out["qw"], out["sw"], out["t"], rot["L2"])
+    assert np.allclose(out["y"], yb, rtol=0, atol=1e-12 * np.abs(yb).max())
