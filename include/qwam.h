@@ -15,6 +15,16 @@
  *     App. B.1).
  *   - lambda is the per-channel smoothing factor of Eq. 3 / App. B.1 (the
  *     activation is divided by it, the weight multiplied by it).
+ *   - Optionally (layer field `hadamard` = B, the block size), the block
+ *     Hadamard rotation of Eq. 3: x~ = H diag(lambda)^-1 x with H
+ *     block-diagonal, orthonormal Hadamard blocks of size B; App. B.1 takes B
+ *     = the largest power of two dividing K, at most 1024.  The weights must
+ *     have been rotated the same way before packing (R is then the rotated
+ *     residual and L1 a basis in rotated coordinates); the activation
+ *     kernels rotate x online with the fast Walsh-Hadamard transform in
+ *     float32: one rounding per butterfly, stages on channel bit 0, 1, ..,
+ *     log2(B)-1 in that order (channel index within the block), then one
+ *     multiply by fl32(1/sqrt(B)).
  *   - L1 = bf16(V) and L2 = bf16(V^T W~) are the factors of the 16-bit branch
  *     (V^T W~)^T (V^T x~) of Eq. 9, V being the top-r eigenvectors of the
  *     layer's Gramian (Eq. 7); R = W~ - L1 L2 is the deflated weight W~_perp.
@@ -67,6 +77,10 @@
  * word rotated right by 4 bits with the same mask, yields the codes as FP8
  * e4m3 bytes of value code * 2^-9, which is how the GEMM consumes them.)
  *
+ * Rotation: hadamard == 0, or a power of two with 16 <= hadamard <= 1024
+ * dividing K (QWAM_ERR_INVALID_ARG otherwise).  It affects the activation
+ * calls only; qwam_pack_weights and qwam_asp_linear do not read it.
+ *
  * Shape limits: group == 64; K % 64 == 0, 64 <= K <= 65536; N % 16 == 0,
  * 16 <= N <= 1048576; r in {16, 32, 48, 64}; 1 <= M <= 1048576; for
  * qwam_asp_linear also M * K / 64 < 2^29 and N * K / 64 < 2^29
@@ -81,7 +95,7 @@
 extern "C" {
 #endif
 
-#define QWAM_ABI_VERSION 3
+#define QWAM_ABI_VERSION 4
 #define QWAM_GROUP 64
 
 typedef enum {
@@ -99,6 +113,7 @@ typedef struct qwam_layer {
     int32_t N;                  /* output channels (multiple of 16)                 */
     int32_t r;                  /* rank of the protected subspace (16/32/48/64)     */
     int32_t group;              /* must be 64                                        */
+    int32_t hadamard;           /* block size B of the rotation, or 0 for none       */
     const uint8_t *wq;          /* [N][K/2]  packed residual codes                   */
     const float *ws;            /* [K/64][N] residual group scales                   */
     const float *inv_smooth;    /* [K]       fl32(1/lambda)                          */
@@ -131,8 +146,9 @@ qwam_status qwam_pack_weights(int32_t K, int32_t N, int32_t group,
  * multiply by the packed reciprocal), per-token group quantization of x~
  * (Eq. 2, absmax / 7 per token and group), code-word packing, and the rank-r
  * down-projection t = V^T x~ of Eq. 9 (bf16 inputs, float32 accumulation,
- * bf16 result), in one pass over x.
- *   L   in   layer (reads K, r, group, inv_smooth, L1t)
+ * bf16 result), in one pass over x.  With L->hadamard != 0, x~ is also
+ * rotated (Eq. 3) before it is quantized and projected.
+ *   L   in   layer (reads K, r, group, hadamard, inv_smooth, L1t)
  *   x   in   bf16 [M][K]
  *   xq  out  uint8 [M][K/2]
  *   xs  out  float [K/64][M]

@@ -1,0 +1,203 @@
+// Per-group steps of the activation kernels (plain, deflated, rotated), in
+// one lane layout: a wave holds one group of 64 channels of 16 tokens, lane l
+// holding token l % 16 and the 16 consecutive channels 16*(l/16) .. +15, so
+// the four lanes l, l^16, l^32, l^48 hold one token's group.  That is the
+// A-operand layout of v_mfma_f32_16x16x32_bf16 (row = token, k slots of lane
+// l shared with lane l of the B operand) and, with one k slot per lane group,
+// of v_mfma_f64_16x16x4_f64.
+#pragma once
+#include "qwam_device.h"
+
+namespace qwam {
+
+typedef double v4d __attribute__((ext_vector_type(4)));
+typedef float v16f_t __attribute__((ext_vector_type(16)));
+
+template <int RANK>
+struct ActFetch {
+  uint4 xa, xb;                 // 16 bf16 of x
+  v8s l1[RANK / 16][2];         // L1t fragments: 16 channels of 16 columns of t
+};
+
+// Waves per workgroup: 16 (4 per SIMD) up to rank 32, 8 above (more registers
+// for the larger L1t prefetch).
+template <int RANK>
+constexpr int act_waves() { return RANK <= 32 ? 16 : 8; }
+
+// x~ = fl32(x * fl32(1/lambda)) for the lane's 16 channels (xa, xb: 16 bf16 of
+// x; ip: the matching 16 entries of 1/lambda).
+__device__ __forceinline__ void smooth16(const uint4& xa, const uint4& xb, const float4* ip, float (&v)[16]) {
+  const uint32_t xw[8] = {xa.x, xa.y, xa.z, xa.w, xb.x, xb.y, xb.z, xb.w};
+  const float4 i0 = ip[0], i1 = ip[1], i2 = ip[2], i3 = ip[3];
+  const float iv[16] = {i0.x, i0.y, i0.z, i0.w, i1.x, i1.y, i1.z, i1.w,
+                        i2.x, i2.y, i2.z, i2.w, i3.x, i3.y, i3.z, i3.w};
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    v[2 * j] = __uint_as_float(xw[j] << 16) * iv[2 * j];
+    v[2 * j + 1] = __uint_as_float(xw[j] & 0xFFFF0000u) * iv[2 * j + 1];
+  }
+}
+
+// Quantizes one token's group, held by the four lanes l, l^16, l^32, l^48 (16
+// consecutive channels each, Eq. 2), and stores the lane's two code words at
+// byte q_off of q_rsrc and, if xs_dst is not null, the group's scale.
+__device__ __forceinline__ void quantize_pack_store(const float (&v)[16], buf_rsrc q_rsrc, uint32_t q_off,
+                                                    float* xs_dst) {
+  float amax = 0.0f;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) amax = __builtin_fmaxf(amax, __builtin_fabsf(v[j]));
+  amax = __builtin_fmaxf(amax, __shfl_xor(amax, 16));
+  amax = __builtin_fmaxf(amax, __shfl_xor(amax, 32));
+  const float s = q4_scale(amax);
+  const float inv = q4_inv(s);
+  // codes: q = clamp(rint(v * inv), -8, 7); a byte holds (q_odd + 8) * 16 + (q_even + 8),
+  // XOR 0x88 turns that into the two's-complement nibbles (q & 15) | (q_odd & 15) << 4,
+  // and those become the packed code word
+  uint32_t packed[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    uint32_t wv = 0;
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const float qe = __builtin_fminf(__builtin_fmaxf(__builtin_rintf(v[8 * h + 2 * b] * inv), -8.0f), 7.0f);
+      const float qo = __builtin_fminf(__builtin_fmaxf(__builtin_rintf(v[8 * h + 2 * b + 1] * inv), -8.0f), 7.0f);
+      wv = __builtin_amdgcn_cvt_pk_u8_f32(__builtin_fmaf(qo, 16.0f, qe) + 136.0f, b, wv);
+    }
+    packed[h] = twos_nibbles_to_code_word(wv ^ 0x88888888u);
+  }
+  buf_store8(make_uint2(packed[0], packed[1]), q_rsrc, q_off);
+  if (xs_dst != nullptr) *xs_dst = s;
+}
+
+template <int RANK>
+struct DeflFetch {
+  uint4 xa, xb;                 // 16 bf16 of x
+  uint32_t l1[RANK / 2];        // L1[a_ch][j], two bf16 per word (j even in the low half)
+};
+
+// L1t fragments of the lane's 16 channels ch0 .. ch0+15 (ch0 = first channel
+// of its group slice) for the RB blocks of 16 columns of t: row rb*16 + l%16.
+template <int RB>
+__device__ __forceinline__ void load_l1_fragments(const uint16_t* __restrict__ L1t, int K, int ch0, int row,
+                                                  v8s (&l1)[RB][2]) {
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    const uint16_t* lp = L1t + static_cast<int64_t>(rb * 16 + row) * K + ch0;
+    l1[rb][0] = *reinterpret_cast<const v8s*>(lp);
+    l1[rb][1] = *reinterpret_cast<const v8s*>(lp + 8);
+  }
+}
+
+// t partial on the bf16 matrix cores: A = bf16(x~) of the lane's token and
+// channels, B = the matching L1t fragments; two k-steps of 32 per group.
+template <int RB>
+__device__ __forceinline__ void t_step_bf16(const float (&v)[16], const v8s (&l1)[RB][2], v4f (&acc)[RB]) {
+  typedef __bf16 v8b __attribute__((ext_vector_type(8)));
+  v8b a_lo, a_hi;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    a_lo[j] = static_cast<__bf16>(v[j]);
+    a_hi[j] = static_cast<__bf16>(v[8 + j]);
+  }
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_lo, __builtin_bit_cast(v8bf, l1[rb][0]), acc[rb], 0, 0, 0);
+    acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_hi, __builtin_bit_cast(v8bf, l1[rb][1]), acc[rb], 0, 0, 0);
+  }
+}
+
+// t partial in double on the FP64 matrix cores: A lane l = token l%16, k-slot
+// l/16 -> channel 16*(l/16) + s at step s; B lane l = column l%16 of block rb,
+// same k-slot.  Products of two bf16 values are exact in double.
+template <int RB>
+__device__ __forceinline__ void t_step_f64(const float (&v)[16], const v8s (&l1)[RB][2], v4d (&acc)[RB]) {
+#pragma unroll
+  for (int s = 0; s < 16; ++s) {
+    const double a = static_cast<double>(static_cast<float>(static_cast<__bf16>(v[s])));
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const uint32_t lb = static_cast<uint16_t>(l1[rb][s >> 3][s & 7]);
+      acc[rb] = __builtin_amdgcn_mfma_f64_16x16x4f64(a, static_cast<double>(bf16_to_f32(lb)), acc[rb], 0, 0, 0);
+    }
+  }
+}
+
+// Deflation column of L1 for A-operand lane l of v_mfma_f32_16x16x1_4b_f32:
+// lane 16B + 4Q + I supplies channel 16Q + 4B + I of the group, which lands in
+// result register 4B + I of the lanes with l/16 = Q (token l%16), i.e. the
+// layout above.  Two bf16 per word, j even in the low half.
+__device__ __forceinline__ int deflate_channel(int lane) {
+  return 16 * ((lane >> 2) & 3) + 4 * (lane >> 4) + (lane & 3);
+}
+
+template <int RANK>
+__device__ __forceinline__ void load_l1_column(const uint16_t* __restrict__ L1t, int K, int ch,
+                                               uint32_t (&l1w)[RANK / 2]) {
+  const uint16_t* lp = L1t + ch;
+#pragma unroll
+  for (int j = 0; j < RANK; j += 2)
+    l1w[j / 2] = static_cast<uint32_t>(lp[j * K]) | (static_cast<uint32_t>(lp[(j + 1) * K]) << 16);
+}
+
+// x~_perp = x~ - L1 t: r rank-1 updates on the FP32 matrix cores, K = 1 each,
+// j ascending; each step adds L1[:, j] * (-t_j), an exact product, with one
+// rounding.  tn_row: -t of the lane's token (float, RANK entries, LDS).
+template <int RANK>
+__device__ __forceinline__ void deflate_step(float (&v)[16], const uint32_t (&l1w)[RANK / 2], const float* tn_row) {
+  v16f_t c;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) c[i] = v[i];
+#pragma unroll
+  for (int j = 0; j < RANK; j += 4) {
+    const float4 tv = *reinterpret_cast<const float4*>(tn_row + j);
+    c = __builtin_amdgcn_mfma_f32_16x16x1f32(__uint_as_float(l1w[j / 2] << 16), tv.x, c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x1f32(__uint_as_float(l1w[j / 2] & 0xFFFF0000u), tv.y, c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x1f32(__uint_as_float(l1w[j / 2 + 1] << 16), tv.z, c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x1f32(__uint_as_float(l1w[j / 2 + 1] & 0xFFFF0000u), tv.w, c, 0, 0, 0);
+  }
+#pragma unroll
+  for (int i = 0; i < 16; ++i) v[i] = c[i];
+}
+
+// Partial t tiles -> LDS [wave][16][RANK].  bf16 MFMA: register i of lane l is
+// token 4*(l/16) + i; f64 MFMA: token l/16 + 4 i; column l%16 of block rb.
+template <int RB>
+__device__ __forceinline__ void store_t_partials(float* red, int wave, int lane, const v4f (&acc)[RB]) {
+  constexpr int RANK = RB * 16;
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      red[(wave * 16 + 4 * (lane >> 4) + i) * RANK + rb * 16 + (lane & 15)] = acc[rb][i];
+}
+
+template <int RB>
+__device__ __forceinline__ void store_t_partials(double* red, int wave, int lane, const v4d (&acc)[RB]) {
+  constexpr int RANK = RB * 16;
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      red[(wave * 16 + (lane >> 4) + 4 * i) * RANK + rb * 16 + (lane & 15)] = acc[rb][i];
+}
+
+// Sums the partial tiles in wave order and writes bf16 t (tokens < rows);
+// with tneg != nullptr also -t as float into LDS [16][RANK].  Float partials
+// are summed in float and rounded once; double partials in double, then
+// rounded once to bf16 (f64_to_bf16_rne).  Call between two barriers.
+template <int RANK, typename T>
+__device__ __forceinline__ void reduce_t(const T* red, int nwaves, int rows, uint16_t* __restrict__ t_rows,
+                                         float* tneg) {
+  for (int e = threadIdx.x; e < 16 * RANK; e += blockDim.x) {
+    const int i = e / RANK, j = e % RANK;
+    T sum = 0;
+    for (int w = 0; w < nwaves; ++w) sum += red[(w * 16 + i) * RANK + j];
+    uint32_t b;
+    if constexpr (sizeof(T) == 8) b = f64_to_bf16_rne(sum);
+    else b = f32_to_bf16_rne(sum);
+    if (i < rows) t_rows[static_cast<int64_t>(i) * RANK + j] = static_cast<uint16_t>(b);
+    if (tneg != nullptr) tneg[i * RANK + j] = -bf16_to_f32(b);
+  }
+}
+
+}  // namespace qwam

@@ -55,6 +55,10 @@ qwam_status check_layer(const char* fn, const qwam_layer* L, bool need_branch) {
   if (s != QWAM_OK) return s;
   if (need_branch && !(L->r == 16 || L->r == 32 || L->r == 48 || L->r == 64))
     return fail(QWAM_ERR_UNSUPPORTED, "%s: rank r must be 16, 32, 48 or 64 (got %d)", fn, L->r);
+  const int32_t B = L->hadamard;
+  if (B != 0 && (B < 16 || B > 1024 || (B & (B - 1)) != 0 || L->K % B != 0))
+    return fail(QWAM_ERR_INVALID_ARG, "%s: hadamard must be 0 or a power of two in [16, 1024] dividing K (got %d)",
+                fn, B);
   return QWAM_OK;
 }
 
@@ -110,10 +114,7 @@ qwam_status qwam_pack_weights(int32_t K, int32_t N, int32_t group, const float* 
 
 namespace {
 
-typedef hipError_t (*act_launcher)(int, int, int, const uint16_t*, const float*, const uint16_t*, uint8_t*,
-                                   float*, uint16_t*, hipStream_t);
-
-qwam_status quantize_act_common(const char* fn, act_launcher launch, const qwam_layer* L, int32_t M,
+qwam_status quantize_act_common(const char* fn, bool deflate, const qwam_layer* L, int32_t M,
                                 const uint16_t* x, uint8_t* xq, float* xs, uint16_t* t, void* stream) {
   qwam_status s = check_layer(fn, L, true);
   if (s != QWAM_OK) return s;
@@ -125,7 +126,12 @@ qwam_status quantize_act_common(const char* fn, act_launcher launch, const qwam_
   QWAM_REQUIRE_PTR(xs);
   QWAM_REQUIRE_PTR(t);
   if ((s = check_device(fn)) != QWAM_OK) return s;
-  return launched(fn, launch(M, L->K, L->r, x, L->inv_smooth, L->L1t, xq, xs, t, static_cast<hipStream_t>(stream)));
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  if (L->hadamard != 0)
+    return launched(fn, qwam::launch_quantize_act_rotated(M, L->K, L->r, L->hadamard, deflate, x, L->inv_smooth,
+                                                          L->L1t, xq, xs, t, st));
+  return launched(fn, (deflate ? qwam::launch_quantize_act_deflated : qwam::launch_quantize_act)(
+                          M, L->K, L->r, x, L->inv_smooth, L->L1t, xq, xs, t, st));
 }
 
 }  // namespace
@@ -134,13 +140,12 @@ extern "C" {
 
 qwam_status qwam_quantize_act(const qwam_layer* L, int32_t M, const uint16_t* x, uint8_t* xq, float* xs,
                               uint16_t* t, void* stream) {
-  return quantize_act_common("qwam_quantize_act", qwam::launch_quantize_act, L, M, x, xq, xs, t, stream);
+  return quantize_act_common("qwam_quantize_act", false, L, M, x, xq, xs, t, stream);
 }
 
 qwam_status qwam_quantize_act_deflated(const qwam_layer* L, int32_t M, const uint16_t* x, uint8_t* xq,
                                        float* xs, uint16_t* t, void* stream) {
-  return quantize_act_common("qwam_quantize_act_deflated", qwam::launch_quantize_act_deflated, L, M, x, xq, xs,
-                             t, stream);
+  return quantize_act_common("qwam_quantize_act_deflated", true, L, M, x, xq, xs, t, stream);
 }
 
 qwam_status qwam_asp_linear(const qwam_layer* L, int32_t M, const uint8_t* xq, const float* xs,

@@ -17,6 +17,12 @@ hipError_t launch_quantize_act_deflated(int M, int K, int r, const uint16_t* x, 
                                         const uint16_t* L1t, uint8_t* xq, float* xs, uint16_t* t,
                                         hipStream_t stream);
 
+// the same two activation kernels with the block Hadamard rotation of Eq. 3
+// (block B, a power of two with 16 <= B <= 1024 dividing K)
+hipError_t launch_quantize_act_rotated(int M, int K, int r, int B, bool deflate, const uint16_t* x,
+                                       const float* inv_smooth, const uint16_t* L1t, uint8_t* xq, float* xs,
+                                       uint16_t* t, hipStream_t stream);
+
 hipError_t launch_asp_gemm(int M, int N, int K, int r, const uint8_t* xq, const float* xs,
                            const uint16_t* t, const uint8_t* wq, const float* ws,
                            const uint16_t* L2t, const uint16_t* bias, uint16_t* y,

@@ -5,6 +5,7 @@
 //         codes xq [M][K/2] and scales xs [G][M] (Eq. 2), and the rank-r
 //         down-projection t = bf16(x~) . L1 on bf16 matrix cores (V^T x~ of
 //         Eq. 9), all in one pass over x.
+#include "qwam_act.h"
 #include "qwam_device.h"
 #include "qwam_internal.h"
 
@@ -58,74 +59,14 @@ __global__ __launch_bounds__(256) void inverse_smoothing_kernel(const float* __r
 // Fused activation kernel.
 //
 // A workgroup owns 16 tokens and all of K; its waves split the K groups into
-// contiguous ranges.  In a wave, lane l handles token (l % 16) and the 16
-// consecutive channels 16*(l/16) .. +15 of the current group, so the 4 lanes
-// l, l^16, l^32, l^48 together hold one token's group of 64.  That is also the
-// A-operand layout of v_mfma_f32_16x16x32_bf16 (row = l % 16, the k slots of
-// lane l shared with lane l of the B operand), so the smoothed values feed the
-// down-projection directly from registers: two MFMA steps of 32 channels per
-// group and 16 columns of t.  Each wave prefetches the next group (x, 1/lambda,
-// L1t) while it quantizes the current one; x is read with buffer loads and the
-// codes / scales are written with buffer stores, so rows past M need no
-// branches.  The per-wave partial t tiles are summed in LDS in wave order
-// (deterministic) and rounded to bf16 once.
+// contiguous ranges, in the lane layout of qwam_act.h (lane l: token l % 16,
+// channels 16*(l/16) .. +15 of the current group), so the smoothed values feed
+// the down-projection on the bf16 matrix cores straight from registers.  Each
+// wave prefetches the next group (x, L1t) while it quantizes the current one;
+// x is read with buffer loads and the codes / scales are written with buffer
+// stores, so rows past M need no branches.  The per-wave partial t tiles are
+// summed in LDS in wave order (deterministic) and rounded to bf16 once.
 // ---------------------------------------------------------------------------
-template <int RANK>
-struct ActFetch {
-  uint4 xa, xb;                 // 16 bf16 of x
-  v8s l1[RANK / 16][2];         // L1t fragments: 16 channels of 16 columns of t
-};
-
-// Waves per workgroup: 16 (4 per SIMD) up to rank 32, 8 above (more registers
-// for the larger L1t prefetch).
-template <int RANK>
-constexpr int act_waves() { return RANK <= 32 ? 16 : 8; }
-
-// x~ = fl32(x * fl32(1/lambda)) for the lane's 16 channels (xa, xb: 16 bf16 of
-// x; ip: the matching 16 entries of 1/lambda).
-__device__ __forceinline__ void smooth16(const uint4& xa, const uint4& xb, const float4* ip, float (&v)[16]) {
-  const uint32_t xw[8] = {xa.x, xa.y, xa.z, xa.w, xb.x, xb.y, xb.z, xb.w};
-  const float4 i0 = ip[0], i1 = ip[1], i2 = ip[2], i3 = ip[3];
-  const float iv[16] = {i0.x, i0.y, i0.z, i0.w, i1.x, i1.y, i1.z, i1.w,
-                        i2.x, i2.y, i2.z, i2.w, i3.x, i3.y, i3.z, i3.w};
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    v[2 * j] = __uint_as_float(xw[j] << 16) * iv[2 * j];
-    v[2 * j + 1] = __uint_as_float(xw[j] & 0xFFFF0000u) * iv[2 * j + 1];
-  }
-}
-
-// Quantizes one token's group, held by the four lanes l, l^16, l^32, l^48 (16
-// consecutive channels each, Eq. 2), and stores the lane's two code words at
-// byte q_off of q_rsrc and, if xs_dst is not null, the group's scale.
-__device__ __forceinline__ void quantize_pack_store(const float (&v)[16], buf_rsrc q_rsrc, uint32_t q_off,
-                                                    float* xs_dst) {
-  float amax = 0.0f;
-#pragma unroll
-  for (int j = 0; j < 16; ++j) amax = __builtin_fmaxf(amax, __builtin_fabsf(v[j]));
-  amax = __builtin_fmaxf(amax, __shfl_xor(amax, 16));
-  amax = __builtin_fmaxf(amax, __shfl_xor(amax, 32));
-  const float s = q4_scale(amax);
-  const float inv = q4_inv(s);
-  // codes: q = clamp(rint(v * inv), -8, 7); a byte holds (q_odd + 8) * 16 + (q_even + 8),
-  // XOR 0x88 turns that into the two's-complement nibbles (q & 15) | (q_odd & 15) << 4,
-  // and those become the packed code word
-  uint32_t packed[2];
-#pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    uint32_t wv = 0;
-#pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const float qe = __builtin_fminf(__builtin_fmaxf(__builtin_rintf(v[8 * h + 2 * b] * inv), -8.0f), 7.0f);
-      const float qo = __builtin_fminf(__builtin_fmaxf(__builtin_rintf(v[8 * h + 2 * b + 1] * inv), -8.0f), 7.0f);
-      wv = __builtin_amdgcn_cvt_pk_u8_f32(__builtin_fmaf(qo, 16.0f, qe) + 136.0f, b, wv);
-    }
-    packed[h] = twos_nibbles_to_code_word(wv ^ 0x88888888u);
-  }
-  buf_store8(make_uint2(packed[0], packed[1]), q_rsrc, q_off);
-  if (xs_dst != nullptr) *xs_dst = s;
-}
-
 template <int RANK, bool INV_LDS>
 __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_kernel(
     const uint16_t* __restrict__ x, const float* __restrict__ inv_smooth,
@@ -161,23 +102,18 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_kernel(
     for (int i = lane; i < n4; i += 64) reinterpret_cast<float4*>(inv_w)[i] = src[i];
   }
 
-  auto fetch = [&](int g, ActFetch<RANK>& f) {
+  auto fetch = [&](int g, ActFetch<RANK>& f) __attribute__((always_inline)) {
     const uint32_t go = static_cast<uint32_t>(g) * kGroup * 2u;
     f.xa = buf_load16(x_rsrc, x_off + go);
     f.xb = buf_load16(x_rsrc, x_off + go + 16u);
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      const uint16_t* lp = L1t + static_cast<int64_t>(rb * 16 + row) * K + g * kGroup + chunk * 16;
-      f.l1[rb][0] = *reinterpret_cast<const v8s*>(lp);
-      f.l1[rb][1] = *reinterpret_cast<const v8s*>(lp + 8);
-    }
+    load_l1_fragments<RB>(L1t, K, g * kGroup + chunk * 16, row, f.l1);
   };
 
   v4f acc[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) acc[rb] = v4f{0.f, 0.f, 0.f, 0.f};
 
-  auto work = [&](int g, const ActFetch<RANK>& f) {
+  auto work = [&](int g, const ActFetch<RANK>& f) __attribute__((always_inline)) {
     const float4* ip = INV_LDS ? reinterpret_cast<const float4*>(inv_w + (g - g_begin) * kGroup + chunk * 16)
                                : reinterpret_cast<const float4*>(inv_smooth + g * kGroup + chunk * 16);
     float v[16];
@@ -185,20 +121,7 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_kernel(
     // every lane of a row holds the same scale; lanes of row r write it at r
     quantize_pack_store(v, q_rsrc, q_off + static_cast<uint32_t>(g) * (kGroup / 2),
                         row < rows ? xs + static_cast<int64_t>(g) * M + m0 + row : nullptr);
-
-    // down-projection: A = bf16(x~) of this token, B = L1t rows (columns of t)
-    typedef __bf16 v8b __attribute__((ext_vector_type(8)));
-    v8b a_lo, a_hi;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      a_lo[j] = static_cast<__bf16>(v[j]);
-      a_hi[j] = static_cast<__bf16>(v[8 + j]);
-    }
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_lo, __builtin_bit_cast(v8bf, f.l1[rb][0]), acc[rb], 0, 0, 0);
-      acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_hi, __builtin_bit_cast(v8bf, f.l1[rb][1]), acc[rb], 0, 0, 0);
-    }
+    t_step_bf16<RB>(v, f.l1, acc);
   };
 
   // software pipeline, two groups per trip so the fetch registers are named statically;
@@ -216,19 +139,9 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_kernel(
     if (g < g_end) work(g, fa);
   }
 
-  // partial t tiles -> LDS: result row 4*(l/16)+i, column l%16 of block rb
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      red[(wave * 16 + 4 * chunk + i) * RANK + rb * 16 + row] = acc[rb][i];
+  store_t_partials<RB>(red, wave, lane, acc);
   __syncthreads();
-  for (int e = threadIdx.x; e < 16 * RANK; e += blockDim.x) {
-    const int i = e / RANK, j = e % RANK;
-    float sum = 0.0f;
-    for (int w = 0; w < nwaves; ++w) sum += red[(w * 16 + i) * RANK + j];
-    if (i < rows) t[static_cast<int64_t>(m0 + i) * RANK + j] = static_cast<uint16_t>(f32_to_bf16_rne(sum));
-  }
+  reduce_t<RANK>(red, nwaves, rows, t + static_cast<int64_t>(m0) * RANK, static_cast<float*>(nullptr));
 }
 
 // ---------------------------------------------------------------------------
@@ -238,34 +151,20 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_kernel(
 // them), so the workgroup of 16 tokens runs two phases:
 //
 //  1. t = bf16(sum_k bf16(x~_k) L1[k, :]) on the FP64 matrix cores
-//     (v_mfma_f64_16x16x4_f64): the products are exact in double and the
-//     double sum is within ~1e-13 of the exact one, far inside bf16's half
-//     ulp, so the single rounding to bf16 (f64_to_bf16_rne) gives the bf16 of
-//     the exact sum.  The lane layout is the plain kernel's: lane l feeds token
-//     l%16 and channels 16*(l/16) + s, one k-slot per lane group, 16 steps a
-//     group.  The per-wave partial tiles are summed in LDS in wave order.
-//  2. every wave walks its groups again.  The re-read, re-smoothed x~ is the C
-//     operand of r rank-1 updates on the FP32 matrix cores
-//     (v_mfma_f32_16x16x1_4b_f32, K = 1): step j adds L1[:, j] * (-t_j), an
-//     exact product, to C with one rounding, j ascending.  The A-operand
-//     lanes supply the group's channels in the order that puts channel
-//     16*(l/16) + v of token l%16 in result register v of lane l: the plain
-//     kernel's layout, so the quantizer runs unchanged.
+//     (t_step_f64): the products are exact in double and the double sum is
+//     within ~1e-13 of the exact one, far inside bf16's half ulp, so the
+//     single rounding to bf16 gives the bf16 of the exact sum.  The per-wave
+//     partial tiles are summed in LDS in wave order.
+//  2. every wave walks its groups again: the re-read, re-smoothed x~ goes
+//     through r rank-1 updates on the FP32 matrix cores (deflate_step), whose
+//     result is in the quantizer's lane layout.
 // ---------------------------------------------------------------------------
-template <int RANK>
-struct DeflFetch {
-  uint4 xa, xb;                 // 16 bf16 of x
-  uint32_t l1[RANK / 2];        // L1[a_ch][j], two bf16 per word (j even in the low half)
-};
-
 template <int RANK, bool INV_LDS>
 __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_deflated_kernel(
     const uint16_t* __restrict__ x, const float* __restrict__ inv_smooth,
     const uint16_t* __restrict__ L1t, uint8_t* __restrict__ xq, float* __restrict__ xs,
     uint16_t* __restrict__ t, int M, int K, int groups_per_wave) {
   constexpr int RB = RANK / 16;
-  typedef double v4d __attribute__((ext_vector_type(4)));
-  typedef float v16f_t __attribute__((ext_vector_type(16)));
   // dynamic LDS: [nwaves][16][RANK] double partial t | [16][RANK] float -t |
   // (INV_LDS) [nwaves][groups_per_wave * 64] 1/lambda
   extern __shared__ double red64[];
@@ -303,12 +202,7 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_deflated_
     const uint32_t go = static_cast<uint32_t>(g) * kGroup * 2u;
     f.xa = buf_load16(x_rsrc, x_off + go);
     f.xb = buf_load16(x_rsrc, x_off + go + 16u);
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      const uint16_t* lp = L1t + static_cast<int64_t>(rb * 16 + row) * K + g * kGroup + chunk * 16;
-      f.l1[rb][0] = *reinterpret_cast<const v8s*>(lp);
-      f.l1[rb][1] = *reinterpret_cast<const v8s*>(lp + 8);
-    }
+    load_l1_fragments<RB>(L1t, K, g * kGroup + chunk * 16, row, f.l1);
   };
   v4d acc[RB];
 #pragma unroll
@@ -316,17 +210,7 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_deflated_
   auto work1 = [&](int g, const ActFetch<RANK>& f) __attribute__((always_inline)) {
     float v[16];
     smooth16(f.xa, f.xb, inv_ptr(g), v);
-    // A: lane l = token l%16, k-slot l/16 -> channel 16*(l/16) + s; B: lane l =
-    // column l%16 of block rb, same k-slot
-#pragma unroll
-    for (int s = 0; s < 16; ++s) {
-      const double a = static_cast<double>(static_cast<float>(static_cast<__bf16>(v[s])));
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        const uint32_t lb = static_cast<uint16_t>(f.l1[rb][s >> 3][s & 7]);
-        acc[rb] = __builtin_amdgcn_mfma_f64_16x16x4f64(a, static_cast<double>(bf16_to_f32(lb)), acc[rb], 0, 0, 0);
-      }
-    }
+    t_step_f64<RB>(v, f.l1, acc);
   };
   if (g_begin < g_end) {
     ActFetch<RANK> fa, fb;
@@ -340,54 +224,24 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_deflated_
     }
     if (g < g_end) work1(g, fa);
   }
-  // partial tiles -> LDS: result register i of lane l is token l/16 + 4 i, column l%16
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      red64[(wave * 16 + chunk + 4 * i) * RANK + rb * 16 + row] = acc[rb][i];
+  store_t_partials<RB>(red64, wave, lane, acc);
   __syncthreads();
-  for (int e = threadIdx.x; e < 16 * RANK; e += blockDim.x) {
-    const int i = e / RANK, j = e % RANK;
-    double sum = 0.0;
-    for (int w = 0; w < nwaves; ++w) sum += red64[(w * 16 + i) * RANK + j];
-    const uint32_t b = f64_to_bf16_rne(sum);
-    if (i < rows) t[static_cast<int64_t>(m0 + i) * RANK + j] = static_cast<uint16_t>(b);
-    tneg[i * RANK + j] = -bf16_to_f32(b);
-  }
+  reduce_t<RANK>(red64, nwaves, rows, t + static_cast<int64_t>(m0) * RANK, tneg);
   __syncthreads();
 
   // ---- phase 2: deflate with r rank-1 updates, then quantize ----
-  // A-operand lane l supplies channel a_ch of the group: lane 16B + 4Q + I holds
-  // channel 16Q + 4B + I, which lands in result register 4B + I of the lanes
-  // with l/16 = Q
-  const int a_ch = 16 * ((lane >> 2) & 3) + 4 * (lane >> 4) + (lane & 3);
+  const int a_ch = deflate_channel(lane);
   auto fetch2 = [&](int g, DeflFetch<RANK>& f) __attribute__((always_inline)) {
     const uint32_t go = static_cast<uint32_t>(g) * kGroup * 2u;
     f.xa = buf_load16(x_rsrc, x_off + go);
     f.xb = buf_load16(x_rsrc, x_off + go + 16u);
-    const uint16_t* lp = L1t + g * kGroup + a_ch;
-#pragma unroll
-    for (int j = 0; j < RANK; j += 2)
-      f.l1[j / 2] = static_cast<uint32_t>(lp[j * K]) | (static_cast<uint32_t>(lp[(j + 1) * K]) << 16);
+    load_l1_column<RANK>(L1t, K, g * kGroup + a_ch, f.l1);
   };
   const float* tn_row = tneg + row * RANK;
   auto work2 = [&](int g, const DeflFetch<RANK>& f) __attribute__((always_inline)) {
     float v[16];
     smooth16(f.xa, f.xb, inv_ptr(g), v);
-    v16f_t c;
-#pragma unroll
-    for (int i = 0; i < 16; ++i) c[i] = v[i];
-#pragma unroll
-    for (int j = 0; j < RANK; j += 4) {
-      const float4 tv = *reinterpret_cast<const float4*>(tn_row + j);
-      c = __builtin_amdgcn_mfma_f32_16x16x1f32(__uint_as_float(f.l1[j / 2] << 16), tv.x, c, 0, 0, 0);
-      c = __builtin_amdgcn_mfma_f32_16x16x1f32(__uint_as_float(f.l1[j / 2] & 0xFFFF0000u), tv.y, c, 0, 0, 0);
-      c = __builtin_amdgcn_mfma_f32_16x16x1f32(__uint_as_float(f.l1[j / 2 + 1] << 16), tv.z, c, 0, 0, 0);
-      c = __builtin_amdgcn_mfma_f32_16x16x1f32(__uint_as_float(f.l1[j / 2 + 1] & 0xFFFF0000u), tv.w, c, 0, 0, 0);
-    }
-#pragma unroll
-    for (int i = 0; i < 16; ++i) v[i] = c[i];
+    deflate_step<RANK>(v, f.l1, tn_row);
     quantize_pack_store(v, q_rsrc, q_off + static_cast<uint32_t>(g) * (kGroup / 2),
                         row < rows ? xs + static_cast<int64_t>(g) * M + m0 + row : nullptr);
   };

@@ -1,0 +1,211 @@
+// Activation kernels with the block Hadamard rotation of Eq. 3:
+//     x~ = H diag(lambda)^-1 x,
+// H block-diagonal with Hadamard blocks of size B (the largest power of two
+// dividing K, at most 1024, App. B.1), applied online with the fast
+// Walsh-Hadamard transform (the weights were rotated offline).  The transform
+// runs in float32, one rounding per butterfly, stages on element bit 0, 1, ..
+// in that order, then one multiply by fl32(1/sqrt(B)).
+//
+// A block spans several groups, so a workgroup (16 tokens) works in tiles of
+// T channels (a multiple of B and of 64 dividing K, at most 1024):
+//   rotate:   pass p of a tile is 1024 consecutive elements of the [16][T]
+//             tile; lane l holds 16 consecutive channels of one token, so
+//             butterfly stages 0-3 run in registers and stages 4 .. log2(B)-1
+//             between lanes l and l ^ 2^(s-4).  The rotated tile goes to LDS
+//             (rows padded by 4 floats against bank conflicts).
+//   quantize: each wave reads its groups of the tile back in the lane layout
+//             of qwam_act.h and runs the plain kernel's per-group steps (or,
+//             deflated, the two phases of the deflated kernel, rotating the
+//             tiles again in phase 2).
+#include <cmath>
+#include <type_traits>
+
+#include "qwam_act.h"
+#include "qwam_device.h"
+#include "qwam_internal.h"
+
+namespace qwam {
+
+namespace {
+
+constexpr int kTilePad = 4;   // floats of padding per LDS tile row
+
+// Fast Walsh-Hadamard transform of a block of 2^logB elements held 16 per lane
+// (lane bit b <-> element bit 4 + b): v becomes v H_B, unnormalized.
+__device__ __forceinline__ void fwht16(float (&v)[16], int lane, int logB) {
+#pragma unroll
+  for (int h = 1; h < 16; h <<= 1)
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      if (!(i & h)) {
+        const float a = v[i], b = v[i + h];
+        v[i] = a + b;
+        v[i + h] = a - b;
+      }
+  for (int s = 4; s < logB; ++s) {
+    const int m = 1 << (s - 4);
+    const bool upper = (lane & m) != 0;   // this lane holds the element with bit s set
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const float p = __shfl_xor(v[i], m);
+      v[i] = upper ? p - v[i] : v[i] + p;
+    }
+  }
+}
+
+}  // namespace
+
+template <int RANK, bool DEFLATE>
+__global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_rotated_kernel(
+    const uint16_t* __restrict__ x, const float* __restrict__ inv_smooth,
+    const uint16_t* __restrict__ L1t, uint8_t* __restrict__ xq, float* __restrict__ xs,
+    uint16_t* __restrict__ t, int M, int K, int logB, int T, float hscale) {
+  constexpr int RB = RANK / 16;
+  using Acc = std::conditional_t<DEFLATE, double, float>;
+  // dynamic LDS: tile [16][T + pad] float | partial t [nwaves][16][RANK] Acc |
+  // (DEFLATE) -t [16][RANK] float
+  extern __shared__ double lds_raw[];
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int nwaves = blockDim.x >> 6;
+  const int row = lane & 15;
+  const int chunk = lane >> 4;
+  const int m0 = blockIdx.x * 16;
+  const int rows = min(16, M - m0);
+  const int TS = T + kTilePad;
+  const int ntiles = K / T;
+  const int npass = T / kGroup;          // 1024-element passes per tile = groups per tile
+
+  float* tile = reinterpret_cast<float*>(lds_raw);
+  Acc* red = reinterpret_cast<Acc*>(tile + 16 * TS);
+  float* tneg = reinterpret_cast<float*>(red + nwaves * 16 * RANK);
+
+  const buf_rsrc x_rsrc = make_rsrc(x + static_cast<int64_t>(m0) * K, static_cast<uint32_t>(rows) * K * 2u);
+  const buf_rsrc q_rsrc = make_rsrc(xq + static_cast<int64_t>(m0) * (K / 2), static_cast<uint32_t>(rows) * (K / 2));
+  const uint32_t q_off = static_cast<uint32_t>(row * (K / 2) + chunk * 8);
+
+  // smooth and rotate tile `tb` into LDS (tokens past M read as zero)
+  auto rotate_tile = [&](int tb) __attribute__((always_inline)) {
+    for (int p = wave; p < npass; p += nwaves) {
+      const int e = p * 1024 + 16 * lane;
+      const int tok = e / T, col = e % T;
+      const int ch = tb * T + col;
+      const uint32_t xo = static_cast<uint32_t>(tok * K + ch) * 2u;
+      const uint4 xa = buf_load16(x_rsrc, xo), xb = buf_load16(x_rsrc, xo + 16u);
+      float v[16];
+      smooth16(xa, xb, reinterpret_cast<const float4*>(inv_smooth + ch), v);
+      fwht16(v, lane, logB);
+      float4* dst = reinterpret_cast<float4*>(tile + tok * TS + col);
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        dst[q] = make_float4(v[4 * q] * hscale, v[4 * q + 1] * hscale, v[4 * q + 2] * hscale, v[4 * q + 3] * hscale);
+    }
+  };
+  auto read_group = [&](int gl, float (&v)[16]) __attribute__((always_inline)) {
+    const float4* src = reinterpret_cast<const float4*>(tile + row * TS + gl * kGroup + chunk * 16);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float4 f = src[q];
+      v[4 * q] = f.x; v[4 * q + 1] = f.y; v[4 * q + 2] = f.z; v[4 * q + 3] = f.w;
+    }
+  };
+  auto store_codes = [&](int g, const float (&v)[16]) __attribute__((always_inline)) {
+    quantize_pack_store(v, q_rsrc, q_off + static_cast<uint32_t>(g) * (kGroup / 2),
+                        row < rows ? xs + static_cast<int64_t>(g) * M + m0 + row : nullptr);
+  };
+
+  std::conditional_t<DEFLATE, v4d, v4f> acc[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) acc[rb] = {};
+
+  // pass over the tiles: t partials (and, without deflation, the codes)
+  for (int tb = 0; tb < ntiles; ++tb) {
+    rotate_tile(tb);
+    __syncthreads();
+    for (int gl = wave; gl < npass; gl += nwaves) {
+      const int g = tb * npass + gl;
+      v8s l1[RB][2];
+      load_l1_fragments<RB>(L1t, K, g * kGroup + chunk * 16, row, l1);
+      float v[16];
+      read_group(gl, v);
+      if constexpr (DEFLATE) {
+        t_step_f64<RB>(v, l1, acc);
+      } else {
+        store_codes(g, v);
+        t_step_bf16<RB>(v, l1, acc);
+      }
+    }
+    __syncthreads();
+  }
+  store_t_partials<RB>(red, wave, lane, acc);
+  __syncthreads();
+  reduce_t<RANK>(red, nwaves, rows, t + static_cast<int64_t>(m0) * RANK, DEFLATE ? tneg : nullptr);
+
+  if constexpr (DEFLATE) {
+    __syncthreads();
+    // second pass: rotate again, deflate, quantize
+    const int a_ch = deflate_channel(lane);
+    const float* tn_row = tneg + row * RANK;
+    for (int tb = 0; tb < ntiles; ++tb) {
+      rotate_tile(tb);
+      __syncthreads();
+      for (int gl = wave; gl < npass; gl += nwaves) {
+        const int g = tb * npass + gl;
+        uint32_t l1w[RANK / 2];
+        load_l1_column<RANK>(L1t, K, g * kGroup + a_ch, l1w);
+        float v[16];
+        read_group(gl, v);
+        deflate_step<RANK>(v, l1w, tn_row);
+        store_codes(g, v);
+      }
+      __syncthreads();
+    }
+  }
+}
+
+// Tile width: the largest multiple of max(B, 64) that divides K and is at
+// most 1024.
+static int rotate_tile_width(int K, int B) {
+  const int base = B > kGroup ? B : kGroup;
+  for (int c = 1024 / base; c > 1; --c)
+    if ((K / base) % c == 0) return base * c;
+  return base;
+}
+
+hipError_t launch_quantize_act_rotated(int M, int K, int r, int B, bool deflate, const uint16_t* x,
+                                       const float* inv_smooth, const uint16_t* L1t, uint8_t* xq, float* xs,
+                                       uint16_t* t, hipStream_t stream) {
+  int logB = 0;
+  while ((1 << logB) < B) ++logB;
+  if ((1 << logB) != B || B < 16 || B > 1024 || K % B != 0) return hipErrorInvalidValue;
+  const int T = rotate_tile_width(K, B);
+  const float hscale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(B)));
+  auto go = [&](auto kernel, int nwaves, size_t acc_bytes) {
+    const size_t lds = static_cast<size_t>(16) * (T + kTilePad) * sizeof(float) +
+                       static_cast<size_t>(nwaves) * 16 * r * acc_bytes + (deflate ? 16 * r * sizeof(float) : 0);
+    if (lds > 64 * 1024) {
+      const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+      if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(kernel, dim3((M + 15) / 16), dim3(64 * nwaves), lds, stream, x, inv_smooth, L1t, xq, xs, t,
+                       M, K, logB, T, hscale);
+    return hipGetLastError();
+  };
+#define QWAM_ROT_CASE(R)                                                                            \
+  case R:                                                                                           \
+    return deflate ? go(quantize_act_rotated_kernel<R, true>, act_waves<R>(), sizeof(double))       \
+                   : go(quantize_act_rotated_kernel<R, false>, act_waves<R>(), sizeof(float));
+  switch (r) {
+    QWAM_ROT_CASE(16)
+    QWAM_ROT_CASE(32)
+    QWAM_ROT_CASE(48)
+    QWAM_ROT_CASE(64)
+    default:
+      return hipErrorInvalidValue;
+  }
+#undef QWAM_ROT_CASE
+}
+
+}  // namespace qwam

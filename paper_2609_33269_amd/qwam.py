@@ -30,7 +30,7 @@ _c_void_p, _i32 = ctypes.c_void_p, ctypes.c_int32
 
 class QwamLayerC(ctypes.Structure):
     _fields_ = [("K", ctypes.c_int32), ("N", ctypes.c_int32), ("r", ctypes.c_int32),
-                ("group", ctypes.c_int32), ("wq", ctypes.c_void_p), ("ws", ctypes.c_void_p),
+                ("group", ctypes.c_int32), ("hadamard", ctypes.c_int32), ("wq", ctypes.c_void_p), ("ws", ctypes.c_void_p),
                 ("inv_smooth", ctypes.c_void_p), ("L1t", ctypes.c_void_p),
                 ("L2t", ctypes.c_void_p), ("bias", ctypes.c_void_p)]
 
@@ -111,11 +111,12 @@ class PackedLayer:
     L1t: torch.Tensor         # bf16 [r][K]
     L2t: torch.Tensor         # bf16 [N][r]
     bias: Optional[torch.Tensor] = None   # bf16 [N]
+    hadamard: int = 0                     # block size of the rotation (Eq. 3), 0 = none
 
     def c_struct(self) -> QwamLayerC:
         G = self.K // GROUP
         c = QwamLayerC()
-        c.K, c.N, c.r, c.group = self.K, self.N, self.r, GROUP
+        c.K, c.N, c.r, c.group, c.hadamard = self.K, self.N, self.r, GROUP, self.hadamard
         c.wq = _req(self.wq, "wq", torch.uint8, (self.N, self.K // 2))
         c.ws = _req(self.ws, "ws", torch.float32, (G, self.N))
         c.inv_smooth = _req(self.inv_smooth, "inv_smooth", torch.float32, (self.K,))
@@ -141,15 +142,16 @@ def pack_weights(R: torch.Tensor, smooth: torch.Tensor, stream=None):
 
 
 def make_layer(R: torch.Tensor, smooth: torch.Tensor, L1: torch.Tensor, L2: torch.Tensor,
-               bias: Optional[torch.Tensor] = None, stream=None) -> PackedLayer:
+               bias: Optional[torch.Tensor] = None, stream=None, hadamard: int = 0) -> PackedLayer:
     """Pack R and lambda and lay out the branch factors: L1 bf16 [K][r] and
-    L2 bf16 [r][N] are stored transposed (L1t [r][K], L2t [N][r])."""
+    L2 bf16 [r][N] are stored transposed (L1t [r][K], L2t [N][r]).  With
+    `hadamard` = B, R, L1 and L2 must be those of the rotated layer (Eq. 3)."""
     N, K = R.shape
     r = L1.shape[1]
     wq, ws, inv = pack_weights(R, smooth, stream)
     return PackedLayer(K=K, N=N, r=r, wq=wq, ws=ws, inv_smooth=inv,
                        L1t=L1.t().contiguous(), L2t=L2.t().contiguous(),
-                       bias=None if bias is None else bias.contiguous())
+                       bias=None if bias is None else bias.contiguous(), hadamard=hadamard)
 
 
 def quantize_act(layer: PackedLayer, x: torch.Tensor, stream=None, out=None):

@@ -33,10 +33,10 @@ def bits(t: torch.Tensor) -> np.ndarray:
     return t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
 
 
-def oracle_factors(draws, r=None):
+def oracle_factors(draws, r=None, hadamard=False):
     r = draws.shape.r if r is None else r
     V = O.protected_basis_from_factor(draws.a, r)
-    return O.build_layer(draws.x, draws.w, V)
+    return O.build_layer(draws.x, draws.w, V, hadamard=hadamard)
 
 
 def gpu_layer(factors, bias_bits=None) -> Q.PackedLayer:
@@ -44,7 +44,8 @@ def gpu_layer(factors, bias_bits=None) -> Q.PackedLayer:
     L1 = bf16_dev(factors["L1"])
     L2 = bf16_dev(factors["L2"])
     bias = None if bias_bits is None else bf16_dev(bias_bits)
-    return Q.make_layer(f32_dev(factors["R"]), f32_dev(factors["lam"]), L1, L2, bias)
+    return Q.make_layer(f32_dev(factors["R"]), f32_dev(factors["lam"]), L1, L2, bias,
+                        hadamard=int(factors.get("hadamard", 0)))
 
 
 def rel_fro(a: np.ndarray, b: np.ndarray) -> float:
@@ -52,6 +53,25 @@ def rel_fro(a: np.ndarray, b: np.ndarray) -> float:
     b = np.asarray(b, dtype=np.float64)
     nb = np.linalg.norm(b)
     return float(np.linalg.norm(a - b) / (nb if nb > 0 else 1.0))
+
+
+Y_TOL = 2e-3
+
+
+def y_tolerance(y_ref: np.ndarray) -> float:
+    """Relative Frobenius tolerance of y against the unrounded float64 oracle:
+    2e-3, unless the output is so small that its own bf16 rounding (the
+    correctly rounded bf16 of y_ref) is already further away; then that
+    rounding error plus 1e-4 for the float32 accumulation."""
+    return max(Y_TOL, rel_fro(O.round_to_bf16(y_ref), y_ref) + 1e-4)
+
+
+def check_y(y_gpu_bits: np.ndarray, y_ref: np.ndarray) -> float:
+    err = rel_fro(O.bf16_bits_to_f64(y_gpu_bits), y_ref)
+    tol = y_tolerance(y_ref)
+    log(f"    y rel Frobenius error {err:.3e} (tolerance {tol:.3e})")
+    assert err <= tol
+    return err
 
 
 def bf16_ulp(v: np.ndarray) -> np.ndarray:

@@ -38,13 +38,13 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == set(Q.SIGNATURES), "binding and header disagree"
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.qwam_abi_version() == 3
+    assert lib.qwam_abi_version() == 4
     assert lib.qwam_status_string(3) == b"QWAM_ERR_MISALIGNED"
 
 
-def _layer(K=256, N=256, r=16, group=64, **ptrs):
+def _layer(K=256, N=256, r=16, group=64, hadamard=0, **ptrs):
     c = Q.QwamLayerC()
-    c.K, c.N, c.r, c.group = K, N, r, group
+    c.K, c.N, c.r, c.group, c.hadamard = K, N, r, group, hadamard
     for f in ("wq", "ws", "inv_smooth", "L1t", "L2t"):
         setattr(c, f, ptrs.get(f, FAKE))
     c.bias = ptrs.get("bias", None)
@@ -110,6 +110,11 @@ def test_layer_calls_reject_bad_arguments(lib):
     assert _act(lib, _layer(**{"L1t": FAKE + 2}), deflated=True) == MISALIGNED
     assert _act(lib, _layer(), t=None, deflated=True) == INVALID
     assert lib.qwam_last_error().startswith(b"qwam_quantize_act_deflated")
+    # the rotation block: a power of two in [16, 1024] dividing K, or 0
+    for B in (8, 2048, 96, 512):        # too small, too large, not a power of two, does not divide K = 256
+        assert _act(lib, _layer(hadamard=B)) == INVALID
+        assert _act(lib, _layer(hadamard=B), deflated=True) == INVALID
+    assert b"hadamard" in lib.qwam_last_error()
     # partials: rank is not used, but shapes and pointers are checked
     assert lib.qwam_debug_group_partials(ctypes.byref(_layer(r=7)), 1, None, FAKE, None) == INVALID
 

@@ -14,12 +14,11 @@ from oracle import qwam_oracle as O
 from paper_2609_33269_amd import inputs as I
 from paper_2609_33269_amd import qwam as Q
 
-from parity_helpers import (bf16_dev, bits, check_t, f32_dev, gpu_layer, log, oracle_factors,
-                            rel_fro, run_gpu)
+from parity_helpers import (bf16_dev, bits, check_t, check_y, f32_dev, gpu_layer, log, oracle_factors,
+                            rel_fro, run_gpu, y_tolerance)
 
 pytestmark = pytest.mark.gpu
 
-Y_TOL = 2e-3
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -47,11 +46,7 @@ def _full_parity(draws, factors, bias_bits=None, check_partials=True):
         P = Q.debug_group_partials(layer, xq)
         torch.cuda.synchronize()
         assert (P.cpu().numpy() == ref["P"]).all(), "int32 group partials"
-    yg = O.bf16_bits_to_f64(bits(y))
-    err = rel_fro(yg, ref["y"])
-    log(f"    y rel Frobenius error {err:.3e}")
-    assert err <= Y_TOL
-    return err
+    return check_y(bits(y), ref["y"])
 
 
 @pytest.mark.parametrize("with_bias", [False, True])
@@ -145,7 +140,7 @@ def _large_parity(draws, n_rows=24):
     err = rel_fro(yg, y_ref)
     row_err = max(rel_fro(yg[i], y_ref[i]) for i in range(len(rows)))
     log(f"    y rel Frobenius error on {len(rows)} sampled tokens {err:.3e} (worst token {row_err:.3e})")
-    assert err <= Y_TOL
+    assert err <= y_tolerance(y_ref)
     P = Q.debug_group_partials(layer, xq[torch.from_numpy(rows).cuda()].contiguous())
     torch.cuda.synchronize()
     assert (P.cpu().numpy() == P_ref).all(), "int32 group partials of sampled tokens"

@@ -1,0 +1,143 @@
+"""GPU parity of the rotated activation path (Eq. 3, block Hadamard rotation
+applied online with the fast Walsh-Hadamard transform), with and without
+deflation (Eq. 8 / Eq. 9).
+
+Bit-exact: the rotated activation codes, packed bytes and scales (the float32
+transform follows the oracle's butterfly order), the int32 group partials, and
+with deflation also t.  Without deflation t is checked against its rounding
+bound (parity_helpers.check_t) on the rotated x~.  y within relative Frobenius
+error 2e-3 of the float64 oracle on the same codes.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import qwam_oracle as O
+from paper_2609_33269_amd import inputs as I
+from paper_2609_33269_amd import qwam as Q
+
+from parity_helpers import (bf16_dev, bits, check_t, check_y, gpu_layer, log, oracle_factors, rel_fro,
+                            run_gpu, y_tolerance)
+
+pytestmark = pytest.mark.gpu
+
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    Q.lib()
+
+
+def _rotated_parity(draws, factors, bias_bits=None, deflate=False, check_partials=True):
+    M, K, N = draws.shape.M, draws.shape.K, draws.shape.N
+    B = factors["hadamard"]
+    log(f"  rotated parity {draws.shape.name}: M={M} K={K} N={N} r={factors['L1'].shape[1]} B={B} "
+        f"deflate={deflate} bias={bias_bits is not None}")
+    ref = O.asp_linear(draws.x, factors, bias_bits=bias_bits, deflate=deflate)
+    layer = gpu_layer(factors, bias_bits)
+    assert layer.hadamard == B
+    x, xq, xs, t, y = run_gpu(layer, draws.x, deflate=deflate)
+    assert (xq.cpu().numpy() == ref["xq"]).all(), "packed rotated activation bytes"
+    assert (xs.cpu().numpy() == ref["sx"].T).all(), "rotated activation scales"
+    if deflate:
+        assert (bits(t) == ref["t"]).all(), "t (bf16 of the exact sum)"
+    else:
+        xt = O.transformed_activations(draws.x, ref["inv_lam"], B)
+        check_t(bits(t), ref["t"], xt, factors["L1"])
+    if check_partials:
+        P = Q.debug_group_partials(layer, xq)
+        torch.cuda.synchronize()
+        assert (P.cpu().numpy() == ref["P"]).all(), "int32 group partials"
+    check_y(bits(y), ref["y"])
+    return ref, (xq, xs, t, y)
+
+
+ROTATED_SHAPES = [
+    # M, K, N, r, bias          block B, tile width
+    (1, 64, 16, 16, False),     # B 64,  T 64
+    (15, 128, 48, 32, True),    # B 128, T 128
+    (17, 192, 144, 48, False),  # B 64,  T 192
+    (129, 256, 272, 64, True),  # B 256, T 256
+    (200, 320, 400, 32, False),  # B 64, T 320
+    (130, 1024, 1040, 16, True),  # B 1024, T 1024
+    (40, 640, 96, 32, False),   # B 128, T 640
+    (33, 3072, 64, 32, True),   # B 1024, three tiles
+    (20, 16448, 32, 64, False),  # B 64, T 64, 257 tiles
+]
+
+
+@pytest.mark.parametrize("deflate", [False, True])
+@pytest.mark.parametrize("M,K,N,r,bias", ROTATED_SHAPES)
+def test_rotated_shapes(M, K, N, r, bias, deflate):
+    d = I.custom(M=M, K=K, N=N, r=r, seed=M * 13 + K, n_outliers=max(1, K // 100), with_bias=bias)
+    _rotated_parity(d, oracle_factors(d, r, hadamard=True), d.bias, deflate=deflate)
+
+
+def test_rotated_one_hot_closed_form():
+    """x = e_k (lambda = 1, B = 1024): the rotated token is +-2^-5 on the whole
+    block, so every code of that block is +-7 with the sign of row k of H and
+    every scale is fl32(2^-5 / 7); the other block is zero."""
+    M, K, N, r = 4, 2048, 32, 16
+    ks = [3, 1024 + 77, 700, 2047]
+    xf = np.zeros((M, K))
+    for m, k in enumerate(ks):
+        xf[m, k] = 1.0
+    xb = O.f64_to_bf16_bits(xf)
+    L1b = O.f64_to_bf16_bits(np.eye(K)[:, :r])
+    layer = Q.make_layer(torch.zeros((N, K), dtype=torch.float32, device="cuda:0"),
+                         torch.ones(K, dtype=torch.float32, device="cuda:0"), bf16_dev(L1b),
+                         bf16_dev(np.zeros((r, N), dtype=np.uint16)), hadamard=1024)
+    xq, xs, t = Q.quantize_act(layer, bf16_dev(xb))
+    torch.cuda.synchronize()
+    codes = O.unpack_codes(xq.cpu().numpy())
+    scales = xs.cpu().numpy().T
+    s7 = np.float32(np.float32(2.0 ** -5) / np.float32(7.0))
+    j = np.arange(1024)
+    for m, k in enumerate(ks):
+        blk, kk = divmod(k, 1024)
+        signs = np.array([(-1) ** bin(int(v) & kk).count("1") for v in j])
+        assert (codes[m, blk * 1024:(blk + 1) * 1024] == 7 * signs).all()
+        assert not np.delete(codes[m], np.arange(blk * 1024, (blk + 1) * 1024)).any()
+        assert (scales[m, blk * 16:(blk + 1) * 16] == s7).all()
+
+
+@pytest.mark.parametrize("deflate", [False, True])
+def test_rotated_full_size(deflate):
+    """The FFN up-projection at full size (B = 1024, three tiles per token
+    row): every code and scale compared (and t with deflation); y and the
+    partials on sampled tokens."""
+    draws = I.video_dit_ffn_up()
+    M, K, N = draws.shape.M, draws.shape.K, draws.shape.N
+    log(f"  rotated full size {draws.shape.name} deflate={deflate}")
+    f = oracle_factors(draws, hadamard=True)
+    wq, sw, inv_lam, _ = O.pack_weights(f["R"], f["lam"])
+    layer = gpu_layer(f)
+    x, xq, xs, t, y = run_gpu(layer, draws.x, deflate=deflate)
+    quant = O.quantize_activations_deflated if deflate else O.quantize_activations
+    xq_ref, sx_ref, t_ref, _, xt = quant(draws.x, inv_lam, f["L1"], f["hadamard"])
+    assert (xq.cpu().numpy() == xq_ref).all(), "packed rotated activation bytes"
+    assert (xs.cpu().numpy() == sx_ref.T).all(), "rotated activation scales"
+    if deflate:
+        assert (bits(t) == t_ref).all(), "t"
+    else:
+        check_t(bits(t), t_ref, O.transformed_activations(draws.x, inv_lam, f["hadamard"]), f["L1"])
+    rng = np.random.default_rng(M + 7)
+    rows = np.array(sorted(set([0, M - 1]) | set(int(v) for v in rng.choice(M, 16, replace=False))))
+    y_ref, P_ref = O.asp_output_rows(xq_ref[rows], sx_ref[rows], t_ref[rows], wq, sw, f["L2"])
+    sel = torch.from_numpy(rows).cuda()
+    err = rel_fro(O.bf16_bits_to_f64(bits(y[sel])), y_ref)
+    log(f"    y rel Frobenius error on {len(rows)} sampled tokens {err:.3e}")
+    assert err <= y_tolerance(y_ref)
+    P = Q.debug_group_partials(layer, xq[sel].contiguous())
+    torch.cuda.synchronize()
+    assert (P.cpu().numpy() == P_ref).all(), "int32 group partials of sampled tokens"
+    del x, xq, xs, t, y, P, layer
+    torch.cuda.empty_cache()
+
+
+def test_rotated_action_expert_layer():
+    d = I.action_expert(32, 4096)
+    _rotated_parity(d, oracle_factors(d, hadamard=True))
