@@ -30,6 +30,11 @@ Secondary measurement (not the headline line):
       (Eq. 8 / Eq. 9: the 4-bit path quantizes x~ - L1 t), i.e. with
       qwam_quantize_act_deflated as the activation kernel; its roofline is the
       FP64 + FP32 matrix-core work of t and of the r rank-1 updates.
+  python bench.py --rotated [--deflated]
+      the same layer with the block Hadamard rotation of Eq. 3 (B = 1024,
+      applied online to the activation by the fast Walsh-Hadamard transform;
+      the weights rotated offline), optionally with deflation as well: the
+      paper's full deployed layer (smoothing, rotation, protected subspace).
   python bench.py --small-m
       the action-expert layers (M in {16, 32, 64}, K = 1024, N in {4096, 1024},
       r = 16): per-call latency of both kernels and algorithmic HBM GB/s, one
@@ -306,7 +311,7 @@ def deflated_act_roofline(k1_ms: float):
             "ideal_us": round(ideal_s * 1e6, 2), "flops": 2.0 * flops}
 
 
-def cpu_baseline(draws, seconds: float = 12.0, deflate: bool = False):
+def cpu_baseline(draws, seconds: float = 12.0, deflate: bool = False, rotate: bool = False):
     """The CPU oracle as it stands, timed on a bounded token sample of the same
     layer (weights packed beforehand, as on the GPU)."""
     from oracle import qwam_oracle as O
@@ -316,7 +321,7 @@ def cpu_baseline(draws, seconds: float = 12.0, deflate: bool = False):
     except Exception:   # pragma: no cover
         threads = 1
     V = O.protected_basis_from_factor(draws.a, R_RANK)
-    f = O.build_layer(draws.x, draws.w, V)
+    f = O.build_layer(draws.x, draws.w, V, hadamard=rotate)
     wq, sw, inv_lam, qw = O.pack_weights(f["R"], f["lam"])
     chunk = 32
     done = 0
@@ -324,7 +329,7 @@ def cpu_baseline(draws, seconds: float = 12.0, deflate: bool = False):
     while done + chunk <= M:
         rows = slice(done, done + chunk)
         quant = O.quantize_activations_deflated if deflate else O.quantize_activations
-        xq, sx, t, qx, _ = quant(draws.x[rows], inv_lam, f["L1"])
+        xq, sx, t, qx, _ = quant(draws.x[rows], inv_lam, f["L1"], f["hadamard"])
         P = O.group_partials(qx, qw)
         O.asp_output(sx, sw, P, t, f["L2"])
         done += chunk
@@ -334,7 +339,7 @@ def cpu_baseline(draws, seconds: float = 12.0, deflate: bool = False):
     return {"value": 2.0 * done * K * N / dt / 1e12, "unit": "TOPS", "cores": int(threads),
             "kind": "oracle",
             "sample": f"{done} of {M} tokens (chunks of {chunk}) of the {M}x{K}x{N} r{R_RANK} layer"
-                      f"{' with deflation' if deflate else ''}, "
+                      f"{' with rotation' if rotate else ''}{' with deflation' if deflate else ''}, "
                       f"weights packed beforehand; {dt:.1f} s; value = 2*tokens*K*N/time"}
 
 
@@ -352,6 +357,8 @@ def main():
     ap.add_argument("--copy-mib", type=int, default=256, help="copy-probe size the counters were taken with")
     ap.add_argument("--deflated", action="store_true",
                     help="the same layer with the deflated activation kernel (Eq. 8 / Eq. 9)")
+    ap.add_argument("--rotated", action="store_true",
+                    help="the same layer with the block Hadamard rotation (Eq. 3) on both operands")
     ap.add_argument("--small-m", action="store_true", help="report the action-expert layers instead")
     ap.add_argument("--denoise-step", action="store_true", help="report one 120-layer denoising step instead")
     args = ap.parse_args()
@@ -385,8 +392,8 @@ def main():
     x0 = torch.from_numpy(draws.x.view(np.int16)).view(torch.bfloat16).to(dev)
     w0 = torch.from_numpy(draws.w.view(np.int16)).view(torch.bfloat16).to(dev)
     V = calib.protected_basis(torch.from_numpy(draws.a), R_RANK)
-    f = calib.build_layer(x0, w0, V)
-    layer0 = qwam.make_layer(f["R"], f["lam"], f["L1"], f["L2"])
+    f = calib.build_layer(x0, w0, V, hadamard=args.rotated)
+    layer0 = qwam.make_layer(f["R"], f["lam"], f["L1"], f["L2"], hadamard=f["hadamard"])
     del f, w0
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
@@ -396,7 +403,8 @@ def main():
     for i in range(nrot):
         L = layer0 if i == 0 else qwam.PackedLayer(
             K=K, N=N, r=R_RANK, wq=layer0.wq.clone(), ws=layer0.ws.clone(),
-            inv_smooth=layer0.inv_smooth.clone(), L1t=layer0.L1t.clone(), L2t=layer0.L2t.clone())
+            inv_smooth=layer0.inv_smooth.clone(), L1t=layer0.L1t.clone(), L2t=layer0.L2t.clone(),
+            hadamard=layer0.hadamard)
         layers.append(L)
         xins.append(x0 if i == 0 else x0.clone())
         outs.append((torch.empty((M, K // 2), dtype=torch.uint8, device=dev),
@@ -468,6 +476,7 @@ def main():
         del src_t, dst_t
 
     traffic = measured_traffic()
+    act_name = ("quantize_act_rotated" if args.rotated else "quantize_act") + ("_deflated" if args.deflated else "")
     out = {
         "metric": METRIC,
         "value": round(eff_tops, 2),
@@ -481,15 +490,15 @@ def main():
         "vs_baseline": None,
         "dtype": "int4 codes on fp8-e4m3 MFMA (exact), f32 scale/accumulate, bf16 out",
         "data": "synthetic",
-        "config": {"workload": "video_dit_ffn_up_deflated" if args.deflated else "video_dit_ffn_up", "M": M, "K": K, "N": N, "r": R_RANK, "group": GROUP,
+        "config": {"workload": "video_dit_ffn_up" + ("_rotated" if args.rotated else "")
+                   + ("_deflated" if args.deflated else ""), "M": M, "K": K, "N": N, "r": R_RANK, "group": GROUP,
                    "act": "N(0,1), 1% channels x U_log(10,50)", "weights": "N(0,1/K)",
                    "rotated_buffer_sets": nrot},
         "roofline": {"bound": "mfma", "kernel": GEMM_KERNEL, "achieved": round(k2_tops, 1),
                      "peak": MFMA_PEAK, "unit": "TFLOP/s", "frac": round(k2_tops / MFMA_PEAK, 4),
                      "traffic": traffic, "algorithmic_bytes": gemm_bytes},
         "layer_frac_int8_peak": round(eff_tops / MFMA_PEAK, 4),
-        "kernels_us": {("quantize_act_deflated" if args.deflated else "quantize_act"): round(k1_ms * 1e3, 2),
-                       "asp_gemm": round(k2_ms * 1e3, 2)},
+        "kernels_us": {act_name: round(k1_ms * 1e3, 2), "asp_gemm": round(k2_ms * 1e3, 2)},
         "quantize_act_roofline": {"bound": "hbm", "achieved": round(k1_gbs, 1), "peak": HBM_PEAK_GBS,
                                   "unit": "GB/s", "frac": round(k1_gbs / HBM_PEAK_GBS, 4),
                                   "algorithmic_bytes": act_bytes},
@@ -501,10 +510,16 @@ def main():
         "speedup_vs_bf16_linear": round(bf16_ms / ms_step, 3),
     }
     if args.deflated:
-        out["quantize_act_deflated_roofline"] = deflated_act_roofline(k1_ms)
+        out[act_name + "_roofline"] = deflated_act_roofline(k1_ms)
+    if args.rotated:
+        # the transform's own work: log2(B) float32 additions per element, on the
+        # non-packed VALU (16 lanes per SIMD per clock, 1024 SIMDs, 2.4 GHz)
+        adds = float(M) * K * 10
+        out["fwht_adds"] = adds
+        out["fwht_valu_us"] = round(adds / (1024 * 16 * 2.4e9) * 1e6, 2)
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a token sample", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(draws, args.cpu_seconds, deflate=args.deflated)
+        out["cpu_baseline"] = cpu_baseline(draws, args.cpu_seconds, deflate=args.deflated, rotate=args.rotated)
     print(json.dumps(out), flush=True)
 
 

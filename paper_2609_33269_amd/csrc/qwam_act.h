@@ -38,6 +38,18 @@ __device__ __forceinline__ void smooth16(const uint4& xa, const uint4& xb, const
   }
 }
 
+// The same with the 16 entries of 1/lambda already in registers.
+__device__ __forceinline__ void smooth16_regs(const uint4& xa, const uint4& xb, const float4 (&iv4)[4], float (&v)[16]) {
+  const uint32_t xw[8] = {xa.x, xa.y, xa.z, xa.w, xb.x, xb.y, xb.z, xb.w};
+  const float iv[16] = {iv4[0].x, iv4[0].y, iv4[0].z, iv4[0].w, iv4[1].x, iv4[1].y, iv4[1].z, iv4[1].w,
+                        iv4[2].x, iv4[2].y, iv4[2].z, iv4[2].w, iv4[3].x, iv4[3].y, iv4[3].z, iv4[3].w};
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    v[2 * j] = __uint_as_float(xw[j] << 16) * iv[2 * j];
+    v[2 * j + 1] = __uint_as_float(xw[j] & 0xFFFF0000u) * iv[2 * j + 1];
+  }
+}
+
 // Quantizes one token's group, held by the four lanes l, l^16, l^32, l^48 (16
 // consecutive channels each, Eq. 2), and stores the lane's two code words at
 // byte q_off of q_rsrc and, if xs_dst is not null, the group's scale.

@@ -55,12 +55,28 @@ __device__ __forceinline__ void fwht16(float (&v)[16], int lane, int logB) {
 
 }  // namespace
 
+// Registers of one rotation pass: 16 bf16 of x and the matching 1/lambda.
+struct RotFetch {
+  uint4 xa, xb;
+  float4 inv[4];
+};
+
+// Rotation passes (= groups) of a tile per wave: a tile of at most 1024
+// channels has at most 16, spread over act_waves<RANK>() waves.
+template <int RANK>
+constexpr int per_wave() { return 16 / act_waves<RANK>(); }
+
+// Barrier for LDS hand-offs between the waves: waits for this wave's LDS
+// operations only, so prefetched global loads stay in flight across it.
+__device__ __forceinline__ void lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 template <int RANK, bool DEFLATE>
 __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_rotated_kernel(
     const uint16_t* __restrict__ x, const float* __restrict__ inv_smooth,
     const uint16_t* __restrict__ L1t, uint8_t* __restrict__ xq, float* __restrict__ xs,
     uint16_t* __restrict__ t, int M, int K, int logB, int T, float hscale) {
   constexpr int RB = RANK / 16;
+  constexpr int kMaxPerWave = per_wave<RANK>();
   using Acc = std::conditional_t<DEFLATE, double, float>;
   // dynamic LDS: tile [16][T + pad] float | partial t [nwaves][16][RANK] Acc |
   // (DEFLATE) -t [16][RANK] float
@@ -85,21 +101,38 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_rotated_k
   const buf_rsrc q_rsrc = make_rsrc(xq + static_cast<int64_t>(m0) * (K / 2), static_cast<uint32_t>(rows) * (K / 2));
   const uint32_t q_off = static_cast<uint32_t>(row * (K / 2) + chunk * 8);
 
-  // smooth and rotate tile `tb` into LDS (tokens past M read as zero)
-  auto rotate_tile = [&](int tb) __attribute__((always_inline)) {
-    for (int p = wave; p < npass; p += nwaves) {
-      const int e = p * 1024 + 16 * lane;
-      const int tok = e / T, col = e % T;
-      const int ch = tb * T + col;
-      const uint32_t xo = static_cast<uint32_t>(tok * K + ch) * 2u;
-      const uint4 xa = buf_load16(x_rsrc, xo), xb = buf_load16(x_rsrc, xo + 16u);
-      float v[16];
-      smooth16(xa, xb, reinterpret_cast<const float4*>(inv_smooth + ch), v);
-      fwht16(v, lane, logB);
-      float4* dst = reinterpret_cast<float4*>(tile + tok * TS + col);
+  // pass k of this wave in a tile covers elements (wave + k nwaves) * 1024 + 16 lane .. +15
+  auto fetch_tile = [&](int tb, RotFetch (&rf)[kMaxPerWave]) __attribute__((always_inline)) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        dst[q] = make_float4(v[4 * q] * hscale, v[4 * q + 1] * hscale, v[4 * q + 2] * hscale, v[4 * q + 3] * hscale);
+    for (int k = 0; k < kMaxPerWave; ++k) {
+      const int p = wave + k * nwaves;
+      if (p < npass) {
+        const int e = p * 1024 + 16 * lane;
+        const int ch = tb * T + e % T;
+        const uint32_t xo = static_cast<uint32_t>((e / T) * K + ch) * 2u;
+        rf[k].xa = buf_load16(x_rsrc, xo);
+        rf[k].xb = buf_load16(x_rsrc, xo + 16u);
+        const float4* ip = reinterpret_cast<const float4*>(inv_smooth + ch);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) rf[k].inv[q] = ip[q];
+      }
+    }
+  };
+  // smooth, transform and scale the fetched passes into the LDS tile (tokens past M are zero)
+  auto rotate_tile = [&](const RotFetch (&rf)[kMaxPerWave]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int k = 0; k < kMaxPerWave; ++k) {
+      const int p = wave + k * nwaves;
+      if (p < npass) {
+        const int e = p * 1024 + 16 * lane;
+        float v[16];
+        smooth16_regs(rf[k].xa, rf[k].xb, rf[k].inv, v);
+        fwht16(v, lane, logB);
+        float4* dst = reinterpret_cast<float4*>(tile + (e / T) * TS + e % T);
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          dst[q] = make_float4(v[4 * q] * hscale, v[4 * q + 1] * hscale, v[4 * q + 2] * hscale, v[4 * q + 3] * hscale);
+      }
     }
   };
   auto read_group = [&](int gl, float (&v)[16]) __attribute__((always_inline)) {
@@ -119,47 +152,67 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_rotated_k
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) acc[rb] = {};
 
-  // pass over the tiles: t partials (and, without deflation, the codes)
+  // pass over the tiles: t partials (and, without deflation, the codes).  The
+  // next tile's x and 1/lambda are requested as soon as this tile's are in LDS.
+  RotFetch rf[kMaxPerWave];
+  fetch_tile(0, rf);
   for (int tb = 0; tb < ntiles; ++tb) {
-    rotate_tile(tb);
-    __syncthreads();
-    for (int gl = wave; gl < npass; gl += nwaves) {
-      const int g = tb * npass + gl;
-      v8s l1[RB][2];
-      load_l1_fragments<RB>(L1t, K, g * kGroup + chunk * 16, row, l1);
-      float v[16];
-      read_group(gl, v);
-      if constexpr (DEFLATE) {
-        t_step_f64<RB>(v, l1, acc);
-      } else {
-        store_codes(g, v);
-        t_step_bf16<RB>(v, l1, acc);
+    rotate_tile(rf);
+    if (tb + 1 < ntiles) fetch_tile(tb + 1, rf);
+    v8s l1[kMaxPerWave][RB][2];
+#pragma unroll
+    for (int k = 0; k < kMaxPerWave; ++k) {
+      const int gl = wave + k * nwaves;
+      if (gl < npass) load_l1_fragments<RB>(L1t, K, (tb * npass + gl) * kGroup + chunk * 16, row, l1[k]);
+    }
+    lds_sync();
+#pragma unroll
+    for (int k = 0; k < kMaxPerWave; ++k) {
+      const int gl = wave + k * nwaves;
+      if (gl < npass) {
+        float v[16];
+        read_group(gl, v);
+        if constexpr (DEFLATE) {
+          t_step_f64<RB>(v, l1[k], acc);
+        } else {
+          store_codes(tb * npass + gl, v);
+          t_step_bf16<RB>(v, l1[k], acc);
+        }
       }
     }
-    __syncthreads();
+    lds_sync();
   }
+  if constexpr (DEFLATE) fetch_tile(0, rf);     // the second pass starts over
   store_t_partials<RB>(red, wave, lane, acc);
-  __syncthreads();
+  lds_sync();
   reduce_t<RANK>(red, nwaves, rows, t + static_cast<int64_t>(m0) * RANK, DEFLATE ? tneg : nullptr);
 
   if constexpr (DEFLATE) {
-    __syncthreads();
+    lds_sync();
     // second pass: rotate again, deflate, quantize
     const int a_ch = deflate_channel(lane);
     const float* tn_row = tneg + row * RANK;
     for (int tb = 0; tb < ntiles; ++tb) {
-      rotate_tile(tb);
-      __syncthreads();
-      for (int gl = wave; gl < npass; gl += nwaves) {
-        const int g = tb * npass + gl;
-        uint32_t l1w[RANK / 2];
-        load_l1_column<RANK>(L1t, K, g * kGroup + a_ch, l1w);
-        float v[16];
-        read_group(gl, v);
-        deflate_step<RANK>(v, l1w, tn_row);
-        store_codes(g, v);
+      rotate_tile(rf);
+      if (tb + 1 < ntiles) fetch_tile(tb + 1, rf);
+      uint32_t l1w[kMaxPerWave][RANK / 2];
+#pragma unroll
+      for (int k = 0; k < kMaxPerWave; ++k) {
+        const int gl = wave + k * nwaves;
+        if (gl < npass) load_l1_column<RANK>(L1t, K, (tb * npass + gl) * kGroup + a_ch, l1w[k]);
       }
-      __syncthreads();
+      lds_sync();
+#pragma unroll
+      for (int k = 0; k < kMaxPerWave; ++k) {
+        const int gl = wave + k * nwaves;
+        if (gl < npass) {
+          float v[16];
+          read_group(gl, v);
+          deflate_step<RANK>(v, l1w[k], tn_row);
+          store_codes(tb * npass + gl, v);
+        }
+      }
+      lds_sync();
     }
   }
 }
@@ -180,6 +233,8 @@ hipError_t launch_quantize_act_rotated(int M, int K, int r, int B, bool deflate,
   while ((1 << logB) < B) ++logB;
   if ((1 << logB) != B || B < 16 || B > 1024 || K % B != 0) return hipErrorInvalidValue;
   const int T = rotate_tile_width(K, B);
+  // a tile has at most 16 passes / groups: per_wave<r>() per wave
+  if (T / kGroup > 16) return hipErrorInvalidValue;
   const float hscale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(B)));
   auto go = [&](auto kernel, int nwaves, size_t acc_bytes) {
     const size_t lds = static_cast<size_t>(16) * (T + kTilePad) * sizeof(float) +
