@@ -556,3 +556,43 @@ def bits_per_weight(K: int, N: int, r: int, group: int = GROUP, scale_bits: int 
     smoothing reciprocal, divided by the K*N weights it replaces."""
     total = 4 * K * N + scale_bits * (K // group) * N + branch_bits * r * (K + N) + smooth_bits * K
     return total / (K * N)
+
+
+# ----------------------------------------------------------------------------
+# The Action Observability Gramian (AOG) estimate (Sec. 4.1, App. A probe
+# estimator): accumulation of probe vector-Jacobian products, the rotated AOG
+# of Sec. 4.2 and the action mass of Sec. 4.3
+# ----------------------------------------------------------------------------
+
+
+def aog_accumulate(A: np.ndarray, gT_bits: np.ndarray) -> np.ndarray:
+    """A + sum_i g_i g_i^T over the n vectors g_i, float64.
+
+    The procedure of the probe estimator adds g g^T to a d x d accumulator
+    for every probe VJP g = J^T u.  gT_bits: bf16 bits [d][n] (column i is
+    g_i); A: [d][d].  Products of two bf16 values are exact in float64."""
+    g = bf16_bits_to_f64(gT_bits)
+    return np.asarray(A, dtype=np.float64) + g @ g.T
+
+
+def aog_estimate(A: np.ndarray, n_inputs: int, n_probes: int) -> np.ndarray:
+    """G^ = A / (N P): the unbiased probe estimate of Eq. (AOG estimate)."""
+    return np.asarray(A, dtype=np.float64) / float(n_inputs * n_probes)
+
+
+def rotated_aog(G: np.ndarray, lam: np.ndarray, B: int = 0) -> np.ndarray:
+    """The AOG in the quantizer's coordinates (Sec. 4.2): an error delta of
+    x~ = H diag(lam)^-1 x moves x by diag(lam) H delta, so
+    G~ = H diag(lam) G diag(lam) H (H the orthonormal block Hadamard matrix of
+    block B, or the identity for B = 0).  float64."""
+    lam = np.asarray(lam, dtype=np.float64)
+    X = lam[:, None] * np.asarray(G, dtype=np.float64) * lam[None, :]
+    if B:
+        X = rotate_exact(X, B)            # X H (H symmetric)
+        X = rotate_exact(X.T, B).T        # H (X H)
+    return X
+
+
+def action_mass(G_tilde_list) -> float:
+    """mu_E = sum over the layers of an expert of tr G~ (Eq. action mass)."""
+    return float(sum(np.trace(np.asarray(G, dtype=np.float64)) for G in G_tilde_list))

@@ -656,3 +656,76 @@ def test_rotation_spreads_outliers_and_helps_4bit():
     out = O.asp_linear(d.x, rot)
     yb = O.asp_output_bruteforce(out["qx"], out["sx"], out["qw"], out["sw"], out["t"], rot["L2"])
     assert np.allclose(out["y"], yb, rtol=0, atol=1e-12 * np.abs(yb).max())
+
+
+# --------------------------------------------------------------------------
+# AOG estimate (Sec. 4.1, the probe estimator's procedure), rotated AOG
+# (Sec. 4.2), action mass (Sec. 4.3)
+# --------------------------------------------------------------------------
+
+def test_aog_accumulate_bruteforce_outer_products():
+    """The accumulator equals adding the outer products one vector at a time
+    (exact integers: small bf16 integers make every sum exact)."""
+    rng = np.random.default_rng(61)
+    d, n = 24, 40
+    g = rng.integers(-20, 21, size=(d, n)).astype(np.float64)
+    A0 = rng.integers(-50, 51, size=(d, d)).astype(np.float64)
+    A0 = A0 + A0.T
+    out = O.aog_accumulate(A0, O.f64_to_bf16_bits(g))
+    ref = A0.copy()
+    for i in range(n):
+        for a in range(d):
+            for b in range(d):
+                ref[a, b] += g[a, i] * g[b, i]
+    assert (out == ref).all()
+    assert (out == out.T).all()
+
+
+def test_unit_vector_probes_give_the_exact_gram_matrix():
+    """Probing with the m unit vectors e_k gives sum_k (J^T e_k)(J^T e_k)^T =
+    J^T J exactly (the exact computation the estimator replaces)."""
+    rng = np.random.default_rng(62)
+    m, d = 6, 10
+    J = rng.integers(-8, 9, size=(m, d)).astype(np.float64)
+    vjps = np.stack([J.T @ np.eye(m)[:, k] for k in range(m)], axis=1)     # [d][m]
+    A = O.aog_accumulate(np.zeros((d, d)), O.f64_to_bf16_bits(vjps))
+    assert (A == J.T @ J).all()
+
+
+def test_gaussian_probe_estimate_is_unbiased():
+    """E[u u^T] = I, so the probe average converges to J^T J: with 40000
+    Gaussian probes the relative Frobenius error is within a few times the
+    predicted standard deviation sqrt((||J^T J||_F^2 + tr(J^T J)^2) / (NP ||J^T J||_F^2))."""
+    rng = np.random.default_rng(63)
+    m, d, NP = 8, 12, 40000
+    J = rng.standard_normal((m, d))
+    U = rng.standard_normal((m, NP))
+    vjps = J.T @ U                                   # [d][NP], float64 (not rounded)
+    G = (vjps @ vjps.T) / NP
+    exact = J.T @ J
+    err = np.linalg.norm(G - exact) / np.linalg.norm(exact)
+    sd = np.sqrt((np.linalg.norm(exact) ** 2 + np.trace(exact) ** 2) / (NP * np.linalg.norm(exact) ** 2))
+    assert err < 4 * sd
+    assert O.aog_estimate(np.eye(3) * 6, 2, 3)[0, 0] == 1.0
+
+
+def test_rotated_aog_identities():
+    """Sec. 4.2: delta^T G~ delta equals (diag(lam) H delta)^T G (diag(lam) H delta);
+    H is orthonormal, so G~ and diag(lam) G diag(lam) share their spectrum and
+    trace; without rotation and with lam = 1, G~ = G."""
+    rng = np.random.default_rng(64)
+    d = 256
+    Z = rng.standard_normal((d, 40))
+    G = Z @ Z.T
+    lam = np.exp(rng.uniform(-1, 1, d))
+    Gt = O.rotated_aog(G, lam, 64)
+    H = np.kron(np.eye(d // 64), O.sylvester_hadamard(64) / 8.0)
+    for _ in range(5):
+        delta = rng.standard_normal(d)
+        dx = lam * (H @ delta)
+        assert np.isclose(delta @ Gt @ delta, dx @ G @ dx, rtol=1e-10)
+    DGD = lam[:, None] * G * lam[None, :]
+    assert np.isclose(np.trace(Gt), np.trace(DGD), rtol=1e-12)
+    assert np.allclose(np.linalg.eigvalsh(Gt), np.linalg.eigvalsh(DGD), rtol=0, atol=1e-9 * np.abs(DGD).max())
+    assert np.allclose(O.rotated_aog(G, np.ones(d), 0), G, rtol=0, atol=0)
+    assert O.action_mass([Gt, DGD]) == pytest.approx(2 * np.trace(DGD), rel=1e-12)
