@@ -35,6 +35,10 @@ Secondary measurement (not the headline line):
       applied online to the activation by the fast Walsh-Hadamard transform;
       the weights rotated offline), optionally with deflation as well: the
       paper's full deployed layer (smoothing, rotation, protected subspace).
+  python bench.py --aog
+      the AOG accumulation (Sec. 4.1, probe estimator): A [4096][4096] float32
+      += gT gT^T for a batch of 4096 bf16 probe VJPs, the SYRK on the bf16
+      matrix cores; one JSON line with its roofline and the oracle beside it.
   python bench.py --small-m
       the action-expert layers (M in {16, 32, 64}, K = 1024, N in {4096, 1024},
       r = 16): per-call latency of both kernels and algorithmic HBM GB/s, one
@@ -65,6 +69,7 @@ sys.path.insert(0, ROOT)
 M, K, N, R_RANK, GROUP = 4096, 3072, 14336, 32, 64
 G = K // GROUP
 MFMA_PEAK = 5000.0             # MI355X dense FP8 (= dense INT8) matrix peak, TFLOP/s (TOP/s)
+BF16_MFMA_PEAK = 2500.0        # MI355X dense bf16 matrix peak, TFLOP/s
 FP64_MFMA_PEAK = 78.6          # MI355X dense FP64 matrix peak, TFLOP/s
 FP32_MFMA_PEAK = 157.3         # MI355X dense FP32 matrix peak, TFLOP/s
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
@@ -311,6 +316,64 @@ def deflated_act_roofline(k1_ms: float):
             "ideal_us": round(ideal_s * 1e6, 2), "flops": 2.0 * flops}
 
 
+def aog_report(args):
+    """AOG accumulation A += gT gT^T (d = 4096, n = 4096 per call), rotating
+    through distinct gT batches and accumulators so that the 256 MB Infinity
+    Cache does not hold them; the CPU oracle timed on a row sample."""
+    import torch
+    from paper_2609_33269_amd import qwam
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    d, n, nrot = 4096, 4096, 6
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(5_000_000)
+    col = torch.exp(-torch.arange(d, device=dev, dtype=torch.float32) / (d / 8.0))
+    gts = [(torch.randn((d, n), generator=gen, device=dev) * col[torch.randperm(d, generator=gen, device=dev)][:, None])
+           .to(torch.bfloat16) for _ in range(nrot)]
+    accs = [torch.zeros((d, d), dtype=torch.float32, device=dev) for _ in range(nrot)]
+    stream = torch.cuda.current_stream()
+    for i in range(args.warmup):
+        qwam.aog_accumulate(gts[i % nrot], accs[i % nrot])
+    torch.cuda.synchronize()
+    steps = args.steps
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for i in range(steps):
+        qwam.aog_accumulate(gts[i % nrot], accs[i % nrot])
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / steps
+    flops = float(n) * d * (d + 1)               # the symmetric rank-n update
+    bytes_ = d * n * 2 + 2 * d * d * 4            # gT once, A read and written once
+    tflops = flops / (us * 1e-6) / 1e12
+    # the CPU oracle (float64 rank-k update) on column samples of the same batch
+    from oracle import qwam_oracle as O
+    g_bits = gts[0].view(torch.int16).cpu().numpy().view(np.uint16)
+    cols = 256
+    A_cpu = np.zeros((d, d))
+    t0 = time.perf_counter()
+    reps = 0
+    while reps == 0 or time.perf_counter() - t0 < min(args.cpu_seconds, 10.0):
+        A_cpu = O.aog_accumulate(A_cpu, g_bits[:, (reps * cols) % n:(reps * cols) % n + cols])
+        reps += 1
+    dt = time.perf_counter() - t0
+    cpu_tflops = float(cols) * d * (d + 1) * reps / dt / 1e12
+    print(json.dumps({
+        "metric": "AOG accumulation A += gT gT^T: TFLOP/s", "value": round(tflops, 1), "unit": "TFLOP/s",
+        "n_gpus": 1, "steps": steps, "warmup": args.warmup, "ms_per_step": round(us / 1e3, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16 products (exact), f32 accumulate", "data": "synthetic",
+        "config": {"workload": "aog_accumulate", "d": d, "n": n, "rotated_buffer_sets": nrot},
+        "roofline": {"bound": "mfma", "kernel": "aog_syrk_kernel", "achieved": round(tflops, 1),
+                     "peak": BF16_MFMA_PEAK, "unit": "TFLOP/s", "frac": round(tflops / BF16_MFMA_PEAK, 4),
+                     "traffic": None, "algorithmic_bytes": bytes_,
+                     "hbm_GBs": round(bytes_ / (us * 1e-6) / 1e9, 1)},
+        "cpu_baseline": {"value": round(cpu_tflops, 5), "unit": "TFLOP/s", "cores": os.cpu_count(), "kind": "oracle",
+                         "sample": f"{reps} calls of the oracle on {cols} of the {n} VJPs (all {d} channels) in "
+                                   f"{dt:.1f} s; value = cols*d*(d+1)*calls/time"}}), flush=True)
+
+
 def cpu_baseline(draws, seconds: float = 12.0, deflate: bool = False, rotate: bool = False):
     """The CPU oracle as it stands, timed on a bounded token sample of the same
     layer (weights packed beforehand, as on the GPU)."""
@@ -359,6 +422,7 @@ def main():
                     help="the same layer with the deflated activation kernel (Eq. 8 / Eq. 9)")
     ap.add_argument("--rotated", action="store_true",
                     help="the same layer with the block Hadamard rotation (Eq. 3) on both operands")
+    ap.add_argument("--aog", action="store_true", help="report the AOG accumulation kernel instead")
     ap.add_argument("--small-m", action="store_true", help="report the action-expert layers instead")
     ap.add_argument("--denoise-step", action="store_true", help="report one 120-layer denoising step instead")
     args = ap.parse_args()
@@ -375,6 +439,9 @@ def main():
               f"implemented and measured on a single GPU, with no sharding", file=sys.stderr)
         sys.exit(2)
 
+    if args.aog:
+        aog_report(args)
+        return
     if args.small_m:
         small_m_report(args)
         return

@@ -95,7 +95,7 @@
 extern "C" {
 #endif
 
-#define QWAM_ABI_VERSION 4
+#define QWAM_ABI_VERSION 5
 #define QWAM_GROUP 64
 
 typedef enum {
@@ -198,6 +198,23 @@ qwam_status qwam_asp_linear(const qwam_layer *L, int32_t M, const uint8_t *xq,
  */
 qwam_status qwam_debug_group_partials(const qwam_layer *L, int32_t M, const uint8_t *xq,
                                       int32_t *P, void *stream);
+
+/*
+ * Accumulation of the Action Observability Gramian estimate (Sec. 4.1 and the
+ * procedure of the probe estimator): every probe vector-Jacobian product
+ * g = J^T u adds g g^T to a d x d accumulator, and G^ = A / (N P) after the
+ * last input.  A batch of n such vectors, stored channel-major, is added at
+ * once:
+ *     A[i][j] += sum_k gT[i][k] gT[j][k]
+ * (products of two bf16 values exact, sums in float32).  Only the tiles on or
+ * above the diagonal are computed, and each is also written transposed, so a
+ * symmetric A stays exactly symmetric.
+ *   d   in      channels of the layer input, d % 16 == 0, 16 <= d <= 16384
+ *   n   in      vectors in the batch, n % 64 == 0, n >= 64, d * n < 2^30
+ *   gT  in      bf16 [d][n]: row c holds channel c of the n vectors
+ *   A   in/out  float [d][d], accumulated in place
+ */
+qwam_status qwam_aog_accumulate(int32_t d, int32_t n, const uint16_t *gT, float *A, void *stream);
 
 /* Message describing the calling thread's last non-OK status ("" if none). */
 const char *qwam_last_error(void);

@@ -188,6 +188,22 @@ qwam_status qwam_debug_group_partials(const qwam_layer* L, int32_t M, const uint
                                                   static_cast<hipStream_t>(stream)));
 }
 
+qwam_status qwam_aog_accumulate(int32_t d, int32_t n, const uint16_t* gT, float* A, void* stream) {
+  const char* fn = "qwam_aog_accumulate";
+  if (d < 16 || d % 16 != 0)
+    return fail(QWAM_ERR_INVALID_ARG, "%s: d must be a positive multiple of 16 (got %d)", fn, d);
+  if (n < 64 || n % 64 != 0)
+    return fail(QWAM_ERR_INVALID_ARG, "%s: n must be a positive multiple of 64 (got %d)", fn, n);
+  if (d > 16384) return fail(QWAM_ERR_UNSUPPORTED, "%s: d = %d exceeds 16384", fn, d);
+  if (static_cast<int64_t>(d) * n >= (int64_t(1) << 30))
+    return fail(QWAM_ERR_UNSUPPORTED, "%s: d * n must be below 2^30", fn);
+  QWAM_REQUIRE_PTR(gT);
+  QWAM_REQUIRE_PTR(A);
+  qwam_status s = check_device(fn);
+  if (s != QWAM_OK) return s;
+  return launched(fn, qwam::launch_aog_accumulate(d, n, gT, A, static_cast<hipStream_t>(stream)));
+}
+
 const char* qwam_last_error(void) { return g_err; }
 
 const char* qwam_status_string(qwam_status s) {

@@ -31,6 +31,9 @@ hipError_t launch_asp_gemm(int M, int N, int K, int r, const uint8_t* xq, const 
 hipError_t launch_group_partials(int M, int N, int K, const uint8_t* xq, const uint8_t* wq,
                                  int32_t* P, hipStream_t stream);
 
+// AOG accumulation: A [d][d] += gT gT^T, gT bf16 [d][n], n % 64 == 0
+hipError_t launch_aog_accumulate(int d, int n, const uint16_t* gT, float* A, hipStream_t stream);
+
 // the few-token GEMM (one wave per 32 x 32 block), used for M <= kSmallM
 constexpr int kSmallM = 64;
 

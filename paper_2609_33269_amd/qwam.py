@@ -6,7 +6,7 @@ raw device pointers plus the current HIP stream across the C ABI.  If the
 library is not built, every call raises: there is no fallback.
 
 Names follow the C ABI (include/qwam.h): pack_weights, quantize_act,
-quantize_act_deflated, asp_linear, debug_group_partials.
+quantize_act_deflated, asp_linear, debug_group_partials, aog_accumulate.
 """
 
 from __future__ import annotations
@@ -46,6 +46,7 @@ SIGNATURES = {
     "qwam_asp_linear": (ctypes.c_int, [_LP, _i32, _c_void_p, _c_void_p, _c_void_p, _c_void_p,
                                        _c_void_p]),
     "qwam_debug_group_partials": (ctypes.c_int, [_LP, _i32, _c_void_p, _c_void_p, _c_void_p]),
+    "qwam_aog_accumulate": (ctypes.c_int, [_i32, _i32, _c_void_p, _c_void_p, _c_void_p]),
     "qwam_last_error": (ctypes.c_char_p, []),
     "qwam_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "qwam_abi_version": (ctypes.c_int32, []),
@@ -218,3 +219,13 @@ def debug_group_partials(layer: PackedLayer, xq: torch.Tensor, stream=None) -> t
                                          P.data_ptr(), _stream_ptr(stream))
     _check("qwam_debug_group_partials", st)
     return P
+
+
+def aog_accumulate(gT: torch.Tensor, A: torch.Tensor, stream=None) -> torch.Tensor:
+    """qwam_aog_accumulate: A float32 [d][d] += gT gT^T for a batch of probe
+    VJPs gT bf16 [d][n] (row c = channel c).  Returns A (updated in place)."""
+    d, n = gT.shape
+    st = lib().qwam_aog_accumulate(d, n, _req(gT, "gT", torch.bfloat16, (d, n)),
+                                   _req(A, "A", torch.float32, (d, d)), _stream_ptr(stream))
+    _check("qwam_aog_accumulate", st)
+    return A

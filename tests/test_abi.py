@@ -38,7 +38,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == set(Q.SIGNATURES), "binding and header disagree"
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.qwam_abi_version() == 4
+    assert lib.qwam_abi_version() == 5
     assert lib.qwam_status_string(3) == b"QWAM_ERR_MISALIGNED"
 
 
@@ -119,6 +119,15 @@ def test_layer_calls_reject_bad_arguments(lib):
     assert lib.qwam_debug_group_partials(ctypes.byref(_layer(r=7)), 1, None, FAKE, None) == INVALID
 
 
+def test_aog_accumulate_rejects_bad_arguments(lib):
+    for d, n, st in ((0, 64, INVALID), (24, 64, INVALID), (64, 0, INVALID), (64, 96, INVALID),
+                     (32768, 64, UNSUPPORTED), (16384, 65536, UNSUPPORTED)):
+        assert lib.qwam_aog_accumulate(d, n, FAKE, FAKE, None) == st, (d, n)
+    assert lib.qwam_aog_accumulate(64, 64, None, FAKE, None) == INVALID
+    assert lib.qwam_aog_accumulate(64, 64, FAKE, FAKE + 4, None) == MISALIGNED
+    assert lib.qwam_last_error().startswith(b"qwam_aog_accumulate")
+
+
 @pytest.mark.skipif(torch.cuda.device_count() > 0, reason="a GPU is visible: the no-device path cannot be forced")
 def test_no_device_is_reported_before_any_launch(lib):
     assert lib.qwam_pack_weights(256, 256, 64, FAKE, FAKE, FAKE, FAKE, FAKE, None) == NO_DEVICE
@@ -126,6 +135,7 @@ def test_no_device_is_reported_before_any_launch(lib):
     assert _act(lib, _layer(), deflated=True) == NO_DEVICE
     assert _lin(lib, _layer()) == NO_DEVICE
     assert lib.qwam_debug_group_partials(ctypes.byref(_layer()), 4, FAKE, FAKE, None) == NO_DEVICE
+    assert lib.qwam_aog_accumulate(64, 64, FAKE, FAKE, None) == NO_DEVICE
     assert b"no HIP device" in lib.qwam_last_error()
 
 

@@ -1,0 +1,114 @@
+"""GPU parity of the AOG accumulation (qwam_aog_accumulate): A += gT gT^T
+for a batch of probe VJPs, against the float64 oracle.
+
+Per element, the float32 result must lie within the rigorous bound of a
+float32 sum in any order of the exact bf16 products:
+    |A_gpu - A_ref| <= (n + 1) 2^-24 (|A_0| + sum_k |g_ik g_jk|) + 2^-149
+(every product is exact; each of the n additions rounds once).  Symmetry is
+exact: A_gpu == A_gpu^T bit for bit when A_0 is symmetric.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import qwam_oracle as O
+from paper_2609_33269_amd import qwam as Q
+
+from parity_helpers import log
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    Q.lib()
+
+
+def _vjp_batch(d, n, seed, scale=1.0):
+    """Seeded stand-in VJPs: Gaussian channels with a decaying spectrum of
+    channel scales (a few directions dominate, as in the paper's AOGs)."""
+    rng = np.random.default_rng(seed)
+    col = scale * np.exp(-np.arange(d) / max(1.0, d / 8.0))
+    g = rng.standard_normal((d, n)) * col[rng.permutation(d)][:, None]
+    return O.f64_to_bf16_bits(g)
+
+
+def _check(d, n, seed, A0=None):
+    log(f"  aog accumulate d={d} n={n} seed={seed}")
+    gb = _vjp_batch(d, n, seed)
+    if A0 is None:
+        A0 = np.zeros((d, d), dtype=np.float32)
+    A = torch.from_numpy(A0.copy()).cuda()
+    gT = torch.from_numpy(gb.view(np.int16)).view(torch.bfloat16).cuda()
+    Q.aog_accumulate(gT, A)
+    torch.cuda.synchronize()
+    got = A.cpu().numpy().astype(np.float64)
+    ref = O.aog_accumulate(A0.astype(np.float64), gb)
+    g = O.bf16_bits_to_f64(gb)
+    bound = (n + 1) * 2.0 ** -24 * (np.abs(A0.astype(np.float64)) + np.abs(g) @ np.abs(g).T) + 2.0 ** -149
+    assert (np.abs(got - ref) <= bound).all(), np.argwhere(np.abs(got - ref) > bound)[:5].tolist()
+    if (A0 == A0.T).all():
+        assert (A.cpu().numpy() == A.cpu().numpy().T).all(), "symmetry"
+    return got, ref
+
+
+@pytest.mark.parametrize("d,n", [(16, 64), (128, 64), (144, 128), (320, 192), (1024, 256), (1040, 640)])
+def test_aog_accumulate_shapes(d, n):
+    _check(d, n, seed=d + n)
+
+
+def test_aog_accumulate_adds_to_existing_accumulator():
+    """Two batches in a row equal one batch of both; a symmetric start stays symmetric."""
+    d, n = 384, 256
+    rng = np.random.default_rng(71)
+    Z = rng.standard_normal((d, 32)).astype(np.float32)
+    A0 = (Z @ Z.T).astype(np.float32)
+    _check(d, n, seed=72, A0=A0)
+    g1, g2 = _vjp_batch(d, 128, 73), _vjp_batch(d, 128, 74)
+    A = torch.zeros((d, d), dtype=torch.float32, device="cuda:0")
+    for gb in (g1, g2):
+        Q.aog_accumulate(torch.from_numpy(gb.view(np.int16)).view(torch.bfloat16).cuda(), A)
+    torch.cuda.synchronize()
+    both = np.concatenate([g1, g2], axis=1)
+    ref = O.aog_accumulate(np.zeros((d, d)), both)
+    g = O.bf16_bits_to_f64(both)
+    bound = 257 * 2.0 ** -24 * (np.abs(g) @ np.abs(g).T) + 2.0 ** -149
+    assert (np.abs(A.cpu().numpy() - ref) <= bound).all()
+
+
+def test_aog_unit_vector_probes_exact():
+    """Integer VJPs whose every partial sum is an integer below 2^24: the
+    float32 result is exact (the J^T J of unit-vector probes)."""
+    d, m = 64, 64
+    rng = np.random.default_rng(75)
+    J = rng.integers(-8, 9, size=(m, d)).astype(np.float64)
+    gb = np.ascontiguousarray(O.f64_to_bf16_bits(J.T))  # [d][m]: VJPs of the m unit probes
+    A = torch.zeros((d, d), dtype=torch.float32, device="cuda:0")
+    Q.aog_accumulate(torch.from_numpy(gb.view(np.int16)).view(torch.bfloat16).cuda(), A)
+    torch.cuda.synchronize()
+    assert (A.cpu().numpy().astype(np.float64) == J.T @ J).all()
+
+
+def test_aog_full_size_sampled():
+    """d = 4096 (the largest accumulator of the paper's models), n = 4096 VJPs
+    (one calibration input: 12 probes x 340 token-step pairs, rounded up):
+    symmetry everywhere, the bound on sampled rows."""
+    d, n = 4096, 4096
+    gb = _vjp_batch(d, n, seed=76)
+    A = torch.zeros((d, d), dtype=torch.float32, device="cuda:0")
+    gT = torch.from_numpy(gb.view(np.int16)).view(torch.bfloat16).cuda()
+    Q.aog_accumulate(gT, A)
+    torch.cuda.synchronize()
+    assert torch.equal(A, A.t()), "symmetry"
+    rng = np.random.default_rng(77)
+    rows = np.array(sorted(set([0, 127, 128, d - 1]) | set(int(v) for v in rng.choice(d, 12, replace=False))))
+    g = O.bf16_bits_to_f64(gb)
+    got = A[torch.from_numpy(rows).cuda()].cpu().numpy().astype(np.float64)
+    ref = g[rows] @ g.T
+    bound = (n + 1) * 2.0 ** -24 * (np.abs(g[rows]) @ np.abs(g).T) + 2.0 ** -149
+    assert (np.abs(got - ref) <= bound).all()
+    del A, gT
+    torch.cuda.empty_cache()
