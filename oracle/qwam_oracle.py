@@ -26,7 +26,8 @@ Paper references used below
       reference rule only in floating-point accumulation order.
 
 Readings taken where the paper is silent (all are listed in the design notes):
-  * group = 64 along K; scales are float32; rounding is half-to-even;
+  * group = 64 along K (the paper's 32 is the group-32 variant, `group`
+    arguments below); scales are float32 in both; rounding is half-to-even;
     scale = fl32(absmax / 7), codes = clamp(rint(fl32(v * fl32(1/scale))), -8, 7);
     a group whose absmax is below 7 * 2**-126 gets scale 0 and all codes 0.
   * the activation is smoothed by multiplying with fl32(1/lambda) (the
@@ -343,13 +344,13 @@ def inverse_smoothing(lam: np.ndarray) -> np.ndarray:
     return (np.float32(1) / lam).astype(np.float32)
 
 
-def pack_weights(R: np.ndarray, lam: np.ndarray):
+def pack_weights(R: np.ndarray, lam: np.ndarray, group: int = GROUP):
     """Offline weight pack (weights are quantized once, Sec. 3 / App. B.1).
 
     R: float32 [N][K] residual weight.  Returns (packed codes uint8 [N][K/2],
     scales float32 [N][G], inverse smoothing float32 [K], codes int8 [N][K]).
     """
-    codes, scales = quantize_groups(np.asarray(R, dtype=np.float32))
+    codes, scales = quantize_groups(np.asarray(R, dtype=np.float32), group)
     return pack_codes(codes), scales, inverse_smoothing(lam), codes
 
 
@@ -409,14 +410,15 @@ def transformed_activations(x_bits: np.ndarray, inv_lam: np.ndarray, hadamard: i
     return rotate_activations(xt, hadamard) if hadamard else xt
 
 
-def quantize_activations(x_bits: np.ndarray, inv_lam: np.ndarray, L1_bits: np.ndarray, hadamard: int = 0):
+def quantize_activations(x_bits: np.ndarray, inv_lam: np.ndarray, L1_bits: np.ndarray, hadamard: int = 0,
+                         group: int = GROUP):
     """The activation side of one layer call: smoothing (and the rotation, if
     `hadamard` is the block size), per-token group quantization (Eq. 2,
     absmax/7 per token, App. B.1), code packing and the rank-r
     down-projection.  Returns (packed uint8 [M][K/2], scales f32 [M][G],
     t bf16 bits [M][r], codes int8 [M][K], x~ float32 [M][K])."""
     xt = transformed_activations(x_bits, inv_lam, hadamard)
-    codes, scales = quantize_groups(xt)
+    codes, scales = quantize_groups(xt, group)
     t = down_projection(xt, L1_bits)
     return pack_codes(codes), scales, t, codes, xt
 
@@ -445,7 +447,7 @@ def deflate_activations(xt: np.ndarray, t_bits: np.ndarray, L1_bits: np.ndarray)
 
 
 def quantize_activations_deflated(x_bits: np.ndarray, inv_lam: np.ndarray, L1_bits: np.ndarray,
-                                  hadamard: int = 0):
+                                  hadamard: int = 0, group: int = GROUP):
     """The activation side with the paper's deflation (Eq. 8 / Eq. 9): t is
     computed from x~ as in quantize_activations, then x~_perp (deflate_activations)
     is quantized per token and group.  Returns (packed uint8 [M][K/2], scales
@@ -453,7 +455,7 @@ def quantize_activations_deflated(x_bits: np.ndarray, inv_lam: np.ndarray, L1_bi
     xt = transformed_activations(x_bits, inv_lam, hadamard)
     t = down_projection(xt, L1_bits)
     xp = deflate_activations(xt, t, L1_bits)
-    codes, scales = quantize_groups(xp)
+    codes, scales = quantize_groups(xp, group)
     return pack_codes(codes), scales, t, codes, xp
 
 
@@ -493,9 +495,11 @@ def asp_output(sx: np.ndarray, sw: np.ndarray, P: np.ndarray, t_bits: np.ndarray
 
 
 def asp_output_bruteforce(qx, sx, qw, sw, t_bits, L2_bits, bias_bits=None) -> np.ndarray:
-    """Same output computed the other way: dequantize both operands, multiply."""
-    xd = dequantize_groups(qx, sx)
-    wd = dequantize_groups(qw, sw)
+    """Same output computed the other way: dequantize both operands, multiply
+    (the group size follows from the scales' shape)."""
+    group = qx.shape[1] // sx.shape[1]
+    xd = dequantize_groups(qx, sx, group)
+    wd = dequantize_groups(qw, sw, group)
     y = xd @ wd.T + bf16_bits_to_f64(t_bits) @ bf16_bits_to_f64(L2_bits)
     if bias_bits is not None:
         y = y + bf16_bits_to_f64(bias_bits)[None, :]
@@ -506,14 +510,16 @@ def asp_linear(x_bits, layer, bias_bits=None, rows=None, deflate=False):
     """Whole deployed layer for the tokens `rows` (all if None); with
     `deflate` the 4-bit path quantizes x~_perp (Eq. 9) instead of x~.
 
-    layer: dict from build_layer (lam, L1, L2, R).  Returns a dict with every
-    intermediate: wq, sw, inv_lam, qw, xq, sx, t, qx, P, y.
+    layer: dict from build_layer (lam, L1, L2, R; optional hadamard, group).
+    Returns a dict with every intermediate: wq, sw, inv_lam, qw, xq, sx, t, qx,
+    P, y.
     """
-    wq, sw, inv_lam, qw = pack_weights(layer["R"], layer["lam"])
+    group = layer.get("group", GROUP)
+    wq, sw, inv_lam, qw = pack_weights(layer["R"], layer["lam"], group)
     xb = x_bits if rows is None else x_bits[rows]
     quant = quantize_activations_deflated if deflate else quantize_activations
-    xq, sx, t, qx, _ = quant(xb, inv_lam, layer["L1"], layer.get("hadamard", 0))
-    P = group_partials(qx, qw)
+    xq, sx, t, qx, _ = quant(xb, inv_lam, layer["L1"], layer.get("hadamard", 0), group)
+    P = group_partials(qx, qw, group)
     y = asp_output(sx, sw, P, t, layer["L2"], bias_bits)
     return {"wq": wq, "sw": sw, "inv_lam": inv_lam, "qw": qw, "xq": xq, "sx": sx,
             "t": t, "qx": qx, "P": P, "y": y}
@@ -524,7 +530,7 @@ def asp_output_rows(xq_rows, sx_rows, t_rows, wq, sw, L2_bits, bias_bits=None):
     scales (no full [M][N][G] tensor): used to check sampled rows of large layers."""
     qx = unpack_codes(xq_rows)
     qw = unpack_codes(wq)
-    P = group_partials(qx, qw)
+    P = group_partials(qx, qw, qx.shape[1] // sx_rows.shape[1])
     return asp_output(sx_rows, sw, P, t_rows, L2_bits, bias_bits), P
 
 
@@ -533,7 +539,7 @@ def asp_output_rows(xq_rows, sx_rows, t_rows, wq, sw, L2_bits, bias_bits=None):
 # ----------------------------------------------------------------------------
 
 
-def asp_linear_exact(x: np.ndarray, layer_exact, deflate=False) -> np.ndarray:
+def asp_linear_exact(x: np.ndarray, layer_exact, deflate=False, group: int = GROUP) -> np.ndarray:
     """y = Q4(x~) Q4(R)^T + (x~ V)(V^T W~), all float64 (Eq. 9 with the 4-bit
     path applied to x~, or with `deflate` to x~_perp = x~ - (x~ V) V^T; the
     quantizer itself run in float64)."""
@@ -543,9 +549,9 @@ def asp_linear_exact(x: np.ndarray, layer_exact, deflate=False) -> np.ndarray:
         xt = rotate_exact(xt, layer_exact["hadamard"])
     V = layer_exact["V"]
     x4 = xt - (xt @ V) @ V.T if deflate else xt
-    qx, sx = quantize_groups(x4, dtype=np.float64)
-    qw, sw = quantize_groups(layer_exact["R"], dtype=np.float64)
-    y4 = dequantize_groups(qx, sx) @ dequantize_groups(qw, sw).T
+    qx, sx = quantize_groups(x4, group, dtype=np.float64)
+    qw, sw = quantize_groups(layer_exact["R"], group, dtype=np.float64)
+    y4 = dequantize_groups(qx, sx, group) @ dequantize_groups(qw, sw, group).T
     return y4 + (xt @ layer_exact["V"]) @ layer_exact["VtW"]
 
 

@@ -729,3 +729,60 @@ def test_rotated_aog_identities():
     assert np.allclose(np.linalg.eigvalsh(Gt), np.linalg.eigvalsh(DGD), rtol=0, atol=1e-9 * np.abs(DGD).max())
     assert np.allclose(O.rotated_aog(G, np.ones(d), 0), G, rtol=0, atol=0)
     assert O.action_mass([Gt, DGD]) == pytest.approx(2 * np.trace(DGD), rel=1e-12)
+
+
+# --------------------------------------------------------------------------
+# group-32 variant (App. B.1's group size)
+# --------------------------------------------------------------------------
+
+def test_group32_scales_follow_each_half_group():
+    """A row whose two 32-channel halves differ by 100x: with group 32 each
+    half gets its own scale (absmax/7 of that half), with group 64 the small
+    half shares the large scale and rounds to fewer levels."""
+    v = np.zeros((1, 64), dtype=np.float32)
+    v[0, :32] = np.linspace(-7, 7, 32).astype(np.float32) * np.float32(0.01)
+    v[0, 32:] = np.linspace(-7, 7, 32).astype(np.float32)
+    c32, s32 = O.quantize_groups(v, 32)
+    c64, s64 = O.quantize_groups(v, 64)
+    assert s32.shape == (1, 2) and s64.shape == (1, 1)
+    assert s32[0, 1] == np.float32(1.0) and s64[0, 0] == np.float32(1.0)    # 7 / 7
+    assert 0.0099 < s32[0, 0] < 0.0101                                       # 0.07 / 7
+    assert np.abs(c32[0, :32]).max() == 7 and np.abs(c64[0, :32]).max() == 0
+
+
+def test_group32_partials_and_output_bruteforce():
+    """Group-32 partials against the triple loop, and y against
+    dequantize-and-multiply, on the same small layer."""
+    d = I.custom(M=5, K=128, N=24, r=16, seed=81, n_outliers=1)
+    V = O.protected_basis_from_factor(d.a, 16)
+    L = dict(O.build_layer(d.x, d.w, V), group=32)
+    out = O.asp_linear(d.x, L)
+    assert out["sx"].shape == (5, 4) and out["sw"].shape == (24, 4) and out["P"].shape == (5, 24, 4)
+    qx, qw = out["qx"].astype(np.int64), out["qw"].astype(np.int64)
+    for m in range(5):
+        for n in range(24):
+            for g in range(4):
+                assert out["P"][m, n, g] == sum(qx[m, k] * qw[n, k] for k in range(32 * g, 32 * g + 32))
+    yb = O.asp_output_bruteforce(out["qx"], out["sx"], out["qw"], out["sw"], out["t"], L["L2"])
+    assert np.allclose(out["y"], yb, rtol=0, atol=1e-12 * np.abs(yb).max())
+    # the codes are the quantizer of Eq. 2 applied per 32 channels
+    inv = O.inverse_smoothing(L["lam"])
+    c, s = O.quantize_groups(O.smooth_activations(d.x, inv), 32)
+    assert (out["qx"] == c).all() and (out["sx"] == s).all()
+
+
+def test_group32_error_not_larger_on_outlier_inputs():
+    """Smaller groups isolate outliers: on outlier-heavy activations the
+    group-32 4-bit product is at least as close to the exact product."""
+    d = I.custom(M=32, K=1024, N=64, r=16, seed=82, n_outliers=8)
+    V = O.protected_basis_from_factor(d.a, 16)
+    L = O.build_layer(d.x, d.w, V)
+    ref = O.asp_linear_exact(O.bf16_bits_to_f64(d.x), O.build_layer_exact(O.bf16_bits_to_f64(d.x),
+                                                                        O.bf16_bits_to_f64(d.w), V))
+    xw = O.bf16_bits_to_f64(d.x) @ O.bf16_bits_to_f64(d.w).T
+    e = {}
+    for g in (64, 32):
+        y = O.asp_linear(d.x, dict(L, group=g))["y"]
+        e[g] = np.linalg.norm(y - xw) / np.linalg.norm(xw)
+    assert e[32] <= e[64]
+    assert np.isfinite(ref).all()
