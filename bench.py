@@ -30,6 +30,10 @@ Secondary measurement (not the headline line):
       (Eq. 8 / Eq. 9: the 4-bit path quantizes x~ - L1 t), i.e. with
       qwam_quantize_act_deflated as the activation kernel; its roofline is the
       FP64 + FP32 matrix-core work of t and of the r rank-1 updates.
+  python bench.py --group 32 [--rotated] [--deflated]
+      the same layer with App. B.1's group size of 32 (one float32 scale per 32
+      channels, two integer partials per 64-channel MFMA); with --rotated
+      --deflated this is the paper's full deployed setting.
   python bench.py --rotated [--deflated]
       the same layer with the block Hadamard rotation of Eq. 3 (B = 1024,
       applied online to the activation by the fast Walsh-Hadamard transform;
@@ -81,7 +85,8 @@ GEMM_KERNEL = "asp_gemm_kernel<32, false>"
 COPY_KERNEL = "neg_kernel"
 
 
-def algorithmic_bytes():
+def algorithmic_bytes(group: int = GROUP):
+    G = K // group
     act = M * K * 2 + K * 4 + R_RANK * K * 2 + M * K // 2 + M * G * 4 + M * R_RANK * 2
     gemm = M * K // 2 + M * G * 4 + M * R_RANK * 2 + N * K // 2 + N * G * 4 + N * R_RANK * 2 + M * N * 2
     return act, gemm
@@ -374,7 +379,7 @@ def aog_report(args):
                                    f"{dt:.1f} s; value = cols*d*(d+1)*calls/time"}}), flush=True)
 
 
-def cpu_baseline(draws, seconds: float = 12.0, deflate: bool = False, rotate: bool = False):
+def cpu_baseline(draws, seconds: float = 12.0, deflate: bool = False, rotate: bool = False, group: int = GROUP):
     """The CPU oracle as it stands, timed on a bounded token sample of the same
     layer (weights packed beforehand, as on the GPU)."""
     from oracle import qwam_oracle as O
@@ -385,15 +390,15 @@ def cpu_baseline(draws, seconds: float = 12.0, deflate: bool = False, rotate: bo
         threads = 1
     V = O.protected_basis_from_factor(draws.a, R_RANK)
     f = O.build_layer(draws.x, draws.w, V, hadamard=rotate)
-    wq, sw, inv_lam, qw = O.pack_weights(f["R"], f["lam"])
+    wq, sw, inv_lam, qw = O.pack_weights(f["R"], f["lam"], group)
     chunk = 32
     done = 0
     t0 = time.perf_counter()
     while done + chunk <= M:
         rows = slice(done, done + chunk)
         quant = O.quantize_activations_deflated if deflate else O.quantize_activations
-        xq, sx, t, qx, _ = quant(draws.x[rows], inv_lam, f["L1"], f["hadamard"])
-        P = O.group_partials(qx, qw)
+        xq, sx, t, qx, _ = quant(draws.x[rows], inv_lam, f["L1"], f["hadamard"], group)
+        P = O.group_partials(qx, qw, group)
         O.asp_output(sx, sw, P, t, f["L2"])
         done += chunk
         if time.perf_counter() - t0 >= seconds:
@@ -402,7 +407,8 @@ def cpu_baseline(draws, seconds: float = 12.0, deflate: bool = False, rotate: bo
     return {"value": 2.0 * done * K * N / dt / 1e12, "unit": "TOPS", "cores": int(threads),
             "kind": "oracle",
             "sample": f"{done} of {M} tokens (chunks of {chunk}) of the {M}x{K}x{N} r{R_RANK} layer"
-                      f"{' with rotation' if rotate else ''}{' with deflation' if deflate else ''}, "
+                      f"{' with rotation' if rotate else ''}{' with deflation' if deflate else ''}"
+                      f"{', group 32' if group == 32 else ''}, "
                       f"weights packed beforehand; {dt:.1f} s; value = 2*tokens*K*N/time"}
 
 
@@ -420,6 +426,8 @@ def main():
     ap.add_argument("--copy-mib", type=int, default=256, help="copy-probe size the counters were taken with")
     ap.add_argument("--deflated", action="store_true",
                     help="the same layer with the deflated activation kernel (Eq. 8 / Eq. 9)")
+    ap.add_argument("--group", type=int, default=GROUP, choices=(32, 64),
+                    help="channels per quantization scale (64, or the paper's 32)")
     ap.add_argument("--rotated", action="store_true",
                     help="the same layer with the block Hadamard rotation (Eq. 3) on both operands")
     ap.add_argument("--aog", action="store_true", help="report the AOG accumulation kernel instead")
@@ -460,7 +468,7 @@ def main():
     w0 = torch.from_numpy(draws.w.view(np.int16)).view(torch.bfloat16).to(dev)
     V = calib.protected_basis(torch.from_numpy(draws.a), R_RANK)
     f = calib.build_layer(x0, w0, V, hadamard=args.rotated)
-    layer0 = qwam.make_layer(f["R"], f["lam"], f["L1"], f["L2"], hadamard=f["hadamard"])
+    layer0 = qwam.make_layer(f["R"], f["lam"], f["L1"], f["L2"], hadamard=f["hadamard"], group=args.group)
     del f, w0
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
@@ -471,11 +479,11 @@ def main():
         L = layer0 if i == 0 else qwam.PackedLayer(
             K=K, N=N, r=R_RANK, wq=layer0.wq.clone(), ws=layer0.ws.clone(),
             inv_smooth=layer0.inv_smooth.clone(), L1t=layer0.L1t.clone(), L2t=layer0.L2t.clone(),
-            hadamard=layer0.hadamard)
+            hadamard=layer0.hadamard, group=layer0.group)
         layers.append(L)
         xins.append(x0 if i == 0 else x0.clone())
         outs.append((torch.empty((M, K // 2), dtype=torch.uint8, device=dev),
-                     torch.empty((G, M), dtype=torch.float32, device=dev),
+                     torch.empty((K // args.group, M), dtype=torch.float32, device=dev),
                      torch.empty((M, R_RANK), dtype=torch.bfloat16, device=dev),
                      torch.empty((M, N), dtype=torch.bfloat16, device=dev)))
     stream = torch.cuda.current_stream()
@@ -516,7 +524,7 @@ def main():
     int_ops = 2.0 * M * K * N
     eff_tops = int_ops / (ms_step * 1e-3) / 1e12
     k2_tops = int_ops / (k2_ms * 1e-3) / 1e12
-    act_bytes, gemm_bytes = algorithmic_bytes()
+    act_bytes, gemm_bytes = algorithmic_bytes(args.group)
     k1_gbs = act_bytes / (k1_ms * 1e-3) / 1e9
 
     # secondary: the bf16 linear the layer replaces (hipBLASLt through torch), same shape
@@ -542,7 +550,7 @@ def main():
         torch.cuda.synchronize()
         del src_t, dst_t
 
-    traffic = measured_traffic()
+    traffic = measured_traffic() if args.group == GROUP else None
     act_name = ("quantize_act_rotated" if args.rotated else "quantize_act") + ("_deflated" if args.deflated else "")
     out = {
         "metric": METRIC,
@@ -558,7 +566,8 @@ def main():
         "dtype": "int4 codes on fp8-e4m3 MFMA (exact), f32 scale/accumulate, bf16 out",
         "data": "synthetic",
         "config": {"workload": "video_dit_ffn_up" + ("_rotated" if args.rotated else "")
-                   + ("_deflated" if args.deflated else ""), "M": M, "K": K, "N": N, "r": R_RANK, "group": GROUP,
+                   + ("_deflated" if args.deflated else "") + ("_group32" if args.group == 32 else ""),
+                   "M": M, "K": K, "N": N, "r": R_RANK, "group": args.group,
                    "act": "N(0,1), 1% channels x U_log(10,50)", "weights": "N(0,1/K)",
                    "rotated_buffer_sets": nrot},
         "roofline": {"bound": "mfma", "kernel": GEMM_KERNEL, "achieved": round(k2_tops, 1),
@@ -586,7 +595,8 @@ def main():
         out["fwht_valu_us"] = round(adds / (1024 * 16 * 2.4e9) * 1e6, 2)
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a token sample", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(draws, args.cpu_seconds, deflate=args.deflated, rotate=args.rotated)
+        out["cpu_baseline"] = cpu_baseline(draws, args.cpu_seconds, deflate=args.deflated, rotate=args.rotated,
+                                           group=args.group)
     print(json.dumps(out), flush=True)
 
 

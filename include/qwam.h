@@ -9,7 +9,8 @@
  * following "Q-WAM: 4-Bit Quantization of World Action Models with
  * Action-Subspace Protection":
  *   - Q4 is the symmetric 4-bit group quantizer of Eq. 2 (Sec. 3), one float32
- *     scale per group of 64 consecutive input channels: scale = absmax / 7,
+ *     scale per group of 64 consecutive input channels (or of 32, App. B.1's
+ *     group size, with group = 32): scale = absmax / 7,
  *     code = clamp(round_half_even(v * (1 / scale)), -8, 7).  Weights are
  *     quantized once offline, activations per token at run time (Sec. 3,
  *     App. B.1).
@@ -52,7 +53,7 @@
  *   - Inputs must be finite (no NaN / Inf); other inputs give unspecified
  *     codes.
  *
- * Layouts (row-major, G = K / 64)
+ * Layouts (row-major, G = K / group)
  *   x    bf16    [M][K]      activations (row = token)
  *   R    float   [N][K]      residual weight, row = output channel
  *   smooth float [K]         lambda
@@ -81,7 +82,7 @@
  * dividing K (QWAM_ERR_INVALID_ARG otherwise).  It affects the activation
  * calls only; qwam_pack_weights and qwam_asp_linear do not read it.
  *
- * Shape limits: group == 64; K % 64 == 0, 64 <= K <= 65536; N % 16 == 0,
+ * Shape limits: group == 64 or 32; K % 64 == 0, 64 <= K <= 65536; N % 16 == 0,
  * 16 <= N <= 1048576; r in {16, 32, 48, 64}; 1 <= M <= 1048576; for
  * qwam_asp_linear also M * K / 64 < 2^29 and N * K / 64 < 2^29
  * (QWAM_ERR_UNSUPPORTED otherwise).
@@ -95,7 +96,7 @@
 extern "C" {
 #endif
 
-#define QWAM_ABI_VERSION 5
+#define QWAM_ABI_VERSION 6
 #define QWAM_GROUP 64
 
 typedef enum {
@@ -112,10 +113,10 @@ typedef struct qwam_layer {
     int32_t K;                  /* input channels (multiple of 64)                  */
     int32_t N;                  /* output channels (multiple of 16)                 */
     int32_t r;                  /* rank of the protected subspace (16/32/48/64)     */
-    int32_t group;              /* must be 64                                        */
+    int32_t group;              /* 64 or 32: channels per scale                       */
     int32_t hadamard;           /* block size B of the rotation, or 0 for none       */
     const uint8_t *wq;          /* [N][K/2]  packed residual codes                   */
-    const float *ws;            /* [K/64][N] residual group scales                   */
+    const float *ws;            /* [K/group][N] residual group scales                */
     const float *inv_smooth;    /* [K]       fl32(1/lambda)                          */
     const uint16_t *L1t;        /* [r][K]    bf16                                    */
     const uint16_t *L2t;        /* [N][r]    bf16                                    */
@@ -124,15 +125,15 @@ typedef struct qwam_layer {
 
 /*
  * Offline weight pack (weights are quantized once, Sec. 3; the exported codes
- * of App. B.1).  Quantizes each group of 64 consecutive entries of each row of
- * R with the quantizer of Eq. 2 (scale = fl32(absmax / 7); a group with absmax
+ * of App. B.1).  Quantizes each group of `group` (64 or 32) consecutive entries
+ * of each row of R with the quantizer of Eq. 2 (scale = fl32(absmax / 7); a group with absmax
  * below 7 * 2^-126 gets scale 0 and codes 0), packs the codes into code words
  * and writes
  * inv_smooth[k] = fl32(1 / smooth[k]).
  *   R          in   float [N][K]
  *   smooth     in   float [K], every entry finite and nonzero
  *   wq         out  uint8 [N][K/2]
- *   ws         out  float [K/64][N]
+ *   ws         out  float [K/group][N]
  *   inv_smooth out  float [K]
  */
 qwam_status qwam_pack_weights(int32_t K, int32_t N, int32_t group,
@@ -151,7 +152,7 @@ qwam_status qwam_pack_weights(int32_t K, int32_t N, int32_t group,
  *   L   in   layer (reads K, r, group, hadamard, inv_smooth, L1t)
  *   x   in   bf16 [M][K]
  *   xq  out  uint8 [M][K/2]
- *   xs  out  float [K/64][M]
+ *   xs  out  float [K/group][M]
  *   t   out  bf16 [M][r]
  */
 qwam_status qwam_quantize_act(const qwam_layer *L, int32_t M, const uint16_t *x,
@@ -194,7 +195,7 @@ qwam_status qwam_asp_linear(const qwam_layer *L, int32_t M, const uint8_t *xq,
  * integer GEMM (same unpack and matrix-core path).
  *   L   in   packed layer (reads K, N, group, wq)
  *   xq  in   uint8 [M][K/2]
- *   P   out  int32 [M][N][K/64]
+ *   P   out  int32 [M][N][K/group]
  */
 qwam_status qwam_debug_group_partials(const qwam_layer *L, int32_t M, const uint8_t *xq,
                                       int32_t *P, void *stream);

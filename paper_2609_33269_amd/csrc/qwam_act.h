@@ -50,16 +50,18 @@ __device__ __forceinline__ void smooth16_regs(const uint4& xa, const uint4& xb, 
   }
 }
 
-// Quantizes one token's group, held by the four lanes l, l^16, l^32, l^48 (16
-// consecutive channels each, Eq. 2), and stores the lane's two code words at
-// byte q_off of q_rsrc and, if xs_dst is not null, the group's scale.
+// Quantizes the lane's token over one 64-channel span (Eq. 2): with group 64
+// the four lanes l, l^16, l^32, l^48 (16 consecutive channels each) share one
+// scale; with group 32 (g32) the lanes l, l^16 share the scale of channels
+// 0-31 or 32-63 of the span.  Stores the lane's two code words at byte q_off
+// of q_rsrc and, if xs_dst is not null, the lane's group scale.
 __device__ __forceinline__ void quantize_pack_store(const float (&v)[16], buf_rsrc q_rsrc, uint32_t q_off,
-                                                    float* xs_dst) {
+                                                    float* xs_dst, bool g32 = false) {
   float amax = 0.0f;
 #pragma unroll
   for (int j = 0; j < 16; ++j) amax = __builtin_fmaxf(amax, __builtin_fabsf(v[j]));
   amax = __builtin_fmaxf(amax, __shfl_xor(amax, 16));
-  amax = __builtin_fmaxf(amax, __shfl_xor(amax, 32));
+  if (!g32) amax = __builtin_fmaxf(amax, __shfl_xor(amax, 32));
   const float s = q4_scale(amax);
   const float inv = q4_inv(s);
   // codes: q = clamp(rint(v * inv), -8, 7); a byte holds (q_odd + 8) * 16 + (q_even + 8),
@@ -79,6 +81,14 @@ __device__ __forceinline__ void quantize_pack_store(const float (&v)[16], buf_rs
   }
   buf_store8(make_uint2(packed[0], packed[1]), q_rsrc, q_off);
   if (xs_dst != nullptr) *xs_dst = s;
+}
+
+// Where the lane of token `row` (chunk = lane / 16) stores the scale of the
+// 64-channel span g: xs is [K / group][M]; null for tokens past M.
+__device__ __forceinline__ float* xs_slot(float* xs, int g, int M, int m0, int row, int rows, int chunk, bool g32) {
+  if (row >= rows) return nullptr;
+  const int gi = g32 ? 2 * g + (chunk >> 1) : g;
+  return xs + static_cast<int64_t>(gi) * M + m0 + row;
 }
 
 template <int RANK>

@@ -41,7 +41,8 @@ constexpr int32_t kMaxN = 1 << 20;
 constexpr int32_t kMaxM = 1 << 20;
 
 qwam_status check_kn(const char* fn, int32_t K, int32_t N, int32_t group) {
-  if (group != QWAM_GROUP) return fail(QWAM_ERR_INVALID_ARG, "%s: group must be 64 (got %d)", fn, group);
+  if (group != QWAM_GROUP && group != 32)
+    return fail(QWAM_ERR_INVALID_ARG, "%s: group must be 64 or 32 (got %d)", fn, group);
   if (K <= 0 || K % QWAM_GROUP != 0) return fail(QWAM_ERR_INVALID_ARG, "%s: K must be a positive multiple of 64 (got %d)", fn, K);
   if (N <= 0 || N % 16 != 0) return fail(QWAM_ERR_INVALID_ARG, "%s: N must be a positive multiple of 16 (got %d)", fn, N);
   if (K > kMaxK) return fail(QWAM_ERR_UNSUPPORTED, "%s: K = %d exceeds %d", fn, K, kMaxK);
@@ -106,7 +107,7 @@ qwam_status qwam_pack_weights(int32_t K, int32_t N, int32_t group, const float* 
   QWAM_REQUIRE_PTR(ws);
   QWAM_REQUIRE_PTR(inv_smooth);
   if ((s = check_device(fn)) != QWAM_OK) return s;
-  return launched(fn, qwam::launch_pack_weights(K, N, R, smooth, wq, ws, inv_smooth,
+  return launched(fn, qwam::launch_pack_weights(K, N, group, R, smooth, wq, ws, inv_smooth,
                                                 static_cast<hipStream_t>(stream)));
 }
 
@@ -128,10 +129,10 @@ qwam_status quantize_act_common(const char* fn, bool deflate, const qwam_layer* 
   if ((s = check_device(fn)) != QWAM_OK) return s;
   const hipStream_t st = static_cast<hipStream_t>(stream);
   if (L->hadamard != 0)
-    return launched(fn, qwam::launch_quantize_act_rotated(M, L->K, L->r, L->hadamard, deflate, x, L->inv_smooth,
-                                                          L->L1t, xq, xs, t, st));
+    return launched(fn, qwam::launch_quantize_act_rotated(M, L->K, L->r, L->group, L->hadamard, deflate, x,
+                                                          L->inv_smooth, L->L1t, xq, xs, t, st));
   return launched(fn, (deflate ? qwam::launch_quantize_act_deflated : qwam::launch_quantize_act)(
-                          M, L->K, L->r, x, L->inv_smooth, L->L1t, xq, xs, t, st));
+                          M, L->K, L->r, L->group, x, L->inv_smooth, L->L1t, xq, xs, t, st));
 }
 
 }  // namespace
@@ -164,12 +165,12 @@ qwam_status qwam_asp_linear(const qwam_layer* L, int32_t M, const uint8_t* xq, c
   QWAM_REQUIRE_PTR(t);
   QWAM_REQUIRE_PTR(y);
   // the kernel addresses each scale array with 32-bit byte offsets
-  if (static_cast<int64_t>(M) * (L->K / QWAM_GROUP) >= (int64_t(1) << 29) ||
-      static_cast<int64_t>(L->N) * (L->K / QWAM_GROUP) >= (int64_t(1) << 29))
-    return fail(QWAM_ERR_UNSUPPORTED, "%s: M*K/64 and N*K/64 must be below 2^29", fn);
+  if (static_cast<int64_t>(M) * (L->K / L->group) >= (int64_t(1) << 29) ||
+      static_cast<int64_t>(L->N) * (L->K / L->group) >= (int64_t(1) << 29))
+    return fail(QWAM_ERR_UNSUPPORTED, "%s: M*K/group and N*K/group must be below 2^29", fn);
   if ((s = check_device(fn)) != QWAM_OK) return s;
-  return launched(fn, qwam::launch_asp_gemm(M, L->N, L->K, L->r, xq, xs, t, L->wq, L->ws, L->L2t, L->bias, y,
-                                            static_cast<hipStream_t>(stream)));
+  return launched(fn, qwam::launch_asp_gemm(M, L->N, L->K, L->r, L->group, xq, xs, t, L->wq, L->ws, L->L2t,
+                                            L->bias, y, static_cast<hipStream_t>(stream)));
 }
 
 qwam_status qwam_debug_group_partials(const qwam_layer* L, int32_t M, const uint8_t* xq, int32_t* P,
@@ -181,10 +182,10 @@ qwam_status qwam_debug_group_partials(const qwam_layer* L, int32_t M, const uint
   QWAM_REQUIRE_PTR(L->wq);
   QWAM_REQUIRE_PTR(xq);
   QWAM_REQUIRE_PTR(P);
-  if (static_cast<int64_t>(M) * L->N * (L->K / QWAM_GROUP) > (int64_t(1) << 34))
-    return fail(QWAM_ERR_UNSUPPORTED, "%s: M*N*K/64 too large for a partials dump", fn);
+  if (static_cast<int64_t>(M) * L->N * (L->K / L->group) > (int64_t(1) << 34))
+    return fail(QWAM_ERR_UNSUPPORTED, "%s: M*N*K/group too large for a partials dump", fn);
   if ((s = check_device(fn)) != QWAM_OK) return s;
-  return launched(fn, qwam::launch_group_partials(M, L->N, L->K, xq, L->wq, P,
+  return launched(fn, qwam::launch_group_partials(M, L->N, L->K, L->group, xq, L->wq, P,
                                                   static_cast<hipStream_t>(stream)));
 }
 

@@ -42,6 +42,15 @@
 //     as the integer blocks) starts from acc, the bias is added, the
 //     result is rounded to bf16 and stored through LDS so that every lane
 //     writes 16 contiguous bytes.
+//
+// Group 32 (GS = 32, the paper's setting): the MFMA's K = 64 covers two groups.
+// Its two E8M0 block scales govern bytes 0-15 and 16-31 of every lane's
+// operand, so each lane takes 8 bytes of each group (32 codes: bytes 0-15 of
+// the operand from the first group, 16-31 from the second), and each block
+// runs twice, once per group, with the other block's scales set to 2^-127 on
+// both operands: its products (2^-254 and below) underflow to zero, so each
+// result is one group's integer partial, exactly.  Twice the MFMA work and
+// twice the scaling per output.
 #include "qwam_device.h"
 #include "qwam_internal.h"
 #include "qwam_mfma.h"
@@ -60,13 +69,14 @@ constexpr int BAND = 8;            // tile-rows per band of the tile order
 constexpr int KC = 4;              // groups per ring stage
 constexpr int ROWB = KC * 32;      // bytes of one packed row per stage (one cache line)
 
-struct Stage {
+template <int GPS>                 // scale groups per stage
+struct StageT {
   uint8_t a[BM * ROWB];            // [row][8 chunk slots of 16 bytes], swizzled
   uint8_t b[BN * ROWB];
-  float sx[KC][BM];
-  float sw[KC][BN];
+  float sx[GPS][BM];
+  float sw[GPS][BN];
 };
-static_assert(4 * 64 * LDY * 2 <= sizeof(Stage), "the output staging of all four waves must fit in one stage");
+static_assert(4 * 64 * LDY * 2 <= sizeof(StageT<KC>), "the output staging of all four waves must fit in one stage");
 
 // chunk slot permutation of a row inside a stage
 __device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
@@ -77,6 +87,12 @@ __device__ __forceinline__ uint4 lds_load16_volatile(const uint8_t* p) {
   typedef const volatile __attribute__((address_space(3))) v4u lds_v4u;
   const v4u v = *(lds_v4u*)(p);
   return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ uint2 lds_load8_volatile(const uint8_t* p) {
+  typedef unsigned v2u __attribute__((ext_vector_type(2)));
+  typedef const volatile __attribute__((address_space(3))) v2u lds_v2u;
+  const v2u v = *(lds_v2u*)(p);
+  return make_uint2(v.x, v.y);
 }
 __device__ __forceinline__ float lds_load4_volatile(const float* p) {
   typedef const volatile __attribute__((address_space(3))) float lds_f;
@@ -100,12 +116,15 @@ __device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& 
 
 }  // namespace
 
-template <int RANK, bool PARTIALS>
+template <int RANK, bool PARTIALS, int GS>
 __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
     const uint8_t* __restrict__ xq, const float* __restrict__ xs, const uint16_t* __restrict__ t,
     const uint8_t* __restrict__ wq, const float* __restrict__ ws, const uint16_t* __restrict__ L2t,
     const uint16_t* __restrict__ bias, uint16_t* __restrict__ y, int32_t* __restrict__ P, int M,
     int N, int K) {
+  constexpr int NS = kGroup / GS;                               // scale groups per 64-channel span
+  constexpr int GPS = KC * NS;                                  // scale groups per stage
+  typedef StageT<GPS> Stage;
   // two distinct LDS objects (not one indexed array), so that the compiler
   // can tell which ring stage a copy writes and a fragment load reads
   __shared__ __attribute__((aligned(16))) Stage st0, st1;
@@ -114,7 +133,8 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform (SGPR)
   const int wm = wave >> 1, wn = wave & 1;                      // 2 x 2 waves
-  const int G = K / kGroup;
+  const int G = K / kGroup;                                     // 64-channel spans
+  const int GSC = K / GS;                                       // scale groups
   const int KB = K / 2;
   const int S = (G + KC - 1) / KC;                              // ring stages
   const int S_full = G / KC;                                    // stages with KC groups
@@ -139,16 +159,16 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
     d_off[i] = static_cast<uint32_t>(row * KB + (((lane & 7) ^ swz(row)) * 16));
   }
   // scales: waves 0-1 copy xs of the tile's rows, waves 2-3 ws of its columns;
-  // copy i of such a wave covers group (2*(w%2) + i/2) of the stage, rows
-  // 64*(i%2) .. +63
+  // copy i of such a wave covers scale group (GPS/2 * (w%2) + i/2) of the
+  // stage, rows 64*(i%2) .. +63
   const bool s_is_x = wave < 2;
-  const buf_rsrc s_rsrc = s_is_x ? make_rsrc(xs, static_cast<uint32_t>(G) * M * 4u)
-                                 : make_rsrc(ws, static_cast<uint32_t>(G) * N * 4u);
+  const buf_rsrc s_rsrc = s_is_x ? make_rsrc(xs, static_cast<uint32_t>(GSC) * M * 4u)
+                                 : make_rsrc(ws, static_cast<uint32_t>(GSC) * N * 4u);
   const uint32_t s_stride = static_cast<uint32_t>(s_is_x ? M : N) * 4u;
-  uint32_t s_off[4];
+  uint32_t s_off[GPS];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int q = 2 * (wave & 1) + (i >> 1);
+  for (int i = 0; i < GPS; ++i) {
+    const int q = (GPS / 2) * (wave & 1) + (i >> 1);
     s_off[i] = static_cast<uint32_t>(q) * s_stride +
                static_cast<uint32_t>((s_is_x ? m0 : n0) + (i & 1) * 64 + lane) * 4u;
   }
@@ -160,10 +180,10 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
 #pragma unroll
     for (int i = 0; i < 4; ++i) buf_load16_lds(b_rsrc, d_off[i] + ko, st.b + (4 * wave + i) * 1024);
     if (!PARTIALS) {
-      const uint32_t so = static_cast<uint32_t>(s) * KC * s_stride;
+      const uint32_t so = static_cast<uint32_t>(s) * GPS * s_stride;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int q = 2 * (wave & 1) + (i >> 1);
+      for (int i = 0; i < GPS; ++i) {
+        const int q = (GPS / 2) * (wave & 1) + (i >> 1);
         buf_load4_lds(s_rsrc, s_off[i] + so,
                       s_is_x ? static_cast<void*>(&st.sx[q][(i & 1) * 64])
                              : static_cast<void*>(&st.sw[q][(i & 1) * 64]));
@@ -190,28 +210,39 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
   // row 8*(v/4) + 4*(lane/32) + v%4
   const int sx_row = 8 * ((lane & 15) >> 2) + 4 * (lane >> 5) + (lane & 3);
 
-  // LDS data of one group: packed A / B fragments and the lane's scales
+  // LDS data of one 64-channel span: packed A / B fragments and the lane's
+  // scales (NS groups).  With group 32 a fragment is 8 bytes of each group.
   struct GroupData {
     uint4 a[2], b[2];
-    float sx[2], sw[2];
+    float sx[2][NS], sw[2][NS];
   };
   // Reads group q's data one group ahead of its use.  The loads are volatile
   // and followed by a compiler-only fence, so they are issued here and not
   // sunk next to their first use; the wait for them lands at that use.
+  auto load_frag = [&](const uint8_t* rowp, int q) __attribute__((always_inline)) {
+    if constexpr (GS == 64) {
+      return lds_load16_volatile(rowp + ((2 * q) ^ fslot) * 16);
+    } else {
+      const int sw0 = swz(frow);
+      const uint2 lo = lds_load8_volatile(rowp + ((2 * q) ^ sw0) * 16 + fhalf * 8);
+      const uint2 hi = lds_load8_volatile(rowp + ((2 * q + 1) ^ sw0) * 16 + fhalf * 8);
+      return make_uint4(lo.x, lo.y, hi.x, hi.y);
+    }
+  };
   auto load_group = [&](const Stage& cur, int q) __attribute__((always_inline)) {
-    const int slot_off = ((2 * q) ^ fslot) * 16;
     GroupData d;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
-      d.a[i] = lds_load16_volatile(cur.a + (wm * 64 + i * 32) * ROWB + frow_off + slot_off);
+    for (int i = 0; i < 2; ++i) d.a[i] = load_frag(cur.a + (wm * 64 + i * 32) * ROWB + frow_off, q);
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
-      d.b[j] = lds_load16_volatile(cur.b + (wn * 64 + j * 32) * ROWB + frow_off + slot_off);
+    for (int j = 0; j < 2; ++j) d.b[j] = load_frag(cur.b + (wn * 64 + j * 32) * ROWB + frow_off, q);
     if (!PARTIALS) {
 #pragma unroll
-      for (int i = 0; i < 2; ++i) d.sx[i] = lds_load4_volatile(&cur.sx[q][wm * 64 + i * 32 + sx_row]);
+      for (int h = 0; h < NS; ++h) {
 #pragma unroll
-      for (int j = 0; j < 2; ++j) d.sw[j] = lds_load4_volatile(&cur.sw[q][wn * 64 + j * 32 + frow]);
+        for (int i = 0; i < 2; ++i) d.sx[i][h] = lds_load4_volatile(&cur.sx[NS * q + h][wm * 64 + i * 32 + sx_row]);
+#pragma unroll
+        for (int j = 0; j < 2; ++j) d.sw[j][h] = lds_load4_volatile(&cur.sw[NS * q + h][wn * 64 + j * 32 + frow]);
+      }
     }
     asm volatile("" ::: "memory");
     return d;
@@ -225,35 +256,53 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
 #pragma unroll
     for (int j = 0; j < 2; ++j) bf[j] = codes_to_e4m3(d.b[j]);
 
-    // the exact integer partial of block (i, j), as float32
-    auto mfma_block = [&](int i, int j) __attribute__((always_inline)) {
-      return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af[i], bf[j], v16f{}, 0, 0, 0, kE8M0Code, 0,
-                                                             kE8M0Code);
+    // the exact integer partial of block (i, j) for group h of the span, as
+    // float32 (group 64: the whole span; group 32: the other group's block
+    // scales are 2^-127 on both operands, so its products underflow to zero)
+    auto mfma_block = [&](int i, int j, int h) __attribute__((always_inline)) {
+      int sc = kE8M0Code;
+      if constexpr (GS == 32) sc = ((lane >> 5) == h) ? kE8M0Code : 0;
+      return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af[i], bf[j], v16f{}, 0, 0, 0, sc, 0, sc);
     };
     // result layout of a 32x32 block: lane l holds column l%32 and rows
     // 8*(v/4) + 4*(l/32) + v%4, v = 0..15
-    auto consume = [&](int i, int j, const v16f& p) __attribute__((always_inline)) {
+    auto consume = [&](int i, int j, int h, const v16f& p) __attribute__((always_inline)) {
       if (PARTIALS) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int m = m0 + wm * 64 + i * 32 + 8 * (v >> 2) + rsub + (v & 3);
           const int n = n0 + wn * 64 + j * 32 + frow;
-          if (m < M && n < N) P[(static_cast<int64_t>(m) * N + n) * G + g] = static_cast<int32_t>(p[v]);
+          if (m < M && n < N) P[(static_cast<int64_t>(m) * N + n) * GSC + NS * g + h] = static_cast<int32_t>(p[v]);
         }
       } else {
-        scale_accumulate(std::make_integer_sequence<int, 16>{}, accf[i][j], p, d.sx[i], d.sw[j]);
+        scale_accumulate(std::make_integer_sequence<int, 16>{}, accf[i][j], p, d.sx[i][h], d.sw[j][h]);
       }
     };
     // software pipeline: three MFMAs in flight before the first update, so
     // that no update waits for the block it reads
-    const v16f p00 = mfma_block(0, 0);
-    const v16f p01 = mfma_block(0, 1);
-    const v16f p10 = mfma_block(1, 0);
-    consume(0, 0, p00);
-    const v16f p11 = mfma_block(1, 1);
-    consume(0, 1, p01);
-    consume(1, 0, p10);
-    consume(1, 1, p11);
+    if constexpr (GS == 64) {
+      const v16f p00 = mfma_block(0, 0, 0);
+      const v16f p01 = mfma_block(0, 1, 0);
+      const v16f p10 = mfma_block(1, 0, 0);
+      consume(0, 0, 0, p00);
+      const v16f p11 = mfma_block(1, 1, 0);
+      consume(0, 1, 0, p01);
+      consume(1, 0, 0, p10);
+      consume(1, 1, 0, p11);
+    } else {
+      // eight blocks (2 x 2 tiles x 2 groups), two in flight: three would not
+      // fit the registers next to the doubled scale data
+      v16f p0 = mfma_block(0, 0, 0);
+      v16f p1 = mfma_block(0, 0, 1);
+#pragma unroll
+      for (int b = 0; b < 8; ++b) {
+        const int i = b >> 2, j = (b >> 1) & 1, h = b & 1;
+        const v16f cur_p = p0;
+        p0 = p1;
+        if (b + 2 < 8) p1 = mfma_block((b + 2) >> 2, ((b + 2) >> 1) & 1, (b + 2) & 1);
+        consume(i, j, h, cur_p);
+      }
+    }
   };
 
   // one stage: `cur` holds stage s (groups KC*s ..), `nxt` (the stage of s-1)
@@ -353,24 +402,23 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
 
 static int gemm_tiles(int M, int N) { return ((M + BM - 1) / BM) * ((N + BN - 1) / BN); }
 
-hipError_t launch_asp_gemm(int M, int N, int K, int r, const uint8_t* xq, const float* xs,
-                           const uint16_t* t, const uint8_t* wq, const float* ws,
-                           const uint16_t* L2t, const uint16_t* bias, uint16_t* y,
-                           hipStream_t stream) {
-  if (M <= kSmallM) return launch_asp_gemm_small(M, N, K, r, xq, xs, t, wq, ws, L2t, bias, y, stream);
+template <int GS>
+static hipError_t launch_asp_gemm_gs(int M, int N, int K, int r, const uint8_t* xq, const float* xs,
+                                     const uint16_t* t, const uint8_t* wq, const float* ws, const uint16_t* L2t,
+                                     const uint16_t* bias, uint16_t* y, hipStream_t stream) {
   const dim3 grid(gemm_tiles(M, N)), block(NT);
   switch (r) {
     case 16:
-      hipLaunchKernelGGL((asp_gemm_kernel<16, false>), grid, block, 0, stream, xq, xs, t, wq, ws, L2t, bias, y, nullptr, M, N, K);
+      hipLaunchKernelGGL((asp_gemm_kernel<16, false, GS>), grid, block, 0, stream, xq, xs, t, wq, ws, L2t, bias, y, nullptr, M, N, K);
       break;
     case 32:
-      hipLaunchKernelGGL((asp_gemm_kernel<32, false>), grid, block, 0, stream, xq, xs, t, wq, ws, L2t, bias, y, nullptr, M, N, K);
+      hipLaunchKernelGGL((asp_gemm_kernel<32, false, GS>), grid, block, 0, stream, xq, xs, t, wq, ws, L2t, bias, y, nullptr, M, N, K);
       break;
     case 48:
-      hipLaunchKernelGGL((asp_gemm_kernel<48, false>), grid, block, 0, stream, xq, xs, t, wq, ws, L2t, bias, y, nullptr, M, N, K);
+      hipLaunchKernelGGL((asp_gemm_kernel<48, false, GS>), grid, block, 0, stream, xq, xs, t, wq, ws, L2t, bias, y, nullptr, M, N, K);
       break;
     case 64:
-      hipLaunchKernelGGL((asp_gemm_kernel<64, false>), grid, block, 0, stream, xq, xs, t, wq, ws, L2t, bias, y, nullptr, M, N, K);
+      hipLaunchKernelGGL((asp_gemm_kernel<64, false, GS>), grid, block, 0, stream, xq, xs, t, wq, ws, L2t, bias, y, nullptr, M, N, K);
       break;
     default:
       return hipErrorInvalidValue;
@@ -378,11 +426,24 @@ hipError_t launch_asp_gemm(int M, int N, int K, int r, const uint8_t* xq, const 
   return hipGetLastError();
 }
 
-hipError_t launch_group_partials(int M, int N, int K, const uint8_t* xq, const uint8_t* wq,
+hipError_t launch_asp_gemm(int M, int N, int K, int r, int group, const uint8_t* xq, const float* xs,
+                           const uint16_t* t, const uint8_t* wq, const float* ws,
+                           const uint16_t* L2t, const uint16_t* bias, uint16_t* y,
+                           hipStream_t stream) {
+  if (M <= kSmallM) return launch_asp_gemm_small(M, N, K, r, group, xq, xs, t, wq, ws, L2t, bias, y, stream);
+  return group == 32 ? launch_asp_gemm_gs<32>(M, N, K, r, xq, xs, t, wq, ws, L2t, bias, y, stream)
+                     : launch_asp_gemm_gs<64>(M, N, K, r, xq, xs, t, wq, ws, L2t, bias, y, stream);
+}
+
+hipError_t launch_group_partials(int M, int N, int K, int group, const uint8_t* xq, const uint8_t* wq,
                                  int32_t* P, hipStream_t stream) {
-  if (M <= kSmallM) return launch_group_partials_small(M, N, K, xq, wq, P, stream);
-  hipLaunchKernelGGL((asp_gemm_kernel<32, true>), dim3(gemm_tiles(M, N)), dim3(NT), 0, stream, xq, nullptr,
-                     nullptr, wq, nullptr, nullptr, nullptr, nullptr, P, M, N, K);
+  if (M <= kSmallM) return launch_group_partials_small(M, N, K, group, xq, wq, P, stream);
+  if (group == 32)
+    hipLaunchKernelGGL((asp_gemm_kernel<32, true, 32>), dim3(gemm_tiles(M, N)), dim3(NT), 0, stream, xq, nullptr,
+                       nullptr, wq, nullptr, nullptr, nullptr, nullptr, P, M, N, K);
+  else
+    hipLaunchKernelGGL((asp_gemm_kernel<32, true, 64>), dim3(gemm_tiles(M, N)), dim3(NT), 0, stream, xq, nullptr,
+                       nullptr, wq, nullptr, nullptr, nullptr, nullptr, P, M, N, K);
   return hipGetLastError();
 }
 

@@ -14,7 +14,10 @@
 //     codes), eight groups per chunk, two chunks in flight: a K of 4096 is one
 //     memory round trip;
 //   * the activation scales are broadcast across each row of 16 lanes by DPP
-//     inside the scale multiply, as in the large-tile kernel.
+//     inside the scale multiply, as in the large-tile kernel;
+//   * group 32 (GS = 32): as in the large-tile kernel, a lane takes 8 bytes of
+//     each group of the 64-channel span and each block runs once per group with
+//     the other group's block scales at 2^-127.
 #include <type_traits>
 
 #include "qwam_device.h"
@@ -29,14 +32,15 @@ constexpr int SB = 32;             // block edge (rows and columns)
 constexpr int CH = 8;              // groups per chunk
 constexpr int KW = 4;              // waves per block, each a contiguous range of groups
 
+template <int NS>
 struct Chunk {
   uint4 a[CH], b[CH];              // packed codes of this lane's row / column and half
-  float sx[CH], sw[CH];            // the lane's activation scale (DPP source) and weight scale
+  float sx[CH][NS], sw[CH][NS];    // the lane's activation scale (DPP source) and weight scale
 };
 
 }  // namespace
 
-template <int RANK, bool PARTIALS>
+template <int RANK, bool PARTIALS, int GS>
 __global__ __launch_bounds__(64 * KW) void asp_gemm_small_kernel(
     const uint8_t* __restrict__ xq, const float* __restrict__ xs, const uint16_t* __restrict__ t,
     const uint8_t* __restrict__ wq, const float* __restrict__ ws, const uint16_t* __restrict__ L2t,
@@ -49,7 +53,9 @@ __global__ __launch_bounds__(64 * KW) void asp_gemm_small_kernel(
   const int tiles_n = (N + SB - 1) / SB;
   const int m0 = (blockIdx.x / tiles_n) * SB;
   const int n0 = (blockIdx.x % tiles_n) * SB;
+  constexpr int NS = kGroup / GS;  // scale groups per 64-channel span
   const int G = K / kGroup;
+  const int GSC = K / GS;
   const int KB = K / 2;
   // this wave's groups: [g_lo, g_hi)
   const int gpw = (G + KW - 1) / KW;
@@ -67,59 +73,76 @@ __global__ __launch_bounds__(64 * KW) void asp_gemm_small_kernel(
   // rows / columns past M / N read as zero
   const buf_rsrc a_rsrc = make_rsrc(xq + static_cast<int64_t>(m0) * KB, static_cast<uint32_t>(min(SB, M - m0)) * KB);
   const buf_rsrc b_rsrc = make_rsrc(wq + static_cast<int64_t>(n0) * KB, static_cast<uint32_t>(min(SB, N - n0)) * KB);
-  const buf_rsrc xs_rsrc = make_rsrc(xs, static_cast<uint32_t>(G) * M * 4u);
-  const buf_rsrc ws_rsrc = make_rsrc(ws, static_cast<uint32_t>(G) * N * 4u);
-  const uint32_t ab_off = static_cast<uint32_t>(frow * KB + fhalf * 16);
+  const buf_rsrc xs_rsrc = make_rsrc(xs, static_cast<uint32_t>(GSC) * M * 4u);
+  const buf_rsrc ws_rsrc = make_rsrc(ws, static_cast<uint32_t>(GSC) * N * 4u);
+  // group 64: the lane's 16-byte half of the span; group 32: 8 bytes of each group
+  const uint32_t ab_off = static_cast<uint32_t>(frow * KB + fhalf * (GS == 64 ? 16 : 8));
   const uint32_t sx_off = static_cast<uint32_t>(m0 + sx_row) * 4u;
   const uint32_t sw_off = static_cast<uint32_t>(n0 + frow) * 4u;
 
   // chunk c holds groups g_lo + CH*c .. + CH-1; in the last chunk, groups
   // past g_hi are never loaded (a row's next bytes belong to the next row) and
   // never multiplied.  FULL chunks need no per-group check.
-  auto load = [&](int c, Chunk& ch, auto full) __attribute__((always_inline)) {
+  auto load_frag = [&](buf_rsrc r, uint32_t off) __attribute__((always_inline)) {
+    if constexpr (GS == 64) {
+      return buf_load16(r, off);
+    } else {
+      const uint2 lo = buf_load8(r, off), hi = buf_load8(r, off + 16u);
+      return make_uint4(lo.x, lo.y, hi.x, hi.y);
+    }
+  };
+  auto load = [&](int c, Chunk<NS>& ch, auto full) __attribute__((always_inline)) {
 #pragma unroll
     for (int q = 0; q < CH; ++q) {
       const int g = g_lo + c * CH + q;
       if (decltype(full)::value || g < g_hi) {
-        ch.a[q] = buf_load16(a_rsrc, ab_off + static_cast<uint32_t>(g) * 32u);
-        ch.b[q] = buf_load16(b_rsrc, ab_off + static_cast<uint32_t>(g) * 32u);
+        ch.a[q] = load_frag(a_rsrc, ab_off + static_cast<uint32_t>(g) * 32u);
+        ch.b[q] = load_frag(b_rsrc, ab_off + static_cast<uint32_t>(g) * 32u);
         if (!PARTIALS) {
-          ch.sx[q] = buf_load4f(xs_rsrc, sx_off + static_cast<uint32_t>(g) * M * 4u);
-          ch.sw[q] = buf_load4f(ws_rsrc, sw_off + static_cast<uint32_t>(g) * N * 4u);
+#pragma unroll
+          for (int h = 0; h < NS; ++h) {
+            ch.sx[q][h] = buf_load4f(xs_rsrc, sx_off + static_cast<uint32_t>(NS * g + h) * M * 4u);
+            ch.sw[q][h] = buf_load4f(ws_rsrc, sw_off + static_cast<uint32_t>(NS * g + h) * N * 4u);
+          }
         }
       }
     }
   };
 
   v16f acc = v16f{};
-  auto process = [&](int c, const Chunk& ch, auto full) __attribute__((always_inline)) {
+  auto process = [&](int c, const Chunk<NS>& ch, auto full) __attribute__((always_inline)) {
 #pragma unroll
     for (int q = 0; q < CH; ++q) {
       const int g = g_lo + c * CH + q;
       if (decltype(full)::value || g < g_hi) {
-        const v16f p = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-            codes_to_e4m3(ch.a[q]), codes_to_e4m3(ch.b[q]), v16f{}, 0, 0, 0, kE8M0Code, 0, kE8M0Code);
-        if (PARTIALS) {
-          // result layout: lane l holds column l%32 and rows 8*(v/4) + 4*(l/32) + v%4
+        const v8i af = codes_to_e4m3(ch.a[q]), bf = codes_to_e4m3(ch.b[q]);
 #pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const int m = m0 + 8 * (v >> 2) + rsub + (v & 3);
-            const int n = n0 + frow;
-            if (m < M && n < N) P[(static_cast<int64_t>(m) * N + n) * G + g] = static_cast<int32_t>(p[v]);
+        for (int h = 0; h < NS; ++h) {
+          int sc = kE8M0Code;
+          if constexpr (GS == 32) sc = ((lane >> 5) == h) ? kE8M0Code : 0;
+          const v16f p = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af, bf, v16f{}, 0, 0, 0, sc, 0, sc);
+          if (PARTIALS) {
+            // result layout: lane l holds column l%32 and rows 8*(v/4) + 4*(l/32) + v%4
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+              const int m = m0 + 8 * (v >> 2) + rsub + (v & 3);
+              const int n = n0 + frow;
+              if (m < M && n < N) P[(static_cast<int64_t>(m) * N + n) * GSC + NS * g + h] = static_cast<int32_t>(p[v]);
+            }
+          } else {
+            scale_accumulate(std::make_integer_sequence<int, 16>{}, acc, p, ch.sx[q][h], ch.sw[q][h]);
           }
-        } else {
-          scale_accumulate(std::make_integer_sequence<int, 16>{}, acc, p, ch.sx[q], ch.sw[q]);
         }
       }
     }
   };
   using Full = std::true_type;
   using Tail = std::false_type;
-  auto load_any = [&](int c, Chunk& ch) __attribute__((always_inline)) {
+  auto load_any = [&](int c, Chunk<NS>& ch) __attribute__((always_inline)) {
     if (g_lo + (c + 1) * CH <= g_hi) load(c, ch, Full{});
     else load(c, ch, Tail{});
   };
-  auto process_any = [&](int c, const Chunk& ch) __attribute__((always_inline)) {
+  auto process_any = [&](int c, const Chunk<NS>& ch) __attribute__((always_inline)) {
     if (g_lo + (c + 1) * CH <= g_hi) process(c, ch, Full{});
     else process(c, ch, Tail{});
   };
@@ -143,7 +166,7 @@ __global__ __launch_bounds__(64 * KW) void asp_gemm_small_kernel(
   }
 
   // two chunks in flight: chunk c+1 is requested before chunk c is multiplied
-  Chunk c0, c1;
+  Chunk<NS> c0, c1;
   if (NC > 0) load_any(0, c0);
   for (int c = 0; c < NC; c += 2) {
     if (c + 1 < NC) load_any(c + 1, c1);
@@ -184,23 +207,23 @@ static unsigned small_blocks(int M, int N) {
   return static_cast<unsigned>(((M + SB - 1) / SB) * ((N + SB - 1) / SB));
 }
 
-hipError_t launch_asp_gemm_small(int M, int N, int K, int r, const uint8_t* xq, const float* xs,
-                                 const uint16_t* t, const uint8_t* wq, const float* ws,
-                                 const uint16_t* L2t, const uint16_t* bias, uint16_t* y,
-                                 hipStream_t stream) {
+template <int GS>
+static hipError_t launch_small_gs(int M, int N, int K, int r, const uint8_t* xq, const float* xs, const uint16_t* t,
+                                  const uint8_t* wq, const float* ws, const uint16_t* L2t, const uint16_t* bias,
+                                  uint16_t* y, hipStream_t stream) {
   const dim3 grid(small_blocks(M, N)), block(64 * KW);
   switch (r) {
     case 16:
-      hipLaunchKernelGGL((asp_gemm_small_kernel<16, false>), grid, block, 0, stream, xq, xs, t, wq, ws, L2t, bias, y, nullptr, M, N, K);
+      hipLaunchKernelGGL((asp_gemm_small_kernel<16, false, GS>), grid, block, 0, stream, xq, xs, t, wq, ws, L2t, bias, y, nullptr, M, N, K);
       break;
     case 32:
-      hipLaunchKernelGGL((asp_gemm_small_kernel<32, false>), grid, block, 0, stream, xq, xs, t, wq, ws, L2t, bias, y, nullptr, M, N, K);
+      hipLaunchKernelGGL((asp_gemm_small_kernel<32, false, GS>), grid, block, 0, stream, xq, xs, t, wq, ws, L2t, bias, y, nullptr, M, N, K);
       break;
     case 48:
-      hipLaunchKernelGGL((asp_gemm_small_kernel<48, false>), grid, block, 0, stream, xq, xs, t, wq, ws, L2t, bias, y, nullptr, M, N, K);
+      hipLaunchKernelGGL((asp_gemm_small_kernel<48, false, GS>), grid, block, 0, stream, xq, xs, t, wq, ws, L2t, bias, y, nullptr, M, N, K);
       break;
     case 64:
-      hipLaunchKernelGGL((asp_gemm_small_kernel<64, false>), grid, block, 0, stream, xq, xs, t, wq, ws, L2t, bias, y, nullptr, M, N, K);
+      hipLaunchKernelGGL((asp_gemm_small_kernel<64, false, GS>), grid, block, 0, stream, xq, xs, t, wq, ws, L2t, bias, y, nullptr, M, N, K);
       break;
     default:
       return hipErrorInvalidValue;
@@ -208,10 +231,22 @@ hipError_t launch_asp_gemm_small(int M, int N, int K, int r, const uint8_t* xq, 
   return hipGetLastError();
 }
 
-hipError_t launch_group_partials_small(int M, int N, int K, const uint8_t* xq, const uint8_t* wq, int32_t* P,
-                                       hipStream_t stream) {
-  hipLaunchKernelGGL((asp_gemm_small_kernel<32, true>), dim3(small_blocks(M, N)), dim3(64 * KW), 0, stream, xq, nullptr,
-                     nullptr, wq, nullptr, nullptr, nullptr, nullptr, P, M, N, K);
+hipError_t launch_asp_gemm_small(int M, int N, int K, int r, int group, const uint8_t* xq, const float* xs,
+                                 const uint16_t* t, const uint8_t* wq, const float* ws,
+                                 const uint16_t* L2t, const uint16_t* bias, uint16_t* y,
+                                 hipStream_t stream) {
+  return group == 32 ? launch_small_gs<32>(M, N, K, r, xq, xs, t, wq, ws, L2t, bias, y, stream)
+                     : launch_small_gs<64>(M, N, K, r, xq, xs, t, wq, ws, L2t, bias, y, stream);
+}
+
+hipError_t launch_group_partials_small(int M, int N, int K, int group, const uint8_t* xq, const uint8_t* wq,
+                                       int32_t* P, hipStream_t stream) {
+  if (group == 32)
+    hipLaunchKernelGGL((asp_gemm_small_kernel<32, true, 32>), dim3(small_blocks(M, N)), dim3(64 * KW), 0, stream, xq,
+                       nullptr, nullptr, wq, nullptr, nullptr, nullptr, nullptr, P, M, N, K);
+  else
+    hipLaunchKernelGGL((asp_gemm_small_kernel<32, true, 64>), dim3(small_blocks(M, N)), dim3(64 * KW), 0, stream, xq,
+                       nullptr, nullptr, wq, nullptr, nullptr, nullptr, nullptr, P, M, N, K);
   return hipGetLastError();
 }
 

@@ -5,30 +5,30 @@
 
 namespace qwam {
 
-hipError_t launch_pack_weights(int K, int N, const float* R, const float* smooth, uint8_t* wq,
+hipError_t launch_pack_weights(int K, int N, int group, const float* R, const float* smooth, uint8_t* wq,
                                float* ws, float* inv_smooth, hipStream_t stream);
 
-hipError_t launch_quantize_act(int M, int K, int r, const uint16_t* x, const float* inv_smooth,
+hipError_t launch_quantize_act(int M, int K, int r, int group, const uint16_t* x, const float* inv_smooth,
                                const uint16_t* L1t, uint8_t* xq, float* xs, uint16_t* t,
                                hipStream_t stream);
 
 // the 4-bit path quantizes the deflated activation x~ - L1 t (Eq. 8 / Eq. 9)
-hipError_t launch_quantize_act_deflated(int M, int K, int r, const uint16_t* x, const float* inv_smooth,
-                                        const uint16_t* L1t, uint8_t* xq, float* xs, uint16_t* t,
-                                        hipStream_t stream);
+hipError_t launch_quantize_act_deflated(int M, int K, int r, int group, const uint16_t* x,
+                                        const float* inv_smooth, const uint16_t* L1t, uint8_t* xq, float* xs,
+                                        uint16_t* t, hipStream_t stream);
 
 // the same two activation kernels with the block Hadamard rotation of Eq. 3
 // (block B, a power of two with 16 <= B <= 1024 dividing K)
-hipError_t launch_quantize_act_rotated(int M, int K, int r, int B, bool deflate, const uint16_t* x,
+hipError_t launch_quantize_act_rotated(int M, int K, int r, int group, int B, bool deflate, const uint16_t* x,
                                        const float* inv_smooth, const uint16_t* L1t, uint8_t* xq, float* xs,
                                        uint16_t* t, hipStream_t stream);
 
-hipError_t launch_asp_gemm(int M, int N, int K, int r, const uint8_t* xq, const float* xs,
+hipError_t launch_asp_gemm(int M, int N, int K, int r, int group, const uint8_t* xq, const float* xs,
                            const uint16_t* t, const uint8_t* wq, const float* ws,
                            const uint16_t* L2t, const uint16_t* bias, uint16_t* y,
                            hipStream_t stream);
 
-hipError_t launch_group_partials(int M, int N, int K, const uint8_t* xq, const uint8_t* wq,
+hipError_t launch_group_partials(int M, int N, int K, int group, const uint8_t* xq, const uint8_t* wq,
                                  int32_t* P, hipStream_t stream);
 
 // AOG accumulation: A [d][d] += gT gT^T, gT bf16 [d][n], n % 64 == 0
@@ -37,12 +37,12 @@ hipError_t launch_aog_accumulate(int d, int n, const uint16_t* gT, float* A, hip
 // the few-token GEMM (one wave per 32 x 32 block), used for M <= kSmallM
 constexpr int kSmallM = 64;
 
-hipError_t launch_asp_gemm_small(int M, int N, int K, int r, const uint8_t* xq, const float* xs,
+hipError_t launch_asp_gemm_small(int M, int N, int K, int r, int group, const uint8_t* xq, const float* xs,
                                  const uint16_t* t, const uint8_t* wq, const float* ws,
                                  const uint16_t* L2t, const uint16_t* bias, uint16_t* y,
                                  hipStream_t stream);
 
-hipError_t launch_group_partials_small(int M, int N, int K, const uint8_t* xq, const uint8_t* wq,
+hipError_t launch_group_partials_small(int M, int N, int K, int group, const uint8_t* xq, const uint8_t* wq,
                                        int32_t* P, hipStream_t stream);
 
 }  // namespace qwam

@@ -17,7 +17,7 @@ namespace qwam {
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void pack_weights_kernel(const float* __restrict__ R,
                                                            uint8_t* __restrict__ wq,
-                                                           float* __restrict__ ws, int N, int K) {
+                                                           float* __restrict__ ws, int N, int K, int g32) {
   const int G = K / kGroup;
   const int64_t team = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) >> 3;
   const int sub = threadIdx.x & 7;
@@ -35,8 +35,10 @@ __global__ __launch_bounds__(256) void pack_weights_kernel(const float* __restri
   float amax = 0.0f;
 #pragma unroll
   for (int i = 0; i < 8; ++i) amax = __builtin_fmaxf(amax, __builtin_fabsf(v[i]));
-#pragma unroll
-  for (int o = 1; o < 8; o <<= 1) amax = __builtin_fmaxf(amax, __shfl_xor(amax, o));
+  // the 8 lanes of a 64-channel span; with group 32 lanes 0-3 and 4-7 separately
+  amax = __builtin_fmaxf(amax, __shfl_xor(amax, 1));
+  amax = __builtin_fmaxf(amax, __shfl_xor(amax, 2));
+  if (!g32) amax = __builtin_fmaxf(amax, __shfl_xor(amax, 4));
   const float s = q4_scale(amax);
   const float inv = q4_inv(s);
   uint32_t t = 0;
@@ -45,7 +47,7 @@ __global__ __launch_bounds__(256) void pack_weights_kernel(const float* __restri
   if (active) {
     *reinterpret_cast<uint32_t*>(wq + static_cast<int64_t>(n) * (K / 2) + g * (kGroup / 2) + sub * 4) =
         twos_nibbles_to_code_word(t);
-    if (sub == 0) ws[static_cast<int64_t>(g) * N + n] = s;
+    if (g32 ? (sub & 3) == 0 : sub == 0) ws[static_cast<int64_t>(g32 ? 2 * g + (sub >> 2) : g) * N + n] = s;
   }
 }
 
@@ -71,7 +73,7 @@ template <int RANK, bool INV_LDS>
 __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_kernel(
     const uint16_t* __restrict__ x, const float* __restrict__ inv_smooth,
     const uint16_t* __restrict__ L1t, uint8_t* __restrict__ xq, float* __restrict__ xs,
-    uint16_t* __restrict__ t, int M, int K, int groups_per_wave) {
+    uint16_t* __restrict__ t, int M, int K, int groups_per_wave, int g32) {
   constexpr int RB = RANK / 16;
   // dynamic LDS: [nwaves][16][RANK] partial t, then (INV_LDS) [nwaves][groups_per_wave * 64] 1/lambda
   extern __shared__ float red[];
@@ -120,7 +122,7 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_kernel(
     smooth16(f.xa, f.xb, ip, v);
     // every lane of a row holds the same scale; lanes of row r write it at r
     quantize_pack_store(v, q_rsrc, q_off + static_cast<uint32_t>(g) * (kGroup / 2),
-                        row < rows ? xs + static_cast<int64_t>(g) * M + m0 + row : nullptr);
+                        xs_slot(xs, g, M, m0, row, rows, chunk, g32), g32);
     t_step_bf16<RB>(v, f.l1, acc);
   };
 
@@ -163,7 +165,7 @@ template <int RANK, bool INV_LDS>
 __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_deflated_kernel(
     const uint16_t* __restrict__ x, const float* __restrict__ inv_smooth,
     const uint16_t* __restrict__ L1t, uint8_t* __restrict__ xq, float* __restrict__ xs,
-    uint16_t* __restrict__ t, int M, int K, int groups_per_wave) {
+    uint16_t* __restrict__ t, int M, int K, int groups_per_wave, int g32) {
   constexpr int RB = RANK / 16;
   // dynamic LDS: [nwaves][16][RANK] double partial t | [16][RANK] float -t |
   // (INV_LDS) [nwaves][groups_per_wave * 64] 1/lambda
@@ -243,7 +245,7 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_deflated_
     smooth16(f.xa, f.xb, inv_ptr(g), v);
     deflate_step<RANK>(v, f.l1, tn_row);
     quantize_pack_store(v, q_rsrc, q_off + static_cast<uint32_t>(g) * (kGroup / 2),
-                        row < rows ? xs + static_cast<int64_t>(g) * M + m0 + row : nullptr);
+                        xs_slot(xs, g, M, m0, row, rows, chunk, g32), g32);
   };
   if (g_begin < g_end) {
     DeflFetch<RANK> fa, fb;
@@ -260,20 +262,21 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_deflated_
 }
 
 // ---------------------------------------------------------------------------
-hipError_t launch_pack_weights(int K, int N, const float* R, const float* smooth, uint8_t* wq,
+hipError_t launch_pack_weights(int K, int N, int group, const float* R, const float* smooth, uint8_t* wq,
                                float* ws, float* inv_smooth, hipStream_t stream) {
   const int64_t teams = static_cast<int64_t>(N) * (K / kGroup);
   const int64_t blocks = (teams * 8 + 255) / 256;
   hipLaunchKernelGGL(pack_weights_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, R,
-                     wq, ws, N, K);
+                     wq, ws, N, K, group == 32 ? 1 : 0);
   hipLaunchKernelGGL(inverse_smoothing_kernel, dim3((K + 255) / 256), dim3(256), 0, stream, smooth,
                      inv_smooth, K);
   return hipGetLastError();
 }
 
-hipError_t launch_quantize_act(int M, int K, int r, const uint16_t* x, const float* inv_smooth,
+hipError_t launch_quantize_act(int M, int K, int r, int group, const uint16_t* x, const float* inv_smooth,
                                const uint16_t* L1t, uint8_t* xq, float* xs, uint16_t* t,
                                hipStream_t stream) {
+  const int g32 = group == 32 ? 1 : 0;
   const int G = K / kGroup;
   // 1/lambda is staged in LDS when the slice fits (K <= 16384); larger K reads it from global memory
   const bool inv_lds = K <= 16384;
@@ -288,10 +291,10 @@ hipError_t launch_quantize_act(int M, int K, int r, const uint16_t* x, const flo
     }
     if (inv_lds)
       hipLaunchKernelGGL(kernel_lds, dim3((M + 15) / 16), dim3(64 * nwaves), lds, stream, x, inv_smooth, L1t,
-                         xq, xs, t, M, K, gpw);
+                         xq, xs, t, M, K, gpw, g32);
     else
       hipLaunchKernelGGL(kernel_global, dim3((M + 15) / 16), dim3(64 * nwaves), lds, stream, x, inv_smooth, L1t,
-                         xq, xs, t, M, K, gpw);
+                         xq, xs, t, M, K, gpw, g32);
     return hipGetLastError();
   };
   switch (r) {
@@ -303,9 +306,10 @@ hipError_t launch_quantize_act(int M, int K, int r, const uint16_t* x, const flo
   }
 }
 
-hipError_t launch_quantize_act_deflated(int M, int K, int r, const uint16_t* x, const float* inv_smooth,
-                                        const uint16_t* L1t, uint8_t* xq, float* xs, uint16_t* t,
-                                        hipStream_t stream) {
+hipError_t launch_quantize_act_deflated(int M, int K, int r, int group, const uint16_t* x,
+                                        const float* inv_smooth, const uint16_t* L1t, uint8_t* xq, float* xs,
+                                        uint16_t* t, hipStream_t stream) {
+  const int g32 = group == 32 ? 1 : 0;
   const int G = K / kGroup;
   const bool inv_lds = K <= 16384;
   auto go = [&](auto kernel_lds, auto kernel_global, int max_waves) {
@@ -320,10 +324,10 @@ hipError_t launch_quantize_act_deflated(int M, int K, int r, const uint16_t* x, 
     }
     if (inv_lds)
       hipLaunchKernelGGL(kernel_lds, dim3((M + 15) / 16), dim3(64 * nwaves), lds, stream, x, inv_smooth, L1t,
-                         xq, xs, t, M, K, gpw);
+                         xq, xs, t, M, K, gpw, g32);
     else
       hipLaunchKernelGGL(kernel_global, dim3((M + 15) / 16), dim3(64 * nwaves), lds, stream, x, inv_smooth, L1t,
-                         xq, xs, t, M, K, gpw);
+                         xq, xs, t, M, K, gpw, g32);
     return hipGetLastError();
   };
   switch (r) {

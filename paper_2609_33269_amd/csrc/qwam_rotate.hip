@@ -74,7 +74,7 @@ template <int RANK, bool DEFLATE>
 __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_rotated_kernel(
     const uint16_t* __restrict__ x, const float* __restrict__ inv_smooth,
     const uint16_t* __restrict__ L1t, uint8_t* __restrict__ xq, float* __restrict__ xs,
-    uint16_t* __restrict__ t, int M, int K, int logB, int T, float hscale) {
+    uint16_t* __restrict__ t, int M, int K, int logB, int T, float hscale, int g32) {
   constexpr int RB = RANK / 16;
   constexpr int kMaxPerWave = per_wave<RANK>();
   using Acc = std::conditional_t<DEFLATE, double, float>;
@@ -145,7 +145,7 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_rotated_k
   };
   auto store_codes = [&](int g, const float (&v)[16]) __attribute__((always_inline)) {
     quantize_pack_store(v, q_rsrc, q_off + static_cast<uint32_t>(g) * (kGroup / 2),
-                        row < rows ? xs + static_cast<int64_t>(g) * M + m0 + row : nullptr);
+                        xs_slot(xs, g, M, m0, row, rows, chunk, g32), g32);
   };
 
   std::conditional_t<DEFLATE, v4d, v4f> acc[RB];
@@ -226,7 +226,7 @@ static int rotate_tile_width(int K, int B) {
   return base;
 }
 
-hipError_t launch_quantize_act_rotated(int M, int K, int r, int B, bool deflate, const uint16_t* x,
+hipError_t launch_quantize_act_rotated(int M, int K, int r, int group, int B, bool deflate, const uint16_t* x,
                                        const float* inv_smooth, const uint16_t* L1t, uint8_t* xq, float* xs,
                                        uint16_t* t, hipStream_t stream) {
   int logB = 0;
@@ -245,7 +245,7 @@ hipError_t launch_quantize_act_rotated(int M, int K, int r, int B, bool deflate,
       if (e != hipSuccess) return e;
     }
     hipLaunchKernelGGL(kernel, dim3((M + 15) / 16), dim3(64 * nwaves), lds, stream, x, inv_smooth, L1t, xq, xs, t,
-                       M, K, logB, T, hscale);
+                       M, K, logB, T, hscale, group == 32 ? 1 : 0);
     return hipGetLastError();
   };
 #define QWAM_ROT_CASE(R)                                                                            \

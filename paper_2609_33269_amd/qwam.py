@@ -113,11 +113,12 @@ class PackedLayer:
     L2t: torch.Tensor         # bf16 [N][r]
     bias: Optional[torch.Tensor] = None   # bf16 [N]
     hadamard: int = 0                     # block size of the rotation (Eq. 3), 0 = none
+    group: int = GROUP                    # channels per scale: 64, or 32 (App. B.1)
 
     def c_struct(self) -> QwamLayerC:
-        G = self.K // GROUP
+        G = self.K // self.group
         c = QwamLayerC()
-        c.K, c.N, c.r, c.group, c.hadamard = self.K, self.N, self.r, GROUP, self.hadamard
+        c.K, c.N, c.r, c.group, c.hadamard = self.K, self.N, self.r, self.group, self.hadamard
         c.wq = _req(self.wq, "wq", torch.uint8, (self.N, self.K // 2))
         c.ws = _req(self.ws, "ws", torch.float32, (G, self.N))
         c.inv_smooth = _req(self.inv_smooth, "inv_smooth", torch.float32, (self.K,))
@@ -127,15 +128,15 @@ class PackedLayer:
         return c
 
 
-def pack_weights(R: torch.Tensor, smooth: torch.Tensor, stream=None):
+def pack_weights(R: torch.Tensor, smooth: torch.Tensor, stream=None, group: int = GROUP):
     """qwam_pack_weights: R float32 [N][K], smooth float32 [K] ->
-    (wq uint8 [N][K/2], ws float32 [K/64][N], inv_smooth float32 [K])."""
+    (wq uint8 [N][K/2], ws float32 [K/group][N], inv_smooth float32 [K])."""
     N, K = R.shape
     dev = R.device
     wq = torch.empty((N, K // 2), dtype=torch.uint8, device=dev)
-    ws = torch.empty((K // GROUP, N), dtype=torch.float32, device=dev)
+    ws = torch.empty((K // group, N), dtype=torch.float32, device=dev)
     inv = torch.empty((K,), dtype=torch.float32, device=dev)
-    st = lib().qwam_pack_weights(K, N, GROUP, _req(R, "R", torch.float32, (N, K)),
+    st = lib().qwam_pack_weights(K, N, group, _req(R, "R", torch.float32, (N, K)),
                                  _req(smooth, "smooth", torch.float32, (K,)),
                                  wq.data_ptr(), ws.data_ptr(), inv.data_ptr(), _stream_ptr(stream))
     _check("qwam_pack_weights", st)
@@ -143,16 +144,17 @@ def pack_weights(R: torch.Tensor, smooth: torch.Tensor, stream=None):
 
 
 def make_layer(R: torch.Tensor, smooth: torch.Tensor, L1: torch.Tensor, L2: torch.Tensor,
-               bias: Optional[torch.Tensor] = None, stream=None, hadamard: int = 0) -> PackedLayer:
+               bias: Optional[torch.Tensor] = None, stream=None, hadamard: int = 0,
+               group: int = GROUP) -> PackedLayer:
     """Pack R and lambda and lay out the branch factors: L1 bf16 [K][r] and
     L2 bf16 [r][N] are stored transposed (L1t [r][K], L2t [N][r]).  With
     `hadamard` = B, R, L1 and L2 must be those of the rotated layer (Eq. 3)."""
     N, K = R.shape
     r = L1.shape[1]
-    wq, ws, inv = pack_weights(R, smooth, stream)
+    wq, ws, inv = pack_weights(R, smooth, stream, group)
     return PackedLayer(K=K, N=N, r=r, wq=wq, ws=ws, inv_smooth=inv,
                        L1t=L1.t().contiguous(), L2t=L2.t().contiguous(),
-                       bias=None if bias is None else bias.contiguous(), hadamard=hadamard)
+                       bias=None if bias is None else bias.contiguous(), hadamard=hadamard, group=group)
 
 
 def quantize_act(layer: PackedLayer, x: torch.Tensor, stream=None, out=None):
@@ -173,14 +175,14 @@ def _quantize(fn, name: str, layer: PackedLayer, x: torch.Tensor, stream, out):
     dev = x.device
     if out is None:
         xq = torch.empty((M, layer.K // 2), dtype=torch.uint8, device=dev)
-        xs = torch.empty((layer.K // GROUP, M), dtype=torch.float32, device=dev)
+        xs = torch.empty((layer.K // layer.group, M), dtype=torch.float32, device=dev)
         t = torch.empty((M, layer.r), dtype=torch.bfloat16, device=dev)
     else:
         xq, xs, t = out
     c = layer.c_struct()
     st = fn(ctypes.byref(c), M, _req(x, "x", torch.bfloat16, (M, layer.K)),
             _req(xq, "xq", torch.uint8, (M, layer.K // 2)),
-            _req(xs, "xs", torch.float32, (layer.K // GROUP, M)),
+            _req(xs, "xs", torch.float32, (layer.K // layer.group, M)),
             _req(t, "t", torch.bfloat16, (M, layer.r)), _stream_ptr(stream))
     _check(name, st)
     return xq, xs, t
@@ -190,7 +192,7 @@ def asp_linear(layer: PackedLayer, xq: torch.Tensor, xs: torch.Tensor, t: torch.
                out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
     """qwam_asp_linear: -> y bf16 [M][N]."""
     M = xq.shape[0]
-    G = layer.K // GROUP
+    G = layer.K // layer.group
     y = torch.empty((M, layer.N), dtype=torch.bfloat16, device=xq.device) if out is None else out
     c = layer.c_struct()
     st = lib().qwam_asp_linear(ctypes.byref(c), M, _req(xq, "xq", torch.uint8, (M, layer.K // 2)),
@@ -209,9 +211,9 @@ def forward(layer: PackedLayer, x: torch.Tensor, stream=None, deflate: bool = Fa
 
 
 def debug_group_partials(layer: PackedLayer, xq: torch.Tensor, stream=None) -> torch.Tensor:
-    """qwam_debug_group_partials: -> P int32 [M][N][K/64] (exact integer partials)."""
+    """qwam_debug_group_partials: -> P int32 [M][N][K/group] (exact integer partials)."""
     M = xq.shape[0]
-    G = layer.K // GROUP
+    G = layer.K // layer.group
     P = torch.empty((M, layer.N, G), dtype=torch.int32, device=xq.device)
     c = layer.c_struct()
     st = lib().qwam_debug_group_partials(ctypes.byref(c), M,

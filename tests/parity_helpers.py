@@ -45,7 +45,7 @@ def gpu_layer(factors, bias_bits=None) -> Q.PackedLayer:
     L2 = bf16_dev(factors["L2"])
     bias = None if bias_bits is None else bf16_dev(bias_bits)
     return Q.make_layer(f32_dev(factors["R"]), f32_dev(factors["lam"]), L1, L2, bias,
-                        hadamard=int(factors.get("hadamard", 0)))
+                        hadamard=int(factors.get("hadamard", 0)), group=int(factors.get("group", 64)))
 
 
 def rel_fro(a: np.ndarray, b: np.ndarray) -> float:

@@ -38,7 +38,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == set(Q.SIGNATURES), "binding and header disagree"
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.qwam_abi_version() == 5
+    assert lib.qwam_abi_version() == 6
     assert lib.qwam_status_string(3) == b"QWAM_ERR_MISALIGNED"
 
 
@@ -61,7 +61,7 @@ def _lin(lib, layer, M=64, xq=FAKE, xs=FAKE, t=FAKE, y=FAKE):
 
 
 @pytest.mark.parametrize("K,N,group,status", [
-    (256, 256, 32, INVALID), (100, 256, 64, INVALID), (0, 256, 64, INVALID), (256, 24, 64, INVALID),
+    (256, 256, 16, INVALID), (256, 256, 128, INVALID), (96, 256, 32, INVALID), (100, 256, 64, INVALID), (0, 256, 64, INVALID), (256, 24, 64, INVALID),
     (256, 0, 64, INVALID), (-64, 256, 64, INVALID), (131072, 256, 64, UNSUPPORTED),
     (256, 1 << 21, 64, UNSUPPORTED)])
 def test_pack_rejects_bad_shapes(lib, K, N, group, status):

@@ -1,0 +1,109 @@
+"""GPU parity of the group-32 variant (App. B.1's group size: one float32
+scale per 32 consecutive input channels, for weights and activations).
+
+Bit-exact: weight and activation codes, bytes and scales, the int32 group
+partials (two per 64-channel span, each from its own matrix-core pass), and
+with deflation also t.  y within the relative Frobenius tolerance of
+parity_helpers.check_y of the float64 oracle on the same codes.  Covers the
+large-tile GEMM (M > 64) and the few-token GEMM (M <= 64), and the plain,
+deflated and rotated activation kernels.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import qwam_oracle as O
+from paper_2609_33269_amd import inputs as I
+from paper_2609_33269_amd import qwam as Q
+
+from parity_helpers import bits, check_t, check_y, gpu_layer, log, oracle_factors, rel_fro, run_gpu, y_tolerance
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    Q.lib()
+
+
+def _g32_parity(draws, factors, bias_bits=None, deflate=False):
+    M, K, N = draws.shape.M, draws.shape.K, draws.shape.N
+    f = dict(factors, group=32)
+    log(f"  group-32 parity {draws.shape.name}: M={M} K={K} N={N} r={f['L1'].shape[1]} "
+        f"B={f.get('hadamard', 0)} deflate={deflate} bias={bias_bits is not None}")
+    ref = O.asp_linear(draws.x, f, bias_bits=bias_bits, deflate=deflate)
+    layer = gpu_layer(f, bias_bits)
+    assert layer.group == 32 and layer.ws.shape == (K // 32, N)
+    x, xq, xs, t, y = run_gpu(layer, draws.x, deflate=deflate)
+    assert (layer.wq.cpu().numpy() == ref["wq"]).all(), "packed weight bytes"
+    assert (layer.ws.cpu().numpy() == ref["sw"].T).all(), "weight scales"
+    assert (xq.cpu().numpy() == ref["xq"]).all(), "packed activation bytes"
+    assert (xs.cpu().numpy() == ref["sx"].T).all(), "activation scales"
+    if deflate:
+        assert (bits(t) == ref["t"]).all(), "t"
+    else:
+        check_t(bits(t), ref["t"], O.transformed_activations(draws.x, ref["inv_lam"], f.get("hadamard", 0)),
+                f["L1"])
+    P = Q.debug_group_partials(layer, xq)
+    torch.cuda.synchronize()
+    assert P.shape == (M, N, K // 32)
+    assert (P.cpu().numpy() == ref["P"]).all(), "int32 group-32 partials"
+    check_y(bits(y), ref["y"])
+
+
+G32_SHAPES = [
+    # M, K, N, r, bias
+    (1, 64, 16, 16, False),
+    (15, 128, 48, 32, True),
+    (64, 1024, 4096, 16, False),     # the few-token GEMM at an action-expert shape
+    (65, 192, 144, 48, True),        # the large-tile GEMM from M = 65 on
+    (129, 256, 272, 64, False),
+    (200, 320, 400, 32, True),
+    (257, 640, 256, 32, False),
+]
+
+
+@pytest.mark.parametrize("M,K,N,r,bias", G32_SHAPES)
+def test_group32_shapes(M, K, N, r, bias):
+    d = I.custom(M=M, K=K, N=N, r=r, seed=M * 17 + K, n_outliers=max(1, K // 100), with_bias=bias)
+    _g32_parity(d, oracle_factors(d, r), d.bias)
+
+
+@pytest.mark.parametrize("M,K,N,r", [(33, 256, 96, 32), (130, 1024, 272, 16)])
+@pytest.mark.parametrize("rotated,deflate", [(False, True), (True, False), (True, True)])
+def test_group32_with_deflation_and_rotation(M, K, N, r, rotated, deflate):
+    d = I.custom(M=M, K=K, N=N, r=r, seed=M * 19 + K, n_outliers=2)
+    _g32_parity(d, oracle_factors(d, r, hadamard=rotated), deflate=deflate)
+
+
+def test_group32_full_size_sampled():
+    """The FFN up-projection at full size with group 32 (the paper's setting,
+    rotated and deflated): every code and scale, y and the partials on sampled
+    tokens."""
+    draws = I.video_dit_ffn_up()
+    M, K, N = draws.shape.M, draws.shape.K, draws.shape.N
+    log(f"  group-32 full size {draws.shape.name}")
+    f = dict(oracle_factors(draws, hadamard=True), group=32)
+    wq, sw, inv_lam, _ = O.pack_weights(f["R"], f["lam"], 32)
+    layer = gpu_layer(f)
+    x, xq, xs, t, y = run_gpu(layer, draws.x, deflate=True)
+    assert (layer.wq.cpu().numpy() == wq).all() and (layer.ws.cpu().numpy() == sw.T).all()
+    xq_ref, sx_ref, t_ref, _, _ = O.quantize_activations_deflated(draws.x, inv_lam, f["L1"], f["hadamard"], 32)
+    assert (bits(t) == t_ref).all(), "t"
+    assert (xq.cpu().numpy() == xq_ref).all(), "packed activation bytes"
+    assert (xs.cpu().numpy() == sx_ref.T).all(), "activation scales"
+    rng = np.random.default_rng(M + 32)
+    rows = np.array(sorted(set([0, M - 1]) | set(int(v) for v in rng.choice(M, 12, replace=False))))
+    y_ref, P_ref = O.asp_output_rows(xq_ref[rows], sx_ref[rows], t_ref[rows], wq, sw, f["L2"])
+    sel = torch.from_numpy(rows).cuda()
+    err = rel_fro(O.bf16_bits_to_f64(bits(y[sel])), y_ref)
+    log(f"    y rel Frobenius error on {len(rows)} sampled tokens {err:.3e}")
+    assert err <= y_tolerance(y_ref)
+    P = Q.debug_group_partials(layer, xq[sel].contiguous())
+    torch.cuda.synchronize()
+    assert (P.cpu().numpy() == P_ref).all(), "int32 group partials of sampled tokens"
+    del x, xq, xs, t, y, P, layer
+    torch.cuda.empty_cache()
