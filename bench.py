@@ -80,7 +80,7 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 VALU_OPS_PER_OUTPUT_GROUP = 2  # scale product, fused multiply-add
 METRIC = "ASP W4A4+r32 linear: effective TOPS & % int8 MFMA peak at 4096×3072×14336"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_asp_gemm_ffn_up.json")
-GEMM_SRCS = [os.path.join(ROOT, "paper_2609_33269_amd", "csrc", f) for f in ("qwam_gemm.hip", "qwam_device.h")]
+GEMM_SRCS = [os.path.join(ROOT, "paper_2609_33269_amd", "csrc", f) for f in ("qwam_gemm.hip", "qwam_device.h", "qwam_mfma.h")]
 GEMM_KERNEL = "asp_gemm_kernel<32, false, 64>"
 COPY_KERNEL = "neg_kernel"
 
