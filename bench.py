@@ -203,6 +203,7 @@ def small_m_report(args):
             qwam.asp_linear(L, xq, xs, t, out=y)
 
         us = graph_us(call, nrot)
+        us_fused = graph_us(lambda i: qwam.asp_layer(layers[i], x0, out=y), nrot)
         us1 = graph_us(lambda i: qwam.quantize_act(layers[i], x0, out=(xq, xs, t)), nrot)
         us2 = graph_us(lambda i: qwam.asp_linear(layers[i], xq, xs, t, out=y), nrot)
         # the bf16 linear it replaces (hipBLASLt through torch), same graph method,
@@ -218,6 +219,8 @@ def small_m_report(args):
         print(json.dumps({
             "workload": "action_expert", "M": Ms, "K": Ka, "N": Ns, "r": ra,
             "us_per_call": round(us, 2), "us_quantize_act": round(us1, 2), "us_asp_gemm": round(us2, 2),
+            "us_fused_layer": round(us_fused, 2), "fused_GBs": round((b1 + b2) / (us_fused * 1e-6) / 1e9, 1),
+            "fused_speedup_vs_bf16_linear": round(us_bf16 / us_fused, 3),
             "algorithmic_bytes": b1 + b2, "GBs": round((b1 + b2) / (us * 1e-6) / 1e9, 1),
             "gemm_GBs": round(b2 / (us2 * 1e-6) / 1e9, 1),
             "hbm_frac": round((b1 + b2) / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),

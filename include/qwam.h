@@ -96,7 +96,7 @@
 extern "C" {
 #endif
 
-#define QWAM_ABI_VERSION 6
+#define QWAM_ABI_VERSION 7
 #define QWAM_GROUP 64
 
 typedef enum {
@@ -189,6 +189,22 @@ qwam_status qwam_quantize_act_deflated(const qwam_layer *L, int32_t M, const uin
 qwam_status qwam_asp_linear(const qwam_layer *L, int32_t M, const uint8_t *xq,
                             const float *xs, const uint16_t *t, uint16_t *y,
                             void *stream);
+
+/*
+ * The whole layer for few tokens in one call: the activation step of
+ * qwam_quantize_act and the GEMM of qwam_asp_linear fused into one launch
+ * (App. B.1 deploys them as two kernels; with at most 64 tokens both are
+ * latency-bound, so every workgroup quantizes the tokens it needs itself).
+ * The codes, scales and t are those qwam_quantize_act produces (t may differ
+ * in float32 summation order); y as qwam_asp_linear.
+ *   L   in   packed layer: r = 16 or 32, group 64, hadamard 0, K <= 16384
+ *   M   in   1 <= M <= 64 (QWAM_ERR_UNSUPPORTED above)
+ *   x   in   bf16 [M][K]
+ *   y   out  bf16 [M][N]
+ *   xq, xs, t  out, optional: all NULL, or all set (as for qwam_quantize_act)
+ */
+qwam_status qwam_asp_layer(const qwam_layer *L, int32_t M, const uint16_t *x, uint16_t *y,
+                           uint8_t *xq, float *xs, uint16_t *t, void *stream);
 
 /*
  * Test access to the exact integer group partials of qwam_asp_linear's

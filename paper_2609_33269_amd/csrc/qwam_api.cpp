@@ -189,6 +189,38 @@ qwam_status qwam_debug_group_partials(const qwam_layer* L, int32_t M, const uint
                                                   static_cast<hipStream_t>(stream)));
 }
 
+qwam_status qwam_asp_layer(const qwam_layer* L, int32_t M, const uint16_t* x, uint16_t* y, uint8_t* xq, float* xs,
+                           uint16_t* t, void* stream) {
+  const char* fn = "qwam_asp_layer";
+  qwam_status s = check_layer(fn, L, true);
+  if (s != QWAM_OK) return s;
+  if ((s = check_m(fn, M)) != QWAM_OK) return s;
+  if (M > qwam::kSmallM) return fail(QWAM_ERR_UNSUPPORTED, "%s: M = %d exceeds %d", fn, M, qwam::kSmallM);
+  if (L->r != 16 && L->r != 32) return fail(QWAM_ERR_UNSUPPORTED, "%s: rank r must be 16 or 32 (got %d)", fn, L->r);
+  if (L->group != QWAM_GROUP || L->hadamard != 0)
+    return fail(QWAM_ERR_UNSUPPORTED, "%s: group 64 without rotation only", fn);
+  if (L->K > 16384) return fail(QWAM_ERR_UNSUPPORTED, "%s: K = %d exceeds 16384", fn, L->K);
+  QWAM_REQUIRE_PTR(L->wq);
+  QWAM_REQUIRE_PTR(L->ws);
+  QWAM_REQUIRE_PTR(L->inv_smooth);
+  QWAM_REQUIRE_PTR(L->L1t);
+  QWAM_REQUIRE_PTR(L->L2t);
+  if (L->bias != nullptr && !aligned16(L->bias))
+    return fail(QWAM_ERR_MISALIGNED, "%s: bias is not 16-byte aligned", fn);
+  QWAM_REQUIRE_PTR(x);
+  QWAM_REQUIRE_PTR(y);
+  const int given = (xq != nullptr) + (xs != nullptr) + (t != nullptr);
+  if (given != 0 && given != 3) return fail(QWAM_ERR_INVALID_ARG, "%s: xq, xs and t must be all NULL or all set", fn);
+  if (given == 3) {
+    QWAM_REQUIRE_PTR(xq);
+    QWAM_REQUIRE_PTR(xs);
+    QWAM_REQUIRE_PTR(t);
+  }
+  if ((s = check_device(fn)) != QWAM_OK) return s;
+  return launched(fn, qwam::launch_asp_layer_small(M, L->N, L->K, L->r, x, L->inv_smooth, L->L1t, L->wq, L->ws,
+                                                   L->L2t, L->bias, y, xq, xs, t, static_cast<hipStream_t>(stream)));
+}
+
 qwam_status qwam_aog_accumulate(int32_t d, int32_t n, const uint16_t* gT, float* A, void* stream) {
   const char* fn = "qwam_aog_accumulate";
   if (d < 16 || d % 16 != 0)

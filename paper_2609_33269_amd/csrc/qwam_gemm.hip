@@ -31,10 +31,12 @@
 //     code * 2^-9 (subnormals and the first binade are evenly spaced).  The
 //     instruction's E8M0 block scales (2^9 on each side) cancel the 2^-18, so
 //     the float32 result is the integer partial P itself, exactly (|P| <= 3136);
-//   * the MFMAs of the next block are issued before the scaling of the current
-//     one (scale product, fused multiply-add into float32 accumulators), so the
-//     VALU never waits on a just-issued MFMA: two VALU operations per output
-//     and group;
+//   * the per-output scale products sx[m] * sw[n] of a group are an outer
+//     product: one v_mfma_f32_32x32x1_2b_f32 (K = 1, one rounding per product,
+//     as a VALU multiply) gives them for two 32 x 32 blocks at once, in the
+//     result layout of the integer blocks, so the VALU is left with one fused
+//     multiply-add per output and group; the MFMAs of the next block are
+//     issued before the update of the current one;
 //   * workgroups are mapped XCD-major: the 8 XCDs each take a contiguous range
 //     of tiles, ordered in bands of 8 tile-rows so that the concurrently
 //     resident tiles of one XCD share their A and B panels in its L2;
@@ -211,10 +213,13 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
   const int sx_row = 8 * ((lane & 15) >> 2) + 4 * (lane >> 5) + (lane & 3);
 
   // LDS data of one 64-channel span: packed A / B fragments and the lane's
-  // scales (NS groups).  With group 32 a fragment is 8 bytes of each group.
+  // scales (NS groups): the activation scale of row l%32 of each row block
+  // (A operand of the scale product) and the weight scale of column l%32 of
+  // column block l/32 (B operand).  With group 32 a fragment is 8 bytes of
+  // each group.
   struct GroupData {
     uint4 a[2], b[2];
-    float sx[2][NS], sw[2][NS];
+    float sx[2][NS], sw[NS];
   };
   // Reads group q's data one group ahead of its use.  The loads are volatile
   // and followed by a compiler-only fence, so they are issued here and not
@@ -239,9 +244,8 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
 #pragma unroll
       for (int h = 0; h < NS; ++h) {
 #pragma unroll
-        for (int i = 0; i < 2; ++i) d.sx[i][h] = lds_load4_volatile(&cur.sx[NS * q + h][wm * 64 + i * 32 + sx_row]);
-#pragma unroll
-        for (int j = 0; j < 2; ++j) d.sw[j][h] = lds_load4_volatile(&cur.sw[NS * q + h][wn * 64 + j * 32 + frow]);
+        for (int i = 0; i < 2; ++i) d.sx[i][h] = lds_load4_volatile(&cur.sx[NS * q + h][wm * 64 + i * 32 + frow]);
+        d.sw[h] = lds_load4_volatile(&cur.sw[NS * q + h][wn * 64 + fhalf * 32 + frow]);
       }
     }
     asm volatile("" ::: "memory");
@@ -264,9 +268,14 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
       if constexpr (GS == 32) sc = ((lane >> 5) == h) ? kE8M0Code : 0;
       return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af[i], bf[j], v16f{}, 0, 0, 0, sc, 0, sc);
     };
+    // scale products of row block i and both column blocks, group h:
+    // registers 0-15 belong to column block 0, 16-31 to column block 1
+    auto scale_block = [&](int i, int h) __attribute__((always_inline)) {
+      return __builtin_amdgcn_mfma_f32_32x32x1f32(d.sx[i][h], d.sw[h], v32f{}, 0, 0, 0);
+    };
     // result layout of a 32x32 block: lane l holds column l%32 and rows
     // 8*(v/4) + 4*(l/32) + v%4, v = 0..15
-    auto consume = [&](int i, int j, int h, const v16f& p) __attribute__((always_inline)) {
+    auto consume = [&](int i, int j, int h, const v16f& p, const v32f& sc) __attribute__((always_inline)) {
       if (PARTIALS) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
@@ -275,34 +284,26 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
           if (m < M && n < N) P[(static_cast<int64_t>(m) * N + n) * GSC + NS * g + h] = static_cast<int32_t>(p[v]);
         }
       } else {
-        scale_accumulate(std::make_integer_sequence<int, 16>{}, accf[i][j], p, d.sx[i][h], d.sw[j][h]);
+#pragma unroll
+        for (int v = 0; v < 16; ++v) accf[i][j][v] = __builtin_fmaf(p[v], sc[16 * j + v], accf[i][j][v]);
       }
     };
     // software pipeline: three MFMAs in flight before the first update, so
     // that no update waits for the block it reads
-    if constexpr (GS == 64) {
-      const v16f p00 = mfma_block(0, 0, 0);
-      const v16f p01 = mfma_block(0, 1, 0);
-      const v16f p10 = mfma_block(1, 0, 0);
-      consume(0, 0, 0, p00);
-      const v16f p11 = mfma_block(1, 1, 0);
-      consume(0, 1, 0, p01);
-      consume(1, 0, 0, p10);
-      consume(1, 1, 0, p11);
-    } else {
-      // eight blocks (2 x 2 tiles x 2 groups), two in flight: three would not
-      // fit the registers next to the doubled scale data
-      v16f p0 = mfma_block(0, 0, 0);
-      v16f p1 = mfma_block(0, 0, 1);
+    // per group h and row block i: the scale products (one MFMA for both
+    // column blocks), the two integer blocks, then their updates; each update
+    // reads results issued at least one MFMA earlier
+    const v32f none = {};
 #pragma unroll
-      for (int b = 0; b < 8; ++b) {
-        const int i = b >> 2, j = (b >> 1) & 1, h = b & 1;
-        const v16f cur_p = p0;
-        p0 = p1;
-        if (b + 2 < 8) p1 = mfma_block((b + 2) >> 2, ((b + 2) >> 1) & 1, (b + 2) & 1);
-        consume(i, j, h, cur_p);
+    for (int h = 0; h < NS; ++h)
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const v32f sc = PARTIALS ? none : scale_block(i, h);
+        const v16f p0 = mfma_block(i, 0, h);
+        const v16f p1 = mfma_block(i, 1, h);
+        consume(i, 0, h, p0, sc);
+        consume(i, 1, h, p1, sc);
       }
-    }
   };
 
   // one stage: `cur` holds stage s (groups KC*s ..), `nxt` (the stage of s-1)

@@ -42,6 +42,13 @@ hipError_t launch_asp_gemm_small(int M, int N, int K, int r, int group, const ui
                                  const uint16_t* L2t, const uint16_t* bias, uint16_t* y,
                                  hipStream_t stream);
 
+// the whole layer for M <= kSmallM in one launch (r = 16 or 32, group 64, no
+// rotation); xq / xs / t are optional outputs (all null or none)
+hipError_t launch_asp_layer_small(int M, int N, int K, int r, const uint16_t* x, const float* inv_smooth,
+                                  const uint16_t* L1t, const uint8_t* wq, const float* ws, const uint16_t* L2t,
+                                  const uint16_t* bias, uint16_t* y, uint8_t* xq, float* xs, uint16_t* t,
+                                  hipStream_t stream);
+
 hipError_t launch_group_partials_small(int M, int N, int K, int group, const uint8_t* xq, const uint8_t* wq,
                                        int32_t* P, hipStream_t stream);
 

@@ -1,0 +1,253 @@
+// The whole ASP layer for few tokens (M <= 64, the action-expert layers) in
+// one launch: the activation step of qwam_quantize_act and the GEMM of
+// qwam_asp_linear, fused.  With so few tokens both steps are latency-bound
+// (a launch floor of ~1.5 us each and a dependent memory round trip in
+// between), so every workgroup quantizes the tokens it needs itself.
+//
+//   * a workgroup owns a 32 x 32 block of y (32 tokens x 32 output channels)
+//     and all of K; its 4 waves split the 64-channel spans into contiguous
+//     ranges, one per wave;
+//   * lane l of a wave holds token l % 32 and channels 32*(l/32) .. +31 of the
+//     current span: the A-operand rows of v_mfma_scale_f32_32x32x64_f8f6f4.
+//     It smooths them (x * 1/lambda, fetched with x), takes the
+//     span's absmax with its partner lane l ^ 32, quantizes (Eq. 2, the same
+//     arithmetic as the activation kernel, so the codes are identical), packs
+//     the codes into code words and turns those into e4m3 bytes exactly as the
+//     weights' code words are turned (codes_to_e4m3): both operands then carry
+//     the same permutation of k, and the MFMA returns the span's exact integer
+//     partial;
+//   * the same registers feed the down-projection t = bf16(x~) . L1 on
+//     v_mfma_f32_32x32x16_bf16 (rank columns, four 16-deep steps per span);
+//   * per span: acc += P * xs * ws as in the GEMMs (the token scale of each
+//     result row reaches its lanes through one cross-lane read);
+//   * the waves' partial blocks (acc and t) are summed in LDS in wave order,
+//     t is rounded to bf16, and wave 0 adds t . L2 (bf16 MFMA) and the bias
+//     and stores y.
+//   * optionally (xq / xs / t not null) the workgroups of the first column
+//     block also store the codes, scales and t, as qwam_quantize_act would.
+#include "qwam_device.h"
+#include "qwam_internal.h"
+#include "qwam_mfma.h"
+
+namespace qwam {
+
+namespace {
+
+constexpr int LW = 4;              // waves per workgroup (one per SIMD: the registers of a 32-channel lane slice fit)
+constexpr int LB = 32;             // block edge (tokens and output channels)
+
+}  // namespace
+
+template <int RANK>
+__global__ __launch_bounds__(64 * LW) void asp_layer_small_kernel(
+    const uint16_t* __restrict__ x, const float* __restrict__ inv_smooth, const uint16_t* __restrict__ L1t,
+    const uint8_t* __restrict__ wq, const float* __restrict__ ws, const uint16_t* __restrict__ L2t,
+    const uint16_t* __restrict__ bias, uint16_t* __restrict__ y, uint8_t* __restrict__ xq_out,
+    float* __restrict__ xs_out, uint16_t* __restrict__ t_out, int M, int N, int K) {
+  static_assert(RANK == 16 || RANK == 32, "one 32-column block of t");
+  // dynamic LDS: partial acc [LW][16][64] | partial t [LW][16][64] | t bf16 [32][RANK]
+  extern __shared__ float lds[];
+  float* red_acc = lds;
+  float* red_t = red_acc + LW * 16 * 64;
+  uint16_t* t_l = reinterpret_cast<uint16_t*>(red_t + LW * 16 * 64);
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int tiles_n = (N + LB - 1) / LB;
+  const int m0 = (blockIdx.x / tiles_n) * LB;
+  const int n0 = (blockIdx.x % tiles_n) * LB;
+  const bool write_act = xq_out != nullptr && blockIdx.x % tiles_n == 0;
+  const int G = K / kGroup;
+  const int KB = K / 2;
+  const int gpw = (G + LW - 1) / LW;
+  const int g_lo = min(G, wave * gpw), g_hi = min(G, g_lo + gpw);
+  const int rows = min(LB, M - m0);
+
+  const int frow = lane & 31;
+  const int fhalf = lane >> 5;
+  const int rsub = fhalf * 4;
+  const int sx_row = 8 * ((lane & 15) >> 2) + 4 * (lane >> 5) + (lane & 3);
+
+  // the workgroup's tokens (rows past M read as zero) and output channels
+  const buf_rsrc x_rsrc = make_rsrc(x + static_cast<int64_t>(m0) * K, static_cast<uint32_t>(rows) * K * 2u);
+  const buf_rsrc w_rsrc = make_rsrc(wq + static_cast<int64_t>(n0) * KB, static_cast<uint32_t>(min(LB, N - n0)) * KB);
+  const buf_rsrc ws_rsrc = make_rsrc(ws, static_cast<uint32_t>(G) * N * 4u);
+  const uint32_t x_off = static_cast<uint32_t>(frow * K + fhalf * 32) * 2u;
+  const uint32_t w_off = static_cast<uint32_t>(frow * KB + fhalf * 16);
+  const uint32_t sw_off = static_cast<uint32_t>(n0 + frow) * 4u;
+  // t columns j = lane % 32 (zero past RANK), channels 32*half + 8 s of a span
+  const bool l1_ok = frow < RANK;
+
+  struct Fetch {
+    uint4 x[4];                    // 32 bf16 of x: channels 32*half .. +31 of the span
+    float4 inv[8];                 // the matching 1/lambda (the same for the 32 lanes of a half)
+    uint4 w;                       // 32 packed weight codes of column n0 + lane%32
+    float sw;
+    v8s l1[4];                     // L1t[j][span + 32*half + 8 s .. +7], s = 0..3
+  };
+  auto fetch = [&](int g, Fetch& f) __attribute__((always_inline)) {
+    const uint32_t go = static_cast<uint32_t>(g) * kGroup * 2u;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) f.x[q] = buf_load16(x_rsrc, x_off + go + 16u * q);
+    const float4* ip = reinterpret_cast<const float4*>(inv_smooth + g * kGroup + fhalf * 32);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) f.inv[q] = ip[q];
+    f.w = buf_load16(w_rsrc, w_off + static_cast<uint32_t>(g) * 32u);
+    f.sw = buf_load4f(ws_rsrc, sw_off + static_cast<uint32_t>(g) * N * 4u);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      f.l1[s] = v8s{0, 0, 0, 0, 0, 0, 0, 0};
+      if (l1_ok) f.l1[s] = *reinterpret_cast<const v8s*>(L1t + static_cast<int64_t>(frow) * K + g * kGroup + fhalf * 32 + 8 * s);
+    }
+  };
+
+  v16f acc = v16f{};
+  v16f tacc = v16f{};
+  auto work = [&](int g, const Fetch& f) __attribute__((always_inline)) {
+    // x~ = x * (1/lambda) for the lane's 32 channels
+    float v[32];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t xw[4] = {f.x[q].x, f.x[q].y, f.x[q].z, f.x[q].w};
+      const float4 i0 = f.inv[2 * q];
+      const float4 i1 = f.inv[2 * q + 1];
+      const float iv[8] = {i0.x, i0.y, i0.z, i0.w, i1.x, i1.y, i1.z, i1.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        v[8 * q + 2 * j] = __uint_as_float(xw[j] << 16) * iv[2 * j];
+        v[8 * q + 2 * j + 1] = __uint_as_float(xw[j] & 0xFFFF0000u) * iv[2 * j + 1];
+      }
+    }
+    // the span's scale (Eq. 2): absmax of the token's 64 channels (lanes l, l^32)
+    float amax = 0.0f;
+#pragma unroll
+    for (int i = 0; i < 32; ++i) amax = __builtin_fmaxf(amax, __builtin_fabsf(v[i]));
+    amax = __builtin_fmaxf(amax, __shfl_xor(amax, 32));
+    const float s = q4_scale(amax);
+    const float inv = q4_inv(s);
+    // codes -> code words (the storage format) -> e4m3 operand bytes
+    uint32_t cw[4];
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      uint32_t wv = 0;
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const float qe = __builtin_fminf(__builtin_fmaxf(__builtin_rintf(v[8 * h + 2 * b] * inv), -8.0f), 7.0f);
+        const float qo = __builtin_fminf(__builtin_fmaxf(__builtin_rintf(v[8 * h + 2 * b + 1] * inv), -8.0f), 7.0f);
+        wv = __builtin_amdgcn_cvt_pk_u8_f32(__builtin_fmaf(qo, 16.0f, qe) + 136.0f, b, wv);
+      }
+      cw[h] = twos_nibbles_to_code_word(wv ^ 0x88888888u);
+    }
+    const uint4 cw4 = make_uint4(cw[0], cw[1], cw[2], cw[3]);
+    if (write_act && m0 + frow < M) {
+      *reinterpret_cast<uint4*>(xq_out + static_cast<int64_t>(m0 + frow) * KB + g * 32 + fhalf * 16) = cw4;
+      if (fhalf == 0) xs_out[static_cast<int64_t>(g) * M + m0 + frow] = s;
+    }
+    // exact integer partial of the span, then acc += P * xs * ws
+    const v16f p = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(codes_to_e4m3(cw4), codes_to_e4m3(f.w), v16f{}, 0,
+                                                                   0, 0, kE8M0Code, 0, kE8M0Code);
+    const float sx_lane = __shfl(s, sx_row);            // scale of the token of result register v
+    scale_accumulate(std::make_integer_sequence<int, 16>{}, acc, p, sx_lane, f.sw);
+    // t partial: A = bf16(x~) of 8 channels per step, B = the matching L1t slice
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+      v8bf a;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) a[i] = static_cast<__bf16>(v[8 * st + i]);
+      tacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, __builtin_bit_cast(v8bf, f.l1[st]), tacc, 0, 0, 0);
+    }
+  };
+
+  // epilogue operands (wave 0): L2t rows of the block's columns, bias
+  constexpr int KSTEPS = RANK / 16;
+  const int nt = n0 + frow;
+  v8s lv[KSTEPS];
+  float bv = 0.0f;
+  if (wave == 0) {
+#pragma unroll
+    for (int k = 0; k < KSTEPS; ++k) {
+      lv[k] = v8s{0, 0, 0, 0, 0, 0, 0, 0};
+      if (nt < N) lv[k] = *reinterpret_cast<const v8s*>(L2t + static_cast<int64_t>(nt) * RANK + k * 16 + fhalf * 8);
+    }
+    if (bias != nullptr && nt < N) bv = bf16_to_f32(bias[nt]);
+  }
+
+  // the wave's spans, one fetched ahead
+  if (g_lo < g_hi) {
+    Fetch fa, fb;
+    fetch(g_lo, fa);
+    int g = g_lo;
+    for (; g + 1 < g_hi; g += 2) {
+      fetch(g + 1, fb);
+      work(g, fa);
+      fetch(min(g + 2, g_hi - 1), fa);
+      work(g + 1, fb);
+    }
+    if (g < g_hi) work(g, fa);
+  }
+
+  // partial blocks -> LDS; wave 0 sums them in wave order
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    red_acc[(wave * 16 + v) * 64 + lane] = acc[v];
+    red_t[(wave * 16 + v) * 64 + lane] = tacc[v];
+  }
+  __syncthreads();
+  if (wave != 0) return;
+  v16f c = v16f{}, tsum = v16f{};
+#pragma unroll
+  for (int w = 0; w < LW; ++w)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      c[v] += red_acc[(w * 16 + v) * 64 + lane];
+      tsum[v] += red_t[(w * 16 + v) * 64 + lane];
+    }
+  // t = bf16(sum): result register v of lane l is token 8(v/4) + 4(l/32) + v%4, column l%32
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int row = 8 * (v >> 2) + rsub + (v & 3);
+    if (frow < RANK) {
+      const uint16_t b = static_cast<uint16_t>(f32_to_bf16_rne(tsum[v]));
+      t_l[row * RANK + frow] = b;
+      if (write_act && m0 + row < M) t_out[static_cast<int64_t>(m0 + row) * RANK + frow] = b;
+    }
+  }
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): this wave's t stores are in LDS
+  // y = acc + t . L2 + bias; A operand: token l%32, rank slots 16 k + 8(l/32) .. +7
+#pragma unroll
+  for (int k = 0; k < KSTEPS; ++k) {
+    const v8s tv = *reinterpret_cast<const v8s*>(t_l + frow * RANK + k * 16 + fhalf * 8);
+    c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, tv), __builtin_bit_cast(v8bf, lv[k]), c, 0,
+                                                0, 0);
+  }
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int m = m0 + 8 * (v >> 2) + rsub + (v & 3);
+    if (m < M && nt < N) y[static_cast<int64_t>(m) * N + nt] = static_cast<uint16_t>(f32_to_bf16_rne(c[v] + bv));
+  }
+}
+
+hipError_t launch_asp_layer_small(int M, int N, int K, int r, const uint16_t* x, const float* inv_smooth,
+                                  const uint16_t* L1t, const uint8_t* wq, const float* ws, const uint16_t* L2t,
+                                  const uint16_t* bias, uint16_t* y, uint8_t* xq, float* xs, uint16_t* t,
+                                  hipStream_t stream) {
+  const dim3 grid(((M + LB - 1) / LB) * ((N + LB - 1) / LB)), block(64 * LW);
+  const size_t lds = static_cast<size_t>(2) * LW * 16 * 64 * 4 + LB * r * 2;
+  auto go = [&](auto kernel) {
+    if (lds > 64 * 1024) {
+      const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+      if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(kernel, grid, block, lds, stream, x, inv_smooth, L1t, wq, ws, L2t, bias, y, xq, xs, t, M, N,
+                       K);
+    return hipGetLastError();
+  };
+  switch (r) {
+    case 16: return go(asp_layer_small_kernel<16>);
+    case 32: return go(asp_layer_small_kernel<32>);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace qwam

@@ -10,6 +10,7 @@
 namespace qwam {
 
 typedef float v16f __attribute__((ext_vector_type(16)));
+typedef float v32f __attribute__((ext_vector_type(32)));
 typedef int v8i __attribute__((ext_vector_type(8)));
 
 // 32 packed codes (16 bytes of one row) -> one FP8 MFMA operand of 32 e4m3

@@ -6,7 +6,8 @@ raw device pointers plus the current HIP stream across the C ABI.  If the
 library is not built, every call raises: there is no fallback.
 
 Names follow the C ABI (include/qwam.h): pack_weights, quantize_act,
-quantize_act_deflated, asp_linear, debug_group_partials, aog_accumulate.
+quantize_act_deflated, asp_linear, asp_layer, debug_group_partials,
+aog_accumulate.
 """
 
 from __future__ import annotations
@@ -46,6 +47,8 @@ SIGNATURES = {
     "qwam_asp_linear": (ctypes.c_int, [_LP, _i32, _c_void_p, _c_void_p, _c_void_p, _c_void_p,
                                        _c_void_p]),
     "qwam_debug_group_partials": (ctypes.c_int, [_LP, _i32, _c_void_p, _c_void_p, _c_void_p]),
+    "qwam_asp_layer": (ctypes.c_int, [_LP, _i32, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p,
+                                      _c_void_p]),
     "qwam_aog_accumulate": (ctypes.c_int, [_i32, _i32, _c_void_p, _c_void_p, _c_void_p]),
     "qwam_last_error": (ctypes.c_char_p, []),
     "qwam_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -208,6 +211,26 @@ def forward(layer: PackedLayer, x: torch.Tensor, stream=None, deflate: bool = Fa
     then asp_linear."""
     xq, xs, t = (quantize_act_deflated if deflate else quantize_act)(layer, x, stream)
     return asp_linear(layer, xq, xs, t, stream=stream)
+
+
+def asp_layer(layer: PackedLayer, x: torch.Tensor, out=None, act_out=None, stream=None):
+    """qwam_asp_layer: the whole layer for M <= 64 tokens in one launch.
+    x bf16 [M][K] -> y bf16 [M][N].  `act_out` = (xq, xs, t) receives the
+    activation step's outputs as well (optional)."""
+    M = x.shape[0]
+    y = torch.empty((M, layer.N), dtype=torch.bfloat16, device=x.device) if out is None else out
+    c = layer.c_struct()
+    if act_out is None:
+        pq = ps = pt = None
+    else:
+        xq, xs, t = act_out
+        pq = _req(xq, "xq", torch.uint8, (M, layer.K // 2))
+        ps = _req(xs, "xs", torch.float32, (layer.K // layer.group, M))
+        pt = _req(t, "t", torch.bfloat16, (M, layer.r))
+    st = lib().qwam_asp_layer(ctypes.byref(c), M, _req(x, "x", torch.bfloat16, (M, layer.K)),
+                              _req(y, "y", torch.bfloat16, (M, layer.N)), pq, ps, pt, _stream_ptr(stream))
+    _check("qwam_asp_layer", st)
+    return y
 
 
 def debug_group_partials(layer: PackedLayer, xq: torch.Tensor, stream=None) -> torch.Tensor:

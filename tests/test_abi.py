@@ -38,7 +38,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == set(Q.SIGNATURES), "binding and header disagree"
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.qwam_abi_version() == 6
+    assert lib.qwam_abi_version() == 7
     assert lib.qwam_status_string(3) == b"QWAM_ERR_MISALIGNED"
 
 
@@ -117,6 +117,20 @@ def test_layer_calls_reject_bad_arguments(lib):
     assert b"hadamard" in lib.qwam_last_error()
     # partials: rank is not used, but shapes and pointers are checked
     assert lib.qwam_debug_group_partials(ctypes.byref(_layer(r=7)), 1, None, FAKE, None) == INVALID
+
+
+def test_asp_layer_rejects_bad_arguments(lib):
+    def call(layer, M=16, x=FAKE, y=FAKE, xq=None, xs=None, t=None):
+        return lib.qwam_asp_layer(ctypes.byref(layer), M, x, y, xq, xs, t, None)
+    assert call(_layer(), M=65) == UNSUPPORTED
+    assert call(_layer(r=48)) == UNSUPPORTED
+    assert call(_layer(group=32)) == UNSUPPORTED
+    assert call(_layer(hadamard=256)) == UNSUPPORTED
+    assert call(_layer(), M=0) == INVALID
+    assert call(_layer(), x=None) == INVALID
+    assert call(_layer(), y=FAKE + 2) == MISALIGNED
+    assert call(_layer(), xq=FAKE) == INVALID          # xq without xs and t
+    assert lib.qwam_last_error().startswith(b"qwam_asp_layer")
 
 
 def test_aog_accumulate_rejects_bad_arguments(lib):
