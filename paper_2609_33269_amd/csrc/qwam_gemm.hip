@@ -17,7 +17,9 @@
 //     8 cache lines: the vector-memory address path (about one line per clock
 //     per CU) is what limits a copy of one 16-byte piece per row and group;
 //   * two stages: stage s+1 is copied while stage s is multiplied, one barrier
-//     per stage;
+//     per stage; each tile and scale array of a stage is an LDS variable of
+//     its own, so that the compiler can tell a copy into one stage from a read
+//     of the other and does not make the read wait for the copy;
 //   * inside a stage, row r keeps its eight 16-byte chunks in slot order
 //     chunk ^ swz(r), swz(r) = (r & 7) ^ ((r >> 3) & 1), so that the fragment
 //     loads (one ds_read_b128 = 32 codes of one row per lane, 32 consecutive
@@ -35,15 +37,18 @@
 //     product: one v_mfma_f32_32x32x1_2b_f32 (K = 1, one rounding per product,
 //     as a VALU multiply) gives them for two 32 x 32 blocks at once, in the
 //     result layout of the integer blocks, so the VALU is left with one fused
-//     multiply-add per output and group; the MFMAs of the next block are
-//     issued before the update of the current one;
+//     multiply-add per output and group;
+//   * group 64 runs as a software pipeline across groups: every MFMA is
+//     followed by VALU work that does not depend on it (the updates of blocks
+//     whose products landed earlier, the unpacking of the next group);
 //   * workgroups are mapped XCD-major: the 8 XCDs each take a contiguous range
 //     of tiles, ordered in bands of 8 tile-rows so that the concurrently
 //     resident tiles of one XCD share their A and B panels in its L2;
-//   * epilogue: the bf16 branch (v_mfma_f32_32x32x16_bf16, same result layout
-//     as the integer blocks) starts from acc, the bias is added, the
-//     result is rounded to bf16 and stored through LDS so that every lane
-//     writes 16 contiguous bytes.
+//   * the accumulators start from the bias plus the bf16 branch
+//     (v_mfma_f32_32x32x16_bf16, same result layout as the integer blocks),
+//     computed while the first stage is copied; the epilogue rounds to bf16
+//     (v_cvt_pk_bf16_f32) and stores through LDS so that every lane writes 16
+//     contiguous bytes.
 //
 // Group 32 (GS = 32, the paper's setting): the MFMA's K = 64 covers two groups.
 // Its two E8M0 block scales govern bytes 0-15 and 16-31 of every lane's
@@ -53,6 +58,8 @@
 // both operands: its products (2^-254 and below) underflow to zero, so each
 // result is one group's integer partial, exactly.  Twice the MFMA work and
 // twice the scaling per output.
+#include <type_traits>
+
 #include "qwam_device.h"
 #include "qwam_internal.h"
 #include "qwam_mfma.h"
@@ -71,25 +78,30 @@ constexpr int BAND = 8;            // tile-rows per band of the tile order
 constexpr int KC = 4;              // groups per ring stage
 constexpr int ROWB = KC * 32;      // bytes of one packed row per stage (one cache line)
 
-template <int GPS>                 // scale groups per stage
-struct StageT {
-  uint8_t a[BM * ROWB];            // [row][8 chunk slots of 16 bytes], swizzled
-  uint8_t b[BN * ROWB];
-  float sx[GPS][BM];
-  float sw[GPS][BN];
+// One ring stage: the A and B tiles ([row][8 chunk slots of 16 bytes],
+// swizzled) and the scales of its GPS scale groups.  Each array is its own
+// LDS variable: the compiler then keeps the copies into one stage apart from
+// the reads of the other and does not make those reads wait for the copies.
+template <int GPS>
+struct StageRef {
+  uint8_t* a;
+  uint8_t* b;
+  float (*sx)[BM];
+  float (*sw)[BN];
 };
-static_assert(4 * 64 * LDY * 2 <= sizeof(StageT<KC>), "the output staging of all four waves must fit in one stage");
+static_assert(64 * LDY * 2 <= BM * ROWB && BM == BN, "a wave's 64 x 64 bf16 output block must fit in one tile buffer");
+
+typedef float v2f __attribute__((ext_vector_type(2)));
+typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
+
+// waits for this wave's LDS reads, then a workgroup barrier (outstanding
+// global-to-LDS copies stay in flight)
+__device__ __forceinline__ void lds_wait_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 // chunk slot permutation of a row inside a stage
 __device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
-// 16-byte LDS read that the compiler keeps in program order (volatile)
-__device__ __forceinline__ uint4 lds_load16_volatile(const uint8_t* p) {
-  typedef unsigned v4u __attribute__((ext_vector_type(4)));
-  typedef const volatile __attribute__((address_space(3))) v4u lds_v4u;
-  const v4u v = *(lds_v4u*)(p);
-  return make_uint4(v.x, v.y, v.z, v.w);
-}
+// LDS reads that the compiler keeps in program order (volatile)
 __device__ __forceinline__ uint2 lds_load8_volatile(const uint8_t* p) {
   typedef unsigned v2u __attribute__((ext_vector_type(2)));
   typedef const volatile __attribute__((address_space(3))) v2u lds_v2u;
@@ -126,10 +138,13 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
     int N, int K) {
   constexpr int NS = kGroup / GS;                               // scale groups per 64-channel span
   constexpr int GPS = KC * NS;                                  // scale groups per stage
-  typedef StageT<GPS> Stage;
-  // two distinct LDS objects (not one indexed array), so that the compiler
-  // can tell which ring stage a copy writes and a fragment load reads
-  __shared__ __attribute__((aligned(16))) Stage st0, st1;
+  typedef StageRef<GPS> Stage;
+  __shared__ __attribute__((aligned(16))) uint8_t lds_a0[BM * ROWB], lds_b0[BN * ROWB];
+  __shared__ __attribute__((aligned(16))) uint8_t lds_a1[BM * ROWB], lds_b1[BN * ROWB];
+  __shared__ __attribute__((aligned(16))) float lds_sx0[GPS][BM], lds_sw0[GPS][BN];
+  __shared__ __attribute__((aligned(16))) float lds_sx1[GPS][BM], lds_sw1[GPS][BN];
+  const Stage st0{lds_a0, lds_b0, lds_sx0, lds_sw0};
+  const Stage st1{lds_a1, lds_b1, lds_sx1, lds_sw1};
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -175,7 +190,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
                static_cast<uint32_t>((s_is_x ? m0 : n0) + (i & 1) * 64 + lane) * 4u;
   }
 
-  auto issue = [&](int s, Stage& st) __attribute__((always_inline)) {
+  auto issue = [&](int s, const Stage& st) __attribute__((always_inline)) {
     const uint32_t ko = static_cast<uint32_t>(s) * ROWB;
 #pragma unroll
     for (int i = 0; i < 4; ++i) buf_load16_lds(a_rsrc, d_off[i] + ko, st.a + (4 * wave + i) * 1024);
@@ -226,7 +241,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
   // sunk next to their first use; the wait for them lands at that use.
   auto load_frag = [&](const uint8_t* rowp, int q) __attribute__((always_inline)) {
     if constexpr (GS == 64) {
-      return lds_load16_volatile(rowp + ((2 * q) ^ fslot) * 16);
+      return *reinterpret_cast<const uint4*>(rowp + ((2 * q) ^ fslot) * 16);
     } else {
       const int sw0 = swz(frow);
       const uint2 lo = lds_load8_volatile(rowp + ((2 * q) ^ sw0) * 16 + fhalf * 8);
@@ -244,15 +259,36 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
 #pragma unroll
       for (int h = 0; h < NS; ++h) {
 #pragma unroll
-        for (int i = 0; i < 2; ++i) d.sx[i][h] = lds_load4_volatile(&cur.sx[NS * q + h][wm * 64 + i * 32 + frow]);
-        d.sw[h] = lds_load4_volatile(&cur.sw[NS * q + h][wn * 64 + fhalf * 32 + frow]);
+        for (int i = 0; i < 2; ++i) {
+          const float* p = &cur.sx[NS * q + h][wm * 64 + i * 32 + frow];
+          d.sx[i][h] = GS == 64 ? *p : lds_load4_volatile(p);
+        }
+        const float* p = &cur.sw[NS * q + h][wn * 64 + fhalf * 32 + frow];
+        d.sw[h] = GS == 64 ? *p : lds_load4_volatile(p);
       }
     }
     asm volatile("" ::: "memory");
     return d;
   };
 
-  // one group g of a stage, from its LDS data
+  // block (i, j) of group g, scale group h of the span: acc += P * sx * sw
+  // (the partials themselves with PARTIALS).  Result layout of a 32x32 block:
+  // lane l holds column l%32 and rows 8*(v/4) + 4*(l/32) + v%4, v = 0..15.
+  auto update = [&](int i, int j, int g, int h, const v16f& p, const v32f& sc) __attribute__((always_inline)) {
+    if (PARTIALS) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int m = m0 + wm * 64 + i * 32 + 8 * (v >> 2) + rsub + (v & 3);
+        const int n = n0 + wn * 64 + j * 32 + frow;
+        if (m < M && n < N) P[(static_cast<int64_t>(m) * N + n) * GSC + NS * g + h] = static_cast<int32_t>(p[v]);
+      }
+    } else {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) accf[i][j][v] = __builtin_fmaf(p[v], sc[16 * j + v], accf[i][j][v]);
+    }
+  };
+
+  // one group g of a stage, from its LDS data (group 32)
   auto group = [&](int g, const GroupData& d) __attribute__((always_inline)) {
     v8i af[2], bf[2];
 #pragma unroll
@@ -273,23 +309,6 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
     auto scale_block = [&](int i, int h) __attribute__((always_inline)) {
       return __builtin_amdgcn_mfma_f32_32x32x1f32(d.sx[i][h], d.sw[h], v32f{}, 0, 0, 0);
     };
-    // result layout of a 32x32 block: lane l holds column l%32 and rows
-    // 8*(v/4) + 4*(l/32) + v%4, v = 0..15
-    auto consume = [&](int i, int j, int h, const v16f& p, const v32f& sc) __attribute__((always_inline)) {
-      if (PARTIALS) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int m = m0 + wm * 64 + i * 32 + 8 * (v >> 2) + rsub + (v & 3);
-          const int n = n0 + wn * 64 + j * 32 + frow;
-          if (m < M && n < N) P[(static_cast<int64_t>(m) * N + n) * GSC + NS * g + h] = static_cast<int32_t>(p[v]);
-        }
-      } else {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) accf[i][j][v] = __builtin_fmaf(p[v], sc[16 * j + v], accf[i][j][v]);
-      }
-    };
-    // software pipeline: three MFMAs in flight before the first update, so
-    // that no update waits for the block it reads
     // per group h and row block i: the scale products (one MFMA for both
     // column blocks), the two integer blocks, then their updates; each update
     // reads results issued at least one MFMA earlier
@@ -301,14 +320,14 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
         const v32f sc = PARTIALS ? none : scale_block(i, h);
         const v16f p0 = mfma_block(i, 0, h);
         const v16f p1 = mfma_block(i, 1, h);
-        consume(i, 0, h, p0, sc);
-        consume(i, 1, h, p1, sc);
+        update(i, 0, g, h, p0, sc);
+        update(i, 1, g, h, p1, sc);
       }
   };
 
   // one stage: `cur` holds stage s (groups KC*s ..), `nxt` (the stage of s-1)
   // receives s+1; nq groups of the stage are valid
-  auto stage_step = [&](int s, const Stage& cur, Stage& nxt, int nq) __attribute__((always_inline)) {
+  auto stage_step = [&](int s, const Stage& cur, const Stage& nxt, int nq) __attribute__((always_inline)) {
     wait_vmcnt<0>();                  // this thread's copies of stage s have landed
     lds_barrier();                    // ... and every thread's; stage s-1 is fully consumed
     issue(s + 1, nxt);                // past the last stage: harmless reads, never used
@@ -325,68 +344,212 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
   };
 
   issue(0, st0);
-  int s = 0;
-  for (; s + 1 < S_full; s += 2) {
-    stage_step(s, st0, st1, KC);
-    stage_step(s + 1, st1, st0, KC);
+  // The accumulators start from the bias and the low-rank branch t . L2
+  // (v_mfma_f32_32x32x16_bf16: lane l holds row / column l%32 and the 8 rank
+  // slots 8*(l/32) .. +7 of a 16-wide rank step, the same slots for t and
+  // L2t).  Its loads overlap the copy of the first stage.
+  if (!PARTIALS) {
+    constexpr int KSTEPS = RANK / 16;
+    const int kk = fhalf * 8;
+    v8s tf[2][KSTEPS], lf[2][KSTEPS];
+    float bv[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int m = m0 + wm * 64 + i * 32 + frow;
+#pragma unroll
+      for (int s = 0; s < KSTEPS; ++s) {
+        v8s val = {0, 0, 0, 0, 0, 0, 0, 0};
+        if (m < M) val = *reinterpret_cast<const v8s*>(t + static_cast<int64_t>(m) * RANK + s * 16 + kk);
+        tf[i][s] = val;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int n = n0 + wn * 64 + j * 32 + frow;
+#pragma unroll
+      for (int s = 0; s < KSTEPS; ++s) {
+        v8s val = {0, 0, 0, 0, 0, 0, 0, 0};
+        if (n < N) val = *reinterpret_cast<const v8s*>(L2t + static_cast<int64_t>(n) * RANK + s * 16 + kk);
+        lf[j][s] = val;
+      }
+      bv[j] = (bias != nullptr && n < N) ? bf16_to_f32(bias[n]) : 0.0f;
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        v16f c;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) c[v] = bv[j];
+#pragma unroll
+        for (int s = 0; s < KSTEPS; ++s)
+          c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, tf[i][s]),
+                                                      __builtin_bit_cast(v8bf, lf[j][s]), c, 0, 0, 0);
+        accf[i][j] = c;
+      }
   }
-  // at most one full stage and one partial stage remain
-  if (s < S_full) {
-    stage_step(s, st0, st1, KC);
-    ++s;
-    if (s < S) stage_step(s, st1, st0, G - s * KC);
-  } else if (s < S) {
-    stage_step(s, st0, st1, G - s * KC);
+
+  if constexpr (GS == 32) {
+    int s = 0;
+    for (; s + 1 < S_full; s += 2) {
+      stage_step(s, st0, st1, KC);
+      stage_step(s + 1, st1, st0, KC);
+    }
+    // at most one full stage and one partial stage remain
+    if (s < S_full) {
+      stage_step(s, st0, st1, KC);
+      ++s;
+      if (s < S) stage_step(s, st1, st0, G - s * KC);
+    } else if (s < S) {
+      stage_step(s, st0, st1, G - s * KC);
+    }
+  } else {
+    // Group 64: a software pipeline across groups.  The matrix core runs one
+    // MFMA at a time and a wave that issues an MFMA while the previous one is
+    // still running waits for it, so every MFMA gets its own slot, followed by
+    // about 16 VALU instructions (64 cycles, the length of one MFMA) that do not
+    // depend on it: the updates of blocks whose products landed one slot or
+    // more earlier, or the unpacking of the next group's fragments.  Per group
+    // g (S = scale products, P = integer partials):
+    //   slot 1  S0(g)              | update (1,1) of g-1; unpack A1(g)
+    //   slot 2  P00(g) = A0 x B0   | unpack B1(g)
+    //   slot 3  P01(g) = A0 x B1   | LDS reads of g+1; update (0,0)
+    //   slot 4  S1(g)              | update (0,1)
+    //   slot 5  P10(g) = A1 x B0   | unpack A0(g+1)
+    //   slot 6  P11(g) = A1 x B1   | update (1,0); unpack B0(g+1)
+    // A stage ends inside its last group: before the LDS reads of g+1 the
+    // wave waits for its copies of the next stage and for its own LDS reads,
+    // then the barrier frees the stage just read for the copy of the stage
+    // after next.
+    struct Pipe {
+      v8i af0, bf0;        // unpacked A0 / B0 fragments of the current group
+      uint4 ra1, rb1;      // packed A1 / B1 fragments of the current group
+      float sx0, sx1, sw;  // its scales
+      v32f s1;             // scale products and partial of block (1, 1) of
+      v16f p11;            // the previous group, updated in slot 1
+    };
+    auto fp8_partial = [&](const v8i& a, const v8i& b) __attribute__((always_inline)) {
+      return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, v16f{}, 0, 0, 0, kE8M0Code, 0, kE8M0Code);
+    };
+    auto scale_products = [&](float sx, float sw) __attribute__((always_inline)) {
+      if constexpr (PARTIALS) return v32f{};
+      else return __builtin_amdgcn_mfma_f32_32x32x1f32(sx, sw, v32f{}, 0, 0, 0);
+    };
+    auto start = [&](Pipe& pp, const GroupData& d) __attribute__((always_inline)) {
+      pp.af0 = codes_to_e4m3(d.a[0]);
+      pp.bf0 = codes_to_e4m3(d.b[0]);
+      pp.ra1 = d.a[1];
+      pp.rb1 = d.b[1];
+      if (!PARTIALS) { pp.sx0 = d.sx[0][0]; pp.sx1 = d.sx[1][0]; pp.sw = d.sw[0]; }
+    };
+    // group g at position q (0..7) of two consecutive stages: q < 4 reads
+    // st0, q >= 4 st1; the last group of a stage (q % 4 == 3) switches the
+    // ring, issuing stage s_next into the buffer it has just finished
+    auto step = [&](auto qc, int g, Pipe& pp, int s_next) __attribute__((always_inline)) {
+      constexpr int q = decltype(qc)::value;
+      const v32f s0 = scale_products(pp.sx0, pp.sw);
+      __builtin_amdgcn_sched_barrier(0);
+      if (!PARTIALS || g > 0) update(1, 1, g - 1, 0, pp.p11, pp.s1);
+      const v8i af1 = codes_to_e4m3(pp.ra1);
+      __builtin_amdgcn_sched_barrier(0);
+      const v16f p00 = fp8_partial(pp.af0, pp.bf0);
+      __builtin_amdgcn_sched_barrier(0);
+      const v8i bf1 = codes_to_e4m3(pp.rb1);
+      __builtin_amdgcn_sched_barrier(0);
+      const v16f p01 = fp8_partial(pp.af0, bf1);
+      __builtin_amdgcn_sched_barrier(0);
+      if constexpr (q % 4 == 3) {
+        wait_vmcnt<0>();
+        lds_wait_barrier();
+      }
+      // the reads come before the copy into the other buffer, so that the
+      // compiler does not make them wait for it
+      const GroupData nd = load_group(q < 3 || q == 7 ? st0 : st1, (q + 1) % 4);
+      if constexpr (q % 4 == 3) issue(s_next, q == 3 ? st0 : st1);
+      update(0, 0, g, 0, p00, s0);
+      __builtin_amdgcn_sched_barrier(0);
+      const v32f s1 = scale_products(pp.sx1, pp.sw);
+      __builtin_amdgcn_sched_barrier(0);
+      update(0, 1, g, 0, p01, s0);
+      __builtin_amdgcn_sched_barrier(0);
+      const v16f p10 = fp8_partial(af1, pp.bf0);
+      __builtin_amdgcn_sched_barrier(0);
+      const v8i af0n = codes_to_e4m3(nd.a[0]);
+      __builtin_amdgcn_sched_barrier(0);
+      const v16f p11 = fp8_partial(af1, bf1);
+      __builtin_amdgcn_sched_barrier(0);
+      update(1, 0, g, 0, p10, s1);
+      pp.bf0 = codes_to_e4m3(nd.b[0]);
+      __builtin_amdgcn_sched_barrier(0);
+      pp.af0 = af0n;
+      pp.ra1 = nd.a[1];
+      pp.rb1 = nd.b[1];
+      if (!PARTIALS) { pp.sx0 = nd.sx[0][0]; pp.sx1 = nd.sx[1][0]; pp.sw = nd.sw[0]; }
+      pp.s1 = s1;
+      pp.p11 = p11;
+    };
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    using I2 = std::integral_constant<int, 2>;
+    using I3 = std::integral_constant<int, 3>;
+    using I4 = std::integral_constant<int, 4>;
+    using I5 = std::integral_constant<int, 5>;
+    using I6 = std::integral_constant<int, 6>;
+    using I7 = std::integral_constant<int, 7>;
+
+    wait_vmcnt<0>();
+    lds_wait_barrier();
+    issue(1, st1);
+    Pipe pp;
+    start(pp, load_group(st0, 0));
+    pp.s1 = v32f{};
+    pp.p11 = v16f{};
+    // two stages (8 groups) per iteration; stage s is in st0, s + 1 in st1
+    int g = 0;
+    for (; g + 2 * KC <= G; g += 2 * KC) {
+      const int s = g / KC;
+      step(I0{}, g, pp, 0);
+      step(I1{}, g + 1, pp, 0);
+      step(I2{}, g + 2, pp, 0);
+      step(I3{}, g + 3, pp, s + 2);
+      step(I4{}, g + 4, pp, 0);
+      step(I5{}, g + 5, pp, 0);
+      step(I6{}, g + 6, pp, 0);
+      step(I7{}, g + 7, pp, s + 3);
+    }
+    // fewer than 8 groups remain, in the same ring positions
+    const int rest = G - g;
+    const int s = g / KC;
+    if (rest > 0) step(I0{}, g, pp, 0);
+    if (rest > 1) step(I1{}, g + 1, pp, 0);
+    if (rest > 2) step(I2{}, g + 2, pp, 0);
+    if (rest > 3) step(I3{}, g + 3, pp, s + 2);
+    if (rest > 4) step(I4{}, g + 4, pp, 0);
+    if (rest > 5) step(I5{}, g + 5, pp, 0);
+    if (rest > 6) step(I6{}, g + 6, pp, 0);
+    update(1, 1, G - 1, 0, pp.p11, pp.s1);
   }
   wait_vmcnt<0>();     // the copies issued past the last stage must land
   __syncthreads();     // before the LDS is reused below
 
   if (PARTIALS) return;
 
-  // ---- epilogue: acc + t . L2 (bf16 MFMA, float32 accumulate) + bias ----
-  // v_mfma_f32_32x32x16_bf16: lane l holds row/column l%32 and the 8 rank slots
-  // 8*(l/32) .. +7 of a 16-wide rank step (the same slots for t and L2t).
-  constexpr int KSTEPS = RANK / 16;
-  const int kk = fhalf * 8;
-  v8s tf[2][KSTEPS], lf[2][KSTEPS];
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int m = m0 + wm * 64 + i * 32 + frow;
-#pragma unroll
-    for (int s = 0; s < KSTEPS; ++s) {
-      v8s val = {0, 0, 0, 0, 0, 0, 0, 0};
-      if (m < M) val = *reinterpret_cast<const v8s*>(t + static_cast<int64_t>(m) * RANK + s * 16 + kk);
-      tf[i][s] = val;
-    }
-  }
-  float bv[2];
-#pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int n = n0 + wn * 64 + j * 32 + frow;
-#pragma unroll
-    for (int s = 0; s < KSTEPS; ++s) {
-      v8s val = {0, 0, 0, 0, 0, 0, 0, 0};
-      if (n < N) val = *reinterpret_cast<const v8s*>(L2t + static_cast<int64_t>(n) * RANK + s * 16 + kk);
-      lf[j][s] = val;
-    }
-    bv[j] = (bias != nullptr && n < N) ? bf16_to_f32(bias[n]) : 0.0f;
-  }
-  // each wave stages its 64 x 64 bf16 outputs in its quarter of (idle) stage 0
-  uint16_t* ys = reinterpret_cast<uint16_t*>(&st0) + wave * 64 * LDY;   // [64][LDY] bf16
+  // ---- epilogue: round to bf16, staged through LDS so that every lane
+  // stores 16 contiguous bytes; wave w uses the w-th (idle) tile buffer ----
+  uint16_t* ys = reinterpret_cast<uint16_t*>(wave == 0 ? lds_a0 : wave == 1 ? lds_b0 : wave == 2 ? lds_a1 : lds_b1);
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      v16f c = accf[i][j];
+    for (int j = 0; j < 2; ++j)
 #pragma unroll
-      for (int s = 0; s < KSTEPS; ++s)
-        c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, tf[i][s]),
-                                                    __builtin_bit_cast(v8bf, lf[j][s]), c, 0, 0, 0);
-#pragma unroll
-      for (int v = 0; v < 16; ++v)
-        ys[(i * 32 + 8 * (v >> 2) + rsub + (v & 3)) * LDY + j * 32 + frow] =
-            static_cast<uint16_t>(f32_to_bf16_rne(c[v] + bv[j]));
-    }
+      for (int v = 0; v < 16; v += 2) {
+        // rows r and r + 1 of column j * 32 + frow
+        const int r = i * 32 + 8 * (v >> 2) + rsub + (v & 3);
+        const v2f pair = {accf[i][j][v], accf[i][j][v + 1]};
+        const uint32_t h = __builtin_bit_cast(uint32_t, __builtin_convertvector(pair, v2bf));
+        ys[r * LDY + j * 32 + frow] = static_cast<uint16_t>(h);
+        ys[(r + 1) * LDY + j * 32 + frow] = static_cast<uint16_t>(h >> 16);
+      }
   __syncthreads();
   // the wave's 64 rows x 64 columns: 8 lanes per row, 16 bytes each
 #pragma unroll
