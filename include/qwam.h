@@ -57,10 +57,10 @@
  *   x    bf16    [M][K]      activations (row = token)
  *   R    float   [N][K]      residual weight, row = output channel
  *   smooth float [K]         lambda
- *   wq   uint8   [N][K/2]    packed weight codes (code words, below)
+ *   wq   uint8   [N][K/2]    packed weight codes (code blocks, below)
  *   ws   float   [G][N]      weight scales, group-major
  *   inv_smooth float [K]     fl32(1 / lambda)
- *   xq   uint8   [M][K/2]    packed activation codes (code words, below)
+ *   xq   uint8   [M][K/2]    packed activation codes (code blocks, below)
  *   xs   float   [G][M]      activation scales, group-major
  *   L1t  bf16    [r][K]      L1 transposed: row j is the j-th protected direction
  *   L2t  bf16    [N][r]      L2 transposed: row n holds (V^T W~)[:, n]
@@ -68,15 +68,19 @@
  *   bias bf16    [N]         optional
  *   y    bf16    [M][N]      output, round to nearest even from float32
  *
- * Code words: 4 bits per code, sign-magnitude.  The codes c[k0 .. k0+7] of 8
- * consecutive channels of a row (k0 a multiple of 8) form one little-endian
- * 32-bit word (bytes k0/2 .. k0/2+3); byte j of the word holds |c[k0+2j]| in
- * bits 0-2 and the sign of c[k0+2j] in bit 7, |c[k0+2j+1]| in bits 4-6, and in
- * bit 3 the sign of c[k0+2j-1] (of c[k0+7] for j = 0).  A sign bit is 1 exactly
- * for a negative code.  Codes lie in [-7, 7]: with the scale absmax / 7 the
- * clamp of Eq. 2 never reaches -8.  (Masking a word with 0x87878787, and the
- * word rotated right by 4 bits with the same mask, yields the codes as FP8
- * e4m3 bytes of value code * 2^-9, which is how the GEMM consumes them.)
+ * Code blocks: 4 bits per code.  The codes c[k0 .. k0+15] of 16 consecutive
+ * channels of a row (k0 a multiple of 16) form one 8-byte block (bytes
+ * k0/2 .. k0/2+7), read as two little-endian 32-bit words W0, W1.  Code j of
+ * the block is the 6-bit field F_j = s << 5 | |c| (s = 1 exactly for a
+ * negative code), field j at bits 6j .. 6j+5 of the 96-bit stream
+ * D0 | D1 << 32 | D2 << 64, whose bits 3-4 of every field are zero.  Those
+ * bit positions of D0 and D1 (0x18618618 and 0x86186186) together are
+ * exactly the data bits of D2, which is stored there:
+ * W0 = D0 | (D2 & 0x18618618), W1 = D1 | (D2 & 0x86186186).  Codes lie in
+ * [-7, 7]: with the scale absmax / 7 the clamp of Eq. 2 never reaches -8.
+ * (D0 = W0 & ~0x18618618, D1 = W1 & ~0x86186186 and
+ * D2 = (W0 & 0x18618618) | (W1 & 0x86186186) give back the stream, whose
+ * fields are the FP6 e2m3 values code / 8: that is how the GEMM consumes them.)
  *
  * Rotation: hadamard == 0, or a power of two with 16 <= hadamard <= 1024
  * dividing K (QWAM_ERR_INVALID_ARG otherwise).  It affects the activation
@@ -96,7 +100,7 @@
 extern "C" {
 #endif
 
-#define QWAM_ABI_VERSION 7
+#define QWAM_ABI_VERSION 8
 #define QWAM_GROUP 64
 
 typedef enum {
@@ -127,7 +131,7 @@ typedef struct qwam_layer {
  * Offline weight pack (weights are quantized once, Sec. 3; the exported codes
  * of App. B.1).  Quantizes each group of `group` (64 or 32) consecutive entries
  * of each row of R with the quantizer of Eq. 2 (scale = fl32(absmax / 7); a group with absmax
- * below 7 * 2^-126 gets scale 0 and codes 0), packs the codes into code words
+ * below 7 * 2^-126 gets scale 0 and codes 0), packs the codes into code blocks
  * and writes
  * inv_smooth[k] = fl32(1 / smooth[k]).
  *   R          in   float [N][K]
@@ -169,7 +173,7 @@ qwam_status qwam_quantize_act(const qwam_layer *L, int32_t M, const uint16_t *x,
  *             within ~1e-13 relative of a rounding boundary
  *   x~_perp = x~, then for j = 0 .. r-1 in order:
  *             x~_perp <- fl32(x~_perp - t_j L1[:, j])   (exact products)
- *   xq, xs  = group quantization (Eq. 2) and code words of x~_perp
+ *   xq, xs  = group quantization (Eq. 2) and code blocks of x~_perp
  * The outputs feed qwam_asp_linear unchanged: y = Q4(x~_perp) Q4(R)^T + t L2.
  * Arguments, layouts, ownership and errors as for qwam_quantize_act.
  */

@@ -46,10 +46,10 @@ Readings taken where the paper is silent (all are listed in the design notes):
     ascending order, each step rounded to float32 (deflate_activations); each
     product of two bf16 values is exact in float32, so every step is one
     correctly rounded subtraction.
-  * packing: 4 bits per code, sign-magnitude, eight codes per 32-bit word
-    (pack_codes); the paper fixes the code range, not a byte layout.  This one
-    lets a kernel turn a word into FP8 bytes of value code * 2^-9 with one mask
-    (and a rotate for the odd codes), and needs |code| <= 7, which the
+  * packing: 4 bits per code, sixteen codes per 8-byte block (pack_codes);
+    the paper fixes the code range, not a byte layout.  This one lets a kernel
+    turn a block into the FP6 e2m3 fields of value code / 8 (sign, two zero
+    exponent bits, |code|) with four masks, and needs |code| <= 7, which the
     quantizer guarantees.
   * the 16-bit branch is bf16: L1 = bf16(V), L2 = bf16(L1^T W~),
     R = fl32(W~ - L1 L2), t = bf16(sum_k bf16(x~_k) L1[k, j]) with an exact sum.
@@ -289,48 +289,86 @@ def dequantize_groups(codes: np.ndarray, scales: np.ndarray, group: int = GROUP)
     return (c * np.asarray(scales, dtype=np.float64)[:, :, None]).reshape(rows, K)
 
 
-def pack_codes(codes: np.ndarray) -> np.ndarray:
-    """Packed code words: 4 bits per code, sign-magnitude.
+# Code blocks: positions of bits 3-4 of the 6-bit fields in the first two
+# stream words; together they are exactly the data bits of the third.
+FP6_Z0 = 0x18618618
+FP6_Z1 = 0x86186186
 
-    The codes of channels 8i .. 8i+7 of a row form the little-endian 32-bit
-    word i (bytes 4i .. 4i+3).  Byte j of a word holds the magnitude of the code
-    of channel 8i+2j in bits 0-2 and its sign in bit 7, the magnitude of the
-    code of channel 8i+2j+1 in bits 4-6, and in bit 3 the sign of the code of
-    channel 8i+2j-1 (of channel 8i+7 when j = 0).  The sign bit is 1 exactly
-    for negative codes.  Codes must lie in [-7, 7]: with the scale absmax / 7
-    of Eq. 2 the code -8 is never produced.
+
+def _fp6_stream(fields: np.ndarray) -> list:
+    """fields [..., 16] (6-bit ints) -> [D0, D1, D2], field i at bits 6i .. 6i+5
+    of the 96-bit stream D0 | D1 << 32 | D2 << 64 (uint64 arrays)."""
+    f = fields.astype(np.uint64)
+    d = [np.zeros(f.shape[:-1], dtype=np.uint64) for _ in range(3)]
+    for i in range(16):
+        bit = 6 * i
+        w, off = bit // 32, bit % 32
+        d[w] |= (f[..., i] << np.uint64(off)) & np.uint64(0xFFFFFFFF)
+        if off > 26:
+            d[w + 1] |= f[..., i] >> np.uint64(32 - off)
+    return d
+
+
+def _fp6_fields(d: list) -> np.ndarray:
+    """Inverse of _fp6_stream: [D0, D1, D2] -> fields [..., 16]."""
+    out = np.zeros(d[0].shape + (16,), dtype=np.uint64)
+    for i in range(16):
+        bit = 6 * i
+        w, off = bit // 32, bit % 32
+        v = d[w] >> np.uint64(off)
+        if off > 26:
+            v |= d[w + 1] << np.uint64(32 - off)
+        out[..., i] = v & np.uint64(63)
+    return out
+
+
+def pack_codes(codes: np.ndarray) -> np.ndarray:
+    """Packed code blocks: 4 bits per code.
+
+    The codes c[16i .. 16i+15] of 16 consecutive channels of a row form block
+    i, bytes 8i .. 8i+7, read as two little-endian 32-bit words W0, W1.  Code j
+    of the block is the 6-bit field F_j = sign << 5 | |c| (sign 1 exactly for
+    a negative code), field j at bits 6j .. 6j+5 of the 96-bit stream
+    D0 | D1 << 32 | D2 << 64; bits 3-4 of every field are zero.  Those bit
+    positions of D0 and D1 (FP6_Z0, FP6_Z1) together are exactly the data
+    bits of D2, which is stored there: W0 = D0 | (D2 & FP6_Z0),
+    W1 = D1 | (D2 & FP6_Z1).  Codes must lie in [-7, 7]: with the scale
+    absmax / 7 of Eq. 2 the code -8 is never produced.
     """
     c = np.asarray(codes, dtype=np.int16)
     rows, K = c.shape
-    if K % 8:
-        raise ValueError("the channel count must be a multiple of 8")
+    if K % 16:
+        raise ValueError("the channel count must be a multiple of 16")
     if c.size and (c.min() < -7 or c.max() > 7):
         raise ValueError("packed codes must lie in [-7, 7]")
-    mag = np.abs(c)
-    neg = (c < 0).astype(np.int16)
-    out = np.zeros((rows, K // 2), dtype=np.int16)
-    for j in range(4):
-        even, odd, prev_odd = 2 * j, 2 * j + 1, (2 * j - 1) % 8
-        out[:, j::4] = (mag[:, even::8] | (neg[:, even::8] << 7) |
-                        (mag[:, odd::8] << 4) | (neg[:, prev_odd::8] << 3))
-    return out.astype(np.uint8)
+    fields = (np.abs(c) | ((c < 0).astype(np.int16) << 5)).reshape(rows, K // 16, 16)
+    d0, d1, d2 = _fp6_stream(fields)
+    w = np.empty((rows, K // 16, 2), dtype=np.uint32)
+    w[..., 0] = (d0 | (d2 & np.uint64(FP6_Z0))).astype(np.uint32)
+    w[..., 1] = (d1 | (d2 & np.uint64(FP6_Z1))).astype(np.uint32)
+    return w.astype("<u4").view(np.uint8).reshape(rows, K // 2)
+
+
+def code_block_stream(packed: np.ndarray) -> list:
+    """The stream words [D0, D1, D2] of every block of packed rows (uint64
+    arrays [rows][blocks]): D0 = W0 & ~FP6_Z0, D1 = W1 & ~FP6_Z1,
+    D2 = (W0 & FP6_Z0) | (W1 & FP6_Z1)."""
+    p = np.ascontiguousarray(np.asarray(packed, dtype=np.uint8))
+    rows, nbytes = p.shape
+    if nbytes % 8:
+        raise ValueError("packed rows are whole 8-byte blocks")
+    w = p.view("<u4").reshape(rows, nbytes // 8, 2).astype(np.uint64)
+    z0, z1 = np.uint64(FP6_Z0), np.uint64(FP6_Z1)
+    m32 = np.uint64(0xFFFFFFFF)
+    return [w[..., 0] & (~z0 & m32), w[..., 1] & (~z1 & m32), (w[..., 0] & z0) | (w[..., 1] & z1)]
 
 
 def unpack_codes(packed: np.ndarray) -> np.ndarray:
     """Inverse of pack_codes (a negative zero reads as 0)."""
-    p = np.asarray(packed, dtype=np.int16)
-    rows, nbytes = p.shape
-    if nbytes % 4:
-        raise ValueError("packed rows are whole 32-bit words")
-    out = np.empty((rows, 2 * nbytes), dtype=np.int8)
-    for j in range(4):
-        byte = p[:, j::4]
-        next_byte = p[:, (j + 1) % 4::4]
-        e_mag, e_neg = byte & 7, (byte >> 7) & 1
-        o_mag, o_neg = (byte >> 4) & 7, (next_byte >> 3) & 1
-        out[:, 2 * j::8] = np.where(e_neg == 1, -e_mag, e_mag)
-        out[:, 2 * j + 1::8] = np.where(o_neg == 1, -o_mag, o_mag)
-    return out
+    rows = np.asarray(packed).shape[0]
+    f = _fp6_fields(code_block_stream(packed)).astype(np.int16)
+    mag, neg = f & 7, (f >> 5) & 1
+    return np.where(neg == 1, -mag, mag).astype(np.int8).reshape(rows, -1)
 
 
 # ----------------------------------------------------------------------------

@@ -53,8 +53,8 @@ __device__ __forceinline__ void smooth16_regs(const uint4& xa, const uint4& xb, 
 // Quantizes the lane's token over one 64-channel span (Eq. 2): with group 64
 // the four lanes l, l^16, l^32, l^48 (16 consecutive channels each) share one
 // scale; with group 32 (g32) the lanes l, l^16 share the scale of channels
-// 0-31 or 32-63 of the span.  Stores the lane's two code words at byte q_off
-// of q_rsrc and, if xs_dst is not null, the lane's group scale.
+// 0-31 or 32-63 of the span.  Stores the lane's code block (8 bytes) at byte
+// q_off of q_rsrc and, if xs_dst is not null, the lane's group scale.
 __device__ __forceinline__ void quantize_pack_store(const float (&v)[16], buf_rsrc q_rsrc, uint32_t q_off,
                                                     float* xs_dst, bool g32 = false) {
   float amax = 0.0f;
@@ -64,22 +64,11 @@ __device__ __forceinline__ void quantize_pack_store(const float (&v)[16], buf_rs
   if (!g32) amax = __builtin_fmaxf(amax, __shfl_xor(amax, 32));
   const float s = q4_scale(amax);
   const float inv = q4_inv(s);
-  // codes: q = clamp(rint(v * inv), -8, 7); a byte holds (q_odd + 8) * 16 + (q_even + 8),
-  // XOR 0x88 turns that into the two's-complement nibbles (q & 15) | (q_odd & 15) << 4,
-  // and those become the packed code word
-  uint32_t packed[2];
+  // codes q = clamp(rint(v * inv), -8, 7): the lane's 16 channels are one code block
+  float q[16];
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    uint32_t wv = 0;
-#pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const float qe = __builtin_fminf(__builtin_fmaxf(__builtin_rintf(v[8 * h + 2 * b] * inv), -8.0f), 7.0f);
-      const float qo = __builtin_fminf(__builtin_fmaxf(__builtin_rintf(v[8 * h + 2 * b + 1] * inv), -8.0f), 7.0f);
-      wv = __builtin_amdgcn_cvt_pk_u8_f32(__builtin_fmaf(qo, 16.0f, qe) + 136.0f, b, wv);
-    }
-    packed[h] = twos_nibbles_to_code_word(wv ^ 0x88888888u);
-  }
-  buf_store8(make_uint2(packed[0], packed[1]), q_rsrc, q_off);
+  for (int j = 0; j < 16; ++j) q[j] = q4_code(v[j], inv);
+  buf_store8(codes_to_block(q), q_rsrc, q_off);
   if (xs_dst != nullptr) *xs_dst = s;
 }
 

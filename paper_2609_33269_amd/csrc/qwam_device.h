@@ -30,12 +30,9 @@ __device__ __forceinline__ float q4_inv(float scale) {
   return (scale == 0.0f) ? 0.0f : 1.0f / scale;
 }
 
-// Returns the 4-bit two's-complement nibble (0..15) of the code of v.
-__device__ __forceinline__ uint32_t q4_nibble(float v, float inv) {
-  float p = v * inv;
-  p = __builtin_rintf(p);
-  p = __builtin_fminf(__builtin_fmaxf(p, -8.0f), 7.0f);
-  return static_cast<uint32_t>(static_cast<int>(p)) & 0xFu;
+// The code of v (Eq. 2): clamp(rint(v * inv), -8, 7), as a float.
+__device__ __forceinline__ float q4_code(float v, float inv) {
+  return __builtin_fminf(__builtin_fmaxf(__builtin_rintf(v * inv), -8.0f), 7.0f);
 }
 
 // bf16 bits -> float (exact).
@@ -70,22 +67,43 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return f32_to_bf16_rne(lo) | (f32_to_bf16_rne(hi) << 16);
 }
 
-// Packed code word, the storage format of every 4-bit code (qwam.h): the codes
-// c[k0..k0+7] of 8 consecutive channels share one little-endian 32-bit word,
-// byte j holding |c[k0+2j]| in bits 0-2 and its sign in bit 7, |c[k0+2j+1]| in
-// bits 4-6, and in bit 3 the sign of the odd code of byte j-1 (of byte 3 for
-// j = 0).  The quantizer never yields -8 (|v * inv| <= 7 (1 + 3u) < 7.5), so
-// three magnitude bits suffice; a zero code has sign 0.  Masking a word with
-// 0x87878787, and the word rotated right by 4 with the same mask, gives the
-// even and the odd codes as FP8 e4m3 bytes of value code * 2^-9.
-//
-// Conversion from 8 two's-complement nibbles t (nibble i = code of k0+i): the
-// negative nibbles are negated (one's complement + 1: carry-free, as the
-// result lies in 1..7) and every sign bit moves 4 places up, circularly.
-__device__ __forceinline__ uint32_t twos_nibbles_to_code_word(uint32_t t) {
-  const uint32_t neg = (t >> 3) & 0x11111111u;   // 1 in the low bit of each negative nibble
-  const uint32_t mag = ((t ^ (neg * 15u)) + neg) & 0x77777777u;
-  return mag | (__builtin_amdgcn_alignbit(t, t, 28) & 0x88888888u);
+// Code blocks, the storage format of every 4-bit code (qwam.h).  The codes
+// c[k0 .. k0+15] of 16 consecutive channels (k0 a multiple of 16) are written
+// as 6-bit fields F_i = sign << 5 | |c[k0+i]| (the FP6 e2m3 pattern of
+// c / 8), field i at bits 6i .. 6i+5 of a 96-bit stream D0 | D1 << 32 |
+// D2 << 64.  Bits 3-4 of every field are zero; in D0 and D1 those positions
+// (kFp6Z0, kFp6Z1) together are exactly the data bits of D2, which is stored
+// there: word 0 = D0 | (D2 & kFp6Z0), word 1 = D1 | (D2 & kFp6Z1).  A reader
+// gets the MFMA operand back with four ANDs (qwam_mfma.h).  The quantizer
+// never yields -8 (|v * inv| <= 7 (1 + 3u) < 7.5); a zero code has sign 0.
+constexpr uint32_t kFp6Z0 = 0x18618618u;   // bits 3-4 of the fields in D0
+constexpr uint32_t kFp6Z1 = 0x86186186u;   // bits 3-4 of the fields in D1
+
+// 6-bit field of an integral code q in [-7, 7] (float)
+__device__ __forceinline__ uint32_t fp6_field(float q) {
+  return static_cast<uint32_t>(__builtin_fabsf(q)) | (q < 0.0f ? 32u : 0u);
+}
+
+// fields F_0 .. F_15 -> the stream words D0, D1, D2
+__device__ __forceinline__ void fp6_stream(const uint32_t (&f)[16], uint32_t& d0, uint32_t& d1, uint32_t& d2) {
+  d0 = f[0] | (f[1] << 6) | (f[2] << 12) | (f[3] << 18) | (f[4] << 24) | (f[5] << 30);
+  d1 = (f[5] >> 2) | (f[6] << 4) | (f[7] << 10) | (f[8] << 16) | (f[9] << 22) | (f[10] << 28);
+  d2 = (f[10] >> 4) | (f[11] << 2) | (f[12] << 8) | (f[13] << 14) | (f[14] << 20) | (f[15] << 26);
+}
+
+// stream words -> the two stored words of a code block
+__device__ __forceinline__ uint2 fp6_code_block(uint32_t d0, uint32_t d1, uint32_t d2) {
+  return make_uint2(d0 | (d2 & kFp6Z0), d1 | (d2 & kFp6Z1));
+}
+
+// the code block of 16 integral codes q[0..15] (floats in [-7, 7])
+__device__ __forceinline__ uint2 codes_to_block(const float (&q)[16]) {
+  uint32_t f[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) f[i] = fp6_field(q[i]);
+  uint32_t d0, d1, d2;
+  fp6_stream(f, d0, d1, d2);
+  return fp6_code_block(d0, d1, d2);
 }
 
 }  // namespace qwam

@@ -1,4 +1,4 @@
-// The ASP GEMM: W4A4 integer group partial sums on FP8 matrix cores (exact),
+// The ASP GEMM: W4A4 integer group partial sums on FP6 matrix cores (exact),
 // float32 per-group scaling in registers, and the bf16 low-rank branch + bias
 // fused in the epilogue (the second kernel of App. B.1; Eq. 2 and Eq. 9).
 //
@@ -25,14 +25,13 @@
 //     loads (one ds_read_b128 = 32 codes of one row per lane, 32 consecutive
 //     rows per half-wave) hit distinct banks;
 //   * wave (wm, wn) owns rows 64*wm.. and columns 64*wn.. as 2 x 2 blocks of
-//     v_mfma_scale_f32_32x32x64_f8f6f4 (FP8 e4m3 operands, one group per
-//     instruction): lane l holds row l%32 and half l/32 of a group.  A packed
-//     code word w (sign-magnitude codes, see qwam.h) turns into two words of
-//     e4m3 bytes with one AND (w & 0x87878787) and one rotate + AND: each byte
-//     is then sign | |code| in the mantissa field, i.e. the e4m3 value
-//     code * 2^-9 (subnormals and the first binade are evenly spaced).  The
-//     instruction's E8M0 block scales (2^9 on each side) cancel the 2^-18, so
-//     the float32 result is the integer partial P itself, exactly (|P| <= 3136);
+//     v_mfma_scale_f32_32x32x64_f8f6f4 (FP6 e2m3 operands, one 64-channel
+//     span per instruction, twice the FP8 rate): lane l holds row l%32 and
+//     half l/32 of the span.  A code block (16 codes in two words, qwam.h)
+//     turns into three operand words with four ANDs: each 6-bit field is then
+//     sign | |code| in the mantissa field, the e2m3 subnormal code / 8.  The
+//     E8M0 scales (2^3 on each side) cancel the 2^-6, so the float32 result is
+//     the integer partial P itself, exactly (|P| <= 3136);
 //   * the per-output scale products sx[m] * sw[n] of a group are an outer
 //     product: one v_mfma_f32_32x32x1_2b_f32 (K = 1, one rounding per product,
 //     as a VALU multiply) gives them for two 32 x 32 blocks at once, in the
@@ -50,14 +49,12 @@
 //     (v_cvt_pk_bf16_f32) and stores through LDS so that every lane writes 16
 //     contiguous bytes.
 //
-// Group 32 (GS = 32, the paper's setting): the MFMA's K = 64 covers two groups.
-// Its two E8M0 block scales govern bytes 0-15 and 16-31 of every lane's
-// operand, so each lane takes 8 bytes of each group (32 codes: bytes 0-15 of
-// the operand from the first group, 16-31 from the second), and each block
-// runs twice, once per group, with the other block's scales set to 2^-127 on
-// both operands: its products (2^-254 and below) underflow to zero, so each
-// result is one group's integer partial, exactly.  Twice the MFMA work and
-// twice the scaling per output.
+// Group 32 (GS = 32, the paper's setting): the MFMA's K = 64 covers two groups,
+// one per lane half, and each lane's E8M0 scale governs its own 32 values.
+// Each block runs twice, once per group, with the other lane half's scales set
+// to 2^-127 on both operands: its products (2^-254 and below) underflow to
+// zero, so each result is one group's integer partial, exactly.  Twice the
+// MFMA work and twice the scaling per output.
 #include <type_traits>
 
 #include "qwam_device.h"
@@ -102,11 +99,11 @@ __device__ __forceinline__ void lds_wait_barrier() { asm volatile("s_waitcnt lgk
 __device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
 // LDS reads that the compiler keeps in program order (volatile)
-__device__ __forceinline__ uint2 lds_load8_volatile(const uint8_t* p) {
-  typedef unsigned v2u __attribute__((ext_vector_type(2)));
-  typedef const volatile __attribute__((address_space(3))) v2u lds_v2u;
-  const v2u v = *(lds_v2u*)(p);
-  return make_uint2(v.x, v.y);
+__device__ __forceinline__ uint4 lds_load16_volatile(const uint8_t* p) {
+  typedef unsigned v4u __attribute__((ext_vector_type(4)));
+  typedef const volatile __attribute__((address_space(3))) v4u lds_v4u;
+  const v4u v = *(lds_v4u*)(p);
+  return make_uint4(v.x, v.y, v.z, v.w);
 }
 __device__ __forceinline__ float lds_load4_volatile(const float* p) {
   typedef const volatile __attribute__((address_space(3))) float lds_f;
@@ -227,11 +224,10 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
   // row 8*(v/4) + 4*(lane/32) + v%4
   const int sx_row = 8 * ((lane & 15) >> 2) + 4 * (lane >> 5) + (lane & 3);
 
-  // LDS data of one 64-channel span: packed A / B fragments and the lane's
-  // scales (NS groups): the activation scale of row l%32 of each row block
-  // (A operand of the scale product) and the weight scale of column l%32 of
-  // column block l/32 (B operand).  With group 32 a fragment is 8 bytes of
-  // each group.
+  // LDS data of one 64-channel span: packed A / B fragments (16 bytes, the
+  // lane's half of the span) and the lane's scales (NS groups): the activation
+  // scale of row l%32 of each row block (A operand of the scale product) and
+  // the weight scale of column l%32 of column block l/32 (B operand).
   struct GroupData {
     uint4 a[2], b[2];
     float sx[2][NS], sw[NS];
@@ -240,14 +236,8 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
   // and followed by a compiler-only fence, so they are issued here and not
   // sunk next to their first use; the wait for them lands at that use.
   auto load_frag = [&](const uint8_t* rowp, int q) __attribute__((always_inline)) {
-    if constexpr (GS == 64) {
-      return *reinterpret_cast<const uint4*>(rowp + ((2 * q) ^ fslot) * 16);
-    } else {
-      const int sw0 = swz(frow);
-      const uint2 lo = lds_load8_volatile(rowp + ((2 * q) ^ sw0) * 16 + fhalf * 8);
-      const uint2 hi = lds_load8_volatile(rowp + ((2 * q + 1) ^ sw0) * 16 + fhalf * 8);
-      return make_uint4(lo.x, lo.y, hi.x, hi.y);
-    }
+    if constexpr (GS == 64) return *reinterpret_cast<const uint4*>(rowp + ((2 * q) ^ fslot) * 16);
+    else return lds_load16_volatile(rowp + ((2 * q) ^ fslot) * 16);
   };
   auto load_group = [&](const Stage& cur, int q) __attribute__((always_inline)) {
     GroupData d;
@@ -292,17 +282,17 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
   auto group = [&](int g, const GroupData& d) __attribute__((always_inline)) {
     v8i af[2], bf[2];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) af[i] = codes_to_e4m3(d.a[i]);
+    for (int i = 0; i < 2; ++i) af[i] = codes_to_fp6(d.a[i]);
 #pragma unroll
-    for (int j = 0; j < 2; ++j) bf[j] = codes_to_e4m3(d.b[j]);
+    for (int j = 0; j < 2; ++j) bf[j] = codes_to_fp6(d.b[j]);
 
     // the exact integer partial of block (i, j) for group h of the span, as
-    // float32 (group 64: the whole span; group 32: the other group's block
+    // float32 (group 64: the whole span; group 32: the other lane half's
     // scales are 2^-127 on both operands, so its products underflow to zero)
     auto mfma_block = [&](int i, int j, int h) __attribute__((always_inline)) {
       int sc = kE8M0Code;
       if constexpr (GS == 32) sc = ((lane >> 5) == h) ? kE8M0Code : 0;
-      return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af[i], bf[j], v16f{}, 0, 0, 0, sc, 0, sc);
+      return fp6_partial(af[i], bf[j], sc, sc);
     };
     // scale products of row block i and both column blocks, group h:
     // registers 0-15 belong to column block 0, 16-31 to column block 1
@@ -407,16 +397,16 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
     // Group 64: a software pipeline across groups.  The matrix core runs one
     // MFMA at a time and a wave that issues an MFMA while the previous one is
     // still running waits for it, so every MFMA gets its own slot, followed by
-    // about 16 VALU instructions (64 cycles, the length of one MFMA) that do not
-    // depend on it: the updates of blocks whose products landed one slot or
-    // more earlier, or the unpacking of the next group's fragments.  Per group
-    // g (S = scale products, P = integer partials):
-    //   slot 1  S0(g)              | update (1,1) of g-1; unpack A1(g)
-    //   slot 2  P00(g) = A0 x B0   | unpack B1(g)
+    // 16-20 VALU instructions that do not depend on it: the updates of blocks
+    // whose products landed one slot or more earlier, or the unpacking of
+    // fragments (8 instructions each, split in halves to even out the
+    // slots).  Per group g (S = scale products, P = integer partials):
+    //   slot 1  S0(g)              | update (1,1) of g-1; 1/2 A1(g)
+    //   slot 2  P00(g) = A0 x B0   | B1(g); 1/2 A1(g)
     //   slot 3  P01(g) = A0 x B1   | LDS reads of g+1; update (0,0)
-    //   slot 4  S1(g)              | update (0,1)
-    //   slot 5  P10(g) = A1 x B0   | unpack A0(g+1)
-    //   slot 6  P11(g) = A1 x B1   | update (1,0); unpack B0(g+1)
+    //   slot 4  S1(g)              | update (0,1); 1/2 A0(g+1)
+    //   slot 5  P10(g) = A1 x B0   | 1/2 A0(g+1); 1/2 B0(g+1)
+    //   slot 6  P11(g) = A1 x B1   | update (1,0); 1/2 B0(g+1)
     // A stage ends inside its last group: before the LDS reads of g+1 the
     // wave waits for its copies of the next stage and for its own LDS reads,
     // then the barrier frees the stage just read for the copy of the stage
@@ -428,16 +418,16 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
       v32f s1;             // scale products and partial of block (1, 1) of
       v16f p11;            // the previous group, updated in slot 1
     };
-    auto fp8_partial = [&](const v8i& a, const v8i& b) __attribute__((always_inline)) {
-      return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, v16f{}, 0, 0, 0, kE8M0Code, 0, kE8M0Code);
+    auto span_partial = [&](const v8i& a, const v8i& b) __attribute__((always_inline)) {
+      return fp6_partial(a, b, kE8M0Code, kE8M0Code);
     };
     auto scale_products = [&](float sx, float sw) __attribute__((always_inline)) {
       if constexpr (PARTIALS) return v32f{};
       else return __builtin_amdgcn_mfma_f32_32x32x1f32(sx, sw, v32f{}, 0, 0, 0);
     };
     auto start = [&](Pipe& pp, const GroupData& d) __attribute__((always_inline)) {
-      pp.af0 = codes_to_e4m3(d.a[0]);
-      pp.bf0 = codes_to_e4m3(d.b[0]);
+      pp.af0 = codes_to_fp6(d.a[0]);
+      pp.bf0 = codes_to_fp6(d.b[0]);
       pp.ra1 = d.a[1];
       pp.rb1 = d.b[1];
       if (!PARTIALS) { pp.sx0 = d.sx[0][0]; pp.sx1 = d.sx[1][0]; pp.sw = d.sw[0]; }
@@ -445,18 +435,31 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
     // group g at position q (0..7) of two consecutive stages: q < 4 reads
     // st0, q >= 4 st1; the last group of a stage (q % 4 == 3) switches the
     // ring, issuing stage s_next into the buffer it has just finished
+    // half of an unpack: code block (w0, w1) -> operand words 3h .. 3h+2 of r
+    // (words 6-7 are not read with FP6 operands and stay unset)
+    auto unpack_half = [&](v8i& r, int h, uint32_t w0, uint32_t w1) __attribute__((always_inline)) {
+      r[3 * h] = static_cast<int>(w0 & ~kFp6Z0);
+      r[3 * h + 1] = static_cast<int>(w1 & ~kFp6Z1);
+      r[3 * h + 2] = static_cast<int>((w0 & kFp6Z0) | (w1 & kFp6Z1));
+    };
     auto step = [&](auto qc, int g, Pipe& pp, int s_next) __attribute__((always_inline)) {
       constexpr int q = decltype(qc)::value;
+      // slot 1: S0 | update (1,1) of g-1, half of A1
       const v32f s0 = scale_products(pp.sx0, pp.sw);
       __builtin_amdgcn_sched_barrier(0);
       if (!PARTIALS || g > 0) update(1, 1, g - 1, 0, pp.p11, pp.s1);
-      const v8i af1 = codes_to_e4m3(pp.ra1);
+      v8i af1, bf1, af0n, bf0n;
+      unpack_half(af1, 0, pp.ra1.x, pp.ra1.y);
       __builtin_amdgcn_sched_barrier(0);
-      const v16f p00 = fp8_partial(pp.af0, pp.bf0);
+      // slot 2: P00 | B1, other half of A1
+      const v16f p00 = span_partial(pp.af0, pp.bf0);
       __builtin_amdgcn_sched_barrier(0);
-      const v8i bf1 = codes_to_e4m3(pp.rb1);
+      unpack_half(bf1, 0, pp.rb1.x, pp.rb1.y);
+      unpack_half(bf1, 1, pp.rb1.z, pp.rb1.w);
+      unpack_half(af1, 1, pp.ra1.z, pp.ra1.w);
       __builtin_amdgcn_sched_barrier(0);
-      const v16f p01 = fp8_partial(pp.af0, bf1);
+      // slot 3: P01 | LDS reads of g+1, update (0,0)
+      const v16f p01 = span_partial(pp.af0, bf1);
       __builtin_amdgcn_sched_barrier(0);
       if constexpr (q % 4 == 3) {
         wait_vmcnt<0>();
@@ -468,20 +471,26 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
       if constexpr (q % 4 == 3) issue(s_next, q == 3 ? st0 : st1);
       update(0, 0, g, 0, p00, s0);
       __builtin_amdgcn_sched_barrier(0);
+      // slot 4: S1 | update (0,1), half of A0 of g+1
       const v32f s1 = scale_products(pp.sx1, pp.sw);
       __builtin_amdgcn_sched_barrier(0);
       update(0, 1, g, 0, p01, s0);
+      unpack_half(af0n, 0, nd.a[0].x, nd.a[0].y);
       __builtin_amdgcn_sched_barrier(0);
-      const v16f p10 = fp8_partial(af1, pp.bf0);
+      // slot 5: P10 | other half of A0 of g+1, half of B0 of g+1
+      const v16f p10 = span_partial(af1, pp.bf0);
       __builtin_amdgcn_sched_barrier(0);
-      const v8i af0n = codes_to_e4m3(nd.a[0]);
+      unpack_half(af0n, 1, nd.a[0].z, nd.a[0].w);
+      unpack_half(bf0n, 0, nd.b[0].x, nd.b[0].y);
       __builtin_amdgcn_sched_barrier(0);
-      const v16f p11 = fp8_partial(af1, bf1);
+      // slot 6: P11 | update (1,0), other half of B0 of g+1
+      const v16f p11 = span_partial(af1, bf1);
       __builtin_amdgcn_sched_barrier(0);
       update(1, 0, g, 0, p10, s1);
-      pp.bf0 = codes_to_e4m3(nd.b[0]);
+      unpack_half(bf0n, 1, nd.b[0].z, nd.b[0].w);
       __builtin_amdgcn_sched_barrier(0);
       pp.af0 = af0n;
+      pp.bf0 = bf0n;
       pp.ra1 = nd.a[1];
       pp.rb1 = nd.b[1];
       if (!PARTIALS) { pp.sx0 = nd.sx[0][0]; pp.sx1 = nd.sx[1][0]; pp.sw = nd.sw[0]; }

@@ -15,9 +15,9 @@
 //     memory round trip;
 //   * the activation scales are broadcast across each row of 16 lanes by DPP
 //     inside the scale multiply, as in the large-tile kernel;
-//   * group 32 (GS = 32): as in the large-tile kernel, a lane takes 8 bytes of
-//     each group of the 64-channel span and each block runs once per group with
-//     the other group's block scales at 2^-127.
+//   * group 32 (GS = 32): as in the large-tile kernel, lane half h holds group
+//     h of the 64-channel span and each block runs once per group with the
+//     other lane half's scales at 2^-127.
 #include <type_traits>
 
 #include "qwam_device.h"
@@ -75,22 +75,15 @@ __global__ __launch_bounds__(64 * KW) void asp_gemm_small_kernel(
   const buf_rsrc b_rsrc = make_rsrc(wq + static_cast<int64_t>(n0) * KB, static_cast<uint32_t>(min(SB, N - n0)) * KB);
   const buf_rsrc xs_rsrc = make_rsrc(xs, static_cast<uint32_t>(GSC) * M * 4u);
   const buf_rsrc ws_rsrc = make_rsrc(ws, static_cast<uint32_t>(GSC) * N * 4u);
-  // group 64: the lane's 16-byte half of the span; group 32: 8 bytes of each group
-  const uint32_t ab_off = static_cast<uint32_t>(frow * KB + fhalf * (GS == 64 ? 16 : 8));
+  // the lane's 16-byte half of the span (with group 32: one group)
+  const uint32_t ab_off = static_cast<uint32_t>(frow * KB + fhalf * 16);
   const uint32_t sx_off = static_cast<uint32_t>(m0 + sx_row) * 4u;
   const uint32_t sw_off = static_cast<uint32_t>(n0 + frow) * 4u;
 
   // chunk c holds groups g_lo + CH*c .. + CH-1; in the last chunk, groups
   // past g_hi are never loaded (a row's next bytes belong to the next row) and
   // never multiplied.  FULL chunks need no per-group check.
-  auto load_frag = [&](buf_rsrc r, uint32_t off) __attribute__((always_inline)) {
-    if constexpr (GS == 64) {
-      return buf_load16(r, off);
-    } else {
-      const uint2 lo = buf_load8(r, off), hi = buf_load8(r, off + 16u);
-      return make_uint4(lo.x, lo.y, hi.x, hi.y);
-    }
-  };
+  auto load_frag = [&](buf_rsrc r, uint32_t off) __attribute__((always_inline)) { return buf_load16(r, off); };
   auto load = [&](int c, Chunk<NS>& ch, auto full) __attribute__((always_inline)) {
 #pragma unroll
     for (int q = 0; q < CH; ++q) {
@@ -115,12 +108,12 @@ __global__ __launch_bounds__(64 * KW) void asp_gemm_small_kernel(
     for (int q = 0; q < CH; ++q) {
       const int g = g_lo + c * CH + q;
       if (decltype(full)::value || g < g_hi) {
-        const v8i af = codes_to_e4m3(ch.a[q]), bf = codes_to_e4m3(ch.b[q]);
+        const v8i af = codes_to_fp6(ch.a[q]), bf = codes_to_fp6(ch.b[q]);
 #pragma unroll
         for (int h = 0; h < NS; ++h) {
           int sc = kE8M0Code;
           if constexpr (GS == 32) sc = ((lane >> 5) == h) ? kE8M0Code : 0;
-          const v16f p = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af, bf, v16f{}, 0, 0, 0, sc, 0, sc);
+          const v16f p = fp6_partial(af, bf, sc, sc);
           if (PARTIALS) {
             // result layout: lane l holds column l%32 and rows 8*(v/4) + 4*(l/32) + v%4
 #pragma unroll

@@ -11,11 +11,10 @@
 //     current span: the A-operand rows of v_mfma_scale_f32_32x32x64_f8f6f4.
 //     It smooths them (x * 1/lambda, fetched with x), takes the
 //     span's absmax with its partner lane l ^ 32, quantizes (Eq. 2, the same
-//     arithmetic as the activation kernel, so the codes are identical), packs
-//     the codes into code words and turns those into e4m3 bytes exactly as the
-//     weights' code words are turned (codes_to_e4m3): both operands then carry
-//     the same permutation of k, and the MFMA returns the span's exact integer
-//     partial;
+//     arithmetic as the activation kernel, so the codes are identical) and
+//     writes them as FP6 fields in the order codes_to_fp6 gives the weights'
+//     fields: both operands then carry the same channel order, and the MFMA
+//     returns the span's exact integer partial;
 //   * the same registers feed the down-projection t = bf16(x~) . L1 on
 //     v_mfma_f32_32x32x16_bf16 (rank columns, four 16-deep steps per span);
 //   * per span: acc += P * xs * ws as in the GEMMs (the token scale of each
@@ -125,27 +124,31 @@ __global__ __launch_bounds__(64 * LW) void asp_layer_small_kernel(
     amax = __builtin_fmaxf(amax, __shfl_xor(amax, 32));
     const float s = q4_scale(amax);
     const float inv = q4_inv(s);
-    // codes -> code words (the storage format) -> e4m3 operand bytes
+    // codes -> FP6 fields: the MFMA operand itself, and the two code blocks
+    // (the storage format) for the optional copy of the codes
+    v8i af;          // words 6-7 are not read with FP6 operands and stay unset
     uint32_t cw[4];
 #pragma unroll
-    for (int h = 0; h < 4; ++h) {
-      uint32_t wv = 0;
+    for (int h = 0; h < 2; ++h) {
+      uint32_t fl[16];
 #pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        const float qe = __builtin_fminf(__builtin_fmaxf(__builtin_rintf(v[8 * h + 2 * b] * inv), -8.0f), 7.0f);
-        const float qo = __builtin_fminf(__builtin_fmaxf(__builtin_rintf(v[8 * h + 2 * b + 1] * inv), -8.0f), 7.0f);
-        wv = __builtin_amdgcn_cvt_pk_u8_f32(__builtin_fmaf(qo, 16.0f, qe) + 136.0f, b, wv);
-      }
-      cw[h] = twos_nibbles_to_code_word(wv ^ 0x88888888u);
+      for (int i = 0; i < 16; ++i) fl[i] = fp6_field(q4_code(v[16 * h + i], inv));
+      uint32_t d0, d1, d2;
+      fp6_stream(fl, d0, d1, d2);
+      af[3 * h] = static_cast<int>(d0);
+      af[3 * h + 1] = static_cast<int>(d1);
+      af[3 * h + 2] = static_cast<int>(d2);
+      const uint2 blk = fp6_code_block(d0, d1, d2);
+      cw[2 * h] = blk.x;
+      cw[2 * h + 1] = blk.y;
     }
-    const uint4 cw4 = make_uint4(cw[0], cw[1], cw[2], cw[3]);
     if (write_act && m0 + frow < M) {
-      *reinterpret_cast<uint4*>(xq_out + static_cast<int64_t>(m0 + frow) * KB + g * 32 + fhalf * 16) = cw4;
+      *reinterpret_cast<uint4*>(xq_out + static_cast<int64_t>(m0 + frow) * KB + g * 32 + fhalf * 16) =
+          make_uint4(cw[0], cw[1], cw[2], cw[3]);
       if (fhalf == 0) xs_out[static_cast<int64_t>(g) * M + m0 + frow] = s;
     }
     // exact integer partial of the span, then acc += P * xs * ws
-    const v16f p = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(codes_to_e4m3(cw4), codes_to_e4m3(f.w), v16f{}, 0,
-                                                                   0, 0, kE8M0Code, 0, kE8M0Code);
+    const v16f p = fp6_partial(af, codes_to_fp6(f.w), kE8M0Code, kE8M0Code);
     const float sx_lane = __shfl(s, sx_row);            // scale of the token of result register v
     scale_accumulate(std::make_integer_sequence<int, 16>{}, acc, p, sx_lane, f.sw);
     // t partial: A = bf16(x~) of 8 channels per step, B = the matching L1t slice

@@ -1,5 +1,5 @@
-// Matrix-core helpers shared by the ASP GEMM kernels (gfx950): the FP8 view
-// of packed code words, the exact integer partial of one group on
+// Matrix-core helpers shared by the ASP GEMM kernels (gfx950): the FP6 view
+// of packed code blocks, the exact integer partial of one group on
 // v_mfma_scale_f32_32x32x64_f8f6f4, and the per-group float32 scaling of a
 // 32 x 32 result block with the row scales broadcast by DPP.
 #pragma once
@@ -13,22 +13,31 @@ typedef float v16f __attribute__((ext_vector_type(16)));
 typedef float v32f __attribute__((ext_vector_type(32)));
 typedef int v8i __attribute__((ext_vector_type(8)));
 
-// 32 packed codes (16 bytes of one row) -> one FP8 MFMA operand of 32 e4m3
-// bytes, ordered [even k of w0, odd k of w0, even k of w1, ...] (the same
-// permutation for A and B, so the dot product is unchanged).
-__device__ __forceinline__ v8i codes_to_e4m3(const uint4& p) {
-  const uint32_t w[4] = {p.x, p.y, p.z, p.w};
-  v8i r;
-#pragma unroll
-  for (int d = 0; d < 4; ++d) {
-    r[2 * d] = static_cast<int>(w[d] & 0x87878787u);
-    r[2 * d + 1] = static_cast<int>(__builtin_amdgcn_alignbit(w[d], w[d], 4) & 0x87878787u);
-  }
-  return r;
+// 32 packed codes (16 bytes of one row: two code blocks, qwam_device.h) ->
+// one FP6 e2m3 MFMA operand: field i of the 192-bit operand (dwords 0-5) is
+// the code of channel i of the 32, value code / 8.  Four ANDs per block.
+__device__ __forceinline__ v8i codes_to_fp6(const uint4& p) {
+  const v4i lo = {static_cast<int>(p.x & ~kFp6Z0), static_cast<int>(p.y & ~kFp6Z1),
+                  static_cast<int>((p.x & kFp6Z0) | (p.y & kFp6Z1)), 0};
+  const v4i hi = {static_cast<int>(p.z & ~kFp6Z0), static_cast<int>(p.w & ~kFp6Z1),
+                  static_cast<int>((p.z & kFp6Z0) | (p.w & kFp6Z1)), 0};
+  // words 6-7 are not read with FP6 operands (left undefined)
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 4, 5, 6, -1, -1);
 }
 
-// E8M0 scale 2^9 (127 + 9) for both operands: (code * 2^-9 * 2^9) products
-constexpr int kE8M0Code = 127 + 9;
+// operand format of v_mfma_scale_f32_32x32x64_f8f6f4 (cbsz / blgp): FP6 e2m3
+constexpr int kFmtFp6 = 2;
+// E8M0 scale 2^3 (127 + 3) for both operands: (code / 8 * 2^3) products are
+// the integer products; each lane's scale governs its own 32 values
+constexpr int kE8M0Code = 127 + 3;
+
+// exact integer partial of a 32 x 32 block over 32 + 32 channels: lane l holds
+// row / column l % 32 and channels 32 * (l / 32) .. +31 of the span; sa and sb
+// are the lane's E8M0 scales (kE8M0Code, or 0 to mask its channels: with 2^-127
+// on both operands the products underflow to zero)
+__device__ __forceinline__ v16f fp6_partial(const v8i& a, const v8i& b, int sa, int sb) {
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, v16f{}, kFmtFp6, kFmtFp6, 0, sa, 0, sb);
+}
 
 // x of lane 16 * (lane / 16) + V (lane V of this lane's row of 16, DPP
 // row_newbcast) times y, in one instruction.  The DPP source x must not be

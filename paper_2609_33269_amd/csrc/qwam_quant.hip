@@ -12,42 +12,44 @@
 namespace qwam {
 
 // ---------------------------------------------------------------------------
-// Weight pack: 8 lanes per (row, group); each lane owns 8 consecutive floats,
-// i.e. one packed code word.
+// Weight pack: 4 lanes per (row, 64-channel span); each lane owns 16
+// consecutive floats, i.e. one code block.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void pack_weights_kernel(const float* __restrict__ R,
                                                            uint8_t* __restrict__ wq,
                                                            float* __restrict__ ws, int N, int K, int g32) {
   const int G = K / kGroup;
-  const int64_t team = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) >> 3;
-  const int sub = threadIdx.x & 7;
+  const int64_t team = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) >> 2;
+  const int sub = threadIdx.x & 3;
   const bool active = team < static_cast<int64_t>(N) * G;
   const int n = active ? static_cast<int>(team / G) : 0;
   const int g = active ? static_cast<int>(team % G) : 0;
 
-  float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  float v[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) v[i] = 0.0f;
   if (active) {
-    const float4* src = reinterpret_cast<const float4*>(R + static_cast<int64_t>(n) * K + g * kGroup + sub * 8);
-    const float4 a = src[0], b = src[1];
-    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
-    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+    const float4* src = reinterpret_cast<const float4*>(R + static_cast<int64_t>(n) * K + g * kGroup + sub * 16);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float4 a = src[i];
+      v[4 * i] = a.x; v[4 * i + 1] = a.y; v[4 * i + 2] = a.z; v[4 * i + 3] = a.w;
+    }
   }
   float amax = 0.0f;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) amax = __builtin_fmaxf(amax, __builtin_fabsf(v[i]));
-  // the 8 lanes of a 64-channel span; with group 32 lanes 0-3 and 4-7 separately
+  for (int i = 0; i < 16; ++i) amax = __builtin_fmaxf(amax, __builtin_fabsf(v[i]));
+  // the 4 lanes of a 64-channel span; with group 32 lanes 0-1 and 2-3 separately
   amax = __builtin_fmaxf(amax, __shfl_xor(amax, 1));
-  amax = __builtin_fmaxf(amax, __shfl_xor(amax, 2));
-  if (!g32) amax = __builtin_fmaxf(amax, __shfl_xor(amax, 4));
+  if (!g32) amax = __builtin_fmaxf(amax, __shfl_xor(amax, 2));
   const float s = q4_scale(amax);
   const float inv = q4_inv(s);
-  uint32_t t = 0;
+  float q[16];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) t |= q4_nibble(v[i], inv) << (4 * i);
+  for (int i = 0; i < 16; ++i) q[i] = q4_code(v[i], inv);
   if (active) {
-    *reinterpret_cast<uint32_t*>(wq + static_cast<int64_t>(n) * (K / 2) + g * (kGroup / 2) + sub * 4) =
-        twos_nibbles_to_code_word(t);
-    if (g32 ? (sub & 3) == 0 : sub == 0) ws[static_cast<int64_t>(g32 ? 2 * g + (sub >> 2) : g) * N + n] = s;
+    *reinterpret_cast<uint2*>(wq + static_cast<int64_t>(n) * (K / 2) + g * (kGroup / 2) + sub * 8) = codes_to_block(q);
+    if (g32 ? (sub & 1) == 0 : sub == 0) ws[static_cast<int64_t>(g32 ? 2 * g + (sub >> 1) : g) * N + n] = s;
   }
 }
 
@@ -265,7 +267,7 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_deflated_
 hipError_t launch_pack_weights(int K, int N, int group, const float* R, const float* smooth, uint8_t* wq,
                                float* ws, float* inv_smooth, hipStream_t stream) {
   const int64_t teams = static_cast<int64_t>(N) * (K / kGroup);
-  const int64_t blocks = (teams * 8 + 255) / 256;
+  const int64_t blocks = (teams * 4 + 255) / 256;
   hipLaunchKernelGGL(pack_weights_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, R,
                      wq, ws, N, K, group == 32 ? 1 : 0);
   hipLaunchKernelGGL(inverse_smoothing_kernel, dim3((K + 255) / 256), dim3(256), 0, stream, smooth,

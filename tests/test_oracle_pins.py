@@ -134,15 +134,40 @@ def test_quantizer_codes_match_exact_rational_rounding():
 # packing
 # --------------------------------------------------------------------------
 
-def _e4m3_value(byte: int) -> float:
-    """FP8 e4m3 (OCP) decoded from its definition: sign, 4 exponent bits with
-    bias 7, 3 mantissa bits, subnormals at exponent 0."""
-    s = -1.0 if byte & 0x80 else 1.0
-    e = (byte >> 3) & 0xF
-    m = byte & 7
+def _e2m3_value(field: int) -> float:
+    """FP6 e2m3 (OCP MX) decoded from its definition: sign bit 5, 2 exponent
+    bits with bias 1, 3 mantissa bits, subnormals at exponent 0."""
+    s = -1.0 if field & 0x20 else 1.0
+    e = (field >> 3) & 3
+    m = field & 7
     if e == 0:
-        return s * m / 8 * 2.0 ** -6
-    return s * (1 + m / 8) * 2.0 ** (e - 7)
+        return s * m / 8
+    return s * (1 + m / 8) * 2.0 ** (e - 1)
+
+
+def _block_fields(block8: bytes) -> list:
+    """The 16 six-bit fields of one packed block, read bit by bit from the
+    layout's definition: word 0 = D0 | (D2 & Z0), word 1 = D1 | (D2 & Z1),
+    where Z0 / Z1 are the positions of bits 3-4 of the fields lying in D0 / D1."""
+    w0 = int.from_bytes(block8[:4], "little")
+    w1 = int.from_bytes(block8[4:], "little")
+    zero_pos = [6 * i + b for i in range(16) for b in (3, 4)]
+    z0 = sum(1 << p for p in zero_pos if p < 32)
+    z1 = sum(1 << (p - 32) for p in zero_pos if 32 <= p < 64)
+    d0, d1, d2 = w0 & ~z0, w1 & ~z1, (w0 & z0) | (w1 & z1)
+    stream = d0 | (d1 << 32) | (d2 << 64)
+    return [(stream >> (6 * i)) & 63 for i in range(16)]
+
+
+def test_pack_zero_bits_hold_the_third_word():
+    """The layout is a bijection: the exponent bits (3-4) of the fields in the
+    first two words are exactly the data bits of the third."""
+    zero_pos = {6 * i + b for i in range(16) for b in (3, 4)}
+    z0 = sum(1 << p for p in zero_pos if p < 32)
+    z1 = sum(1 << (p - 32) for p in zero_pos if 32 <= p < 64)
+    data2 = sum(1 << (p - 64) for p in range(64, 96) if p not in zero_pos)
+    assert (z0, z1) == (O.FP6_Z0, O.FP6_Z1)
+    assert z0 & z1 == 0 and z0 | z1 == data2
 
 
 def test_pack_roundtrip_random_codes():
@@ -151,58 +176,70 @@ def test_pack_roundtrip_random_codes():
     packed = O.pack_codes(codes)
     assert packed.shape == (17, 128) and packed.dtype == np.uint8
     assert (O.unpack_codes(packed) == codes).all()
-    # every code value at every position of a word, alone in its word
-    for pos in range(8):
+    # every code value at every position of a block, alone in its block
+    for pos in range(16):
         for c in range(-7, 8):
-            one = np.zeros((1, 8), np.int8)
+            one = np.zeros((1, 16), np.int8)
             one[0, pos] = c
             assert (O.unpack_codes(O.pack_codes(one)) == one).all()
 
 
-def test_pack_every_word_decodes_in_range():
+def test_pack_every_block_decodes_in_range():
     rng = np.random.default_rng(15)
     words = rng.integers(0, 2 ** 32, size=(1, 4096), dtype=np.uint64).astype(np.uint32)
     packed = words.view(np.uint8).reshape(1, -1)
     codes = O.unpack_codes(packed)
     assert codes.min() >= -7 and codes.max() <= 7
     again = O.pack_codes(codes)
-    # words without a negative zero are reproduced exactly; one with a
+    # blocks without a negative zero are reproduced exactly; one with a
     # negative zero differs from its canonical form only in sign bits
-    same = (again.reshape(-1, 4) == packed.reshape(-1, 4)).all(axis=1)
-    diff = (again.reshape(-1, 4) ^ packed.reshape(-1, 4))
-    assert ((diff & 0x77) == 0).all()
+    sign_pos = [6 * i + 5 for i in range(16)]
+    d_sign = [sum(1 << (p - 32 * k) for p in sign_pos if 32 * k <= p < 32 * k + 32) for k in range(3)]
+    sign0 = d_sign[0] | (d_sign[2] & O.FP6_Z0)
+    sign1 = d_sign[1] | (d_sign[2] & O.FP6_Z1)
+    a = again.view("<u4").reshape(-1, 2)
+    b = packed.view("<u4").reshape(-1, 2)
+    same = (a == b).all(axis=1)
+    assert (((a[:, 0] ^ b[:, 0]) & ~np.uint32(sign0)) == 0).all()
+    assert (((a[:, 1] ^ b[:, 1]) & ~np.uint32(sign1)) == 0).all()
     assert same.sum() > 0 and (~same).sum() > 0
 
 
-def test_pack_known_words():
-    # hand-derived from the layout: byte j = |even| | sign(even) << 7 |
-    # |odd| << 4 | sign(odd code of byte j-1) << 3
-    codes = np.array([[1, -1, -7, 7, 0, 3, -3, 0]], dtype=np.int8)
-    assert O.pack_codes(codes).tolist() == [[0x11, 0xFF, 0x30, 0x83]]
-    # the last odd code's sign wraps to bit 3 of the word's first byte
-    codes = np.array([[0, 0, 0, 0, 0, 0, 0, -5]], dtype=np.int8)
-    assert O.pack_codes(codes).tolist() == [[0x08, 0x00, 0x00, 0x50]]
+def test_pack_known_blocks():
+    # hand-derived from the layout: code 1 -> field 0b000001 at bits 0-5,
+    # code -1 -> field 0b100001 at bits 6-11: word 0 = 0x841
+    codes = np.zeros((1, 16), np.int8)
+    codes[0, :2] = [1, -1]
+    assert O.pack_codes(codes).tolist() == [[0x41, 0x08, 0, 0, 0, 0, 0, 0]]
+    # code -7 in position 15: field 0b100111 at stream bits 90-95, i.e. D2 bits
+    # 26-28 and 31; bits 27-28 are stored in word 0, bits 26 and 31 in word 1
+    codes = np.zeros((1, 16), np.int8)
+    codes[0, 15] = -7
+    assert O.pack_codes(codes).tolist() == [[0, 0, 0, 0x18, 0, 0, 0, 0x84]]
 
 
 def test_pack_rejects_minus_eight():
     with pytest.raises(ValueError):
-        O.pack_codes(np.array([[-8, 0, 0, 0, 0, 0, 0, 0]], dtype=np.int8))
+        O.pack_codes(np.array([[-8] + [0] * 15], dtype=np.int8))
 
 
-def test_packed_words_are_fp8_codes():
-    """The point of the layout: a word masked with 0x87878787 holds the even
-    codes, and the word rotated right by 4 bits, masked the same way, holds the
-    odd codes, each as an e4m3 byte of value code * 2^-9."""
+def test_packed_blocks_are_fp6_codes():
+    """The point of the layout: the four masks give the FP6 e2m3 operand whose
+    field j is the code of channel j of the block, of value code / 8."""
     rng = np.random.default_rng(16)
     codes = rng.integers(-7, 8, size=(1, 64)).astype(np.int8)
     codes[0, :15] = np.arange(-7, 8)
-    words = O.pack_codes(codes).view("<u4").reshape(-1)
-    for i, w in enumerate(int(x) for x in words):
-        even = w & 0x87878787
-        odd = ((w >> 4) | (w << 28)) & 0xFFFFFFFF & 0x87878787
-        for j in range(4):
-            assert _e4m3_value((even >> (8 * j)) & 0xFF) == codes[0, 8 * i + 2 * j] * 2.0 ** -9
-            assert _e4m3_value((odd >> (8 * j)) & 0xFF) == codes[0, 8 * i + 2 * j + 1] * 2.0 ** -9
+    packed = O.pack_codes(codes).tobytes()
+    for blk in range(4):
+        fields = _block_fields(packed[8 * blk: 8 * blk + 8])
+        for j in range(16):
+            assert _e2m3_value(fields[j]) == codes[0, 16 * blk + j] / 8
+    # and the oracle's own stream words agree with the bit-by-bit reading
+    d = O.code_block_stream(O.pack_codes(codes))
+    for blk in range(4):
+        fields = _block_fields(packed[8 * blk: 8 * blk + 8])
+        stream = int(d[0][0, blk]) | (int(d[1][0, blk]) << 32) | (int(d[2][0, blk]) << 64)
+        assert [(stream >> (6 * i)) & 63 for i in range(16)] == fields
 
 
 # --------------------------------------------------------------------------
