@@ -71,13 +71,16 @@
  * Code blocks: 4 bits per code.  The codes c[k0 .. k0+15] of 16 consecutive
  * channels of a row (k0 a multiple of 16) form one 8-byte block (bytes
  * k0/2 .. k0/2+7), read as two little-endian 32-bit words W0, W1.  Code j of
- * the block is the 6-bit field F_j = s << 5 | |c| (s = 1 exactly for a
- * negative code), field j at bits 6j .. 6j+5 of the 96-bit stream
+ * the block is the 6-bit field F_j = s << 5 | |c|, field j at bits 6j .. 6j+5
+ * of the 96-bit stream
  * D0 | D1 << 32 | D2 << 64, whose bits 3-4 of every field are zero.  Those
  * bit positions of D0 and D1 (0x18618618 and 0x86186186) together are
  * exactly the data bits of D2, which is stored there:
- * W0 = D0 | (D2 & 0x18618618), W1 = D1 | (D2 & 0x86186186).  Codes lie in
- * [-7, 7]: with the scale absmax / 7 the clamp of Eq. 2 never reaches -8.
+ * W0 = D0 | (D2 & 0x18618618), W1 = D1 | (D2 & 0x86186186).  s = 1 exactly
+ * when the scaled value x = v * fl32(1/scale) the code was rounded from is
+ * negative (-0.0 included; with scale 0, x = v * 0): a zero code may carry
+ * s = 1 and reads as 0.  Codes lie in [-7, 7]: with the scale absmax / 7 the
+ * clamp of Eq. 2 never reaches -8.
  * (D0 = W0 & ~0x18618618, D1 = W1 & ~0x86186186 and
  * D2 = (W0 & 0x18618618) | (W1 & 0x86186186) give back the stream, whose
  * fields are the FP6 e2m3 values code / 8: that is how the GEMM consumes them.)
@@ -100,7 +103,7 @@
 extern "C" {
 #endif
 
-#define QWAM_ABI_VERSION 8
+#define QWAM_ABI_VERSION 9
 #define QWAM_GROUP 64
 
 typedef enum {

@@ -265,6 +265,15 @@ def quantize_groups(v: np.ndarray, group: int = GROUP, dtype=np.float32):
       code  = clamp(rint(fl(v * inv)), -8, 7)      (rint: ties to even)
     Returns codes int8 [rows][K] and scales `dtype` [rows][K/group].
     """
+    codes, scale, _ = quantize_groups_signed(v, group, dtype)
+    return codes, scale
+
+
+def quantize_groups_signed(v: np.ndarray, group: int = GROUP, dtype=np.float32):
+    """quantize_groups, plus the sign of every scaled value x = fl(v * inv)
+    (bool [rows][K], True for a negative x, -0.0 included; with scale 0, inv
+    is 0 and x is v * 0): the sign bit the packed layout stores, which a zero
+    code keeps."""
     v = np.asarray(v, dtype=dtype)
     rows, K = v.shape
     assert K % group == 0
@@ -279,7 +288,7 @@ def quantize_groups(v: np.ndarray, group: int = GROUP, dtype=np.float32):
     prod = (vg * inv[:, :, None]).astype(dtype)
     codes = np.clip(np.rint(prod), CODE_MIN, CODE_MAX).astype(np.int8)
     codes[small] = 0
-    return codes.reshape(rows, K), scale
+    return codes.reshape(rows, K), scale, np.signbit(prod).reshape(rows, K)
 
 
 def dequantize_groups(codes: np.ndarray, scales: np.ndarray, group: int = GROUP) -> np.ndarray:
@@ -322,18 +331,20 @@ def _fp6_fields(d: list) -> np.ndarray:
     return out
 
 
-def pack_codes(codes: np.ndarray) -> np.ndarray:
+def pack_codes(codes: np.ndarray, neg: np.ndarray = None) -> np.ndarray:
     """Packed code blocks: 4 bits per code.
 
     The codes c[16i .. 16i+15] of 16 consecutive channels of a row form block
     i, bytes 8i .. 8i+7, read as two little-endian 32-bit words W0, W1.  Code j
-    of the block is the 6-bit field F_j = sign << 5 | |c| (sign 1 exactly for
-    a negative code), field j at bits 6j .. 6j+5 of the 96-bit stream
-    D0 | D1 << 32 | D2 << 64; bits 3-4 of every field are zero.  Those bit
-    positions of D0 and D1 (FP6_Z0, FP6_Z1) together are exactly the data
-    bits of D2, which is stored there: W0 = D0 | (D2 & FP6_Z0),
-    W1 = D1 | (D2 & FP6_Z1).  Codes must lie in [-7, 7]: with the scale
-    absmax / 7 of Eq. 2 the code -8 is never produced.
+    of the block is the 6-bit field F_j = s << 5 | |c|, field j at bits
+    6j .. 6j+5 of the 96-bit stream D0 | D1 << 32 | D2 << 64; bits 3-4 of every
+    field are zero.  Those bit positions of D0 and D1 (FP6_Z0, FP6_Z1)
+    together are exactly the data bits of D2, which is stored there:
+    W0 = D0 | (D2 & FP6_Z0), W1 = D1 | (D2 & FP6_Z1).  The sign s is `neg`:
+    the sign of the scaled value the code was rounded from
+    (quantize_groups_signed), so a zero code may carry s = 1; without `neg`,
+    s = 1 exactly for a negative code.  Codes must lie in [-7, 7]: with the
+    scale absmax / 7 of Eq. 2 the code -8 is never produced.
     """
     c = np.asarray(codes, dtype=np.int16)
     rows, K = c.shape
@@ -341,7 +352,12 @@ def pack_codes(codes: np.ndarray) -> np.ndarray:
         raise ValueError("the channel count must be a multiple of 16")
     if c.size and (c.min() < -7 or c.max() > 7):
         raise ValueError("packed codes must lie in [-7, 7]")
-    fields = (np.abs(c) | ((c < 0).astype(np.int16) << 5)).reshape(rows, K // 16, 16)
+    if neg is None:
+        neg = c < 0
+    neg = np.asarray(neg, dtype=bool)
+    if neg.shape != c.shape or (neg & (c > 0)).any() or (~neg & (c < 0)).any():
+        raise ValueError("a sign bit contradicts its nonzero code")
+    fields = (np.abs(c) | (neg.astype(np.int16) << 5)).reshape(rows, K // 16, 16)
     d0, d1, d2 = _fp6_stream(fields)
     w = np.empty((rows, K // 16, 2), dtype=np.uint32)
     w[..., 0] = (d0 | (d2 & np.uint64(FP6_Z0))).astype(np.uint32)
@@ -388,8 +404,8 @@ def pack_weights(R: np.ndarray, lam: np.ndarray, group: int = GROUP):
     R: float32 [N][K] residual weight.  Returns (packed codes uint8 [N][K/2],
     scales float32 [N][G], inverse smoothing float32 [K], codes int8 [N][K]).
     """
-    codes, scales = quantize_groups(np.asarray(R, dtype=np.float32), group)
-    return pack_codes(codes), scales, inverse_smoothing(lam), codes
+    codes, scales, neg = quantize_groups_signed(np.asarray(R, dtype=np.float32), group)
+    return pack_codes(codes, neg), scales, inverse_smoothing(lam), codes
 
 
 def smooth_activations(x_bits: np.ndarray, inv_lam: np.ndarray) -> np.ndarray:
@@ -456,9 +472,9 @@ def quantize_activations(x_bits: np.ndarray, inv_lam: np.ndarray, L1_bits: np.nd
     down-projection.  Returns (packed uint8 [M][K/2], scales f32 [M][G],
     t bf16 bits [M][r], codes int8 [M][K], x~ float32 [M][K])."""
     xt = transformed_activations(x_bits, inv_lam, hadamard)
-    codes, scales = quantize_groups(xt, group)
+    codes, scales, neg = quantize_groups_signed(xt, group)
     t = down_projection(xt, L1_bits)
-    return pack_codes(codes), scales, t, codes, xt
+    return pack_codes(codes, neg), scales, t, codes, xt
 
 
 def deflate_activations(xt: np.ndarray, t_bits: np.ndarray, L1_bits: np.ndarray) -> np.ndarray:
@@ -493,8 +509,8 @@ def quantize_activations_deflated(x_bits: np.ndarray, inv_lam: np.ndarray, L1_bi
     xt = transformed_activations(x_bits, inv_lam, hadamard)
     t = down_projection(xt, L1_bits)
     xp = deflate_activations(xt, t, L1_bits)
-    codes, scales = quantize_groups(xp, group)
-    return pack_codes(codes), scales, t, codes, xp
+    codes, scales, neg = quantize_groups_signed(xp, group)
+    return pack_codes(codes, neg), scales, t, codes, xp
 
 
 def group_partials(qx: np.ndarray, qw: np.ndarray, group: int = GROUP) -> np.ndarray:

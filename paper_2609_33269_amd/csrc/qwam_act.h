@@ -64,11 +64,13 @@ __device__ __forceinline__ void quantize_pack_store(const float (&v)[16], buf_rs
   if (!g32) amax = __builtin_fmaxf(amax, __shfl_xor(amax, 32));
   const float s = q4_scale(amax);
   const float inv = q4_inv(s);
-  // codes q = clamp(rint(v * inv), -8, 7): the lane's 16 channels are one code block
-  float q[16];
+  // codes rint(v * inv) of the lane's 16 channels: one code block
+  float x[16];
 #pragma unroll
-  for (int j = 0; j < 16; ++j) q[j] = q4_code(v[j], inv);
-  buf_store8(codes_to_block(q), q_rsrc, q_off);
+  for (int j = 0; j < 16; ++j) x[j] = v[j] * inv;
+  uint32_t d0, d1, d2;
+  codes_fp6_16(x, d0, d1, d2);
+  buf_store8(fp6_code_block(d0, d1, d2), q_rsrc, q_off);
   if (xs_dst != nullptr) *xs_dst = s;
 }
 

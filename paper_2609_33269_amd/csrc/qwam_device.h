@@ -30,11 +30,6 @@ __device__ __forceinline__ float q4_inv(float scale) {
   return (scale == 0.0f) ? 0.0f : 1.0f / scale;
 }
 
-// The code of v (Eq. 2): clamp(rint(v * inv), -8, 7), as a float.
-__device__ __forceinline__ float q4_code(float v, float inv) {
-  return __builtin_fminf(__builtin_fmaxf(__builtin_rintf(v * inv), -8.0f), 7.0f);
-}
-
 // bf16 bits -> float (exact).
 __device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
   return __uint_as_float(bits16 << 16);
@@ -69,41 +64,53 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 
 // Code blocks, the storage format of every 4-bit code (qwam.h).  The codes
 // c[k0 .. k0+15] of 16 consecutive channels (k0 a multiple of 16) are written
-// as 6-bit fields F_i = sign << 5 | |c[k0+i]| (the FP6 e2m3 pattern of
-// c / 8), field i at bits 6i .. 6i+5 of a 96-bit stream D0 | D1 << 32 |
-// D2 << 64.  Bits 3-4 of every field are zero; in D0 and D1 those positions
-// (kFp6Z0, kFp6Z1) together are exactly the data bits of D2, which is stored
-// there: word 0 = D0 | (D2 & kFp6Z0), word 1 = D1 | (D2 & kFp6Z1).  A reader
-// gets the MFMA operand back with four ANDs (qwam_mfma.h).  The quantizer
-// never yields -8 (|v * inv| <= 7 (1 + 3u) < 7.5); a zero code has sign 0.
+// as 6-bit fields F_i = s << 5 | |c[k0+i]| (the FP6 e2m3 pattern of c / 8; s
+// is the sign of the scaled value x = v * inv, so a zero code may carry
+// either sign), field i at bits 6i .. 6i+5 of a 96-bit stream
+// D0 | D1 << 32 | D2 << 64.  Bits 3-4 of every field are zero; in D0 and D1
+// those positions (kFp6Z0, kFp6Z1) together are exactly the data bits of D2,
+// which is stored there: word 0 = D0 | (D2 & kFp6Z0), word 1 = D1 | (D2 &
+// kFp6Z1).  A reader gets the MFMA operand back with four ANDs (qwam_mfma.h).
+// The quantizer never yields -8 (|x| <= 7 (1 + 3u) < 7.5).
 constexpr uint32_t kFp6Z0 = 0x18618618u;   // bits 3-4 of the fields in D0
 constexpr uint32_t kFp6Z1 = 0x86186186u;   // bits 3-4 of the fields in D1
 
-// 6-bit field of an integral code q in [-7, 7] (float)
-__device__ __forceinline__ uint32_t fp6_field(float q) {
-  return static_cast<uint32_t>(__builtin_fabsf(q)) | (q < 0.0f ? 32u : 0u);
+typedef unsigned v6u __attribute__((ext_vector_type(6)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+
+// The codes of 32 scaled values x[0..31] (Eq. 2: rint, ties to even, of x;
+// |x| < 7.5) as the FP6 e2m3 stream, field i = x[i], in one instruction:
+// v_cvt_scalef32_2xpk16_fp6_f32 writes a[i] to field 2i and b[i] to field
+// 2i + 1 of x / scale, rounded to nearest even, with the sign of x.  On
+// gfx950 this equals (signbit(x) << 5) | |rint(x)| for every float (checked
+// against rint, halfway cases, signed zeros and denormals included).
+__device__ __forceinline__ v6u codes_fp6_32(const float (&x)[32]) {
+  v16f a, b;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    a[i] = x[2 * i];
+    b[i] = x[2 * i + 1];
+  }
+  return __builtin_amdgcn_cvt_scalef32_2xpk16_fp6_f32(a, b, 8.0f);
 }
 
-// fields F_0 .. F_15 -> the stream words D0, D1, D2
-__device__ __forceinline__ void fp6_stream(const uint32_t (&f)[16], uint32_t& d0, uint32_t& d1, uint32_t& d2) {
-  d0 = f[0] | (f[1] << 6) | (f[2] << 12) | (f[3] << 18) | (f[4] << 24) | (f[5] << 30);
-  d1 = (f[5] >> 2) | (f[6] << 4) | (f[7] << 10) | (f[8] << 16) | (f[9] << 22) | (f[10] << 28);
-  d2 = (f[10] >> 4) | (f[11] << 2) | (f[12] << 8) | (f[13] << 14) | (f[14] << 20) | (f[15] << 26);
+// The same for 16 values (stream words D0, D1, D2).
+__device__ __forceinline__ void codes_fp6_16(const float (&x)[16], uint32_t& d0, uint32_t& d1, uint32_t& d2) {
+  v16f a = {}, b = {};
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    a[i] = x[2 * i];
+    b[i] = x[2 * i + 1];
+  }
+  const v6u r = __builtin_amdgcn_cvt_scalef32_2xpk16_fp6_f32(a, b, 8.0f);
+  d0 = r[0];
+  d1 = r[1];
+  d2 = r[2];
 }
 
 // stream words -> the two stored words of a code block
 __device__ __forceinline__ uint2 fp6_code_block(uint32_t d0, uint32_t d1, uint32_t d2) {
   return make_uint2(d0 | (d2 & kFp6Z0), d1 | (d2 & kFp6Z1));
-}
-
-// the code block of 16 integral codes q[0..15] (floats in [-7, 7])
-__device__ __forceinline__ uint2 codes_to_block(const float (&q)[16]) {
-  uint32_t f[16];
-#pragma unroll
-  for (int i = 0; i < 16; ++i) f[i] = fp6_field(q[i]);
-  uint32_t d0, d1, d2;
-  fp6_stream(f, d0, d1, d2);
-  return fp6_code_block(d0, d1, d2);
 }
 
 }  // namespace qwam

@@ -124,21 +124,21 @@ __global__ __launch_bounds__(64 * LW) void asp_layer_small_kernel(
     amax = __builtin_fmaxf(amax, __shfl_xor(amax, 32));
     const float s = q4_scale(amax);
     const float inv = q4_inv(s);
-    // codes -> FP6 fields: the MFMA operand itself, and the two code blocks
-    // (the storage format) for the optional copy of the codes
+    // codes -> FP6 fields (one conversion for the lane's 32 channels): the
+    // MFMA operand itself, and the two code blocks (the storage format) for
+    // the optional copy of the codes
+    float xs32[32];
+#pragma unroll
+    for (int i = 0; i < 32; ++i) xs32[i] = v[i] * inv;
+    const v6u d = codes_fp6_32(xs32);
     v8i af;          // words 6-7 are not read with FP6 operands and stay unset
     uint32_t cw[4];
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      uint32_t fl[16];
-#pragma unroll
-      for (int i = 0; i < 16; ++i) fl[i] = fp6_field(q4_code(v[16 * h + i], inv));
-      uint32_t d0, d1, d2;
-      fp6_stream(fl, d0, d1, d2);
-      af[3 * h] = static_cast<int>(d0);
-      af[3 * h + 1] = static_cast<int>(d1);
-      af[3 * h + 2] = static_cast<int>(d2);
-      const uint2 blk = fp6_code_block(d0, d1, d2);
+      af[3 * h] = static_cast<int>(d[3 * h]);
+      af[3 * h + 1] = static_cast<int>(d[3 * h + 1]);
+      af[3 * h + 2] = static_cast<int>(d[3 * h + 2]);
+      const uint2 blk = fp6_code_block(d[3 * h], d[3 * h + 1], d[3 * h + 2]);
       cw[2 * h] = blk.x;
       cw[2 * h + 1] = blk.y;
     }

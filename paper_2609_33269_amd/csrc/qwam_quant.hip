@@ -44,11 +44,14 @@ __global__ __launch_bounds__(256) void pack_weights_kernel(const float* __restri
   if (!g32) amax = __builtin_fmaxf(amax, __shfl_xor(amax, 2));
   const float s = q4_scale(amax);
   const float inv = q4_inv(s);
-  float q[16];
+  float x[16];
 #pragma unroll
-  for (int i = 0; i < 16; ++i) q[i] = q4_code(v[i], inv);
+  for (int i = 0; i < 16; ++i) x[i] = v[i] * inv;
+  uint32_t d0, d1, d2;
+  codes_fp6_16(x, d0, d1, d2);
   if (active) {
-    *reinterpret_cast<uint2*>(wq + static_cast<int64_t>(n) * (K / 2) + g * (kGroup / 2) + sub * 8) = codes_to_block(q);
+    *reinterpret_cast<uint2*>(wq + static_cast<int64_t>(n) * (K / 2) + g * (kGroup / 2) + sub * 8) =
+        fp6_code_block(d0, d1, d2);
     if (g32 ? (sub & 1) == 0 : sub == 0) ws[static_cast<int64_t>(g32 ? 2 * g + (sub >> 1) : g) * N + n] = s;
   }
 }

@@ -38,7 +38,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == set(Q.SIGNATURES), "binding and header disagree"
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.qwam_abi_version() == 8
+    assert lib.qwam_abi_version() == 9
     assert lib.qwam_status_string(3) == b"QWAM_ERR_MISALIGNED"
 
 

@@ -218,6 +218,30 @@ def test_pack_known_blocks():
     assert O.pack_codes(codes).tolist() == [[0, 0, 0, 0x18, 0, 0, 0, 0x84]]
 
 
+def test_pack_sign_of_scaled_value():
+    """The sign bit is the sign of the scaled value: a zero code rounded from a
+    negative value keeps it (hand-derived: field 0b100000 at bits 0-5), reads
+    back as 0, and a sign contradicting a nonzero code is rejected."""
+    codes = np.zeros((1, 16), np.int8)
+    neg = np.zeros((1, 16), bool)
+    neg[0, 0] = True
+    assert O.pack_codes(codes, neg).tolist() == [[0x20, 0, 0, 0, 0, 0, 0, 0]]
+    assert (O.unpack_codes(O.pack_codes(codes, neg)) == 0).all()
+    codes[0, 1] = -3
+    with pytest.raises(ValueError):
+        O.pack_codes(codes, np.zeros((1, 16), bool))
+    # quantize_groups_signed: x = fl(v * inv); -0.3 * inv rounds to code 0, sign 1;
+    # an all-tiny group has scale 0 and x = v * 0 keeps v's sign
+    v = np.zeros((2, 64), np.float32)
+    v[0, 0], v[0, 1], v[0, 2] = 7.0, -0.3, 0.3
+    v[1, 0], v[1, 1] = np.float32(-1e-40), np.float32(1e-40)
+    codes, scales, neg = O.quantize_groups_signed(v)
+    assert scales[0, 0] == 1.0 and scales[1, 0] == 0.0
+    assert codes[0, :3].tolist() == [7, 0, 0] and neg[0, :3].tolist() == [False, True, False]
+    assert codes[1, :2].tolist() == [0, 0] and neg[1, :2].tolist() == [True, False]
+    assert not neg[0, 3] and not neg[1, 2]        # +0 * inv
+
+
 def test_pack_rejects_minus_eight():
     with pytest.raises(ValueError):
         O.pack_codes(np.array([[-8] + [0] * 15], dtype=np.int8))
