@@ -3,16 +3,19 @@
 // v_mfma_scale_f32_32x32x64_f8f6f4, float32 scaling per group, the bf16 branch
 // and the bias in the epilogue), organised for latency instead of reuse:
 //
-//   * one 4-wave workgroup per 32 x 32 block of y (rows = tokens, columns =
-//     output channels), the K groups split into four contiguous ranges, one per
-//     wave: with so few tokens the layer is a stream over the packed weights,
-//     and the split spreads that stream and the per-group work over four
-//     waves.  The four partial blocks are summed in LDS in wave order
-//     (deterministic) and wave 0 finishes the block;
+//   * one 8-wave workgroup per 32 x 32 block of y (rows = tokens, columns =
+//     output channels), the K groups split into eight contiguous ranges, one
+//     per wave: with so few tokens the layer is a stream over the packed
+//     weights, and the split spreads that stream and the per-group work over
+//     eight waves.  The eight partial blocks are summed in LDS in wave order
+//     (deterministic); wave w finishes result registers 2w and 2w+1 (the
+//     branch t . L2 on the bf16 matrix cores, the bias, the store).  The
+//     fused few-token layer uses the same split and the same order, so both
+//     paths give the same y from the same codes, scales and t;
 //   * every operand goes straight from HBM/L2 into the MFMA register layout
 //     (lane l: row / column l % 32, half l / 32 of a group, 16 bytes = 32
-//     codes), eight groups per chunk, two chunks in flight: a K of 4096 is one
-//     memory round trip;
+//     codes), four groups per chunk, two chunks in flight: with eight waves a
+//     K of 4096 is one memory round trip;
 //   * the activation scales are broadcast across each row of 16 lanes by DPP
 //     inside the scale multiply, as in the large-tile kernel;
 //   * group 32 (GS = 32): as in the large-tile kernel, lane half h holds group
@@ -29,8 +32,8 @@ namespace qwam {
 namespace {
 
 constexpr int SB = 32;             // block edge (rows and columns)
-constexpr int CH = 8;              // groups per chunk
-constexpr int KW = 4;              // waves per block, each a contiguous range of groups
+constexpr int CH = 4;              // groups per chunk
+constexpr int KW = 8;              // waves per block, each a contiguous range of groups
 
 template <int NS>
 struct Chunk {
@@ -46,7 +49,7 @@ __global__ __launch_bounds__(64 * KW) void asp_gemm_small_kernel(
     const uint8_t* __restrict__ wq, const float* __restrict__ ws, const uint16_t* __restrict__ L2t,
     const uint16_t* __restrict__ bias, uint16_t* __restrict__ y, int32_t* __restrict__ P, int M,
     int N, int K) {
-  __shared__ float red[KW - 1][16][64];   // partial blocks of waves 1.. KW-1
+  __shared__ float red[KW][16][64];       // partial blocks of the waves
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -169,30 +172,38 @@ __global__ __launch_bounds__(64 * KW) void asp_gemm_small_kernel(
   }
   if (PARTIALS) return;
 
-  // partial blocks of waves 1.. -> LDS; wave 0 adds them in wave order
-  if (wave > 0) {
+  // partial blocks -> LDS, summed in wave order: wave w finishes result
+  // registers v0 = 2w and v0 + 1 (token 8(v/4) + 4(l/32) + v%4, column l%32)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) red[wave - 1][v][lane] = acc[v];
-  }
+  for (int v = 0; v < 16; ++v) red[wave][v][lane] = acc[v];
   __syncthreads();
-  if (wave > 0) return;
+  const int v0 = 2 * wave;
+  float c2[2] = {0.0f, 0.0f};
 #pragma unroll
-  for (int w = 0; w < KW - 1; ++w)
+  for (int w = 0; w < KW; ++w)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) acc[v] += red[w][v][lane];
+    for (int e = 0; e < 2; ++e) c2[e] += red[w][v0 + e][lane];
 
-  // ---- epilogue: acc + t . L2 (bf16 MFMA, float32 accumulate) + bias ----
-  v16f c = acc;
-  if constexpr (!PARTIALS) {
+  // ---- epilogue: acc + t . L2 (bf16 MFMA, float32 accumulate) + bias; the
+  // other result registers start at zero and are not used ----
+  v16f c;
 #pragma unroll
-    for (int s = 0; s < KSTEPS; ++s)
-      c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, tv[s]), __builtin_bit_cast(v8bf, lv[s]),
-                                                  c, 0, 0, 0);
-  }
+  for (int v = 0; v < 16; ++v) c[v] = v == v0 ? c2[0] : (v == v0 + 1 ? c2[1] : 0.0f);
+#pragma unroll
+  for (int s = 0; s < KSTEPS; ++s)
+    c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, tv[s]), __builtin_bit_cast(v8bf, lv[s]), c,
+                                                0, 0, 0);
+  float yv[2] = {0.0f, 0.0f};
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
+    if (v == v0) yv[0] = c[v];
+    if (v == v0 + 1) yv[1] = c[v];
+  }
+#pragma unroll
+  for (int e = 0; e < 2; ++e) {
+    const int v = v0 + e;
     const int m = m0 + 8 * (v >> 2) + rsub + (v & 3);
-    if (m < M && nt < N) y[static_cast<int64_t>(m) * N + nt] = static_cast<uint16_t>(f32_to_bf16_rne(c[v] + bv));
+    if (m < M && nt < N) y[static_cast<int64_t>(m) * N + nt] = static_cast<uint16_t>(f32_to_bf16_rne(yv[e] + bv));
   }
 }
 

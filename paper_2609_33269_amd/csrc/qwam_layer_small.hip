@@ -19,9 +19,12 @@
 //     v_mfma_f32_32x32x16_bf16 (rank columns, four 16-deep steps per span);
 //   * per span: acc += P * xs * ws as in the GEMMs (the token scale of each
 //     result row reaches its lanes through one cross-lane read);
-//   * the waves' partial blocks (acc and t) are summed in LDS in wave order,
-//     t is rounded to bf16, and wave 0 adds t . L2 (bf16 MFMA) and the bias
-//     and stores y.
+//   * the waves' partial blocks (acc and t) are summed in LDS in wave order;
+//     wave w finishes result registers 2w and 2w+1 (four rows of the block):
+//     it rounds those rows of t to bf16, adds their t . L2 (bf16 MFMA; the
+//     rows it does not own are ignored, since each result row depends only on
+//     its own row of t) and the bias, and stores them.  The epilogue is spread
+//     over all waves, so no wave sums every partial alone.
 //   * optionally (xq / xs / t not null) the workgroups of the first column
 //     block also store the codes, scales and t, as qwam_quantize_act would.
 #include "qwam_device.h"
@@ -32,7 +35,7 @@ namespace qwam {
 
 namespace {
 
-constexpr int LW = 4;              // waves per workgroup (one per SIMD: the registers of a 32-channel lane slice fit)
+constexpr int LW = 8;              // waves per workgroup (two per SIMD)
 constexpr int LB = 32;             // block edge (tokens and output channels)
 
 }  // namespace
@@ -44,11 +47,12 @@ __global__ __launch_bounds__(64 * LW) void asp_layer_small_kernel(
     const uint16_t* __restrict__ bias, uint16_t* __restrict__ y, uint8_t* __restrict__ xq_out,
     float* __restrict__ xs_out, uint16_t* __restrict__ t_out, int M, int N, int K) {
   static_assert(RANK == 16 || RANK == 32, "one 32-column block of t");
-  // dynamic LDS: partial acc [LW][16][64] | partial t [LW][16][64] | t bf16 [32][RANK]
+  // dynamic LDS: partial acc [LW][16][64] | partial t [LW][16][64] | t bf16 [32][RANK] | 1/lambda [K]
   extern __shared__ float lds[];
   float* red_acc = lds;
   float* red_t = red_acc + LW * 16 * 64;
   uint16_t* t_l = reinterpret_cast<uint16_t*>(red_t + LW * 16 * 64);
+  float* inv_l = red_t + LW * 16 * 64 + LB * RANK / 2;
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -79,7 +83,6 @@ __global__ __launch_bounds__(64 * LW) void asp_layer_small_kernel(
 
   struct Fetch {
     uint4 x[4];                    // 32 bf16 of x: channels 32*half .. +31 of the span
-    float4 inv[8];                 // the matching 1/lambda (the same for the 32 lanes of a half)
     uint4 w;                       // 32 packed weight codes of column n0 + lane%32
     float sw;
     v8s l1[4];                     // L1t[j][span + 32*half + 8 s .. +7], s = 0..3
@@ -88,9 +91,6 @@ __global__ __launch_bounds__(64 * LW) void asp_layer_small_kernel(
     const uint32_t go = static_cast<uint32_t>(g) * kGroup * 2u;
 #pragma unroll
     for (int q = 0; q < 4; ++q) f.x[q] = buf_load16(x_rsrc, x_off + go + 16u * q);
-    const float4* ip = reinterpret_cast<const float4*>(inv_smooth + g * kGroup + fhalf * 32);
-#pragma unroll
-    for (int q = 0; q < 8; ++q) f.inv[q] = ip[q];
     f.w = buf_load16(w_rsrc, w_off + static_cast<uint32_t>(g) * 32u);
     f.sw = buf_load4f(ws_rsrc, sw_off + static_cast<uint32_t>(g) * N * 4u);
 #pragma unroll
@@ -103,13 +103,15 @@ __global__ __launch_bounds__(64 * LW) void asp_layer_small_kernel(
   v16f acc = v16f{};
   v16f tacc = v16f{};
   auto work = [&](int g, const Fetch& f) __attribute__((always_inline)) {
-    // x~ = x * (1/lambda) for the lane's 32 channels
+    // x~ = x * (1/lambda) for the lane's 32 channels (1/lambda from LDS, one
+    // address per lane half)
+    const float4* ip = reinterpret_cast<const float4*>(inv_l + g * kGroup + fhalf * 32);
     float v[32];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const uint32_t xw[4] = {f.x[q].x, f.x[q].y, f.x[q].z, f.x[q].w};
-      const float4 i0 = f.inv[2 * q];
-      const float4 i1 = f.inv[2 * q + 1];
+      const float4 i0 = ip[2 * q];
+      const float4 i1 = ip[2 * q + 1];
       const float iv[8] = {i0.x, i0.y, i0.z, i0.w, i1.x, i1.y, i1.z, i1.w};
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
@@ -161,18 +163,27 @@ __global__ __launch_bounds__(64 * LW) void asp_layer_small_kernel(
     }
   };
 
-  // epilogue operands (wave 0): L2t rows of the block's columns, bias
+  // epilogue operands: L2t rows of the block's columns, bias
   constexpr int KSTEPS = RANK / 16;
   const int nt = n0 + frow;
   v8s lv[KSTEPS];
   float bv = 0.0f;
-  if (wave == 0) {
 #pragma unroll
-    for (int k = 0; k < KSTEPS; ++k) {
-      lv[k] = v8s{0, 0, 0, 0, 0, 0, 0, 0};
-      if (nt < N) lv[k] = *reinterpret_cast<const v8s*>(L2t + static_cast<int64_t>(nt) * RANK + k * 16 + fhalf * 8);
-    }
-    if (bias != nullptr && nt < N) bv = bf16_to_f32(bias[nt]);
+  for (int k = 0; k < KSTEPS; ++k) {
+    lv[k] = v8s{0, 0, 0, 0, 0, 0, 0, 0};
+    if (nt < N) lv[k] = *reinterpret_cast<const v8s*>(L2t + static_cast<int64_t>(nt) * RANK + k * 16 + fhalf * 8);
+  }
+  if (bias != nullptr && nt < N) bv = bf16_to_f32(bias[nt]);
+
+  // the wave's slice of 1/lambda goes to LDS (direct copies, 256 floats per
+  // instruction; lanes past the slice copy nothing), then the first spans are
+  // requested; all of it is waited for before the first span is used
+  if (g_lo < g_hi) {
+    const buf_rsrc i_rsrc = make_rsrc(inv_smooth, static_cast<uint32_t>(K) * 4u);
+    const int nfl = (g_hi - g_lo) * kGroup;
+    for (int c = 0; c < nfl; c += 256)
+      if (c + 4 * lane < nfl)
+        buf_load16_lds(i_rsrc, static_cast<uint32_t>(g_lo * kGroup + c + 4 * lane) * 4u, inv_l + g_lo * kGroup + c);
   }
 
   // the wave's spans, one fetched ahead
@@ -180,53 +191,69 @@ __global__ __launch_bounds__(64 * LW) void asp_layer_small_kernel(
     Fetch fa, fb;
     fetch(g_lo, fa);
     int g = g_lo;
+    if (g + 1 < g_hi) fetch(g + 1, fb);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the 1/lambda copies have landed
     for (; g + 1 < g_hi; g += 2) {
-      fetch(g + 1, fb);
       work(g, fa);
-      fetch(min(g + 2, g_hi - 1), fa);
+      if (g + 2 < g_hi) fetch(g + 2, fa);
       work(g + 1, fb);
+      if (g + 3 < g_hi) fetch(g + 3, fb);
     }
     if (g < g_hi) work(g, fa);
   }
 
-  // partial blocks -> LDS; wave 0 sums them in wave order
+  // partial blocks -> LDS, summed in wave order below
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
     red_acc[(wave * 16 + v) * 64 + lane] = acc[v];
     red_t[(wave * 16 + v) * 64 + lane] = tacc[v];
   }
   __syncthreads();
-  if (wave != 0) return;
-  v16f c = v16f{}, tsum = v16f{};
+  // this wave's result registers v0, v0 + 1: token 8(v/4) + 4(l/32) + v%4, column l%32
+  const int v0 = 2 * wave;
+  float c2[2] = {0.0f, 0.0f}, t2[2] = {0.0f, 0.0f};
 #pragma unroll
   for (int w = 0; w < LW; ++w)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      c[v] += red_acc[(w * 16 + v) * 64 + lane];
-      tsum[v] += red_t[(w * 16 + v) * 64 + lane];
+    for (int e = 0; e < 2; ++e) {
+      c2[e] += red_acc[(w * 16 + v0 + e) * 64 + lane];
+      t2[e] += red_t[(w * 16 + v0 + e) * 64 + lane];
     }
-  // t = bf16(sum): result register v of lane l is token 8(v/4) + 4(l/32) + v%4, column l%32
+  // t = bf16(sum) of those rows, to LDS (and out)
 #pragma unroll
-  for (int v = 0; v < 16; ++v) {
+  for (int e = 0; e < 2; ++e) {
+    const int v = v0 + e;
     const int row = 8 * (v >> 2) + rsub + (v & 3);
     if (frow < RANK) {
-      const uint16_t b = static_cast<uint16_t>(f32_to_bf16_rne(tsum[v]));
+      const uint16_t b = static_cast<uint16_t>(f32_to_bf16_rne(t2[e]));
       t_l[row * RANK + frow] = b;
       if (write_act && m0 + row < M) t_out[static_cast<int64_t>(m0 + row) * RANK + frow] = b;
     }
   }
   __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): this wave's t stores are in LDS
-  // y = acc + t . L2 + bias; A operand: token l%32, rank slots 16 k + 8(l/32) .. +7
+  // y = acc + t . L2 + bias; A operand: token l%32, rank slots 16 k + 8(l/32) .. +7.  Only
+  // the rows of this wave's registers are used; the other rows of t_l may still be written
+  // by other waves, and they reach only result rows this wave discards.
+  v16f c;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) c[v] = v == v0 ? c2[0] : (v == v0 + 1 ? c2[1] : 0.0f);
 #pragma unroll
   for (int k = 0; k < KSTEPS; ++k) {
     const v8s tv = *reinterpret_cast<const v8s*>(t_l + frow * RANK + k * 16 + fhalf * 8);
     c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, tv), __builtin_bit_cast(v8bf, lv[k]), c, 0,
                                                 0, 0);
   }
+  float yv[2] = {0.0f, 0.0f};
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
+    if (v == v0) yv[0] = c[v];
+    if (v == v0 + 1) yv[1] = c[v];
+  }
+#pragma unroll
+  for (int e = 0; e < 2; ++e) {
+    const int v = v0 + e;
     const int m = m0 + 8 * (v >> 2) + rsub + (v & 3);
-    if (m < M && nt < N) y[static_cast<int64_t>(m) * N + nt] = static_cast<uint16_t>(f32_to_bf16_rne(c[v] + bv));
+    if (m < M && nt < N) y[static_cast<int64_t>(m) * N + nt] = static_cast<uint16_t>(f32_to_bf16_rne(yv[e] + bv));
   }
 }
 
@@ -235,7 +262,7 @@ hipError_t launch_asp_layer_small(int M, int N, int K, int r, const uint16_t* x,
                                   const uint16_t* bias, uint16_t* y, uint8_t* xq, float* xs, uint16_t* t,
                                   hipStream_t stream) {
   const dim3 grid(((M + LB - 1) / LB) * ((N + LB - 1) / LB)), block(64 * LW);
-  const size_t lds = static_cast<size_t>(2) * LW * 16 * 64 * 4 + LB * r * 2;
+  const size_t lds = static_cast<size_t>(2) * LW * 16 * 64 * 4 + LB * r * 2 + static_cast<size_t>(K) * 4;
   auto go = [&](auto kernel) {
     if (lds > 64 * 1024) {
       const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
