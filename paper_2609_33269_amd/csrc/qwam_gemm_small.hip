@@ -149,7 +149,7 @@ __global__ __launch_bounds__(64 * KW) void asp_gemm_small_kernel(
   const int kk = fhalf * 8;
   const int mt = m0 + frow, nt = n0 + frow;
   v8s tv[KSTEPS], lv[KSTEPS];
-  float bv = 0.0f;
+  uint32_t bbits = 0;              // bias bits, converted only in the epilogue (no early wait)
   if constexpr (!PARTIALS) {
 #pragma unroll
     for (int s = 0; s < KSTEPS; ++s) {
@@ -158,7 +158,8 @@ __global__ __launch_bounds__(64 * KW) void asp_gemm_small_kernel(
       if (mt < M) tv[s] = *reinterpret_cast<const v8s*>(t + static_cast<int64_t>(mt) * RANK + s * 16 + kk);
       if (nt < N) lv[s] = *reinterpret_cast<const v8s*>(L2t + static_cast<int64_t>(nt) * RANK + s * 16 + kk);
     }
-    if (bias != nullptr && nt < N) bv = bf16_to_f32(bias[nt]);
+    const buf_rsrc b_rsrc = make_rsrc(bias, bias != nullptr ? static_cast<uint32_t>(N) * 2u : 0u);
+    bbits = __builtin_amdgcn_raw_buffer_load_b16(b_rsrc, static_cast<uint32_t>(nt) * 2u, 0, 0);
   }
 
   // two chunks in flight: chunk c+1 is requested before chunk c is multiplied
@@ -193,6 +194,7 @@ __global__ __launch_bounds__(64 * KW) void asp_gemm_small_kernel(
   for (int s = 0; s < KSTEPS; ++s)
     c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, tv[s]), __builtin_bit_cast(v8bf, lv[s]), c,
                                                 0, 0, 0);
+  const float bv = bf16_to_f32(bbits);
   float yv[2] = {0.0f, 0.0f};
 #pragma unroll
   for (int v = 0; v < 16; ++v) {

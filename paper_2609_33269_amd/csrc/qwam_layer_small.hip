@@ -5,11 +5,13 @@
 // between), so every workgroup quantizes the tokens it needs itself.
 //
 //   * a workgroup owns a 32 x 32 block of y (32 tokens x 32 output channels)
-//     and all of K; its 4 waves split the 64-channel spans into contiguous
-//     ranges, one per wave;
+//     and all of K; its 8 waves split the 64-channel spans into contiguous
+//     ranges, one per wave (the split of the few-token GEMM, so that both
+//     paths sum the partial blocks in the same order);
 //   * lane l of a wave holds token l % 32 and channels 32*(l/32) .. +31 of the
 //     current span: the A-operand rows of v_mfma_scale_f32_32x32x64_f8f6f4.
-//     It smooths them (x * 1/lambda, fetched with x), takes the
+//     It smooths them (x * 1/lambda; each wave copies its slice of 1/lambda
+//     into LDS once, where both lane halves read it by broadcast), takes the
 //     span's absmax with its partner lane l ^ 32, quantizes (Eq. 2, the same
 //     arithmetic as the activation kernel, so the codes are identical) and
 //     writes them as FP6 fields in the order codes_to_fp6 gives the weights'
@@ -48,7 +50,7 @@ __global__ __launch_bounds__(64 * LW) void asp_layer_small_kernel(
     float* __restrict__ xs_out, uint16_t* __restrict__ t_out, int M, int N, int K) {
   static_assert(RANK == 16 || RANK == 32, "one 32-column block of t");
   // dynamic LDS: partial acc [LW][16][64] | partial t [LW][16][64] | t bf16 [32][RANK] | 1/lambda [K]
-  extern __shared__ float lds[];
+  extern __shared__ __attribute__((aligned(16))) float lds[];
   float* red_acc = lds;
   float* red_t = red_acc + LW * 16 * 64;
   uint16_t* t_l = reinterpret_cast<uint16_t*>(red_t + LW * 16 * 64);
@@ -78,8 +80,10 @@ __global__ __launch_bounds__(64 * LW) void asp_layer_small_kernel(
   const uint32_t x_off = static_cast<uint32_t>(frow * K + fhalf * 32) * 2u;
   const uint32_t w_off = static_cast<uint32_t>(frow * KB + fhalf * 16);
   const uint32_t sw_off = static_cast<uint32_t>(n0 + frow) * 4u;
-  // t columns j = lane % 32 (zero past RANK), channels 32*half + 8 s of a span
-  const bool l1_ok = frow < RANK;
+  // t columns j = lane % 32 (rows of L1t past RANK read as zero), channels
+  // 32*half + 8 s of a span
+  const buf_rsrc l1_rsrc = make_rsrc(L1t, static_cast<uint32_t>(RANK) * K * 2u);
+  const uint32_t l1_off = static_cast<uint32_t>(frow * K + fhalf * 32) * 2u;
 
   struct Fetch {
     uint4 x[4];                    // 32 bf16 of x: channels 32*half .. +31 of the span
@@ -94,10 +98,7 @@ __global__ __launch_bounds__(64 * LW) void asp_layer_small_kernel(
     f.w = buf_load16(w_rsrc, w_off + static_cast<uint32_t>(g) * 32u);
     f.sw = buf_load4f(ws_rsrc, sw_off + static_cast<uint32_t>(g) * N * 4u);
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      f.l1[s] = v8s{0, 0, 0, 0, 0, 0, 0, 0};
-      if (l1_ok) f.l1[s] = *reinterpret_cast<const v8s*>(L1t + static_cast<int64_t>(frow) * K + g * kGroup + fhalf * 32 + 8 * s);
-    }
+    for (int s = 0; s < 4; ++s) f.l1[s] = __builtin_bit_cast(v8s, buf_load16(l1_rsrc, l1_off + go + 16u * s));
   };
 
   v16f acc = v16f{};
@@ -167,13 +168,15 @@ __global__ __launch_bounds__(64 * LW) void asp_layer_small_kernel(
   constexpr int KSTEPS = RANK / 16;
   const int nt = n0 + frow;
   v8s lv[KSTEPS];
-  float bv = 0.0f;
 #pragma unroll
   for (int k = 0; k < KSTEPS; ++k) {
     lv[k] = v8s{0, 0, 0, 0, 0, 0, 0, 0};
     if (nt < N) lv[k] = *reinterpret_cast<const v8s*>(L2t + static_cast<int64_t>(nt) * RANK + k * 16 + fhalf * 8);
   }
-  if (bias != nullptr && nt < N) bv = bf16_to_f32(bias[nt]);
+  // the bias bits (zero without a bias or past N) are converted only at the end,
+  // so that no wait for this load lands before the spans
+  const buf_rsrc b_rsrc = make_rsrc(bias, bias != nullptr ? static_cast<uint32_t>(N) * 2u : 0u);
+  const uint32_t bbits = __builtin_amdgcn_raw_buffer_load_b16(b_rsrc, static_cast<uint32_t>(nt) * 2u, 0, 0);
 
   // the wave's slice of 1/lambda goes to LDS (direct copies, 256 floats per
   // instruction; lanes past the slice copy nothing), then the first spans are
@@ -243,6 +246,7 @@ __global__ __launch_bounds__(64 * LW) void asp_layer_small_kernel(
     c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, tv), __builtin_bit_cast(v8bf, lv[k]), c, 0,
                                                 0, 0);
   }
+  const float bv = bf16_to_f32(bbits);
   float yv[2] = {0.0f, 0.0f};
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
