@@ -8,9 +8,9 @@
 //
 // an NT matrix product whose two operands are both K-contiguous rows of gT.
 //
-//   * only the tiles (I, J) with I <= J are computed (128 x 128, four waves of
-//     64 x 64 = 2 x 2 blocks of v_mfma_f32_32x32x16_bf16); each is added to
-//     A[I][J] and, transposed, to A[J][I].  On a diagonal tile the upper
+//   * only the tiles (I, J) with I <= J are computed (TB x TB, four waves of
+//     TB/2 x TB/2 = BW x BW blocks of v_mfma_f32_32x32x16_bf16); each is added
+//     to A[I][J] and, transposed, to A[J][I].  On a diagonal tile the upper
 //     triangle comes from the normal write and the strict lower triangle from
 //     the transposed one, so A stays exactly symmetric;
 //   * products of two bf16 values are exact in float32; the sums are float32
@@ -19,11 +19,16 @@
 //     of the two operand tiles, copied straight from HBM/L2 into LDS by
 //     buffer_load ... lds (rows past d read as zero), with the chunk swizzle of
 //     the ASP GEMM so that the fragment loads are bank-conflict free; one
-//     barrier per stage;
-//   * the matrix cores consume a stage (64 x 128 x 128 MACs) far faster than
-//     a copy from the infinity cache or HBM returns, so the ring is four
-//     stages deep (three in flight while one is multiplied, 96 KB per CU) and
-//     a CU runs one workgroup, which owns 128 KB of LDS;
+//     barrier per stage, one workgroup per CU;
+//   * the copies into LDS, not the matrix cores, bound the main loop (about
+//     50 GB/s per CU measured), so the tile is as large as one round of
+//     workgroups allows: TB = 192 when the 192-tile triangle fits on the 256
+//     CUs and the 128-tile one does not (d = 2817 .. 4224, the paper's layer
+//     widths up to 4096), TB = 128 otherwise.  Three stages of 48 KB (192) or
+//     four of 32 KB (128) keep 96 KB in flight per CU;
+//   * the tile goes through LDS (C, then C^T) so that both read-modify-write
+//     passes move 16 bytes per lane along rows of A; with TB = 128 the reads
+//     of A[I][J] are issued during the last stages;
 //   * workgroups are mapped XCD-major onto the triangle of tiles taken in
 //     8 x 8 super-blocks, so that the tiles resident on one XCD at a time
 //     share their row panels of gT in its L2.
@@ -34,18 +39,28 @@ namespace qwam {
 
 namespace {
 
-constexpr int TB = 128;            // tile edge
-constexpr int NST = 2;             // ring stages
-constexpr int WG_PER_CU = 2;       // workgroups per CU (LDS: NST stages or the epilogue tile each)
 constexpr int NWAVES_S = 4;
 constexpr int NT_S = 64 * NWAVES_S;
 constexpr int KS = 64;             // values of n per ring stage (one 128-byte line per row)
 constexpr int ROWB_S = KS * 2;
-constexpr int STAGE_B = 2 * TB * ROWB_S;   // bytes of one stage: A tile, then B tile ([row][8 swizzled chunk slots])
-constexpr int LDC = TB + 4;        // float row stride of the epilogue tile (16-byte rows, conflict-free reads)
-constexpr int SMEM_B = NST * STAGE_B > TB * LDC * 4 ? NST * STAGE_B : TB * LDC * 4;
 
 typedef float v16f_s __attribute__((ext_vector_type(16)));
+
+template <int TB>
+struct SyrkCfg {
+  static_assert(TB == 128 || TB == 192, "tile edge 128 or 192");
+  static constexpr int BW = TB / 64;                       // 32x32 blocks per wave edge
+  static constexpr int NST = TB == 128 ? 4 : 3;            // ring stages
+  static constexpr int STAGE_B = 2 * TB * ROWB_S;          // A tile, then B tile ([row][8 swizzled chunk slots])
+  static constexpr int CPW = TB / 32;                      // 1 KB copies per operand, stage and wave
+  static constexpr int IPS = 2 * CPW;                      // copies per stage and wave
+  static constexpr int LDC = TB + 4;                       // float row stride of the epilogue tile
+  static constexpr int F4 = TB * TB / 4 / NT_S;            // float4 of a tile per thread
+  static constexpr int SMEM_B = NST * STAGE_B > TB * LDC * 4 ? NST * STAGE_B : TB * LDC * 4;
+  // the early reads of A[I][J] (F4 float4 per thread) fit in the registers
+  // beside the accumulators only for TB = 128
+  static constexpr bool PREFETCH = TB == 128;
+};
 
 __device__ __forceinline__ int swz_s(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
@@ -67,10 +82,17 @@ __device__ __forceinline__ v4i lds_read16(uint32_t addr) {
 
 // s_waitcnt lgkmcnt(N), tied to the fragments it makes valid so that no use
 // of them is scheduled before it
-template <int N>
-__device__ __forceinline__ void lgkm_wait_for(v4i (&f)[4]) {
+template <int N, int NF>
+__device__ __forceinline__ void lgkm_wait_for(v4i (&f)[NF]) {
   static_assert(N >= 0 && N < 16, "lgkmcnt range");
-  asm volatile("s_waitcnt lgkmcnt(%4)" : "+v"(f[0]), "+v"(f[1]), "+v"(f[2]), "+v"(f[3]) : "i"(N));
+  if constexpr (NF == 4) {
+    asm volatile("s_waitcnt lgkmcnt(%4)" : "+v"(f[0]), "+v"(f[1]), "+v"(f[2]), "+v"(f[3]) : "i"(N));
+  } else {
+    static_assert(NF == 6, "four or six fragments");
+    asm volatile("s_waitcnt lgkmcnt(%6)"
+                 : "+v"(f[0]), "+v"(f[1]), "+v"(f[2]), "+v"(f[3]), "+v"(f[4]), "+v"(f[5])
+                 : "i"(N));
+  }
 }
 
 constexpr int SBK = 8;             // tiles per edge of a super-block
@@ -115,10 +137,13 @@ __device__ __forceinline__ void triangle_tile(int bid, int T, int& ti, int& tj) 
 
 }  // namespace
 
-__global__ __launch_bounds__(NT_S, WG_PER_CU) void aog_syrk_kernel(const uint16_t* __restrict__ gT,
-                                                                  float* __restrict__ A, int d, int n) {
+template <int TB>
+__global__ __launch_bounds__(NT_S, 1) void aog_syrk_kernel(const uint16_t* __restrict__ gT, float* __restrict__ A,
+                                                          int d, int n) {
+  using Cf = SyrkCfg<TB>;
+  constexpr int BW = Cf::BW, NST = Cf::NST, CPW = Cf::CPW, IPS = Cf::IPS, LDC = Cf::LDC, F4 = Cf::F4;
   // the ring of NST stages; after the main loop, the epilogue tile
-  __shared__ __attribute__((aligned(16))) uint8_t smem[SMEM_B];
+  __shared__ __attribute__((aligned(16))) uint8_t smem[Cf::SMEM_B];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -131,31 +156,32 @@ __global__ __launch_bounds__(NT_S, WG_PER_CU) void aog_syrk_kernel(const uint16_
   const uint32_t RB = static_cast<uint32_t>(n) * 2u;   // bytes per row of gT
   const int S = n / KS;
 
-  // LDS-DMA: copy i (0..3) of wave w fills rows 8*(4w+i) .. +7 of a tile, lane
-  // l taking row 8*(4w+i) + l/8 and slot l%8, which holds chunk (l%8) ^ swz(row)
+  // LDS-DMA: copy i (0..CPW-1) of wave w fills rows 8*(CPW*w+i) .. +7 of a
+  // tile, lane l taking row 8*(CPW*w+i) + l/8 and slot l%8, which holds chunk
+  // (l%8) ^ swz(row)
   const buf_rsrc a_rsrc = make_rsrc(gT + static_cast<int64_t>(m0) * n, static_cast<uint32_t>(min(TB, d - m0)) * RB);
   const buf_rsrc b_rsrc = make_rsrc(gT + static_cast<int64_t>(n0) * n, static_cast<uint32_t>(min(TB, d - n0)) * RB);
-  uint32_t d_off[4];
+  uint32_t d_off[CPW];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int row = 8 * (4 * wave + i) + (lane >> 3);
+  for (int i = 0; i < CPW; ++i) {
+    const int row = 8 * (CPW * wave + i) + (lane >> 3);
     d_off[i] = static_cast<uint32_t>(row) * RB + static_cast<uint32_t>(((lane & 7) ^ swz_s(row)) * 16);
   }
-  auto stage_a = [&](int k) __attribute__((always_inline)) { return smem + k * STAGE_B; };
-  auto stage_b = [&](int k) __attribute__((always_inline)) { return smem + k * STAGE_B + TB * ROWB_S; };
+  auto stage_a = [&](int k) __attribute__((always_inline)) { return smem + k * Cf::STAGE_B; };
+  auto stage_b = [&](int k) __attribute__((always_inline)) { return smem + k * Cf::STAGE_B + TB * ROWB_S; };
   auto issue = [&](int s, int k) __attribute__((always_inline)) {
     const uint32_t ko = static_cast<uint32_t>(s) * ROWB_S;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) buf_load16_lds(a_rsrc, d_off[i] + ko, stage_a(k) + (4 * wave + i) * 1024);
+    for (int i = 0; i < CPW; ++i) buf_load16_lds(a_rsrc, d_off[i] + ko, stage_a(k) + (CPW * wave + i) * 1024);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) buf_load16_lds(b_rsrc, d_off[i] + ko, stage_b(k) + (4 * wave + i) * 1024);
+    for (int i = 0; i < CPW; ++i) buf_load16_lds(b_rsrc, d_off[i] + ko, stage_b(k) + (CPW * wave + i) * 1024);
   };
 
-  v16f_s acc[2][2];
+  v16f_s acc[BW][BW];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < BW; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = v16f_s{};
+    for (int j = 0; j < BW; ++j) acc[i][j] = v16f_s{};
 
   // v_mfma_f32_32x32x16_bf16 operands: lane l holds row l%32 and the 8
   // consecutive k of half l/32 of a 16-wide k step, i.e. chunk 2q + l/32 of
@@ -165,44 +191,84 @@ __global__ __launch_bounds__(NT_S, WG_PER_CU) void aog_syrk_kernel(const uint16_
   const int frow_off = frow * ROWB_S;
   const int fslot = fhalf ^ swz_s(frow);
 
+  // With TB = 128 the epilogue's reads of A[I][J] are issued right after the
+  // last stage's copies (step S - NST), so that their latency hides behind the
+  // last stages: thread t holds float4 number t + NT_S q (q < F4) of the tile, row
+  // (t + NT_S q) / (TB/4), columns 4 ((t + NT_S q) % (TB/4)) .. +3.  Interior
+  // off-diagonal tiles only.
+  const bool diag = ti == tj;
+  const bool fast = m0 + TB <= d && n0 + TB <= d && !diag;
+  const bool pref = Cf::PREFETCH && fast && S >= NST;
+  const buf_rsrc A_rsrc = make_rsrc(A, 0xFFFFFFFFu);
+  auto f4_row = [&](int q) __attribute__((always_inline)) { return (tid + NT_S * q) / (TB / 4); };
+  auto f4_col = [&](int q) __attribute__((always_inline)) { return 4 * ((tid + NT_S * q) % (TB / 4)); };
+  float4 pn[F4];
+  auto load_block = [&](int r0, int c0, float4 (&dst)[F4]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int q = 0; q < F4; ++q)
+      dst[q] = __builtin_bit_cast(
+          float4, buf_load16(A_rsrc, (static_cast<uint32_t>(r0 + f4_row(q)) * d + c0 + f4_col(q)) * 4u));
+  };
+
   // stage s (slot k = s % NST): wait for this wave's copies of stage s (those
-  // of the next NST - 2 stages, when issued, may stay in flight: 8 copies per
-  // stage and wave), barrier, then refill the slot of stage s-1 (every wave
-  // is past it) with stage s + NST - 1
+  // of the next NST - 2 stages, when issued, may stay in flight, and after
+  // step S - NST the F4 reads of A), barrier, then refill the slot of stage
+  // s-1 (every wave is past it) with stage s + NST - 1
+  auto stage_wait = [&](int s) __attribute__((always_inline)) {
+    const bool after = pref && s > S - NST;
+    if constexpr (NST == 4) {
+      if (s + 2 < S) {
+        if (after) wait_vmcnt<2 * IPS + F4>();
+        else wait_vmcnt<2 * IPS>();
+      } else if (s + 1 < S) {
+        if (after) wait_vmcnt<IPS + F4>();
+        else wait_vmcnt<IPS>();
+      } else {
+        if (after) wait_vmcnt<F4>();
+        else wait_vmcnt<0>();
+      }
+    } else {
+      if (s + 1 < S) {
+        if (after) wait_vmcnt<IPS + F4>();
+        else wait_vmcnt<IPS>();
+      } else {
+        if (after) wait_vmcnt<F4>();
+        else wait_vmcnt<0>();
+      }
+    }
+  };
   auto stage_step = [&](int s, int k) __attribute__((always_inline)) {
-    static_assert(NST == 2 || NST == 4, "wait counts for 2 or 4 stages");
-    if (NST == 4 && s + 2 < S) wait_vmcnt<16>();
-    else if (NST == 4 && s + 1 < S) wait_vmcnt<8>();
-    else wait_vmcnt<0>();
+    stage_wait(s);
     lds_barrier();
     if (s + NST - 1 < S) issue(s + NST - 1, (k + NST - 1) % NST);
+    if (pref && s == S - NST) load_block(m0, n0, pn);
     // fragments of k-step q + 1 are read while step q multiplies
-    const uint32_t a_base = lds_addr(stage_a(k)) + (wm * 64) * ROWB_S + frow_off;
-    const uint32_t b_base = lds_addr(stage_b(k)) + (wn * 64) * ROWB_S + frow_off;
-    v4i fr[2][4];
-    auto read_step = [&](int q, v4i (&f)[4]) __attribute__((always_inline)) {
+    const uint32_t a_base = lds_addr(stage_a(k)) + (wm * (TB / 2)) * ROWB_S + frow_off;
+    const uint32_t b_base = lds_addr(stage_b(k)) + (wn * (TB / 2)) * ROWB_S + frow_off;
+    v4i fr[2][2 * BW];
+    auto read_step = [&](int q, v4i (&f)[2 * BW]) __attribute__((always_inline)) {
       const uint32_t so = static_cast<uint32_t>(((2 * q) ^ fslot) * 16);
-      f[0] = lds_read16(a_base + so);
-      f[1] = lds_read16(a_base + so + 32 * ROWB_S);
-      f[2] = lds_read16(b_base + so);
-      f[3] = lds_read16(b_base + so + 32 * ROWB_S);
+#pragma unroll
+      for (int i = 0; i < BW; ++i) f[i] = lds_read16(a_base + so + i * 32 * ROWB_S);
+#pragma unroll
+      for (int j = 0; j < BW; ++j) f[BW + j] = lds_read16(b_base + so + j * 32 * ROWB_S);
     };
     read_step(0, fr[0]);
 #pragma unroll
     for (int q = 0; q < KS / 16; ++q) {
-      v4i(&f)[4] = fr[q & 1];
+      v4i(&f)[2 * BW] = fr[q & 1];
       if (q + 1 < KS / 16) {
         read_step(q + 1, fr[(q + 1) & 1]);
-        lgkm_wait_for<4>(f);
+        lgkm_wait_for<2 * BW>(f);
       } else {
         lgkm_wait_for<0>(f);
       }
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < BW; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < BW; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, f[i]),
-                                                              __builtin_bit_cast(v8bf, f[2 + j]), acc[i][j], 0, 0, 0);
+                                                              __builtin_bit_cast(v8bf, f[BW + j]), acc[i][j], 0, 0, 0);
     }
   };
 
@@ -219,99 +285,85 @@ __global__ __launch_bounds__(NT_S, WG_PER_CU) void aog_syrk_kernel(const uint16_
   for (int k = 0; k + 1 < NST; ++k)
     if (s + k < S) stage_step(s + k, k);
 
-  // ---- epilogue: A[I][J] += C and, transposed, A[J][I] += C^T, through LDS ----
-  // The tile C goes to LDS ([row][LDC] floats); both read-modify-write passes
-  // then touch whole rows of A: the normal one 16 bytes per lane along a row
-  // of C, the transposed one 4 bytes per lane down a column of C (64
-  // consecutive rows of C = 256 contiguous bytes of a row of A).  On a
-  // diagonal tile the normal pass writes r <= c and the transposed one r < c.
-  lds_barrier();                                   // every wave is past the ring
+  // ---- epilogue: A[I][J] += C, then A[J][I] += C^T, through LDS ----
+  // Each pass stages its tile in LDS ([row][LDC] floats) and moves 16 bytes
+  // per lane along rows of A; the reads of A are issued before the tile is
+  // staged.  A diagonal tile (I = J) is one pass over its block: element
+  // (r, c) gets C[r][c] for r <= c and C[c][r] below the diagonal.  Blocks
+  // past d are skipped float4 by float4 (d % 16 == 0, so a float4 is all in
+  // or all out).
   float* C = reinterpret_cast<float*>(smem);
   // result layout of a 32x32 block: lane l holds column l%32 and rows
   // 8*(v/4) + 4*(l/32) + v%4, v = 0..15
+  auto stage_tile = [&](bool transposed) __attribute__((always_inline)) {
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < BW; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+      for (int j = 0; j < BW; ++j)
 #pragma unroll
-      for (int v = 0; v < 16; ++v)
-        C[(wm * 64 + i * 32 + 8 * (v >> 2) + 4 * fhalf + (v & 3)) * LDC + wn * 64 + j * 32 + frow] = acc[i][j][v];
-  __syncthreads();
+        for (int v = 0; v < 16; ++v) {
+          const int r = wm * (TB / 2) + i * 32 + 8 * (v >> 2) + 4 * fhalf + (v & 3);
+          const int c = wn * (TB / 2) + j * 32 + frow;
+          C[transposed ? c * LDC + r : r * LDC + c] = acc[i][j][v];
+        }
+  };
+  auto in_range = [&](int r0, int c0, int q) __attribute__((always_inline)) {
+    return r0 + f4_row(q) < d && c0 + f4_col(q) < d;
+  };
+  auto load_ranged = [&](int r0, int c0, float4 (&dst)[F4]) __attribute__((always_inline)) {
+    if (fast) {
+      load_block(r0, c0, dst);
+    } else {
+#pragma unroll
+      for (int q = 0; q < F4; ++q) {
+        dst[q] = float4{0.0f, 0.0f, 0.0f, 0.0f};
+        if (in_range(r0, c0, q))
+          dst[q] = __builtin_bit_cast(
+              float4, buf_load16(A_rsrc, (static_cast<uint32_t>(r0 + f4_row(q)) * d + c0 + f4_col(q)) * 4u));
+      }
+    }
+  };
+  auto add_store = [&](int r0, int c0, const float4 (&cur)[F4]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int q = 0; q < F4; ++q) {
+      const int r = f4_row(q), c = f4_col(q);
+      float4 cv = *reinterpret_cast<const float4*>(C + r * LDC + c);
+      if (diag) {                                  // below the diagonal: the mirrored element
+        if (r > c) cv.x = C[c * LDC + r];
+        if (r > c + 1) cv.y = C[(c + 1) * LDC + r];
+        if (r > c + 2) cv.z = C[(c + 2) * LDC + r];
+        if (r > c + 3) cv.w = C[(c + 3) * LDC + r];
+      }
+      const float4 o = {cur[q].x + cv.x, cur[q].y + cv.y, cur[q].z + cv.z, cur[q].w + cv.w};
+      if (fast || in_range(r0, c0, q))
+        *reinterpret_cast<float4*>(A + static_cast<int64_t>(r0 + r) * d + c0 + c) = o;
+    }
+  };
 
-  const bool diag = ti == tj;
-  const bool full = m0 + TB <= d && n0 + TB <= d;
-  // normal pass: thread t takes the float4 of columns 4 (t % 32) .. +3 in rows
-  // t / 32 + 8 q, q = 0..15
-  {
-    const int c4 = tid & 31, rr = tid >> 5;
-    float* arow = A + static_cast<int64_t>(m0 + rr) * d + n0 + 4 * c4;
-    if (full && !diag) {
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        float4 o[8];
-#pragma unroll
-        for (int q = 0; q < 8; ++q) o[q] = *reinterpret_cast<const float4*>(arow + static_cast<int64_t>(8 * (8 * h + q)) * d);
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          const float4 cv = *reinterpret_cast<const float4*>(C + (rr + 8 * (8 * h + q)) * LDC + 4 * c4);
-          o[q].x += cv.x;
-          o[q].y += cv.y;
-          o[q].z += cv.z;
-          o[q].w += cv.w;
-          *reinterpret_cast<float4*>(arow + static_cast<int64_t>(8 * (8 * h + q)) * d) = o[q];
-        }
-      }
-    } else {
-      for (int q = 0; q < 16; ++q) {
-        const int r = rr + 8 * q;
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int c = 4 * c4 + u;
-          if (m0 + r < d && n0 + c < d && (!diag || r <= c))
-            arow[static_cast<int64_t>(8 * q) * d + u] += C[r * LDC + c];
-        }
-      }
-    }
-  }
-  // transposed pass: thread t takes row r = t % 128 of C and the columns
-  // 4 (t / 128 + 2 q) .. +3, q = 0..15: A[n0 + c][m0 + r] += C[r][c]
-  {
-    const int r = tid & (TB - 1), cq = tid >> 7;
-    float* acol = A + static_cast<int64_t>(n0) * d + m0 + r;
-    if (full && !diag) {
-#pragma unroll
-      for (int h = 0; h < 4; ++h) {
-        float o[16];
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-#pragma unroll
-          for (int u = 0; u < 4; ++u) o[4 * q + u] = acol[static_cast<int64_t>(4 * (cq + 2 * (4 * h + q)) + u) * d];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int c4 = cq + 2 * (4 * h + q);
-          const float4 cv = *reinterpret_cast<const float4*>(C + r * LDC + 4 * c4);
-          acol[static_cast<int64_t>(4 * c4 + 0) * d] = o[4 * q + 0] + cv.x;
-          acol[static_cast<int64_t>(4 * c4 + 1) * d] = o[4 * q + 1] + cv.y;
-          acol[static_cast<int64_t>(4 * c4 + 2) * d] = o[4 * q + 2] + cv.z;
-          acol[static_cast<int64_t>(4 * c4 + 3) * d] = o[4 * q + 3] + cv.w;
-        }
-      }
-    } else {
-      for (int q = 0; q < 16; ++q) {
-        const int c4 = cq + 2 * q;
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int c = 4 * c4 + u;
-          if (m0 + r < d && n0 + c < d && (!diag || r < c)) acol[static_cast<int64_t>(c) * d] += C[r * LDC + c];
-        }
-      }
-    }
-  }
+  if (!pref) load_ranged(m0, n0, pn);
+  lds_barrier();                                   // every wave is past the ring
+  stage_tile(false);
+  __syncthreads();
+  add_store(m0, n0, pn);
+  if (diag) return;
+  load_ranged(n0, m0, pn);                         // the transposed block's current values
+  __syncthreads();                                 // every thread is done with C
+  stage_tile(true);
+  __syncthreads();
+  add_store(n0, m0, pn);
+}
+
+static int syrk_tiles(int d, int tb) {
+  const int T = (d + tb - 1) / tb;
+  return T * (T + 1) / 2;
 }
 
 hipError_t launch_aog_accumulate(int d, int n, const uint16_t* gT, float* A, hipStream_t stream) {
-  const int T = (d + TB - 1) / TB;
-  hipLaunchKernelGGL(aog_syrk_kernel, dim3(T * (T + 1) / 2), dim3(NT_S), 0, stream, gT, A, d, n);
+  // 192-row tiles when they fit in one round on the 256 CUs and 128-row ones do not
+  if (syrk_tiles(d, 128) > 256 && syrk_tiles(d, 192) <= 256)
+    hipLaunchKernelGGL(aog_syrk_kernel<192>, dim3(syrk_tiles(d, 192)), dim3(NT_S), 0, stream, gT, A, d, n);
+  else
+    hipLaunchKernelGGL(aog_syrk_kernel<128>, dim3(syrk_tiles(d, 128)), dim3(NT_S), 0, stream, gT, A, d, n);
   return hipGetLastError();
 }
 

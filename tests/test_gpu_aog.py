@@ -55,7 +55,10 @@ def _check(d, n, seed, A0=None):
     return got, ref
 
 
-@pytest.mark.parametrize("d,n", [(16, 64), (128, 64), (144, 128), (320, 192), (1024, 256), (1040, 640)])
+# d = 2880 and 3008 run the 192-row tiles (3008: a ragged last tile row), the
+# others the 128-row ones
+@pytest.mark.parametrize("d,n", [(16, 64), (128, 64), (144, 128), (320, 192), (1024, 256), (1040, 640),
+                                 (2880, 128), (3008, 64)])
 def test_aog_accumulate_shapes(d, n):
     _check(d, n, seed=d + n)
 
