@@ -261,12 +261,254 @@ __global__ __launch_bounds__(64 * LW) void asp_layer_small_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------
+// The same layer for at most 16 tokens.  A 32-token block would be half
+// padding, so the workgroup owns 16 tokens x 16 output channels and runs the
+// integer partials on v_mfma_scale_f32_16x16x128_f8f6f4: lane l holds token
+// (or output channel) l % 16 and channels 32*(l/16) .. +31 of a 128-channel
+// step, i.e. two 64-channel spans, lane groups 0-1 the first and 2-3 the
+// second.  Each span's partial is its own instruction, with the other span's
+// lane scales at 2^-127 on both operands (their products underflow to zero).
+// Per lane and step this quantizes 32 real channels (the 32-token form
+// quantizes 32 channels for two tokens of which one is padding at M <= 16).
+//
+// The K split (eight waves, contiguous ranges of spans), the order of the
+// per-span scaling and of the sum over the waves, and the epilogue's
+// v_mfma_f32_32x32x16_bf16 (rows 16-31 zero) are those of the few-token
+// GEMM, so the two paths give the same y from the same codes, scales and t.
+// ---------------------------------------------------------------------------
+template <int RANK>
+__global__ __launch_bounds__(64 * LW) void asp_layer_tiny_kernel(
+    const uint16_t* __restrict__ x, const float* __restrict__ inv_smooth, const uint16_t* __restrict__ L1t,
+    const uint8_t* __restrict__ wq, const float* __restrict__ ws, const uint16_t* __restrict__ L2t,
+    const uint16_t* __restrict__ bias, uint16_t* __restrict__ y, uint8_t* __restrict__ xq_out,
+    float* __restrict__ xs_out, uint16_t* __restrict__ t_out, int M, int N, int K) {
+  static_assert(RANK == 16 || RANK == 32, "one or two 16-column blocks of t");
+  constexpr int TBK = 16;                // tokens and output channels of the block
+  constexpr int RB = RANK / 16;
+  // dynamic LDS: partial acc [LW][16][16] | partial t [LW][16][RANK] | t bf16 [16][RANK] | 1/lambda [K]
+  // and 128 floats that a second span past K reads (its values are discarded)
+  extern __shared__ __attribute__((aligned(16))) float lds[];
+  float* red_acc = lds;
+  float* red_t = red_acc + LW * TBK * TBK;
+  uint16_t* t_l = reinterpret_cast<uint16_t*>(red_t + LW * TBK * RANK);
+  float* inv_l = red_t + LW * TBK * RANK + TBK * RANK / 2;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n0 = blockIdx.x * TBK;
+  const bool write_act = xq_out != nullptr && blockIdx.x == 0;
+  const int G = K / kGroup;
+  const int KB = K / 2;
+  const int gpw = (G + LW - 1) / LW;
+  const int g_lo = min(G, wave * gpw), g_hi = min(G, g_lo + gpw);
+
+  const int frow = lane & 15;            // token (A, t) or output channel (B)
+  const int grp = lane >> 4;             // 32-channel block of the step
+  const int half = grp >> 1;             // span of the step
+  // D of a 16x16 block: lane l holds column l%16 and rows 4*(l/16) + i
+
+  const buf_rsrc x_rsrc = make_rsrc(x, static_cast<uint32_t>(M) * K * 2u);
+  const buf_rsrc w_rsrc = make_rsrc(wq + static_cast<int64_t>(n0) * KB, static_cast<uint32_t>(min(TBK, N - n0)) * KB);
+  const buf_rsrc ws_rsrc = make_rsrc(ws, static_cast<uint32_t>(G) * N * 4u);
+  const buf_rsrc l1_rsrc = make_rsrc(L1t, static_cast<uint32_t>(RANK) * K * 2u);
+  const uint32_t x_off = static_cast<uint32_t>(frow * K + 32 * grp) * 2u;
+  const uint32_t w_off = static_cast<uint32_t>(frow * KB + 16 * grp);
+  const uint32_t sw_off = static_cast<uint32_t>(n0 + frow) * 4u;
+  // t MFMA j of a step (v_mfma_f32_16x16x32_bf16): lane l supplies channels
+  // 32*(l/16) + 8 j .. +7 as its k-slots, so B lane l (t column l%16 of block
+  // rb) takes L1t[16 rb + l%16][the same channels]
+  const uint32_t l1_off = static_cast<uint32_t>(frow * K + 32 * grp) * 2u;
+
+  struct Fetch {
+    uint4 x[4];                    // 32 bf16 of x
+    uint4 w;                       // 32 packed weight codes of column n0 + lane%16
+    float sw[2];                   // weight scales of column n0 + lane%16, both spans
+    v8s l1[RB][4];
+  };
+  // the step of spans g, g+1 (g+1 only when below g_hi)
+  auto fetch = [&](int g, Fetch& f) __attribute__((always_inline)) {
+    const uint32_t go = static_cast<uint32_t>(g) * kGroup * 2u;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) f.x[q] = buf_load16(x_rsrc, x_off + go + 16u * q);
+    f.w = buf_load16(w_rsrc, w_off + static_cast<uint32_t>(g) * 32u);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) f.sw[h] = buf_load4f(ws_rsrc, sw_off + static_cast<uint32_t>(g + h) * N * 4u);
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        f.l1[rb][j] = __builtin_bit_cast(
+            v8s, buf_load16(l1_rsrc, l1_off + static_cast<uint32_t>(16 * rb) * K * 2u + go + 16u * j));
+  };
+
+  v4f acc = v4f{0.f, 0.f, 0.f, 0.f};
+  v4f tacc[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) tacc[rb] = v4f{0.f, 0.f, 0.f, 0.f};
+  auto work = [&](int g, const Fetch& f) __attribute__((always_inline)) {
+    const bool two = g + 1 < g_hi;
+    // x~ = x * (1/lambda) for the lane's 32 channels (1/lambda from LDS)
+    const float4* ip = reinterpret_cast<const float4*>(inv_l + g * kGroup + 32 * grp);
+    float v[32];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t xw[4] = {f.x[q].x, f.x[q].y, f.x[q].z, f.x[q].w};
+      const float4 i0 = ip[2 * q];
+      const float4 i1 = ip[2 * q + 1];
+      const float iv[8] = {i0.x, i0.y, i0.z, i0.w, i1.x, i1.y, i1.z, i1.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        v[8 * q + 2 * j] = __uint_as_float(xw[j] << 16) * iv[2 * j];
+        v[8 * q + 2 * j + 1] = __uint_as_float(xw[j] & 0xFFFF0000u) * iv[2 * j + 1];
+      }
+    }
+    // a second span past the wave's range (its channels belong to the next
+    // wave or lie past K) is zero, so that it adds nothing to t
+    if (half == 1 && !two) {
+#pragma unroll
+      for (int i = 0; i < 32; ++i) v[i] = 0.0f;
+    }
+    // the span's scale (Eq. 2): absmax of the token's 64 channels (lanes l, l^16)
+    float amax = 0.0f;
+#pragma unroll
+    for (int i = 0; i < 32; ++i) amax = __builtin_fmaxf(amax, __builtin_fabsf(v[i]));
+    amax = __builtin_fmaxf(amax, __shfl_xor(amax, 16));
+    const float s = q4_scale(amax);
+    const float inv = q4_inv(s);
+    float xs32[32];
+#pragma unroll
+    for (int i = 0; i < 32; ++i) xs32[i] = v[i] * inv;
+    const v6u d = codes_fp6_32(xs32);
+    v8i af;          // words 6-7 are not read with FP6 operands and stay unset
+#pragma unroll
+    for (int k = 0; k < 6; ++k) af[k] = static_cast<int>(d[k]);
+    if (write_act && frow < M && (half == 0 || two)) {
+      const uint2 b0 = fp6_code_block(d[0], d[1], d[2]);
+      const uint2 b1 = fp6_code_block(d[3], d[4], d[5]);
+      *reinterpret_cast<uint4*>(xq_out + static_cast<int64_t>(frow) * KB + g * 32 + 16 * grp) =
+          make_uint4(b0.x, b0.y, b1.x, b1.y);
+      if ((grp & 1) == 0) xs_out[static_cast<int64_t>(g + half) * M + frow] = s;
+    }
+    // the spans' exact integer partials, then acc += P * xs * ws, span g first
+    const v8i bf = codes_to_fp6(f.w);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      if (h == 1 && !two) break;
+      const int sc = half == h ? kE8M0Code : 0;
+      const v4f p = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(af, bf, v4f{}, kFmtFp6, kFmtFp6, 0, sc, 0, sc);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        // scale of token 4*(l/16) + i for span h: lane (token, 2h)
+        const float sx = __shfl(s, 4 * grp + i + 32 * h);
+        acc[i] = __builtin_fmaf(p[i], sx * f.sw[h], acc[i]);
+      }
+    }
+    // t partial: A = bf16(x~) of 8 channels per MFMA, B = the matching L1t slice
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      v8bf a;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) a[i] = static_cast<__bf16>(v[8 * j + i]);
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+        tacc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, __builtin_bit_cast(v8bf, f.l1[rb][j]), tacc[rb], 0, 0, 0);
+    }
+  };
+
+  // epilogue operands: the 32x32 MFMA's B (L2t rows of the block's columns,
+  // columns 16-31 zero) and the bias bits (converted only at the end)
+  constexpr int KSTEPS = RANK / 16;
+  const int ecol = lane & 31, ehalf = lane >> 5;
+  const int nt = n0 + ecol;
+  const bool col_ok = ecol < TBK && nt < N;
+  const buf_rsrc l2_rsrc = make_rsrc(L2t + static_cast<int64_t>(n0) * RANK,
+                                     static_cast<uint32_t>(min(TBK, N - n0)) * RANK * 2u);
+  v8s lv[KSTEPS];
+#pragma unroll
+  for (int k = 0; k < KSTEPS; ++k)
+    lv[k] = __builtin_bit_cast(v8s, buf_load16(l2_rsrc, static_cast<uint32_t>(ecol * RANK + k * 16 + ehalf * 8) * 2u));
+  const buf_rsrc b_rsrc = make_rsrc(bias, bias != nullptr ? static_cast<uint32_t>(N) * 2u : 0u);
+  const uint32_t bbits = __builtin_amdgcn_raw_buffer_load_b16(b_rsrc, static_cast<uint32_t>(col_ok ? nt : N) * 2u, 0, 0);
+
+  // the wave's slice of 1/lambda to LDS, then the first steps; all of it is
+  // waited for before the first step is used
+  if (g_lo < g_hi) {
+    const buf_rsrc i_rsrc = make_rsrc(inv_smooth, static_cast<uint32_t>(K) * 4u);
+    const int nfl = (g_hi - g_lo) * kGroup;
+    for (int c = 0; c < nfl; c += 256)
+      if (c + 4 * lane < nfl)
+        buf_load16_lds(i_rsrc, static_cast<uint32_t>(g_lo * kGroup + c + 4 * lane) * 4u, inv_l + g_lo * kGroup + c);
+  }
+  if (g_lo < g_hi) {
+    Fetch fa, fb;
+    fetch(g_lo, fa);
+    int g = g_lo;
+    if (g + 2 < g_hi) fetch(g + 2, fb);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the 1/lambda copies have landed
+    for (; g + 2 < g_hi; g += 4) {
+      work(g, fa);
+      if (g + 4 < g_hi) fetch(g + 4, fa);
+      work(g + 2, fb);
+      if (g + 6 < g_hi) fetch(g + 6, fb);
+    }
+    if (g < g_hi) work(g, fa);
+  }
+
+  // partial blocks -> LDS: acc as [wave][token][column], t as [wave][token][column]
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    red_acc[(wave * TBK + 4 * grp + i) * TBK + frow] = acc[i];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) red_t[(wave * TBK + 4 * grp + i) * RANK + 16 * rb + frow] = tacc[rb][i];
+  }
+  __syncthreads();
+  // t = bf16(sum over the waves in order), one element per thread
+  for (int e = tid; e < TBK * RANK; e += 64 * LW) {
+    const int tok = e / RANK, j = e % RANK;
+    float sum = 0.0f;
+#pragma unroll
+    for (int w = 0; w < LW; ++w) sum += red_t[(w * TBK + tok) * RANK + j];
+    const uint16_t b = static_cast<uint16_t>(f32_to_bf16_rne(sum));
+    t_l[tok * RANK + j] = b;
+    if (write_act && tok < M) t_out[static_cast<int64_t>(tok) * RANK + j] = b;
+  }
+  // this wave's result register of the 32x32 epilogue block: v = wave (rows
+  // below 16), token 8(v/4) + 4(l/32) + v%4, column l%32
+  const int v0 = wave;
+  const int tok = 8 * (v0 >> 2) + 4 * ehalf + (v0 & 3);
+  float c2 = 0.0f;
+#pragma unroll
+  for (int w = 0; w < LW; ++w) c2 += ecol < TBK ? red_acc[(w * TBK + tok) * TBK + ecol] : 0.0f;
+  __syncthreads();                      // t_l complete
+  v16f c;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) c[v] = v == v0 ? c2 : 0.0f;
+  const int arow = lane & 31;           // A operand: token l%32 (rows 16-31 zero)
+#pragma unroll
+  for (int k = 0; k < KSTEPS; ++k) {
+    v8s tv = v8s{0, 0, 0, 0, 0, 0, 0, 0};
+    if (arow < TBK) tv = *reinterpret_cast<const v8s*>(t_l + arow * RANK + k * 16 + ehalf * 8);
+    c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, tv), __builtin_bit_cast(v8bf, lv[k]), c, 0,
+                                                0, 0);
+  }
+  float yv = 0.0f;
+#pragma unroll
+  for (int v = 0; v < 16; ++v)
+    if (v == v0) yv = c[v];
+  if (tok < M && col_ok)
+    y[static_cast<int64_t>(tok) * N + nt] = static_cast<uint16_t>(f32_to_bf16_rne(yv + bf16_to_f32(bbits)));
+}
+
 hipError_t launch_asp_layer_small(int M, int N, int K, int r, const uint16_t* x, const float* inv_smooth,
                                   const uint16_t* L1t, const uint8_t* wq, const float* ws, const uint16_t* L2t,
                                   const uint16_t* bias, uint16_t* y, uint8_t* xq, float* xs, uint16_t* t,
                                   hipStream_t stream) {
-  const dim3 grid(((M + LB - 1) / LB) * ((N + LB - 1) / LB)), block(64 * LW);
-  const size_t lds = static_cast<size_t>(2) * LW * 16 * 64 * 4 + LB * r * 2 + static_cast<size_t>(K) * 4;
+  const bool tiny = M <= 16;
+  const dim3 grid(tiny ? (N + 15) / 16 : ((M + LB - 1) / LB) * ((N + LB - 1) / LB)), block(64 * LW);
+  const size_t lds = tiny ? static_cast<size_t>(LW) * 16 * (16 + r) * 4 + 16 * r * 2 + static_cast<size_t>(K + 128) * 4
+                          : static_cast<size_t>(2) * LW * 16 * 64 * 4 + LB * r * 2 + static_cast<size_t>(K) * 4;
   auto go = [&](auto kernel) {
     if (lds > 64 * 1024) {
       const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
@@ -278,8 +520,8 @@ hipError_t launch_asp_layer_small(int M, int N, int K, int r, const uint16_t* x,
     return hipGetLastError();
   };
   switch (r) {
-    case 16: return go(asp_layer_small_kernel<16>);
-    case 32: return go(asp_layer_small_kernel<32>);
+    case 16: return tiny ? go(asp_layer_tiny_kernel<16>) : go(asp_layer_small_kernel<16>);
+    case 32: return tiny ? go(asp_layer_tiny_kernel<32>) : go(asp_layer_small_kernel<32>);
     default: return hipErrorInvalidValue;
   }
 }

@@ -68,6 +68,10 @@ def test_fused_action_expert_layers(M, N):
     (33, 192, 144, 32, False),
     (64, 3072, 272, 32, True),
     (40, 16384, 64, 16, False),
+    # M <= 16 runs the 16-token kernel: 65 spans (an odd count per wave), the
+    # largest K
+    (16, 4160, 80, 32, True),
+    (3, 16384, 48, 16, False),
 ])
 def test_fused_edge_shapes(M, K, N, r, bias):
     d = I.custom(M=M, K=K, N=N, r=r, seed=M * 23 + K, n_outliers=max(1, K // 100), with_bias=bias)
