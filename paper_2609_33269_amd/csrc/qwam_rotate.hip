@@ -11,7 +11,8 @@
 //   rotate:   pass p of a tile is 1024 consecutive elements of the [16][T]
 //             tile; lane l holds 16 consecutive channels of one token, so
 //             butterfly stages 0-3 run in registers and stages 4 .. log2(B)-1
-//             between lanes l and l ^ 2^(s-4).  The rotated tile goes to LDS
+//             between lanes l and l ^ 2^(s-4) (DPP, ds_swizzle and the
+//             permlane swaps of gfx950).  The rotated tile goes to LDS
 //             (rows padded by 4 floats against bank conflicts).
 //   quantize: each wave reads its groups of the tile back in the lane layout
 //             of qwam_act.h and runs the plain kernel's per-group steps (or,
@@ -42,13 +43,37 @@ __device__ __forceinline__ void fwht16(float (&v)[16], int lane, int logB) {
         v[i] = a + b;
         v[i + h] = a - b;
       }
+  // Stages between lanes l and l ^ m.  The partner's value p comes by DPP
+  // (m = 1, 2: quad permutes; m = 8: rotation by 8 inside a row of 16), by
+  // ds_swizzle (m = 4) or by v_permlane16/32_swap (m = 16, 32), instead of a
+  // ds_bpermute per element.  The lane of the pair without bit m gets a + b,
+  // the other a - b, one rounding each: fma(., +-1, .) computes exactly that.
   for (int s = 4; s < logB; ++s) {
     const int m = 1 << (s - 4);
-    const bool upper = (lane & m) != 0;   // this lane holds the element with bit s set
+    const float sgn = (lane & m) != 0 ? -1.0f : 1.0f;   // -1: this lane holds the element with bit s set
+    // the lower lane: v + p = a + b; the upper: p - v = a - b
+    auto near = [&](auto xchg) __attribute__((always_inline)) {
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const float p = __shfl_xor(v[i], m);
-      v[i] = upper ? p - v[i] : v[i] + p;
+      for (int i = 0; i < 16; ++i) v[i] = __builtin_fmaf(v[i], sgn, __int_as_float(xchg(__float_as_int(v[i]))));
+    };
+    // swap results: [0] = own value in the lower half of each pair of rows
+    // (m = 16) or in lanes 0-31 (m = 32), the partner's in the other; [1]
+    // the reverse.  The lower lane computes [0] + [1] = a + b, the upper
+    // [0] - [1] = a - b.
+    auto far = [&](auto swap) __attribute__((always_inline)) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const auto r = swap(__float_as_uint(v[i]));
+        v[i] = __builtin_fmaf(__uint_as_float(r[1]), sgn, __uint_as_float(r[0]));
+      }
+    };
+    switch (m) {
+      case 1: near([](int u) { return __builtin_amdgcn_update_dpp(0, u, 0xB1, 0xF, 0xF, false); }); break;  // quad_perm [1,0,3,2]
+      case 2: near([](int u) { return __builtin_amdgcn_update_dpp(0, u, 0x4E, 0xF, 0xF, false); }); break;  // quad_perm [2,3,0,1]
+      case 4: near([](int u) { return __builtin_amdgcn_ds_swizzle(u, (4 << 10) | 0x1F); }); break;          // xor 4
+      case 8: near([](int u) { return __builtin_amdgcn_update_dpp(0, u, 0x128, 0xF, 0xF, false); }); break; // row_ror:8
+      case 16: far([](unsigned u) { return __builtin_amdgcn_permlane16_swap(u, u, false, false); }); break;
+      default: far([](unsigned u) { return __builtin_amdgcn_permlane32_swap(u, u, false, false); }); break;
     }
   }
 }
