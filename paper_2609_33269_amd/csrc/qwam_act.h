@@ -60,8 +60,8 @@ __device__ __forceinline__ void quantize_pack_store(const float (&v)[16], buf_rs
   float amax = 0.0f;
 #pragma unroll
   for (int j = 0; j < 16; ++j) amax = __builtin_fmaxf(amax, __builtin_fabsf(v[j]));
-  amax = __builtin_fmaxf(amax, __shfl_xor(amax, 16));
-  if (!g32) amax = __builtin_fmaxf(amax, __shfl_xor(amax, 32));
+  amax = max_xor16(amax);
+  if (!g32) amax = max_xor32(amax);
   const float s = q4_scale(amax);
   const float inv = q4_inv(s);
   // codes rint(v * inv) of the lane's 16 channels: one code block

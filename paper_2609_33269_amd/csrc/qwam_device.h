@@ -187,3 +187,21 @@ __device__ __forceinline__ void buf_store4f(float v, buf_rsrc r, uint32_t off) {
 }
 
 }  // namespace qwam
+
+namespace qwam {
+
+// max(v, v of lane l ^ 16) and max(v, v of lane l ^ 32) for every lane l, by
+// gfx950's row / half swaps (each lane gets its own and its partner's value
+// back, in one order or the other) instead of a ds_bpermute
+__device__ __forceinline__ float max_xor16(float v) {
+  const unsigned u = __float_as_uint(v);
+  const auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  return __builtin_fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float max_xor32(float v) {
+  const unsigned u = __float_as_uint(v);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return __builtin_fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+}  // namespace qwam

@@ -124,7 +124,7 @@ __global__ __launch_bounds__(64 * LW) void asp_layer_small_kernel(
     float amax = 0.0f;
 #pragma unroll
     for (int i = 0; i < 32; ++i) amax = __builtin_fmaxf(amax, __builtin_fabsf(v[i]));
-    amax = __builtin_fmaxf(amax, __shfl_xor(amax, 32));
+    amax = max_xor32(amax);
     const float s = q4_scale(amax);
     const float inv = q4_inv(s);
     // codes -> FP6 fields (one conversion for the lane's 32 channels): the
@@ -374,7 +374,7 @@ __global__ __launch_bounds__(64 * LW) void asp_layer_tiny_kernel(
     float amax = 0.0f;
 #pragma unroll
     for (int i = 0; i < 32; ++i) amax = __builtin_fmaxf(amax, __builtin_fabsf(v[i]));
-    amax = __builtin_fmaxf(amax, __shfl_xor(amax, 16));
+    amax = max_xor16(amax);
     const float s = q4_scale(amax);
     const float inv = q4_inv(s);
     float xs32[32];
