@@ -99,12 +99,14 @@ template <int RANK, bool DEFLATE>
 __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_rotated_kernel(
     const uint16_t* __restrict__ x, const float* __restrict__ inv_smooth,
     const uint16_t* __restrict__ L1t, uint8_t* __restrict__ xq, float* __restrict__ xs,
-    uint16_t* __restrict__ t, int M, int K, int logB, int T, float hscale, int g32) {
+    uint16_t* __restrict__ t, int M, int K, int logB, int T, float hscale, int g32, int red_off) {
   constexpr int RB = RANK / 16;
   constexpr int kMaxPerWave = per_wave<RANK>();
   using Acc = std::conditional_t<DEFLATE, double, float>;
-  // dynamic LDS: tile [16][T + pad] float | partial t [nwaves][16][RANK] Acc |
-  // (DEFLATE) -t [16][RANK] float
+  // dynamic LDS: two tiles [16][T + pad] float (tile tb in buffer tb % 2) |
+  // partial t [nwaves][16][RANK] Acc at float offset red_off (after the tiles,
+  // or over the second tile when both do not fit) | (DEFLATE) -t [16][RANK]
+  // float after both
   extern __shared__ double lds_raw[];
 
   const int lane = threadIdx.x & 63;
@@ -118,9 +120,10 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_rotated_k
   const int ntiles = K / T;
   const int npass = T / kGroup;          // 1024-element passes per tile = groups per tile
 
-  float* tile = reinterpret_cast<float*>(lds_raw);
-  Acc* red = reinterpret_cast<Acc*>(tile + 16 * TS);
+  float* tiles = reinterpret_cast<float*>(lds_raw);
+  Acc* red = reinterpret_cast<Acc*>(tiles + red_off);
   float* tneg = reinterpret_cast<float*>(red + nwaves * 16 * RANK);
+  if (red_off < 2 * 16 * TS) tneg = tiles + 2 * 16 * TS;   // red over the second tile
 
   const buf_rsrc x_rsrc = make_rsrc(x + static_cast<int64_t>(m0) * K, static_cast<uint32_t>(rows) * K * 2u);
   const buf_rsrc q_rsrc = make_rsrc(xq + static_cast<int64_t>(m0) * (K / 2), static_cast<uint32_t>(rows) * (K / 2));
@@ -144,7 +147,7 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_rotated_k
     }
   };
   // smooth, transform and scale the fetched passes into the LDS tile (tokens past M are zero)
-  auto rotate_tile = [&](const RotFetch (&rf)[kMaxPerWave]) __attribute__((always_inline)) {
+  auto rotate_tile = [&](const RotFetch (&rf)[kMaxPerWave], float* tile) __attribute__((always_inline)) {
 #pragma unroll
     for (int k = 0; k < kMaxPerWave; ++k) {
       const int p = wave + k * nwaves;
@@ -160,7 +163,7 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_rotated_k
       }
     }
   };
-  auto read_group = [&](int gl, float (&v)[16]) __attribute__((always_inline)) {
+  auto read_group = [&](const float* tile, int gl, float (&v)[16]) __attribute__((always_inline)) {
     const float4* src = reinterpret_cast<const float4*>(tile + row * TS + gl * kGroup + chunk * 16);
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
@@ -179,10 +182,14 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_rotated_k
 
   // pass over the tiles: t partials (and, without deflation, the codes).  The
   // next tile's x and 1/lambda are requested as soon as this tile's are in LDS.
+  // Tile tb goes to buffer tb % 2, so one barrier per tile suffices: a wave
+  // writes buffer tb % 2 only after the barrier of tile tb - 1, which every
+  // wave reaches after its reads of tile tb - 2 from that buffer.
   RotFetch rf[kMaxPerWave];
   fetch_tile(0, rf);
   for (int tb = 0; tb < ntiles; ++tb) {
-    rotate_tile(rf);
+    float* tile = tiles + (tb & 1) * 16 * TS;
+    rotate_tile(rf, tile);
     if (tb + 1 < ntiles) fetch_tile(tb + 1, rf);
     v8s l1[kMaxPerWave][RB][2];
 #pragma unroll
@@ -196,7 +203,7 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_rotated_k
       const int gl = wave + k * nwaves;
       if (gl < npass) {
         float v[16];
-        read_group(gl, v);
+        read_group(tile, gl, v);
         if constexpr (DEFLATE) {
           t_step_f64<RB>(v, l1[k], acc);
         } else {
@@ -205,9 +212,9 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_rotated_k
         }
       }
     }
-    lds_sync();
   }
   if constexpr (DEFLATE) fetch_tile(0, rf);     // the second pass starts over
+  lds_sync();                                   // the partials may overwrite the second tile
   store_t_partials<RB>(red, wave, lane, acc);
   lds_sync();
   reduce_t<RANK>(red, nwaves, rows, t + static_cast<int64_t>(m0) * RANK, DEFLATE ? tneg : nullptr);
@@ -218,7 +225,8 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_rotated_k
     const int a_ch = deflate_channel(lane);
     const float* tn_row = tneg + row * RANK;
     for (int tb = 0; tb < ntiles; ++tb) {
-      rotate_tile(rf);
+      float* tile = tiles + (tb & 1) * 16 * TS;
+      rotate_tile(rf, tile);
       if (tb + 1 < ntiles) fetch_tile(tb + 1, rf);
       uint32_t l1w[kMaxPerWave][RANK / 2];
 #pragma unroll
@@ -232,12 +240,11 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_rotated_k
         const int gl = wave + k * nwaves;
         if (gl < npass) {
           float v[16];
-          read_group(gl, v);
+          read_group(tile, gl, v);
           deflate_step<RANK>(v, l1w[k], tn_row);
           store_codes(tb * npass + gl, v);
         }
       }
-      lds_sync();
     }
   }
 }
@@ -262,15 +269,22 @@ hipError_t launch_quantize_act_rotated(int M, int K, int r, int group, int B, bo
   if (T / kGroup > 16) return hipErrorInvalidValue;
   const float hscale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(B)));
   auto go = [&](auto kernel, int nwaves, size_t acc_bytes) {
-    const size_t lds = static_cast<size_t>(16) * (T + kTilePad) * sizeof(float) +
-                       static_cast<size_t>(nwaves) * 16 * r * acc_bytes + (deflate ? 16 * r * sizeof(float) : 0);
+    // two tiles, then the partial t tiles, or those over the second tile when
+    // all of it would not fit in LDS (and they fit in a tile)
+    const size_t tile_bytes = static_cast<size_t>(16) * (T + kTilePad) * sizeof(float);
+    const size_t red_bytes = static_cast<size_t>(nwaves) * 16 * r * acc_bytes;
+    const size_t tneg_bytes = deflate ? 16 * r * sizeof(float) : 0;
+    const bool over = 2 * tile_bytes + red_bytes + tneg_bytes > 160 * 1024 && red_bytes <= tile_bytes;
+    const int red_off = static_cast<int>((over ? 1 : 2) * tile_bytes / sizeof(float));
+    const size_t lds = 2 * tile_bytes + (over ? 0 : red_bytes) + tneg_bytes;
+    if (lds > 160 * 1024) return hipErrorInvalidValue;
     if (lds > 64 * 1024) {
       const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
                                                hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
       if (e != hipSuccess) return e;
     }
     hipLaunchKernelGGL(kernel, dim3((M + 15) / 16), dim3(64 * nwaves), lds, stream, x, inv_smooth, L1t, xq, xs, t,
-                       M, K, logB, T, hscale, group == 32 ? 1 : 0);
+                       M, K, logB, T, hscale, group == 32 ? 1 : 0, red_off);
     return hipGetLastError();
   };
 #define QWAM_ROT_CASE(R)                                                                            \
