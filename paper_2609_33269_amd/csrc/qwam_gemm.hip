@@ -33,10 +33,11 @@
 //     E8M0 scales (2^3 on each side) cancel the 2^-6, so the float32 result is
 //     the integer partial P itself, exactly (|P| <= 3136);
 //   * the per-output scale products sx[m] * sw[n] of a group are an outer
-//     product: one v_mfma_f32_32x32x1_2b_f32 (K = 1, one rounding per product,
-//     as a VALU multiply) gives them for two 32 x 32 blocks at once, in the
-//     result layout of the integer blocks, so the VALU is left with one fused
-//     multiply-add per output and group;
+//     product: one v_mfma_f32_32x32x4_2b_bf16 over two-piece bf16 splits of
+//     the scales (scale_outer, within about 2^-15 of the float32 product)
+//     gives them for two 32 x 32 blocks at once, in the result layout of the
+//     integer blocks, so the VALU is left with one fused multiply-add per
+//     output and group;
 //   * group 64 runs as a software pipeline across groups: every MFMA is
 //     followed by VALU work that does not depend on it (the updates of blocks
 //     whose products landed earlier, the unpacking of the next group);
@@ -108,6 +109,32 @@ __device__ __forceinline__ uint4 lds_load16_volatile(const uint8_t* p) {
 __device__ __forceinline__ float lds_load4_volatile(const float* p) {
   typedef const volatile __attribute__((address_space(3))) float lds_f;
   return *(lds_f*)(p);
+}
+
+// bf16 bits of (a, b) rounded to nearest even, a in the low half
+__device__ __forceinline__ uint32_t bf16_pair(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v2f{a, b}, v2bf));
+}
+
+// The scale products sx * sw of two 32 x 32 blocks (lane l: row of sx,
+// column of sw, both l%32, of block l/32), in the result layout of the integer
+// blocks.  Each scale is split into two bf16 pieces, hi = bf16(s) and
+// lo = bf16(s - hi) (the difference is exact in float32), and one
+// v_mfma_f32_32x32x4_2b_bf16 sums the four exact products of
+// [hi, hi, lo, lo] (sx) and [hi, lo, hi, lo] (sw) in float32.  That is the
+// product of the two 16-bit splits, each within 2^-16 of its scale, so the
+// result is within about 2^-15 of sx * sw.  Unlike the float32 outer-product
+// MFMA, the bf16 one lets the SIMD issue VALU work while it runs.
+__device__ __forceinline__ v32f scale_outer(float sx, float sw) {
+  typedef short v4s __attribute__((ext_vector_type(4)));
+  const uint32_t hx = bf16_pair(sx, sx);
+  const float lo_x = sx - __builtin_bit_cast(float, hx << 16);
+  const uint32_t lx = bf16_pair(lo_x, lo_x);
+  const uint32_t hw = bf16_pair(sw, sw);
+  const uint32_t w = bf16_pair(sw, sw - __builtin_bit_cast(float, hw << 16));
+  const v4s a = __builtin_bit_cast(v4s, static_cast<uint64_t>(hx) | (static_cast<uint64_t>(lx) << 32));
+  const v4s b = __builtin_bit_cast(v4s, static_cast<uint64_t>(w) | (static_cast<uint64_t>(w) << 32));
+  return __builtin_amdgcn_mfma_f32_32x32x4bf16_1k(a, b, v32f{}, 0, 0, 0);
 }
 
 // Tile of workgroup `bid`: XCD-major remap (hardware places workgroup b on XCD
@@ -297,7 +324,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
     // scale products of row block i and both column blocks, group h:
     // registers 0-15 belong to column block 0, 16-31 to column block 1
     auto scale_block = [&](int i, int h) __attribute__((always_inline)) {
-      return __builtin_amdgcn_mfma_f32_32x32x1f32(d.sx[i][h], d.sw[h], v32f{}, 0, 0, 0);
+      return scale_outer(d.sx[i][h], d.sw[h]);
     };
     // per group h and row block i: the scale products (one MFMA for both
     // column blocks), the two integer blocks, then their updates; each update
@@ -423,7 +450,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
     };
     auto scale_products = [&](float sx, float sw) __attribute__((always_inline)) {
       if constexpr (PARTIALS) return v32f{};
-      else return __builtin_amdgcn_mfma_f32_32x32x1f32(sx, sw, v32f{}, 0, 0, 0);
+      else return scale_outer(sx, sw);
     };
     auto start = [&](Pipe& pp, const GroupData& d) __attribute__((always_inline)) {
       pp.af0 = codes_to_fp6(d.a[0]);
