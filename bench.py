@@ -82,7 +82,7 @@ METRIC = "ASP W4A4+r32 linear: effective TOPS & % int8 MFMA peak at 4096×3072×
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_asp_gemm_ffn_up.json")
 GEMM_SRCS = [os.path.join(ROOT, "paper_2609_33269_amd", "csrc", f) for f in ("qwam_gemm.hip", "qwam_device.h", "qwam_mfma.h")]
 GEMM_KERNEL = "asp_gemm_kernel<32, false, 64>"
-COPY_KERNEL = "neg_kernel"
+COPY_KERNEL = "copy_kernel"
 
 
 def gemm_issue_ceiling(group: int = GROUP) -> float:
@@ -153,6 +153,112 @@ def reduce_counters(fetch_csv: str, write_csv: str, copy_mib: int):
                                          out["write_kib_per_launch"] * out["write_factor"]) * 1024))
     out["algorithmic_bytes"] = algorithmic_bytes()[1]
     return out
+
+
+def settle_clocks(step, min_seconds: float, window: int = 10, max_seconds: float = 8.0):
+    """Run `step` in windows of `window` calls until at least `min_seconds`
+    have passed and the last three windows agree within 2% (or `max_seconds`)."""
+    import torch
+    stream = torch.cuda.current_stream()
+    times, n, t0 = [], 0, time.perf_counter()
+    while True:
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(window):
+            step(n)
+            n += 1
+        e1.record(stream)
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1) * 1e3 / window)
+        elapsed = time.perf_counter() - t0
+        last = times[-3:]
+        stable = len(last) == 3 and max(last) <= 1.02 * min(last)
+        if (elapsed >= min_seconds and stable) or elapsed >= max_seconds:
+            return {"steps": n, "seconds": round(elapsed, 2), "stable": stable,
+                    "window_us": [round(v, 1) for v in last]}
+
+
+def capture_graphs(fn, n: int):
+    """One CUDA/HIP graph per index i < n, each holding fn(i)."""
+    import torch
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for i in range(n):
+            fn(i)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graphs = []
+    for i in range(n):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            fn(i)
+        graphs.append(g)
+    for g in graphs:
+        g.replay()
+    torch.cuda.synchronize()
+    return graphs
+
+
+def graph_floor_us(n: int = 200, replays: int = 10) -> float:
+    """Per-launch time of an empty kernel inside a HIP graph of n launches."""
+    import torch
+    from paper_2609_33269_amd import qwam
+    g = capture_graphs(lambda i: [qwam.probe_empty() for _ in range(n)], 1)[0]
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(replays):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / (n * replays)
+
+
+def measured_peaks():
+    """What the chip sustains in plain loops (the probes of qwam_probe.h): each
+    matrix-core format, the float32 VALU at 1, 2 and 4 waves per SIMD, a
+    streaming copy of 2 x 1 GiB; best of three launches each."""
+    import torch
+    from paper_2609_33269_amd import qwam
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+
+    def best_ms(launch, reps=3):
+        best = None
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            launch()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1)
+            best = ms if best is None else min(best, ms)
+        return best
+
+    wgs = 1024                    # 4 waves per SIMD on 256 CUs
+    out = torch.empty(wgs * 256, device=dev, dtype=torch.float32)
+    mfma = {}
+    for kind, iters in (("fp6", 4096), ("fp4", 4096), ("fp8", 2048), ("i8", 2048), ("bf16", 2048),
+                        ("bf16_2b", 1024)):
+        ops = qwam.probe_mfma(kind, wgs, iters, out)
+        ms = best_ms(lambda: qwam.probe_mfma(kind, wgs, iters, out))
+        mfma[kind] = round(ops / (ms * 1e-3) / 1e12, 1)
+    valu = {}
+    for wps in (1, 2, 4):
+        ow = torch.empty(256 * wps * 256, device=dev, dtype=torch.float32)
+        fl = qwam.probe_valu_fma(256 * wps, 512, ow)
+        ms = best_ms(lambda: qwam.probe_valu_fma(256 * wps, 512, ow))
+        valu[f"{wps}_waves_per_simd"] = round(fl / (ms * 1e-3) / 1e12, 1)
+    src = torch.ones((1 << 30) // 4, device=dev, dtype=torch.float32)
+    dst = torch.empty_like(src)
+    moved = qwam.probe_copy(src, dst)
+    ms = best_ms(lambda: qwam.probe_copy(src, dst))
+    copy_gbs = round(moved / (ms * 1e-3) / 1e9, 1)
+    del src, dst
+    torch.cuda.empty_cache()
+    return {"mfma_TOPS": mfma, "valu_fp32_fma_TFLOPs": valu, "copy_GBs": copy_gbs,
+            "launch_floor_graph_us": round(graph_floor_us(), 2),
+            "method": "probe loops of include/qwam_probe.h, best of 3 launches; MFMA and copy at 4 waves/SIMD"}
 
 
 def small_m_report(args):
@@ -408,7 +514,9 @@ def cpu_baseline(draws, seconds: float = 12.0, deflate: bool = False, rotate: bo
         threads = 1
     V = O.protected_basis_from_factor(draws.a, R_RANK)
     f = O.build_layer(draws.x, draws.w, V, hadamard=rotate)
-    wq, sw, inv_lam, qw = O.pack_weights(f["R"], f["lam"], group)
+    # the weight codes and scales (the packed bytes themselves are not needed here)
+    qw, sw = O.quantize_groups(f["R"], group)
+    inv_lam = O.inverse_smoothing(f["lam"])
     chunk = 32
     done = 0
     t0 = time.perf_counter()
@@ -435,6 +543,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--settle", type=float, default=1.5,
+                    help="seconds of clock-settling steps before the warmup steps (always run)")
+    ap.add_argument("--no-peaks", action="store_true", help="skip the measured-peak probes")
     ap.add_argument("--rotate", type=int, default=24, help="distinct buffer sets cycled through")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
@@ -507,37 +618,68 @@ def main():
     stream = torch.cuda.current_stream()
     act_fn = qwam.quantize_act_deflated if args.deflated else qwam.quantize_act
 
-    def step(i, ev=None):
+    def step(i):
         j = i % nrot
         xq, xs, t, y = outs[j]
-        if ev is not None:
-            ev[0].record(stream)
         act_fn(layers[j], xins[j], out=(xq, xs, t))
-        if ev is not None:
-            ev[1].record(stream)
         qwam.asp_linear(layers[j], xq, xs, t, out=y)
-        if ev is not None:
-            ev[2].record(stream)
 
-    print(f"[bench] warmup {args.warmup} steps", file=sys.stderr, flush=True)
+    # clock settle: the first calls on a fresh box run at lower clocks, so the
+    # steps are warmed by time (at least `--settle` seconds, then until three
+    # consecutive 10-step windows agree within 2%), whatever --warmup says
+    settle = settle_clocks(step, args.settle)
+    print(f"[bench] clocks settled after {settle['steps']} steps / {settle['seconds']:.2f} s "
+          f"(last windows {settle['window_us']} us/step); warmup {args.warmup} steps", file=sys.stderr, flush=True)
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
 
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    # one HIP graph per buffer set holds one step (both kernels); the timed
+    # region replays them, K steps in all, with no event inside it
+    graphs = capture_graphs(lambda j: step(j), nrot)
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record(stream)
     for i in range(args.steps):
-        step(args.warmup + i, evs[i])
+        graphs[i % nrot].replay()
     end.record(stream)
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(end)
     ms_step = total_ms / args.steps
-    k1_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
-    k2_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
-    print(f"[bench] {args.steps} steps: {ms_step * 1e3:.1f} us/step, act kernel {k1_ms * 1e3:.1f} us, "
-          f"gemm {k2_ms * 1e3:.1f} us", file=sys.stderr, flush=True)
+
+    # the same replays, 10 repeats of max(100, K) steps: median per-step time
+    rep_steps = max(100, args.steps)
+    rep_ms = []
+    for _ in range(10):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for i in range(rep_steps):
+            graphs[i % nrot].replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        rep_ms.append(e0.elapsed_time(e1) / rep_steps)
+    med_ms = float(np.median(rep_ms))
+
+    # per-kernel durations: a separate loop of plain launches with events
+    # between the two kernels, on the stream they are launched on
+    kevs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(rep_steps)]
+    for i in range(rep_steps):
+        j = i % nrot
+        xq, xs, t, y = outs[j]
+        kevs[i][0].record(stream)
+        act_fn(layers[j], xins[j], out=(xq, xs, t))
+        kevs[i][1].record(stream)
+        qwam.asp_linear(layers[j], xq, xs, t, out=y)
+        kevs[i][2].record(stream)
+    torch.cuda.synchronize()
+    k1_all = [e[0].elapsed_time(e[1]) for e in kevs]
+    k2_all = [e[1].elapsed_time(e[2]) for e in kevs]
+    k1_ms, k2_ms = float(np.mean(k1_all)), float(np.mean(k2_all))
+    del graphs
+    print(f"[bench] {args.steps} graph-replayed steps: {ms_step * 1e3:.1f} us/step (median of 10 x {rep_steps}: "
+          f"{med_ms * 1e3:.1f}); act kernel {k1_ms * 1e3:.1f} us, gemm {k2_ms * 1e3:.1f} us "
+          f"(median {np.median(k2_all) * 1e3:.1f})", file=sys.stderr, flush=True)
+    floor_us = graph_floor_us()
 
     int_ops = 2.0 * M * K * N
     eff_tops = int_ops / (ms_step * 1e-3) / 1e12
@@ -564,9 +706,10 @@ def main():
         src_t = torch.ones(n, device=dev, dtype=torch.float32)
         dst_t = torch.empty_like(src_t)
         for _ in range(5):
-            torch.neg(src_t, out=dst_t)      # reads and writes copy_probe MiB each
+            qwam.probe_copy(src_t, dst_t)    # reads and writes copy_probe MiB each
         torch.cuda.synchronize()
         del src_t, dst_t
+    peaks = None if args.no_peaks else measured_peaks()
 
     traffic = measured_traffic() if args.group == GROUP else None
     act_name = ("quantize_act_rotated" if args.rotated else "quantize_act") + ("_deflated" if args.deflated else "")
@@ -581,7 +724,8 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "int4 codes on fp6-e2m3 MFMA (exact), f32 scale/accumulate, bf16 out",
+        "dtype": "int4 codes as fp6-e2m3 MFMA operands (exact int partials); per-group scale products "
+                 "sx*sw on bf16 MFMA from two-piece bf16 splits (~2^-15 rel); f32 accumulate; bf16 out",
         "data": "synthetic",
         "config": {"workload": "video_dit_ffn_up" + ("_rotated" if args.rotated else "")
                    + ("_deflated" if args.deflated else "") + ("_group32" if args.group == 32 else ""),
@@ -593,7 +737,13 @@ def main():
                      "peak": FP6_MFMA_PEAK, "unit": "TFLOP/s", "frac": round(k2_tops / FP6_MFMA_PEAK, 4),
                      "traffic": traffic, "algorithmic_bytes": gemm_bytes},
         "layer_frac_int8_peak": round(eff_tops / MFMA_PEAK, 4),
-        "kernels_us": {act_name: round(k1_ms * 1e3, 2), "asp_gemm": round(k2_ms * 1e3, 2)},
+        "kernels_us": {act_name: round(k1_ms * 1e3, 2), "asp_gemm": round(k2_ms * 1e3, 2),
+                       "asp_gemm_median": round(float(np.median(k2_all)) * 1e3, 2),
+                       "timing": f"mean of {rep_steps} event-bracketed launches after the timed region"},
+        "timing": {"method": f"{args.steps} HIP-graph replays of one step (both kernels), no events inside",
+                   "repeat_median_ms_per_step": round(med_ms, 5),
+                   "repeats": f"10 x {rep_steps} replays", "clock_settle": settle,
+                   "graph_launch_floor_us": round(floor_us, 2)},
         "quantize_act_roofline": {"bound": "hbm", "achieved": round(k1_gbs, 1), "peak": HBM_PEAK_GBS,
                                   "unit": "GB/s", "frac": round(k1_gbs / HBM_PEAK_GBS, 4),
                                   "algorithmic_bytes": act_bytes},
@@ -601,6 +751,11 @@ def main():
         "bf16_linear_us": round(bf16_ms * 1e3, 2),
         "speedup_vs_bf16_linear": round(bf16_ms / ms_step, 3),
     }
+    if peaks is not None:
+        out["measured_peaks"] = peaks
+        out["roofline"]["frac_of_measured_fp6_loop"] = round(k2_tops / peaks["mfma_TOPS"]["fp6"], 4)
+        out["layer_frac_measured_i8_loop"] = round(eff_tops / peaks["mfma_TOPS"]["i8"], 4)
+        out["quantize_act_roofline"]["frac_of_measured_copy"] = round(k1_gbs / peaks["copy_GBs"], 4)
     if args.deflated:
         out[act_name + "_roofline"] = deflated_act_roofline(k1_ms)
     if args.rotated:

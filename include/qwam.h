@@ -76,11 +76,12 @@
  * D0 | D1 << 32 | D2 << 64, whose bits 3-4 of every field are zero.  Those
  * bit positions of D0 and D1 (0x18618618 and 0x86186186) together are
  * exactly the data bits of D2, which is stored there:
- * W0 = D0 | (D2 & 0x18618618), W1 = D1 | (D2 & 0x86186186).  s = 1 exactly
- * when the scaled value x = v * fl32(1/scale) the code was rounded from is
- * negative (-0.0 included; with scale 0, x = v * 0): a zero code may carry
- * s = 1 and reads as 0.  Codes lie in [-7, 7]: with the scale absmax / 7 the
- * clamp of Eq. 2 never reaches -8.
+ * W0 = D0 | (D2 & 0x18618618), W1 = D1 | (D2 & 0x86186186).  A field holds
+ * the rounded scaled value rint(x), x = fl32(v * fl32(1/scale)), in sign and
+ * magnitude: s is the IEEE sign bit of rint(x), which is that of x (rint
+ * keeps the sign: rint(-0.3) = -0.0; with scale 0, x = v * 0).  So a zero
+ * code may carry s = 1; it reads as 0.  Codes lie in [-7, 7]: with the scale
+ * absmax / 7 the clamp of Eq. 2 never reaches -8.
  * (D0 = W0 & ~0x18618618, D1 = W1 & ~0x86186186 and
  * D2 = (W0 & 0x18618618) | (W1 & 0x86186186) give back the stream, whose
  * fields are the FP6 e2m3 values code / 8: that is how the GEMM consumes them.)
@@ -185,10 +186,15 @@ qwam_status qwam_quantize_act_deflated(const qwam_layer *L, int32_t M, const uin
 
 /*
  * The ASP GEMM (the second kernel of App. B.1): the integer partial sum of
- * every group, P[m, n, g] = sum_{k in g} qx[m, k] qw[n, k] (exact, on the FP8
- * matrix cores), scaled by xs[g][m] * ws[g][n] and accumulated over the
- * groups in float32, plus the branch t . L2 and the bias, rounded to bf16:
+ * every group, P[m, n, g] = sum_{k in g} qx[m, k] qw[n, k] (exact: the codes
+ * are FP6 e2m3 operands of the matrix cores, every product and sum an integer
+ * below 2^24), scaled by xs[g][m] * ws[g][n] and accumulated over the groups
+ * in float32, plus the branch t . L2 and the bias, rounded to bf16:
  *     y[m, n] = bf16( sum_g xs ws P + sum_j t[m, j] L2t[n, j] + bias[n] )
+ * The scale product xs * ws of a group is formed from two-piece bf16 splits
+ * of each scale (hi = bf16(s), lo = bf16(s - hi)), within about 2^-15 of the
+ * float32 product; the float32 sum runs in any order (App. B.1 allows the
+ * accumulation order to differ).
  *   L   in   packed layer
  *   xq, xs, t  in  outputs of qwam_quantize_act for the same M
  *   y   out  bf16 [M][N]

@@ -47,9 +47,11 @@ Readings taken where the paper is silent (all are listed in the design notes):
     product of two bf16 values is exact in float32, so every step is one
     correctly rounded subtraction.
   * packing: 4 bits per code, sixteen codes per 8-byte block (pack_codes);
-    the paper fixes the code range, not a byte layout.  This one lets a kernel
-    turn a block into the FP6 e2m3 fields of value code / 8 (sign, two zero
-    exponent bits, |code|) with four masks, and needs |code| <= 7, which the
+    the paper fixes the code range, not a byte layout.  Each code is stored as
+    the sign and magnitude of the rounded scaled value (negative zero keeps
+    its sign bit) in a 6-bit field with two zero bits, and the fields of a
+    block are laid out so that those zero bits hold the block's last 32
+    stream bits (format above pack_codes).  Needs |code| <= 7, which the
     quantizer guarantees.
   * the 16-bit branch is bf16: L1 = bf16(V), L2 = bf16(L1^T W~),
     R = fl32(W~ - L1 L2), t = bf16(sum_k bf16(x~_k) L1[k, j]) with an exact sum.
@@ -270,10 +272,11 @@ def quantize_groups(v: np.ndarray, group: int = GROUP, dtype=np.float32):
 
 
 def quantize_groups_signed(v: np.ndarray, group: int = GROUP, dtype=np.float32):
-    """quantize_groups, plus the sign of every scaled value x = fl(v * inv)
-    (bool [rows][K], True for a negative x, -0.0 included; with scale 0, inv
-    is 0 and x is v * 0): the sign bit the packed layout stores, which a zero
-    code keeps."""
+    """quantize_groups, plus the IEEE sign of every rounded scaled value
+    rint(x), x = fl(v * inv) (bool [rows][K]; rint keeps the sign of x, so
+    rint(-0.3) = -0.0 counts as negative; with scale 0, inv is 0 and x = v * 0).
+    The packed format stores each code as the sign and magnitude of rint(x),
+    so a zero code keeps this sign."""
     v = np.asarray(v, dtype=dtype)
     rows, K = v.shape
     assert K % group == 0
@@ -286,9 +289,10 @@ def quantize_groups_signed(v: np.ndarray, group: int = GROUP, dtype=np.float32):
     inv = np.zeros_like(scale)
     inv[~small] = dtype(1) / scale[~small]
     prod = (vg * inv[:, :, None]).astype(dtype)
-    codes = np.clip(np.rint(prod), CODE_MIN, CODE_MAX).astype(np.int8)
+    rounded = np.rint(prod)
+    codes = np.clip(rounded, CODE_MIN, CODE_MAX).astype(np.int8)
     codes[small] = 0
-    return codes.reshape(rows, K), scale, np.signbit(prod).reshape(rows, K)
+    return codes.reshape(rows, K), scale, np.signbit(rounded).reshape(rows, K)
 
 
 def dequantize_groups(codes: np.ndarray, scales: np.ndarray, group: int = GROUP) -> np.ndarray:
@@ -298,55 +302,62 @@ def dequantize_groups(codes: np.ndarray, scales: np.ndarray, group: int = GROUP)
     return (c * np.asarray(scales, dtype=np.float64)[:, :, None]).reshape(rows, K)
 
 
-# Code blocks: positions of bits 3-4 of the 6-bit fields in the first two
-# stream words; together they are exactly the data bits of the third.
-FP6_Z0 = 0x18618618
-FP6_Z1 = 0x86186186
+# Code blocks (the packed format of the codes; the paper fixes the code range,
+# not a byte layout).  Sixteen codes c_0 .. c_15 of consecutive channels form
+# one 8-byte block, two little-endian 32-bit words W0, W1.  Code j is written
+# as the 6-bit field F_j: bit 5 the sign, bits 3-4 zero, bits 0-2 the
+# magnitude |c_j|; F_j occupies bits 6j .. 6j+5 of a 96-bit stream.  Stream
+# bits 0-31 go to the same positions of W0 and bits 32-63 to those of W1.
+# Bits 64-95 (the third 32 bits, D2) go to the positions q = bit - 64 of W0
+# or W1 that the first 64 stream bits leave empty: the zero bits 3-4 of the
+# fields in W0 (mask ZERO_W0) or in W1 (mask ZERO_W1); a pin checks that these
+# free positions are exactly the positions of D2's data bits.  Only data bits
+# are stored; the zero bits are implied.
 
 
-def _fp6_stream(fields: np.ndarray) -> list:
-    """fields [..., 16] (6-bit ints) -> [D0, D1, D2], field i at bits 6i .. 6i+5
-    of the 96-bit stream D0 | D1 << 32 | D2 << 64 (uint64 arrays)."""
-    f = fields.astype(np.uint64)
-    d = [np.zeros(f.shape[:-1], dtype=np.uint64) for _ in range(3)]
-    for i in range(16):
-        bit = 6 * i
-        w, off = bit // 32, bit % 32
-        d[w] |= (f[..., i] << np.uint64(off)) & np.uint64(0xFFFFFFFF)
-        if off > 26:
-            d[w + 1] |= f[..., i] >> np.uint64(32 - off)
-    return d
+def _zero_bit_mask(word: int) -> int:
+    """Positions, within 32-bit word `word` of the stream, of bits 3-4 of the
+    fields that lie there."""
+    m = 0
+    for j in range(16):
+        for b in (3, 4):
+            p = 6 * j + b
+            if 32 * word <= p < 32 * word + 32:
+                m |= 1 << (p - 32 * word)
+    return m
 
 
-def _fp6_fields(d: list) -> np.ndarray:
-    """Inverse of _fp6_stream: [D0, D1, D2] -> fields [..., 16]."""
-    out = np.zeros(d[0].shape + (16,), dtype=np.uint64)
-    for i in range(16):
-        bit = 6 * i
-        w, off = bit // 32, bit % 32
-        v = d[w] >> np.uint64(off)
-        if off > 26:
-            v |= d[w + 1] << np.uint64(32 - off)
-        out[..., i] = v & np.uint64(63)
-    return out
+ZERO_W0 = _zero_bit_mask(0)
+ZERO_W1 = _zero_bit_mask(1)
+
+
+FIELD_DATA_BITS = (0, 1, 2, 5)    # magnitude bits 0-2 and the sign bit; bits 3-4 are zero
+
+
+def _stream_bit_home(p: int):
+    """(word, bit) where data bit p of the stream is stored."""
+    if p < 64:
+        return p // 32, p % 32
+    q = p - 64
+    if (ZERO_W0 >> q) & 1:
+        return 0, q
+    if (ZERO_W1 >> q) & 1:
+        return 1, q
+    raise AssertionError(f"stream bit {p} has no home")
 
 
 def pack_codes(codes: np.ndarray, neg: np.ndarray = None) -> np.ndarray:
-    """Packed code blocks: 4 bits per code.
+    """Packed code blocks, 4 bits per code (format above), built one field bit
+    at a time.
 
-    The codes c[16i .. 16i+15] of 16 consecutive channels of a row form block
-    i, bytes 8i .. 8i+7, read as two little-endian 32-bit words W0, W1.  Code j
-    of the block is the 6-bit field F_j = s << 5 | |c|, field j at bits
-    6j .. 6j+5 of the 96-bit stream D0 | D1 << 32 | D2 << 64; bits 3-4 of every
-    field are zero.  Those bit positions of D0 and D1 (FP6_Z0, FP6_Z1)
-    together are exactly the data bits of D2, which is stored there:
-    W0 = D0 | (D2 & FP6_Z0), W1 = D1 | (D2 & FP6_Z1).  The sign s is `neg`:
-    the sign of the scaled value the code was rounded from
-    (quantize_groups_signed), so a zero code may carry s = 1; without `neg`,
-    s = 1 exactly for a negative code.  Codes must lie in [-7, 7]: with the
-    scale absmax / 7 of Eq. 2 the code -8 is never produced.
+    codes int [rows][K] (K a multiple of 16), every code in [-7, 7] (with the
+    scale absmax / 7 of Eq. 2 the code -8 is never produced).  The sign bit of
+    a field is `neg`: True where the rounded scaled value the code stands for
+    is negative, negative zero included (quantize_groups_signed), so a zero
+    code may carry sign bit 1.  Without `neg` the sign bit is set exactly for
+    the negative codes.  Returns uint8 [rows][K/2].
     """
-    c = np.asarray(codes, dtype=np.int16)
+    c = np.asarray(codes, dtype=np.int64)
     rows, K = c.shape
     if K % 16:
         raise ValueError("the channel count must be a multiple of 16")
@@ -357,34 +368,38 @@ def pack_codes(codes: np.ndarray, neg: np.ndarray = None) -> np.ndarray:
     neg = np.asarray(neg, dtype=bool)
     if neg.shape != c.shape or (neg & (c > 0)).any() or (~neg & (c < 0)).any():
         raise ValueError("a sign bit contradicts its nonzero code")
-    fields = (np.abs(c) | (neg.astype(np.int16) << 5)).reshape(rows, K // 16, 16)
-    d0, d1, d2 = _fp6_stream(fields)
-    w = np.empty((rows, K // 16, 2), dtype=np.uint32)
-    w[..., 0] = (d0 | (d2 & np.uint64(FP6_Z0))).astype(np.uint32)
-    w[..., 1] = (d1 | (d2 & np.uint64(FP6_Z1))).astype(np.uint32)
-    return w.astype("<u4").view(np.uint8).reshape(rows, K // 2)
+    field = (np.abs(c) | (neg.astype(np.int64) << 5)).reshape(rows, K // 16, 16)
+    words = np.zeros((rows, K // 16, 2), dtype=np.uint64)
+    for j in range(16):                       # code j of every block
+        for b in FIELD_DATA_BITS:             # data bit b of its field
+            bit = ((field[:, :, j] >> b) & 1).astype(np.uint64)
+            w, q = _stream_bit_home(6 * j + b)
+            words[:, :, w] |= bit << np.uint64(q)
+    return words.astype("<u4").view(np.uint8).reshape(rows, K // 2)
 
 
-def code_block_stream(packed: np.ndarray) -> list:
-    """The stream words [D0, D1, D2] of every block of packed rows (uint64
-    arrays [rows][blocks]): D0 = W0 & ~FP6_Z0, D1 = W1 & ~FP6_Z1,
-    D2 = (W0 & FP6_Z0) | (W1 & FP6_Z1)."""
+def code_fields(packed: np.ndarray) -> np.ndarray:
+    """The 6-bit fields of packed blocks, read one stream bit at a time:
+    uint8 [rows][K] (zero bits 3-4 of every field read back as 0)."""
     p = np.ascontiguousarray(np.asarray(packed, dtype=np.uint8))
     rows, nbytes = p.shape
     if nbytes % 8:
         raise ValueError("packed rows are whole 8-byte blocks")
-    w = p.view("<u4").reshape(rows, nbytes // 8, 2).astype(np.uint64)
-    z0, z1 = np.uint64(FP6_Z0), np.uint64(FP6_Z1)
-    m32 = np.uint64(0xFFFFFFFF)
-    return [w[..., 0] & (~z0 & m32), w[..., 1] & (~z1 & m32), (w[..., 0] & z0) | (w[..., 1] & z1)]
+    words = p.view("<u4").reshape(rows, nbytes // 8, 2).astype(np.uint64)
+    field = np.zeros((rows, nbytes // 8, 16), dtype=np.uint64)
+    for j in range(16):
+        for b in FIELD_DATA_BITS:
+            w, q = _stream_bit_home(6 * j + b)
+            field[:, :, j] |= ((words[:, :, w] >> np.uint64(q)) & np.uint64(1)) << np.uint64(b)
+    return field.reshape(rows, -1).astype(np.uint8)
 
 
 def unpack_codes(packed: np.ndarray) -> np.ndarray:
-    """Inverse of pack_codes (a negative zero reads as 0)."""
-    rows = np.asarray(packed).shape[0]
-    f = _fp6_fields(code_block_stream(packed)).astype(np.int16)
+    """Inverse of pack_codes: code = (-1)^sign * magnitude (a negative zero
+    reads as 0).  int8 [rows][K]."""
+    f = code_fields(packed).astype(np.int16)
     mag, neg = f & 7, (f >> 5) & 1
-    return np.where(neg == 1, -mag, mag).astype(np.int8).reshape(rows, -1)
+    return np.where(neg == 1, -mag, mag).astype(np.int8)
 
 
 # ----------------------------------------------------------------------------

@@ -18,7 +18,8 @@ LIB = os.path.join(HERE, "libqwam.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["qwam_api.cpp", "qwam_quant.hip", "qwam_rotate.hip", "qwam_aog.hip", "qwam_gemm.hip", "qwam_gemm_small.hip", "qwam_layer_small.hip"]
+SOURCES = ["qwam_api.cpp", "qwam_quant.hip", "qwam_rotate.hip", "qwam_aog.hip", "qwam_gemm.hip", "qwam_gemm_small.hip",
+           "qwam_layer_small.hip", "qwam_probe.hip"]
 
 # Packed-FP32 VALU instructions are disabled on purpose (some of their forms
 # have produced silently wrong results on this hardware).  No fast-math: the

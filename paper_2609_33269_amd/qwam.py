@@ -7,7 +7,8 @@ library is not built, every call raises: there is no fallback.
 
 Names follow the C ABI (include/qwam.h): pack_weights, quantize_act,
 quantize_act_deflated, asp_linear, asp_layer, debug_group_partials,
-aog_accumulate.
+aog_accumulate; and the measurement probes of include/qwam_probe.h:
+probe_mfma, probe_valu_fma, probe_copy, probe_empty.
 """
 
 from __future__ import annotations
@@ -51,6 +52,11 @@ SIGNATURES = {
                                       _c_void_p]),
     "qwam_aog_accumulate": (ctypes.c_int, [_i32, _i32, _c_void_p, _c_void_p, _c_void_p]),
     "qwam_last_error": (ctypes.c_char_p, []),
+    "qwam_probe_mfma": (ctypes.c_int, [_i32, _i32, _i32, _c_void_p, _c_void_p]),
+    "qwam_probe_valu_fma": (ctypes.c_int, [_i32, _i32, _c_void_p, _c_void_p]),
+    "qwam_probe_copy": (ctypes.c_int, [_c_void_p, _c_void_p, ctypes.c_int64, _i32, _c_void_p]),
+    "qwam_probe_empty": (ctypes.c_int, [_c_void_p]),
+    "qwam_probe_last_error": (ctypes.c_char_p, []),
     "qwam_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "qwam_abi_version": (ctypes.c_int32, []),
 }
@@ -254,3 +260,48 @@ def aog_accumulate(gT: torch.Tensor, A: torch.Tensor, stream=None) -> torch.Tens
                                    _req(A, "A", torch.float32, (d, d)), _stream_ptr(stream))
     _check("qwam_aog_accumulate", st)
     return A
+
+
+# ---------------------------------------------------------------------------
+# measurement probes (include/qwam_probe.h): not part of the layer
+# ---------------------------------------------------------------------------
+
+PROBE_MFMA_KINDS = {"fp6": (0, 64, 1), "fp8": (1, 64, 1), "fp4": (2, 64, 1), "i8": (3, 32, 1),
+                    "bf16": (4, 16, 1), "bf16_2b": (5, 4, 2)}   # name -> (kind, K, blocks per instruction)
+
+
+def _probe_check(fn: str, status: int) -> None:
+    if status != 0:
+        raise QwamError(fn, status, lib().qwam_probe_last_error().decode())
+
+
+def probe_mfma(kind: str, workgroups: int, iters: int, out: torch.Tensor, stream=None) -> float:
+    """qwam_probe_mfma; returns the operations the launch performs."""
+    code, k, blocks = PROBE_MFMA_KINDS[kind]
+    _req(out, "out", torch.float32, (workgroups * 256,))
+    _probe_check("qwam_probe_mfma", lib().qwam_probe_mfma(code, workgroups, iters, out.data_ptr(),
+                                                          _stream_ptr(stream)))
+    return float(workgroups) * 4 * 4 * iters * 2 * 32 * 32 * k * blocks
+
+
+def probe_valu_fma(workgroups: int, iters: int, out: torch.Tensor, stream=None) -> float:
+    """qwam_probe_valu_fma; returns the flops the launch performs."""
+    _req(out, "out", torch.float32, (workgroups * 256,))
+    _probe_check("qwam_probe_valu_fma", lib().qwam_probe_valu_fma(workgroups, iters, out.data_ptr(),
+                                                                  _stream_ptr(stream)))
+    return float(workgroups) * 256 * 256 * iters * 2
+
+
+def probe_copy(src: torch.Tensor, dst: torch.Tensor, workgroups: int = 4096, stream=None) -> int:
+    """qwam_probe_copy of all of src into dst (same size); returns the HBM bytes moved."""
+    nbytes = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() != nbytes or not (src.is_cuda and dst.is_cuda):
+        raise ValueError("probe_copy: src and dst must be GPU tensors of the same size")
+    _probe_check("qwam_probe_copy", lib().qwam_probe_copy(src.data_ptr(), dst.data_ptr(), nbytes, workgroups,
+                                                          _stream_ptr(stream)))
+    return 2 * nbytes
+
+
+def probe_empty(stream=None) -> None:
+    """qwam_probe_empty: one empty launch."""
+    _probe_check("qwam_probe_empty", lib().qwam_probe_empty(_stream_ptr(stream)))

@@ -13,7 +13,7 @@ import torch
 from paper_2609_33269_amd import qwam as Q
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "qwam.h")
+HEADERS = [os.path.join(ROOT, "include", h) for h in ("qwam.h", "qwam_probe.h")]
 
 OK, INVALID, UNSUPPORTED, MISALIGNED, NO_DEVICE = 0, 1, 2, 3, 4
 FAKE = 0x10000          # 16-byte aligned, never dereferenced
@@ -28,9 +28,11 @@ def lib():
 
 
 def _declared_functions():
-    src = open(HEADER).read()
-    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(qwam_[a-z_]+)\s*\(", src)))
+    names = set()
+    for h in HEADERS:
+        src = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names |= set(re.findall(r"\b(qwam_[a-z_]+)\s*\(", src))
+    return sorted(names)
 
 
 def test_exports_every_declared_symbol(lib):
@@ -40,6 +42,19 @@ def test_exports_every_declared_symbol(lib):
         assert hasattr(lib, n), n
     assert lib.qwam_abi_version() == 9
     assert lib.qwam_status_string(3) == b"QWAM_ERR_MISALIGNED"
+
+
+def test_probe_argument_checks(lib):
+    """The measurement probes reject bad arguments on the host."""
+    assert lib.qwam_probe_mfma(99, 4, 4, FAKE, None) == INVALID
+    assert lib.qwam_probe_mfma(0, 0, 4, FAKE, None) == INVALID
+    assert lib.qwam_probe_mfma(0, 4, 4, None, None) == INVALID
+    assert lib.qwam_probe_valu_fma(4, 0, FAKE, None) == INVALID
+    assert lib.qwam_probe_copy(FAKE, FAKE, 24, 4, None) == INVALID
+    assert lib.qwam_probe_copy(FAKE + 8, FAKE, 32, 4, None) == MISALIGNED
+    assert lib.qwam_probe_copy(None, FAKE, 32, 4, None) == INVALID
+    assert b"workgroups" in lib.qwam_probe_last_error() or b"bytes" in lib.qwam_probe_last_error() \
+        or b"NULL" in lib.qwam_probe_last_error()
 
 
 def _layer(K=256, N=256, r=16, group=64, hadamard=0, **ptrs):

@@ -166,7 +166,7 @@ def test_pack_zero_bits_hold_the_third_word():
     z0 = sum(1 << p for p in zero_pos if p < 32)
     z1 = sum(1 << (p - 32) for p in zero_pos if 32 <= p < 64)
     data2 = sum(1 << (p - 64) for p in range(64, 96) if p not in zero_pos)
-    assert (z0, z1) == (O.FP6_Z0, O.FP6_Z1)
+    assert (z0, z1) == (O.ZERO_W0, O.ZERO_W1) == (0x18618618, 0x86186186)   # the masks qwam.h states
     assert z0 & z1 == 0 and z0 | z1 == data2
 
 
@@ -195,8 +195,8 @@ def test_pack_every_block_decodes_in_range():
     # negative zero differs from its canonical form only in sign bits
     sign_pos = [6 * i + 5 for i in range(16)]
     d_sign = [sum(1 << (p - 32 * k) for p in sign_pos if 32 * k <= p < 32 * k + 32) for k in range(3)]
-    sign0 = d_sign[0] | (d_sign[2] & O.FP6_Z0)
-    sign1 = d_sign[1] | (d_sign[2] & O.FP6_Z1)
+    sign0 = d_sign[0] | (d_sign[2] & O.ZERO_W0)
+    sign1 = d_sign[1] | (d_sign[2] & O.ZERO_W1)
     a = again.view("<u4").reshape(-1, 2)
     b = packed.view("<u4").reshape(-1, 2)
     same = (a == b).all(axis=1)
@@ -258,12 +258,26 @@ def test_packed_blocks_are_fp6_codes():
         fields = _block_fields(packed[8 * blk: 8 * blk + 8])
         for j in range(16):
             assert _e2m3_value(fields[j]) == codes[0, 16 * blk + j] / 8
-    # and the oracle's own stream words agree with the bit-by-bit reading
-    d = O.code_block_stream(O.pack_codes(codes))
+    # and the oracle's own field reader agrees with the mask-based reading
+    f = O.code_fields(O.pack_codes(codes))
     for blk in range(4):
-        fields = _block_fields(packed[8 * blk: 8 * blk + 8])
-        stream = int(d[0][0, blk]) | (int(d[1][0, blk]) << 32) | (int(d[2][0, blk]) << 64)
-        assert [(stream >> (6 * i)) & 63 for i in range(16)] == fields
+        assert f[0, 16 * blk:16 * blk + 16].tolist() == _block_fields(packed[8 * blk: 8 * blk + 8])
+
+
+def test_pack_against_mask_reading_random():
+    """pack_codes (one field bit at a time) against the independent reading of
+    the format by masks (_block_fields), with signed zeros, on random blocks."""
+    rng = np.random.default_rng(17)
+    codes = rng.integers(-7, 8, size=(6, 160)).astype(np.int8)
+    neg = (codes < 0) | ((codes == 0) & (rng.random(codes.shape) < 0.5))
+    packed = O.pack_codes(codes, neg)
+    for row in range(codes.shape[0]):
+        raw = packed[row].tobytes()
+        for blk in range(codes.shape[1] // 16):
+            fields = _block_fields(raw[8 * blk: 8 * blk + 8])
+            for j in range(16):
+                k = 16 * blk + j
+                assert fields[j] == (int(neg[row, k]) << 5) | abs(int(codes[row, k]))
 
 
 # --------------------------------------------------------------------------
@@ -847,3 +861,119 @@ def test_group32_error_not_larger_on_outlier_inputs():
         e[g] = np.linalg.norm(y - xw) / np.linalg.norm(xw)
     assert e[32] <= e[64]
     assert np.isfinite(ref).all()
+
+
+
+# --------------------------------------------------------------------------
+# the offline rotation against the online one, smoothing rounding, calibration
+# --------------------------------------------------------------------------
+
+def _hadamard_pins():
+    """The checks that tie the offline rotation (weights) to the online one
+    (activations); returns normally only if all hold."""
+    import scipy.linalg
+    for B in (1, 2, 4, 8, 16, 32, 64, 128, 256, 512, 1024):
+        assert (O.sylvester_hadamard(B) == scipy.linalg.hadamard(B)).all(), B
+    for B in (16, 32, 64, 128, 256, 512, 1024):
+        eye = np.eye(B, dtype=np.float32)
+        online = O.fwht_f32(eye, B).astype(np.float64) * np.float64(O.hadamard_scale(B))
+        offline = O.rotate_exact(eye, B)
+        # e_k through both: equal up to the float32 rounding of 1/sqrt(B)
+        # (exactly equal when B is a power of 4)
+        tol = 0.0 if B in (16, 64, 256, 1024) else 2.0 ** -24 / np.sqrt(B)
+        assert np.abs(online - offline).max() <= tol, B
+
+
+def test_offline_hadamard_matches_scipy_and_the_fwht():
+    """sylvester_hadamard is scipy's Hadamard matrix (Sylvester order), and
+    rotate_exact sends every unit vector where the float32 FWHT times
+    fl32(1/sqrt(B)) sends it (App. B.1: the weights are rotated offline, the
+    activations online; both must use the same H)."""
+    _hadamard_pins()
+
+
+def test_planted_row_swap_in_the_offline_hadamard_is_caught(monkeypatch):
+    """Plant a mistake in the oracle (two rows of the offline Hadamard matrix
+    swapped): the pins above must fail, and so must the deployed rotated
+    layer's closeness to x W."""
+    good = O.sylvester_hadamard
+
+    def swapped(B):
+        H = good(B).copy()
+        if B >= 4:
+            H[[1, 2]] = H[[2, 1]]
+        return H
+
+    monkeypatch.setattr(O, "sylvester_hadamard", swapped)
+    with pytest.raises(AssertionError):
+        _hadamard_pins()
+    with pytest.raises(AssertionError):
+        _rotated_layer_close()
+
+
+def _rotated_layer_close():
+    """Deployed rotated layer (App. B.1: smoothing, block Hadamard, bf16
+    branch, 4-bit residual) on a rank-r weight: close to x W."""
+    M, K, N, r = 16, 512, 64, 16
+    x, w = _low_rank_layer(M, K, N, r, 24)
+    xb, wb = O.f64_to_bf16_bits(x), O.f64_to_bf16_bits(w)
+    xf, wf = O.bf16_bits_to_f64(xb), O.bf16_bits_to_f64(wb)
+    lam = O.smoothing_factors(xf, wf).astype(np.float64)
+    wt = O.rotate_exact(wf * lam[None, :], O.hadamard_block(K))
+    V, _ = O.protected_basis_eigh(wt.T @ wt + O.RIDGE * np.eye(K), r)
+    L = O.build_layer(xb, wb, V, hadamard=True)
+    assert L["hadamard"] == 512
+    y = O.asp_linear(xb, L)["y"]
+    ref = xf @ wf.T
+    assert np.linalg.norm(y - ref) / np.linalg.norm(ref) < 2e-2
+
+
+def test_rotated_deployed_layer_is_close():
+    _rotated_layer_close()
+
+
+def test_smoothing_rounding_hand_values():
+    """fl32(1/lambda) and x~ = fl32(x * fl32(1/lambda)), hand-derived:
+    fl32(1/3) = 0x3EAAAAAB (1/3 = 0.0101..b, rounded up) and
+    fl32(1/10) = 0x3DCCCCCD; 5 * fl32(1/3) = 1.66666671633..., between
+    0x3FD55555 (1.66666662693) and 0x3FD55556 (1.66666674614), nearer the
+    latter, whereas the divide 5 / 3 rounds to 0x3FD55555: the multiply by the
+    packed reciprocal is the reading taken.  3 * fl32(1/3) = 1 + 2^-25 + ...
+    rounds to 1.0."""
+    inv = O.inverse_smoothing(np.array([3.0, 10.0, 1.0], np.float32))
+    assert inv.view(np.uint32).tolist() == [0x3EAAAAAB, 0x3DCCCCCD, 0x3F800000]
+    xb = np.array([[0x40A0, 0x4040, 0x3F80]], np.uint16)         # bf16 5, 3, 1
+    xt = O.smooth_activations(xb, np.array([inv[0]] * 3, np.float32))
+    assert xt.view(np.uint32).tolist() == [[0x3FD55556, 0x3F800000, 0x3EAAAAAB]]
+    assert np.float32(np.float32(5.0) / np.float32(3.0)).view(np.uint32) == 0x3FD55555
+
+
+def test_calibration_module_matches_the_oracle_on_the_tiny_layer():
+    """The torch calibration the benchmark uses (calib.build_layer) gives the
+    oracle's factors on the tiny layer: lambda, L1, L2 and R bit for bit (or
+    within float64 summation order where a sum is rounded), plain and rotated."""
+    from paper_2609_33269_amd import calib
+    d = I.tiny()
+    V = O.protected_basis_from_factor(d.a, d.shape.r)
+    Vt = calib.protected_basis(torch.from_numpy(d.a), d.shape.r)
+    assert np.allclose(Vt.numpy(), V, rtol=0, atol=1e-12)
+
+    def bf(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16)
+
+    for rot in (False, True):
+        ref = O.build_layer(d.x, d.w, V, hadamard=rot)
+        got = calib.build_layer(bf(d.x), bf(d.w), torch.from_numpy(V), hadamard=rot)
+        assert got["hadamard"] == ref["hadamard"]
+        assert (got["lam"].numpy() == ref["lam"]).all()
+        assert (got["L1"].view(torch.int16).numpy().view(np.uint16) == ref["L1"]).all()
+        l2 = got["L2"].view(torch.int16).numpy().view(np.uint16)
+        # L2 = bf16 of a float64 sum: equal except where the two summation
+        # orders straddle a bf16 rounding boundary (then one bf16 ulp apart)
+        diff = np.abs(O.bf16_bits_to_f64(l2) - O.bf16_bits_to_f64(ref["L2"]))
+        ulp = np.abs(O.bf16_bits_to_f64(ref["L2"])) * 2.0 ** -7
+        assert (diff <= ulp).all() and (l2 == ref["L2"]).mean() > 0.999
+        same = (l2 == ref["L2"]).all(axis=0)                     # columns with identical L2
+        R = got["R"].numpy()
+        assert (R[same] == ref["R"][same]).mean() > 0.999
+        assert np.allclose(R, ref["R"], rtol=0, atol=1e-6 * np.abs(ref["R"]).max())
