@@ -196,9 +196,21 @@ def rotate_exact(v: np.ndarray, B: int) -> np.ndarray:
     return (v.reshape(rows, K // B, B) @ H).reshape(rows, K)
 
 
-def build_layer(x_bits: np.ndarray, w_bits: np.ndarray, V: np.ndarray, hadamard: bool = False):
+def rotation_block(K: int, hadamard) -> int:
+    """Block size of the rotation: 0 for none (False / 0), App. B.1's block for
+    True, or the given power of two (which must divide K)."""
+    if hadamard is True:
+        return hadamard_block(K)
+    B = int(hadamard)
+    if B and (B & (B - 1) or K % B):
+        raise ValueError("the rotation block must be a power of two dividing K")
+    return B
+
+
+def build_layer(x_bits: np.ndarray, w_bits: np.ndarray, V: np.ndarray, hadamard=False):
     """Deployed ASP factors of one layer from bf16 x [M][K], bf16 w [N][K] and
-    a protected basis V [K][r] (float64, orthonormal columns).
+    a protected basis V [K][r] (float64, orthonormal columns).  `hadamard`:
+    False, True (the block of App. B.1) or a block size B.
 
     Steps (Sec. 3 Eq. 3, Sec. 4.2 Eq. 9, App. B.1):
       lambda = smoothing factors (float32)
@@ -217,7 +229,7 @@ def build_layer(x_bits: np.ndarray, w_bits: np.ndarray, V: np.ndarray, hadamard:
     w = bf16_bits_to_f64(w_bits)
     lam = smoothing_factors(x, w)
     wt = w * lam.astype(np.float64)[None, :]                  # [N][K]
-    B = hadamard_block(wt.shape[1]) if hadamard else 0
+    B = rotation_block(wt.shape[1], hadamard)
     if B:
         wt = rotate_exact(wt, B)
     L1 = f64_to_bf16_bits(V)                                  # [K][r]

@@ -112,3 +112,78 @@ def run_gpu(layer: Q.PackedLayer, x_bits: np.ndarray, deflate: bool = False):
     y = Q.asp_linear(layer, xq, xs, t)
     torch.cuda.synchronize()
     return x, xq, xs, t, y
+
+
+def y_abs_terms(sx, sw, P, t_bits, L2_bits, bias_bits=None) -> np.ndarray:
+    """sum_g |sx sw P| + sum_j |t_j L2[j, n]| (+ |bias|) per output: the scale
+    of the float32 error of y (float64)."""
+    a = np.einsum("mg,ng,mng->mn", np.abs(np.asarray(sx, np.float64)), np.abs(np.asarray(sw, np.float64)),
+                  np.abs(P).astype(np.float64))
+    a += np.abs(O.bf16_bits_to_f64(t_bits)) @ np.abs(O.bf16_bits_to_f64(L2_bits))
+    if bias_bits is not None:
+        a += np.abs(O.bf16_bits_to_f64(bias_bits))[None, :]
+    return a
+
+
+def check_y_elements(y_gpu_bits, y_ref, abs_terms, n_groups, rank, min_identical=0.99):
+    """Element by element: bf16(y_gpu) against the correctly rounded bf16 of the
+    float64 oracle.  Every element within one bf16 ulp plus the float32 error
+    bound of the kernel's arithmetic: each group's scale product is formed from
+    two-piece bf16 splits of the two scales (within 2^-15 of sx * sw), and the
+    G + r + 1 float32 roundings of the accumulation each add at most 2^-24 of
+    the terms' magnitude.  And at least `min_identical` of the elements equal
+    to bf16(y_ref): the error bound is far below a bf16 ulp, so y only differs
+    where y_ref lies next to a rounding boundary."""
+    yg = O.bf16_bits_to_f64(y_gpu_bits)
+    yr = O.round_to_bf16(y_ref)
+    ulp = np.maximum(bf16_ulp(yr), bf16_ulp(yg))
+    bound = ulp + (2.0 ** -15 + (n_groups + rank + 2) * U32) * abs_terms
+    diff = np.abs(yg - yr)
+    bad = np.argwhere(diff > bound)
+    assert bad.size == 0, f"y outside one ulp + float32 bound at {bad[:5].tolist()}"
+    same = float(np.mean(yg == yr))
+    log(f"    y elements equal to bf16(y_ref): {same:.5f}")
+    assert same >= min_identical, f"only {same:.4f} of y elements equal bf16(y_ref)"
+    return same
+
+
+def check_y_per_token(y_gpu_bits, y_ref):
+    """Relative Frobenius error of every token's output row within the tolerance."""
+    yg = O.bf16_bits_to_f64(y_gpu_bits)
+    errs = [rel_fro(yg[i], y_ref[i]) for i in range(y_ref.shape[0])]
+    tols = [y_tolerance(y_ref[i]) for i in range(y_ref.shape[0])]
+    worst = int(np.argmax(np.array(errs) / np.array(tols)))
+    log(f"    worst token error {errs[worst]:.3e} (tolerance {tols[worst]:.3e})")
+    assert all(e <= t for e, t in zip(errs, tols)), "a token's output exceeds the tolerance"
+
+
+def sample_rows(M: int, seed: int, extra: int = 64) -> np.ndarray:
+    """Token sample of a large layer: the first and last token, one token in
+    every 128-token tile and `extra` more at random; more than 64 tokens for
+    M >= 128, so that the debug partials run on the large-tile GEMM."""
+    rng = np.random.default_rng(seed)
+    rows = {0, M - 1}
+    for tile in range(0, M, 128):
+        rows.add(int(min(M - 1, tile + rng.integers(0, 128))))
+    rows.update(int(v) for v in rng.choice(M, size=min(M, extra), replace=False))
+    return np.array(sorted(rows))
+
+
+def check_sampled_rows(layer, xq, y, xq_ref, sx_ref, t_ref, wq, sw, L2_bits, rows, bias_bits=None):
+    """y and the int32 group partials of sampled tokens of a large layer against
+    the oracle computed from the same codes: Frobenius error over the sample,
+    every token's own error, every element (check_y_elements), and the
+    partials bit for bit through the debug entry point on the sampled rows."""
+    y_ref, P_ref = O.asp_output_rows(xq_ref[rows], sx_ref[rows], t_ref[rows], wq, sw, L2_bits, bias_bits)
+    sel = torch.from_numpy(rows).cuda()
+    yb = bits(y[sel])
+    err = rel_fro(O.bf16_bits_to_f64(yb), y_ref)
+    log(f"    y rel Frobenius error on {len(rows)} sampled tokens {err:.3e}")
+    assert err <= y_tolerance(y_ref)
+    check_y_per_token(yb, y_ref)
+    check_y_elements(yb, y_ref, y_abs_terms(sx_ref[rows], sw, P_ref, t_ref[rows], L2_bits, bias_bits),
+                     P_ref.shape[2], np.asarray(L2_bits).shape[0])
+    P = Q.debug_group_partials(layer, xq[sel].contiguous())
+    torch.cuda.synchronize()
+    assert (P.cpu().numpy() == P_ref).all(), "int32 group partials of sampled tokens"
+    del P

@@ -15,8 +15,8 @@ from oracle import qwam_oracle as O
 from paper_2609_33269_amd import inputs as I
 from paper_2609_33269_amd import qwam as Q
 
-from parity_helpers import (bf16_dev, bits, check_y, f32_dev, gpu_layer, log, oracle_factors, rel_fro,
-                            run_gpu, y_tolerance)
+from parity_helpers import (bf16_dev, bits, check_sampled_rows, check_y, f32_dev, gpu_layer, log, oracle_factors,
+                            rel_fro, run_gpu, sample_rows, y_tolerance)
 
 pytestmark = pytest.mark.gpu
 
@@ -114,13 +114,6 @@ def test_deflation_on_coordinate_axes():
     assert (xs.cpu().numpy() == scales.T).all()
 
 
-def _sample_rows(M, n, seed):
-    rng = np.random.default_rng(seed)
-    rows = set([0, M - 1])
-    rows.update(int(v) for v in rng.choice(M, size=min(M, n), replace=False))
-    return np.array(sorted(rows))
-
-
 @pytest.mark.parametrize("which", ["video_dit_ffn_up", "video_dit_ffn_down"])
 def test_deflated_full_size(which):
     """Full-size layer, launch configuration of the benchmark: every t element,
@@ -129,28 +122,22 @@ def test_deflated_full_size(which):
     M, K, N = draws.shape.M, draws.shape.K, draws.shape.N
     log(f"  deflated full size {draws.shape.name}: M={M} K={K} N={N}")
     f = oracle_factors(draws)
-    wq, sw, inv_lam, _ = O.pack_weights(f["R"], f["lam"])
+    _, sw = O.quantize_groups(f["R"])
+    inv_lam = O.inverse_smoothing(f["lam"])
     layer = gpu_layer(f)
+    wq = layer.wq.cpu().numpy()
     x, xq, xs, t, y = run_gpu(layer, draws.x, deflate=True)
     xq_ref, sx_ref, t_ref, _, _ = O.quantize_activations_deflated(draws.x, inv_lam, f["L1"])
     assert (bits(t) == t_ref).all(), "t"
     assert (xq.cpu().numpy() == xq_ref).all(), "packed deflated activation bytes"
     assert (xs.cpu().numpy() == sx_ref.T).all(), "deflated activation scales"
-    rows = _sample_rows(M, 16, seed=M + N + 1)
-    y_ref, P_ref = O.asp_output_rows(xq_ref[rows], sx_ref[rows], t_ref[rows], wq, sw, f["L2"])
-    sel = torch.from_numpy(rows).cuda()
-    err = rel_fro(O.bf16_bits_to_f64(bits(y[sel])), y_ref)
-    log(f"    y rel Frobenius error on {len(rows)} sampled tokens {err:.3e}")
-    assert err <= y_tolerance(y_ref)
-    P = Q.debug_group_partials(layer, xq[sel].contiguous())
-    torch.cuda.synchronize()
-    assert (P.cpu().numpy() == P_ref).all(), "int32 group partials of sampled tokens"
+    check_sampled_rows(layer, xq, y, xq_ref, sx_ref, t_ref, wq, sw, f["L2"], sample_rows(M, seed=M + N + 1))
     # the deflated scales are smaller than the plain ones on the same tokens
     _, xs_plain, _ = Q.quantize_act(layer, x)
     ratio = float(xs.float().mean() / xs_plain.float().mean())
     log(f"    mean activation scale deflated / plain = {ratio:.3f}")
     assert ratio <= 1.0
-    del x, xq, xs, t, y, P, layer, xs_plain
+    del x, xq, xs, t, y, layer, xs_plain
     torch.cuda.empty_cache()
 
 

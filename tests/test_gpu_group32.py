@@ -17,7 +17,8 @@ from oracle import qwam_oracle as O
 from paper_2609_33269_amd import inputs as I
 from paper_2609_33269_amd import qwam as Q
 
-from parity_helpers import bits, check_t, check_y, gpu_layer, log, oracle_factors, rel_fro, run_gpu, y_tolerance
+from parity_helpers import (bits, check_sampled_rows, check_t, check_y, gpu_layer, log, oracle_factors, rel_fro,
+                            run_gpu, sample_rows, y_tolerance)
 
 pytestmark = pytest.mark.gpu
 
@@ -95,15 +96,6 @@ def test_group32_full_size_sampled():
     assert (bits(t) == t_ref).all(), "t"
     assert (xq.cpu().numpy() == xq_ref).all(), "packed activation bytes"
     assert (xs.cpu().numpy() == sx_ref.T).all(), "activation scales"
-    rng = np.random.default_rng(M + 32)
-    rows = np.array(sorted(set([0, M - 1]) | set(int(v) for v in rng.choice(M, 12, replace=False))))
-    y_ref, P_ref = O.asp_output_rows(xq_ref[rows], sx_ref[rows], t_ref[rows], wq, sw, f["L2"])
-    sel = torch.from_numpy(rows).cuda()
-    err = rel_fro(O.bf16_bits_to_f64(bits(y[sel])), y_ref)
-    log(f"    y rel Frobenius error on {len(rows)} sampled tokens {err:.3e}")
-    assert err <= y_tolerance(y_ref)
-    P = Q.debug_group_partials(layer, xq[sel].contiguous())
-    torch.cuda.synchronize()
-    assert (P.cpu().numpy() == P_ref).all(), "int32 group partials of sampled tokens"
-    del x, xq, xs, t, y, P, layer
+    check_sampled_rows(layer, xq, y, xq_ref, sx_ref, t_ref, wq, sw, f["L2"], sample_rows(M, seed=M + 32))
+    del x, xq, xs, t, y, layer
     torch.cuda.empty_cache()

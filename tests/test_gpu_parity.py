@@ -14,8 +14,8 @@ from oracle import qwam_oracle as O
 from paper_2609_33269_amd import inputs as I
 from paper_2609_33269_amd import qwam as Q
 
-from parity_helpers import (bf16_dev, bits, check_t, check_y, f32_dev, gpu_layer, log, oracle_factors,
-                            rel_fro, run_gpu, y_tolerance)
+from parity_helpers import (bf16_dev, bits, check_sampled_rows, check_t, check_y, check_y_elements,
+                            check_y_per_token, gpu_layer, log, oracle_factors, run_gpu, sample_rows, y_abs_terms)
 
 pytestmark = pytest.mark.gpu
 
@@ -46,6 +46,9 @@ def _full_parity(draws, factors, bias_bits=None, check_partials=True):
         P = Q.debug_group_partials(layer, xq)
         torch.cuda.synchronize()
         assert (P.cpu().numpy() == ref["P"]).all(), "int32 group partials"
+    check_y_per_token(bits(y), ref["y"])
+    check_y_elements(bits(y), ref["y"], y_abs_terms(ref["sx"], ref["sw"], ref["P"], ref["t"], factors["L2"], bias_bits),
+                     ref["P"].shape[2], factors["L1"].shape[1])
     return check_y(bits(y), ref["y"])
 
 
@@ -108,43 +111,33 @@ def test_degenerate_activations():
     assert not xq[1, 32:64].any().item() and xs[1, 1].item() == 0.0
 
 
-def _sample_rows(M, n, seed):
-    rng = np.random.default_rng(seed)
-    rows = set([0, M - 1])
-    for tile in range(0, M, 128):                  # at least one row per M tile
-        rows.add(int(min(M - 1, tile + rng.integers(0, 128))))
-    extra = rng.choice(M, size=min(M, n), replace=False)
-    rows.update(int(v) for v in extra)
-    return np.array(sorted(rows))
-
-
-def _large_parity(draws, n_rows=24):
+def _large_parity(draws, extra_rows=64):
     """Full-size layer in the benchmark's launch configuration: every code,
-    scale and t element is checked; partials and y on sampled tokens."""
+    scale and t element is checked; y (whole sample, every token, every
+    element) and the partials on sampled tokens (more than 64, so the
+    partials come from the large-tile GEMM)."""
     M, K, N = draws.shape.M, draws.shape.K, draws.shape.N
     log(f"  large parity {draws.shape.name}: M={M} K={K} N={N} r={draws.shape.r}")
     f = oracle_factors(draws)
-    wq, sw, inv_lam, qw = O.pack_weights(f["R"], f["lam"])
+    qw, sw = O.quantize_groups(f["R"])
+    inv_lam = O.inverse_smoothing(f["lam"])
     layer = gpu_layer(f)
     x, xq, xs, t, y = run_gpu(layer, draws.x)
-    assert (layer.wq.cpu().numpy() == wq).all(), "packed weight bytes"
+    wq = layer.wq.cpu().numpy()
+    assert (O.unpack_codes(wq) == qw).all(), "weight codes"
     assert (layer.ws.cpu().numpy() == sw.T).all(), "weight scales"
     assert (layer.inv_smooth.cpu().numpy() == inv_lam).all()
     xq_ref, sx_ref, t_ref, qx, xt = O.quantize_activations(draws.x, inv_lam, f["L1"])
     assert (xq.cpu().numpy() == xq_ref).all(), "packed activation bytes"
     assert (xs.cpu().numpy() == sx_ref.T).all(), "activation scales"
     check_t(bits(t), t_ref, xt, f["L1"])
-    rows = _sample_rows(M, n_rows, seed=M + N)
-    y_ref, P_ref = O.asp_output_rows(xq_ref[rows], sx_ref[rows], t_ref[rows], wq, sw, f["L2"])
-    yg = O.bf16_bits_to_f64(bits(y[torch.from_numpy(rows).cuda()]))
-    err = rel_fro(yg, y_ref)
-    row_err = max(rel_fro(yg[i], y_ref[i]) for i in range(len(rows)))
-    log(f"    y rel Frobenius error on {len(rows)} sampled tokens {err:.3e} (worst token {row_err:.3e})")
-    assert err <= y_tolerance(y_ref)
-    P = Q.debug_group_partials(layer, xq[torch.from_numpy(rows).cuda()].contiguous())
-    torch.cuda.synchronize()
-    assert (P.cpu().numpy() == P_ref).all(), "int32 group partials of sampled tokens"
-    del x, xq, xs, t, y, P, layer
+    # the packed weight bytes of a sample of rows (the full pack is checked on smaller layers)
+    wrows = sample_rows(N, seed=N + 3, extra=32)
+    assert (wq[wrows] == O.pack_codes(qw[wrows], O.quantize_groups_signed(f["R"][wrows])[2])).all(), \
+        "packed weight bytes"
+    rows = sample_rows(M, seed=M + N, extra=extra_rows)
+    check_sampled_rows(layer, xq, y, xq_ref, sx_ref, t_ref, wq, sw, f["L2"], rows)
+    del x, xq, xs, t, y, layer
     torch.cuda.empty_cache()
 
 
@@ -161,24 +154,46 @@ def test_action_expert_layers(M, N):
 
 @pytest.mark.parametrize("block,which", [(0, 0), (13, 1), (29, 3)])
 def test_denoise_step_sampled_layers(block, which):
-    _large_parity(I.denoise_step_layer(block, which), n_rows=16)
+    _large_parity(I.denoise_step_layer(block, which), extra_rows=32)
 
 
 def test_repeat_runs_bit_identical():
+    """Determinism / race proxy: 20 runs of every kernel of the layer (the
+    large-tile GEMM, its debug partials, the few-token GEMM and the fused
+    layer) on four streams, in varied launch orders and with the outputs of
+    several runs in flight at once, give bit-identical codes, scales, t,
+    partials and y."""
     d = I.custom(M=300, K=512, N=384, r=32, seed=9, n_outliers=5, with_bias=True)
-    f = oracle_factors(d)
-    layer = gpu_layer(f, d.bias)
-    outs = []
-    streams = [torch.cuda.Stream() for _ in range(2)]
-    for i in range(6):
-        s = streams[i % 2]
+    small = I.custom(M=48, K=1024, N=512, r=16, seed=10, n_outliers=4, with_bias=True)
+    layer = gpu_layer(oracle_factors(d), d.bias)
+    layer_s = gpu_layer(oracle_factors(small), small.bias)
+    x, xsm = bf16_dev(d.x), bf16_dev(small.x)
+    streams = [torch.cuda.Stream() for _ in range(4)]
+    rng = np.random.default_rng(99)
+    pending, outs = [], []
+    for i in range(20):
+        s = streams[int(rng.integers(0, 4))]
+        s.wait_stream(torch.cuda.current_stream())
+        order = rng.permutation(3)
+        res = {}
         with torch.cuda.stream(s):
-            x = bf16_dev(d.x)
-            xq, xs, t = Q.quantize_act(layer, x)
-            y = Q.asp_linear(layer, xq, xs, t)
-            P = Q.debug_group_partials(layer, xq)
-        torch.cuda.synchronize()
-        outs.append((xq.cpu().numpy(), xs.cpu().numpy(), bits(t), bits(y), P.cpu().numpy()))
+            for step in order:
+                if step == 0:
+                    xq, xs, t = Q.quantize_act(layer, x)
+                    res["big"] = (xq, xs, t, Q.asp_linear(layer, xq, xs, t), Q.debug_group_partials(layer, xq))
+                elif step == 1:
+                    q2, s2, t2 = Q.quantize_act(layer_s, xsm)
+                    res["small"] = (q2, s2, t2, Q.asp_linear(layer_s, q2, s2, t2))
+                else:
+                    res["fused"] = (Q.asp_layer(layer_s, xsm),)
+        pending.append(res)
+        if i % 5 == 4:                 # several runs in flight before each drain
+            torch.cuda.synchronize()
+            for r in pending:
+                outs.append({k: [v.cpu().numpy() if v.dtype != torch.bfloat16 else bits(v) for v in vals]
+                             for k, vals in r.items()})
+            pending = []
     for o in outs[1:]:
-        for a, b in zip(o, outs[0]):
-            assert (a == b).all()
+        for k in o:
+            for a, b in zip(o[k], outs[0][k]):
+                assert (a == b).all(), k

@@ -17,8 +17,8 @@ from oracle import qwam_oracle as O
 from paper_2609_33269_amd import inputs as I
 from paper_2609_33269_amd import qwam as Q
 
-from parity_helpers import (bf16_dev, bits, check_t, check_y, gpu_layer, log, oracle_factors, rel_fro,
-                            run_gpu, y_tolerance)
+from parity_helpers import (bf16_dev, bits, check_sampled_rows, check_t, check_y, gpu_layer, log, oracle_factors,
+                            run_gpu, sample_rows)
 
 pytestmark = pytest.mark.gpu
 
@@ -68,12 +68,29 @@ ROTATED_SHAPES = [
     (20, 16448, 32, 64, False),  # B 64, T 64, 257 tiles
 ]
 
+# block sizes below App. B.1's choice, which the ABI also accepts: the first
+# butterfly stages stay inside a lane, or end at the lane-pair exchange
+SMALL_BLOCK_SHAPES = [
+    # M, K, N, r, bias, B
+    (5, 64, 32, 16, False, 16),
+    (19, 256, 48, 32, True, 32),
+    (70, 1024, 80, 16, False, 16),
+    (33, 3072, 64, 32, True, 32),
+]
+
 
 @pytest.mark.parametrize("deflate", [False, True])
 @pytest.mark.parametrize("M,K,N,r,bias", ROTATED_SHAPES)
 def test_rotated_shapes(M, K, N, r, bias, deflate):
     d = I.custom(M=M, K=K, N=N, r=r, seed=M * 13 + K, n_outliers=max(1, K // 100), with_bias=bias)
     _rotated_parity(d, oracle_factors(d, r, hadamard=True), d.bias, deflate=deflate)
+
+
+@pytest.mark.parametrize("deflate", [False, True])
+@pytest.mark.parametrize("M,K,N,r,bias,B", SMALL_BLOCK_SHAPES)
+def test_rotated_small_blocks(M, K, N, r, bias, B, deflate):
+    d = I.custom(M=M, K=K, N=N, r=r, seed=M * 17 + K + B, n_outliers=max(1, K // 100), with_bias=bias)
+    _rotated_parity(d, oracle_factors(d, r, hadamard=B), d.bias, deflate=deflate)
 
 
 def test_rotated_one_hot_closed_form():
@@ -113,8 +130,10 @@ def test_rotated_full_size(deflate):
     M, K, N = draws.shape.M, draws.shape.K, draws.shape.N
     log(f"  rotated full size {draws.shape.name} deflate={deflate}")
     f = oracle_factors(draws, hadamard=True)
-    wq, sw, inv_lam, _ = O.pack_weights(f["R"], f["lam"])
+    _, sw = O.quantize_groups(f["R"])
+    inv_lam = O.inverse_smoothing(f["lam"])
     layer = gpu_layer(f)
+    wq = layer.wq.cpu().numpy()
     x, xq, xs, t, y = run_gpu(layer, draws.x, deflate=deflate)
     quant = O.quantize_activations_deflated if deflate else O.quantize_activations
     xq_ref, sx_ref, t_ref, _, xt = quant(draws.x, inv_lam, f["L1"], f["hadamard"])
@@ -124,17 +143,8 @@ def test_rotated_full_size(deflate):
         assert (bits(t) == t_ref).all(), "t"
     else:
         check_t(bits(t), t_ref, O.transformed_activations(draws.x, inv_lam, f["hadamard"]), f["L1"])
-    rng = np.random.default_rng(M + 7)
-    rows = np.array(sorted(set([0, M - 1]) | set(int(v) for v in rng.choice(M, 16, replace=False))))
-    y_ref, P_ref = O.asp_output_rows(xq_ref[rows], sx_ref[rows], t_ref[rows], wq, sw, f["L2"])
-    sel = torch.from_numpy(rows).cuda()
-    err = rel_fro(O.bf16_bits_to_f64(bits(y[sel])), y_ref)
-    log(f"    y rel Frobenius error on {len(rows)} sampled tokens {err:.3e}")
-    assert err <= y_tolerance(y_ref)
-    P = Q.debug_group_partials(layer, xq[sel].contiguous())
-    torch.cuda.synchronize()
-    assert (P.cpu().numpy() == P_ref).all(), "int32 group partials of sampled tokens"
-    del x, xq, xs, t, y, P, layer
+    check_sampled_rows(layer, xq, y, xq_ref, sx_ref, t_ref, wq, sw, f["L2"], sample_rows(M, seed=M + 7))
+    del x, xq, xs, t, y, layer
     torch.cuda.empty_cache()
 
 
