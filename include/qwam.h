@@ -104,7 +104,7 @@
 extern "C" {
 #endif
 
-#define QWAM_ABI_VERSION 9
+#define QWAM_ABI_VERSION 10
 #define QWAM_GROUP 64
 
 typedef enum {
@@ -245,6 +245,42 @@ qwam_status qwam_debug_group_partials(const qwam_layer *L, int32_t M, const uint
  *   A   in/out  float [d][d], accumulated in place
  */
 qwam_status qwam_aog_accumulate(int32_t d, int32_t n, const uint16_t *gT, float *A, void *stream);
+
+/*
+ * The protected subspace from the AOG accumulator (Sec. 4.2, Eq. 7; the
+ * procedure of the probe estimator; Prop. of App. A.3): the top-r eigenvectors
+ * and eigenvalues of the estimate in the quantizer's coordinates,
+ *     G~ = scale * H diag(lam) A diag(lam) H,
+ * scale = 1 / (N P) for N inputs and P probes, lam the smoothing factors, H
+ * the orthonormal block Hadamard matrix of block `hadamard` (the identity for
+ * 0).  By blocked subspace iteration (a block of 64 vectors, `iters` products
+ * with G~, each followed by a CholeskyQR2 orthonormalisation in float64) and a
+ * Rayleigh-Ritz step; products with A on the float32 matrix cores.  The
+ * result is deterministic.  Column i of V is the eigenvector of the i-th
+ * largest eigenvalue, its largest-magnitude entry made positive.
+ *   d       in   channels, d % 64 == 0, 128 <= d <= 16384
+ *   r       in   1 <= r <= 48
+ *   iters   in   0 .. 1000 products with G~ before the Rayleigh-Ritz step;
+ *                the error falls like (lambda_65 / lambda_r)^iters
+ *   A       in   float [d][d], symmetric (the accumulator of
+ *                qwam_aog_accumulate); read as A^T
+ *   scale   in   positive, finite
+ *   lam     in   float [d] or NULL (no smoothing)
+ *   hadamard in  0, or a power of two in [16, 1024] dividing d
+ *   V       out  float [d][r]
+ *   evals   out  float [r], descending
+ *   workspace    device memory of at least
+ *                qwam_aog_protected_basis_workspace(d, r) bytes, 16-byte
+ *                aligned, owned by the caller; its contents on entry do not
+ *                matter; calls that share it must not overlap
+ */
+qwam_status qwam_aog_protected_basis(int32_t d, int32_t r, int32_t iters, const float *A, float scale,
+                                     const float *lam, int32_t hadamard, float *V, float *evals,
+                                     void *workspace, int64_t workspace_bytes, void *stream);
+
+/* Bytes of workspace qwam_aog_protected_basis needs for (d, r); -1 if the
+ * shape is not supported. */
+int64_t qwam_aog_protected_basis_workspace(int32_t d, int32_t r);
 
 /* Message describing the calling thread's last non-OK status ("" if none). */
 const char *qwam_last_error(void);

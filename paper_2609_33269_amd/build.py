@@ -19,7 +19,7 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
 SOURCES = ["qwam_api.cpp", "qwam_quant.hip", "qwam_rotate.hip", "qwam_aog.hip", "qwam_gemm.hip", "qwam_gemm_small.hip",
-           "qwam_layer_small.hip", "qwam_probe.hip"]
+           "qwam_layer_small.hip", "qwam_probe.hip", "qwam_eig.hip"]
 
 # Packed-FP32 VALU instructions are disabled on purpose (some of their forms
 # have produced silently wrong results on this hardware).  No fast-math: the

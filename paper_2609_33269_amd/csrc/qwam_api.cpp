@@ -237,6 +237,55 @@ qwam_status qwam_aog_accumulate(int32_t d, int32_t n, const uint16_t* gT, float*
   return launched(fn, qwam::launch_aog_accumulate(d, n, gT, A, static_cast<hipStream_t>(stream)));
 }
 
+}  // extern "C"
+
+namespace {
+
+qwam_status check_eig(const char* fn, int32_t d, int32_t r, int32_t iters, float scale, int32_t hadamard) {
+  if (d < 128 || d % 64 != 0)
+    return fail(QWAM_ERR_INVALID_ARG, "%s: d must be a multiple of 64, at least 128 (got %d)", fn, d);
+  if (d > 16384) return fail(QWAM_ERR_UNSUPPORTED, "%s: d = %d exceeds 16384", fn, d);
+  if (r < 1 || r > qwam::kEigMaxRank)
+    return fail(QWAM_ERR_UNSUPPORTED, "%s: r must be in [1, %d] (got %d)", fn, qwam::kEigMaxRank, r);
+  if (iters < 0 || iters > 1000) return fail(QWAM_ERR_INVALID_ARG, "%s: iters must be in [0, 1000] (got %d)", fn, iters);
+  if (!(scale > 0.0f) || !(scale < 3.0e38f))
+    return fail(QWAM_ERR_INVALID_ARG, "%s: scale must be positive and finite", fn);
+  if (hadamard != 0 && (hadamard < 16 || hadamard > 1024 || (hadamard & (hadamard - 1)) != 0 || d % hadamard != 0))
+    return fail(QWAM_ERR_INVALID_ARG, "%s: hadamard must be 0 or a power of two in [16, 1024] dividing d (got %d)",
+                fn, hadamard);
+  return QWAM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int64_t qwam_aog_protected_basis_workspace(int32_t d, int32_t r) {
+  if (check_eig("qwam_aog_protected_basis_workspace", d, r, 0, 1.0f, 0) != QWAM_OK) return -1;
+  ok();
+  return qwam::eig_workspace_bytes(d, r);
+}
+
+qwam_status qwam_aog_protected_basis(int32_t d, int32_t r, int32_t iters, const float* A, float scale,
+                                     const float* lam, int32_t hadamard, float* V, float* evals, void* workspace,
+                                     int64_t workspace_bytes, void* stream) {
+  const char* fn = "qwam_aog_protected_basis";
+  qwam_status s = check_eig(fn, d, r, iters, scale, hadamard);
+  if (s != QWAM_OK) return s;
+  QWAM_REQUIRE_PTR(A);
+  QWAM_REQUIRE_PTR(V);
+  QWAM_REQUIRE_PTR(evals);
+  QWAM_REQUIRE_PTR(workspace);
+  if (lam != nullptr && !aligned16(lam)) return fail(QWAM_ERR_MISALIGNED, "%s: lam is not 16-byte aligned", fn);
+  const int64_t need = qwam::eig_workspace_bytes(d, r);
+  if (workspace_bytes < need)
+    return fail(QWAM_ERR_INVALID_ARG, "%s: workspace of %lld bytes is below the %lld needed", fn,
+                static_cast<long long>(workspace_bytes), static_cast<long long>(need));
+  if ((s = check_device(fn)) != QWAM_OK) return s;
+  return launched(fn, qwam::launch_aog_eig(d, r, iters, A, scale, lam, hadamard, V, evals, workspace,
+                                           static_cast<hipStream_t>(stream)));
+}
+
 const char* qwam_last_error(void) { return g_err; }
 
 const char* qwam_status_string(qwam_status s) {

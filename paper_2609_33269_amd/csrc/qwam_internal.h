@@ -34,6 +34,14 @@ hipError_t launch_group_partials(int M, int N, int K, int group, const uint8_t* 
 // AOG accumulation: A [d][d] += gT gT^T, gT bf16 [d][n], n % 64 == 0
 hipError_t launch_aog_accumulate(int d, int n, const uint16_t* gT, float* A, hipStream_t stream);
 
+// top-r eigenvectors of G~ = scale H diag(lam) A diag(lam) H by subspace
+// iteration with a block of kEigBlock vectors; r <= kEigMaxRank, d % 64 == 0
+constexpr int kEigBlock = 64;
+constexpr int kEigMaxRank = 48;
+int64_t eig_workspace_bytes(int d, int r);
+hipError_t launch_aog_eig(int d, int r, int iters, const float* A, float scale, const float* lam, int B, float* V,
+                          float* evals, void* workspace, hipStream_t stream);
+
 // the few-token GEMM (one wave per 32 x 32 block), used for M <= kSmallM
 constexpr int kSmallM = 64;
 

@@ -7,7 +7,7 @@ library is not built, every call raises: there is no fallback.
 
 Names follow the C ABI (include/qwam.h): pack_weights, quantize_act,
 quantize_act_deflated, asp_linear, asp_layer, debug_group_partials,
-aog_accumulate; and the measurement probes of include/qwam_probe.h:
+aog_accumulate, aog_protected_basis; and the measurement probes of include/qwam_probe.h:
 probe_mfma, probe_valu_fma, probe_copy, probe_empty.
 """
 
@@ -51,6 +51,9 @@ SIGNATURES = {
     "qwam_asp_layer": (ctypes.c_int, [_LP, _i32, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p,
                                       _c_void_p]),
     "qwam_aog_accumulate": (ctypes.c_int, [_i32, _i32, _c_void_p, _c_void_p, _c_void_p]),
+    "qwam_aog_protected_basis": (ctypes.c_int, [_i32, _i32, _i32, _c_void_p, ctypes.c_float, _c_void_p, _i32,
+                                                _c_void_p, _c_void_p, _c_void_p, ctypes.c_int64, _c_void_p]),
+    "qwam_aog_protected_basis_workspace": (ctypes.c_int64, [_i32, _i32]),
     "qwam_last_error": (ctypes.c_char_p, []),
     "qwam_probe_mfma": (ctypes.c_int, [_i32, _i32, _i32, _c_void_p, _c_void_p]),
     "qwam_probe_valu_fma": (ctypes.c_int, [_i32, _i32, _c_void_p, _c_void_p]),
@@ -260,6 +263,37 @@ def aog_accumulate(gT: torch.Tensor, A: torch.Tensor, stream=None) -> torch.Tens
                                    _req(A, "A", torch.float32, (d, d)), _stream_ptr(stream))
     _check("qwam_aog_accumulate", st)
     return A
+
+
+def aog_protected_basis_workspace(d: int, r: int) -> int:
+    """qwam_aog_protected_basis_workspace: bytes of workspace for (d, r)."""
+    n = lib().qwam_aog_protected_basis_workspace(d, r)
+    if n < 0:
+        raise QwamError("qwam_aog_protected_basis_workspace", 2, lib().qwam_last_error().decode())
+    return int(n)
+
+
+def aog_protected_basis(A: torch.Tensor, r: int, iters: int = 20, scale: float = 1.0,
+                        lam: Optional[torch.Tensor] = None, hadamard: int = 0,
+                        workspace: Optional[torch.Tensor] = None, stream=None):
+    """qwam_aog_protected_basis: top-r eigenvectors V float32 [d][r] and
+    eigenvalues float32 [r] (descending) of scale * H diag(lam) A diag(lam) H.
+    `workspace` (uint8, at least aog_protected_basis_workspace(d, r) bytes) is
+    allocated here when not given."""
+    d = A.shape[0]
+    need = aog_protected_basis_workspace(d, r)
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=A.device)
+    if workspace.dtype != torch.uint8 or not workspace.is_contiguous() or not workspace.is_cuda:
+        raise ValueError("workspace must be a contiguous uint8 GPU tensor")
+    V = torch.empty((d, r), dtype=torch.float32, device=A.device)
+    ev = torch.empty((r,), dtype=torch.float32, device=A.device)
+    st = lib().qwam_aog_protected_basis(d, r, iters, _req(A, "A", torch.float32, (d, d)), float(scale),
+                                        None if lam is None else _req(lam, "lam", torch.float32, (d,)),
+                                        hadamard, V.data_ptr(), ev.data_ptr(), workspace.data_ptr(),
+                                        workspace.numel(), _stream_ptr(stream))
+    _check("qwam_aog_protected_basis", st)
+    return V, ev
 
 
 # ---------------------------------------------------------------------------

@@ -40,7 +40,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == set(Q.SIGNATURES), "binding and header disagree"
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.qwam_abi_version() == 9
+    assert lib.qwam_abi_version() == 10
     assert lib.qwam_status_string(3) == b"QWAM_ERR_MISALIGNED"
 
 
@@ -175,3 +175,28 @@ def test_binding_rejects_host_tensors():
                           L2t=torch.zeros(16, 16, dtype=torch.bfloat16))
     with pytest.raises(ValueError, match="GPU tensor"):
         layer.c_struct()
+
+
+def test_aog_protected_basis_argument_checks(lib):
+    """Bad shapes, scale, rotation block, pointers and workspace size are
+    rejected on the host with the documented status."""
+    f = lib.qwam_aog_protected_basis
+    need = lib.qwam_aog_protected_basis_workspace(4096, 32)
+    assert need > 0 and lib.qwam_aog_protected_basis_workspace(100, 32) == -1
+    assert lib.qwam_aog_protected_basis_workspace(4096, 49) == -1
+
+    def call(d=4096, r=32, iters=8, A=FAKE, scale=1.0, lam=None, B=0, V=FAKE, ev=FAKE, ws=FAKE, wsb=None):
+        return f(d, r, iters, A, scale, lam, B, V, ev, ws, need if wsb is None else wsb, None)
+
+    assert call(d=4000) == INVALID
+    assert call(d=64) == INVALID
+    assert call(d=16384 + 64) == UNSUPPORTED
+    assert call(r=0) == UNSUPPORTED and call(r=64) == UNSUPPORTED
+    assert call(iters=-1) == INVALID
+    assert call(scale=0.0) == INVALID and call(scale=float("nan")) == INVALID
+    assert call(B=48) == INVALID and call(B=2048) == INVALID and call(B=8) == INVALID
+    assert call(A=None) == INVALID and call(V=None) == INVALID and call(ev=None) == INVALID
+    assert call(ws=None) == INVALID
+    assert call(A=FAKE + 4) == MISALIGNED and call(lam=FAKE + 8) == MISALIGNED
+    assert call(wsb=need - 1) == INVALID
+    assert b"workspace" in lib.qwam_last_error()
