@@ -71,6 +71,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 M, K, N, R_RANK, GROUP = 4096, 3072, 14336, 32, 64
+# the video-DiT layer shapes (M tokens, K in, N out); the headline line is the FFN up-projection
+WORKLOADS = {"video_dit_ffn_up": (4096, 3072, 14336), "video_dit_qkv": (4096, 3072, 9216),
+             "video_dit_ffn_down": (4096, 14336, 3072)}
 G = K // GROUP
 MFMA_PEAK = 5000.0             # MI355X dense FP8 (= dense INT8) matrix peak, TFLOP/s (TOP/s)
 FP6_MFMA_PEAK = 10100.0        # MI355X dense FP6 / FP4 matrix peak, TFLOP/s: the GEMM's own dtype
@@ -82,7 +85,7 @@ METRIC = "ASP W4A4+r32 linear: effective TOPS & % int8 MFMA peak at 4096×3072×
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_asp_gemm_ffn_up.json")
 GEMM_SRCS = [os.path.join(ROOT, "paper_2609_33269_amd", "csrc", f) for f in ("qwam_gemm.hip", "qwam_device.h", "qwam_mfma.h")]
 GEMM_KERNEL = "asp_gemm_kernel<32, false, 64>"
-COPY_KERNEL = "copy_kernel"
+COPY_KERNEL = "(anonymous namespace)::copy_kernel("   # the streaming copy of qwam_probe_copy
 
 
 def gemm_issue_ceiling(group: int = GROUP) -> float:
@@ -142,7 +145,7 @@ def reduce_counters(fetch_csv: str, write_csv: str, copy_mib: int):
     for key, path in (("fetch", fetch_csv), ("write", write_csv)):
         rows = _counter_rows(path)
         gemm = [v for k, v in rows if GEMM_KERNEL in k]
-        copy = [v for k, v in rows if COPY_KERNEL in k]
+        copy = [v for k, v in rows if k.startswith(COPY_KERNEL)]
         if not gemm or not copy:
             raise SystemExit(f"{path}: no {GEMM_KERNEL} or {COPY_KERNEL} dispatches")
         g_kib, c_kib = float(np.mean(gemm)), float(np.mean(copy))
@@ -214,7 +217,7 @@ def graph_floor_us(n: int = 200, replays: int = 10) -> float:
     return e0.elapsed_time(e1) * 1e3 / (n * replays)
 
 
-def measured_peaks():
+def measured_peaks(sweep: bool = False):
     """What the chip sustains in plain loops (the probes of qwam_probe.h): each
     matrix-core format, the float32 VALU at 1, 2 and 4 waves per SIMD, a
     streaming copy of 2 x 1 GiB; best of three launches each."""
@@ -256,9 +259,24 @@ def measured_peaks():
     copy_gbs = round(moved / (ms * 1e-3) / 1e9, 1)
     del src, dst
     torch.cuda.empty_cache()
-    return {"mfma_TOPS": mfma, "valu_fp32_fma_TFLOPs": valu, "copy_GBs": copy_gbs,
-            "launch_floor_graph_us": round(graph_floor_us(), 2),
-            "method": "probe loops of include/qwam_probe.h, best of 3 launches; MFMA and copy at 4 waves/SIMD"}
+    out = {"mfma_TOPS": mfma, "valu_fp32_fma_TFLOPs": valu, "copy_GBs": copy_gbs,
+           "launch_floor_graph_us": round(graph_floor_us(), 2),
+           "method": "probe loops of include/qwam_probe.h, best of 3 launches; MFMA and copy at 4 waves/SIMD"}
+    if sweep:
+        # the copy at smaller sizes: the bandwidth a kernel of that size can see,
+        # each size cycling through more than the 256 MB Infinity Cache
+        rows = {}
+        for mib in (4, 8, 16, 32, 64, 128, 256, 512):
+            n = (mib << 20) // 4
+            srcs = [torch.ones(n, device=dev, dtype=torch.float32) for _ in range(max(2, 768 // mib))]
+            dst = torch.empty(n, device=dev, dtype=torch.float32)
+            it = iter(range(1 << 30))
+            ms = best_ms(lambda: qwam.probe_copy(srcs[next(it) % len(srcs)], dst), reps=20)
+            rows[f"{mib}MiB"] = {"us": round(ms * 1e3, 2), "GBs": round(2 * (mib << 20) / (ms * 1e-3) / 1e9, 1)}
+            del srcs, dst
+            torch.cuda.empty_cache()
+        out["copy_sweep_read_plus_write"] = rows
+    return out
 
 
 def small_m_report(args):
@@ -476,6 +494,24 @@ def aog_report(args):
     flops = float(n) * d * (d + 1)               # the symmetric rank-n update
     bytes_ = d * n * 2 + 2 * d * d * 4            # gT once, A read and written once
     tflops = flops / (us * 1e-6) / 1e12
+    # the eigensolve that follows the last batch: top-32 eigenvectors of
+    # G~ = H diag(lam) (A / (N P)) diag(lam) H (B = 1024), 10 products with G~;
+    # each product reads A once (HBM-bound), so its roofline is HBM
+    r_eig, iters = 32, 10
+    lam = torch.exp(torch.empty(d, device=dev).uniform_(-1.0, 1.0, generator=gen))
+    ws = torch.empty(qwam.aog_protected_basis_workspace(d, r_eig), dtype=torch.uint8, device=dev)
+    for i in range(2):
+        qwam.aog_protected_basis(accs[i], r_eig, iters=iters, scale=1.0 / n, lam=lam, hadamard=1024, workspace=ws)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for i in range(5):
+        qwam.aog_protected_basis(accs[i % nrot], r_eig, iters=iters, scale=1.0 / n, lam=lam, hadamard=1024,
+                                 workspace=ws)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    eig_us = e0.elapsed_time(e1) * 1e3 / 5
+    eig_bytes = (iters + 1) * d * d * 4
     # the CPU oracle (float64 rank-k update) on column samples of the same batch
     from oracle import qwam_oracle as O
     g_bits = gts[0].view(torch.int16).cpu().numpy().view(np.uint16)
@@ -498,6 +534,10 @@ def aog_report(args):
                      "peak": BF16_MFMA_PEAK, "unit": "TFLOP/s", "frac": round(tflops / BF16_MFMA_PEAK, 4),
                      "traffic": None, "algorithmic_bytes": bytes_,
                      "hbm_GBs": round(bytes_ / (us * 1e-6) / 1e9, 1)},
+        "eigensolve": {"kernel": "qwam_aog_protected_basis", "d": d, "r": r_eig, "iters": iters, "block": 64,
+                       "hadamard": 1024, "us": round(eig_us, 1),
+                       "A_bytes_read": eig_bytes, "hbm_GBs": round(eig_bytes / (eig_us * 1e-6) / 1e9, 1),
+                       "frac_of_hbm_peak": round(eig_bytes / (eig_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)},
         "cpu_baseline": {"value": round(cpu_tflops, 5), "unit": "TFLOP/s", "cores": os.cpu_count(), "kind": "oracle",
                          "sample": f"{reps} calls of the oracle on {cols} of the {n} VJPs (all {d} channels) in "
                                    f"{dt:.1f} s; value = cols*d*(d+1)*calls/time"}}), flush=True)
@@ -559,7 +599,11 @@ def main():
                     help="channels per quantization scale (64, or the paper's 32)")
     ap.add_argument("--rotated", action="store_true",
                     help="the same layer with the block Hadamard rotation (Eq. 3) on both operands")
+    ap.add_argument("--workload", default="video_dit_ffn_up", choices=sorted(WORKLOADS),
+                    help="layer shape of the line (the metric is quoted on video_dit_ffn_up)")
     ap.add_argument("--aog", action="store_true", help="report the AOG accumulation kernel instead")
+    ap.add_argument("--peaks", action="store_true",
+                    help="print the measured chip peaks (MFMA loops, VALU, copy and a copy-size sweep) instead")
     ap.add_argument("--small-m", action="store_true", help="report the action-expert layers instead")
     ap.add_argument("--denoise-step", action="store_true", help="report one 120-layer denoising step instead")
     args = ap.parse_args()
@@ -571,11 +615,19 @@ def main():
             f.write("\n")
         print(json.dumps(rec))
         return
+    global M, K, N, G
+    M, K, N = WORKLOADS[args.workload]
+    G = K // GROUP
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the ASP layer is "
               f"implemented and measured on a single GPU, with no sharding", file=sys.stderr)
         sys.exit(2)
 
+    if args.peaks:
+        import torch
+        torch.cuda.set_device(0)
+        print(json.dumps({"measured_peaks": measured_peaks(sweep=True)}), flush=True)
+        return
     if args.aog:
         aog_report(args)
         return
@@ -591,8 +643,8 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    print(f"[bench] drawing inputs {M}x{K}x{N} r{R_RANK}", file=sys.stderr, flush=True)
-    draws = inputs.video_dit_ffn_up()
+    print(f"[bench] drawing inputs {args.workload} {M}x{K}x{N} r{R_RANK}", file=sys.stderr, flush=True)
+    draws = getattr(inputs, args.workload)()
     x0 = torch.from_numpy(draws.x.view(np.int16)).view(torch.bfloat16).to(dev)
     w0 = torch.from_numpy(draws.w.view(np.int16)).view(torch.bfloat16).to(dev)
     V = calib.protected_basis(torch.from_numpy(draws.a), R_RANK)
@@ -624,6 +676,19 @@ def main():
         act_fn(layers[j], xins[j], out=(xq, xs, t))
         qwam.asp_linear(layers[j], xq, xs, t, out=y)
 
+    # HIP graphs of the step (both kernels): one holding the steps of all nrot
+    # buffer sets in order, and one per buffer set for a remainder; replayed
+    # beside the timed region (captured first, so that the clock settle and
+    # the warmup come right before the timed region)
+    block = capture_graphs(lambda _: [step(j) for j in range(nrot)], 1)[0]
+    singles = capture_graphs(lambda j: step(j), nrot)
+
+    def replay_steps(n):
+        for _ in range(n // nrot):
+            block.replay()
+        for i in range(n % nrot):
+            singles[i].replay()
+
     # clock settle: the first calls on a fresh box run at lower clocks, so the
     # steps are warmed by time (at least `--settle` seconds, then until three
     # consecutive 10-step windows agree within 2%), whatever --warmup says
@@ -634,51 +699,56 @@ def main():
         step(i)
     torch.cuda.synchronize()
 
-    # one HIP graph per buffer set holds one step (both kernels); the timed
-    # region replays them, K steps in all, with no event inside it
-    graphs = capture_graphs(lambda j: step(j), nrot)
+    def launch_steps(n):
+        for i in range(n):
+            step(i)
+
+    # the timed region: K steps launched back to back, no event inside
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record(stream)
-    for i in range(args.steps):
-        graphs[i % nrot].replay()
+    launch_steps(args.steps)
     end.record(stream)
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(end)
     ms_step = total_ms / args.steps
 
-    # the same replays, 10 repeats of max(100, K) steps: median per-step time
     rep_steps = max(100, args.steps)
-    rep_ms = []
-    for _ in range(10):
+
+    def timed(fn, n):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
-        for i in range(rep_steps):
-            graphs[i % nrot].replay()
+        fn(n)
         e1.record(stream)
         torch.cuda.synchronize()
-        rep_ms.append(e0.elapsed_time(e1) / rep_steps)
-    med_ms = float(np.median(rep_ms))
+        return e0.elapsed_time(e1) / n
 
-    # per-kernel durations: a separate loop of plain launches with events
-    # between the two kernels, on the stream they are launched on
-    kevs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(rep_steps)]
-    for i in range(rep_steps):
-        j = i % nrot
-        xq, xs, t, y = outs[j]
-        kevs[i][0].record(stream)
-        act_fn(layers[j], xins[j], out=(xq, xs, t))
-        kevs[i][1].record(stream)
-        qwam.asp_linear(layers[j], xq, xs, t, out=y)
-        kevs[i][2].record(stream)
-    torch.cuda.synchronize()
-    k1_all = [e[0].elapsed_time(e[1]) for e in kevs]
-    k2_all = [e[1].elapsed_time(e[2]) for e in kevs]
-    k1_ms, k2_ms = float(np.mean(k1_all)), float(np.mean(k2_all))
-    del graphs
-    print(f"[bench] {args.steps} graph-replayed steps: {ms_step * 1e3:.1f} us/step (median of 10 x {rep_steps}: "
-          f"{med_ms * 1e3:.1f}); act kernel {k1_ms * 1e3:.1f} us, gemm {k2_ms * 1e3:.1f} us "
-          f"(median {np.median(k2_all) * 1e3:.1f})", file=sys.stderr, flush=True)
+    # 10 repeats of max(100, K) steps, launched and replayed from the graphs: medians
+    med_ms = float(np.median([timed(launch_steps, rep_steps) for _ in range(10)]))
+    graph_ms = timed(replay_steps, args.steps)
+    graph_med_ms = float(np.median([timed(replay_steps, rep_steps) for _ in range(10)]))
+
+    # per-kernel durations on the launch stream: `rep_steps` launches of one
+    # kernel back to back over the buffer sets, events only at the two ends
+    # (so the mean includes the gaps between consecutive launches); median of 5
+    def act_only(n):
+        for i in range(n):
+            j = i % nrot
+            act_fn(layers[j], xins[j], out=outs[j][:3])
+
+    def gemm_only(n):
+        for i in range(n):
+            j = i % nrot
+            xq, xs, t, y = outs[j]
+            qwam.asp_linear(layers[j], xq, xs, t, out=y)
+
+    k1_all = [timed(act_only, rep_steps) for _ in range(5)]
+    k2_all = [timed(gemm_only, rep_steps) for _ in range(5)]
+    k1_ms, k2_ms = float(np.median(k1_all)), float(np.median(k2_all))
+    del block, singles
+    print(f"[bench] {args.steps} steps: {ms_step * 1e3:.1f} us/step (median of 10 x {rep_steps}: {med_ms * 1e3:.1f}; "
+          f"graph replay {graph_ms * 1e3:.1f}, median {graph_med_ms * 1e3:.1f}); act kernel {k1_ms * 1e3:.1f} us, "
+          f"gemm {k2_ms * 1e3:.1f} us", file=sys.stderr, flush=True)
     floor_us = graph_floor_us()
 
     int_ops = 2.0 * M * K * N
@@ -711,10 +781,10 @@ def main():
         del src_t, dst_t
     peaks = None if args.no_peaks else measured_peaks()
 
-    traffic = measured_traffic() if args.group == GROUP else None
+    traffic = measured_traffic() if (args.group == GROUP and args.workload == "video_dit_ffn_up") else None
     act_name = ("quantize_act_rotated" if args.rotated else "quantize_act") + ("_deflated" if args.deflated else "")
     out = {
-        "metric": METRIC,
+        "metric": METRIC if args.workload == "video_dit_ffn_up" else METRIC.replace("4096×3072×14336", f"{M}×{K}×{N}"),
         "value": round(eff_tops, 2),
         "unit": "TOPS",
         "n_gpus": 1,
@@ -727,10 +797,11 @@ def main():
         "dtype": "int4 codes as fp6-e2m3 MFMA operands (exact int partials); per-group scale products "
                  "sx*sw on bf16 MFMA from two-piece bf16 splits (~2^-15 rel); f32 accumulate; bf16 out",
         "data": "synthetic",
-        "config": {"workload": "video_dit_ffn_up" + ("_rotated" if args.rotated else "")
+        "config": {"workload": args.workload + ("_rotated" if args.rotated else "")
                    + ("_deflated" if args.deflated else "") + ("_group32" if args.group == 32 else ""),
                    "M": M, "K": K, "N": N, "r": R_RANK, "group": args.group,
-                   "act": "N(0,1), 1% channels x U_log(10,50)", "weights": "N(0,1/K)",
+                   "act": ("bf16(GELU_erf(N(0,1)))" if args.workload == "video_dit_ffn_down"
+                           else "N(0,1), 1% channels x U_log(10,50)"), "weights": "N(0,1/K)",
                    "rotated_buffer_sets": nrot},
         "roofline": {"bound": "mfma", "kernel": f"asp_gemm_kernel<{R_RANK}, false, {args.group}>",
                      "achieved": round(k2_tops, 1),
@@ -738,12 +809,15 @@ def main():
                      "traffic": traffic, "algorithmic_bytes": gemm_bytes},
         "layer_frac_int8_peak": round(eff_tops / MFMA_PEAK, 4),
         "kernels_us": {act_name: round(k1_ms * 1e3, 2), "asp_gemm": round(k2_ms * 1e3, 2),
-                       "asp_gemm_median": round(float(np.median(k2_all)) * 1e3, 2),
-                       "timing": f"mean of {rep_steps} event-bracketed launches after the timed region"},
-        "timing": {"method": f"{args.steps} HIP-graph replays of one step (both kernels), no events inside",
-                   "repeat_median_ms_per_step": round(med_ms, 5),
-                   "repeats": f"10 x {rep_steps} replays", "clock_settle": settle,
-                   "graph_launch_floor_us": round(floor_us, 2)},
+                       "timing": f"per launch: {rep_steps} back-to-back launches of the kernel between two "
+                                 f"events on its stream, median of 5"},
+        "timing": {"method": f"{args.steps} steps (both kernels) launched back to back on one stream, events "
+                             f"only at the two ends",
+                   "repeat_median_ms_per_step": round(med_ms, 5), "repeats": f"10 x {rep_steps} steps",
+                   "graph_replay_ms_per_step": round(graph_ms, 5),
+                   "graph_replay_repeat_median_ms_per_step": round(graph_med_ms, 5),
+                   "graph": f"HIP graphs of {nrot} steps (one per pass over the buffer sets)",
+                   "clock_settle": settle, "graph_launch_floor_us": round(floor_us, 2)},
         "quantize_act_roofline": {"bound": "hbm", "achieved": round(k1_gbs, 1), "peak": HBM_PEAK_GBS,
                                   "unit": "GB/s", "frac": round(k1_gbs / HBM_PEAK_GBS, 4),
                                   "algorithmic_bytes": act_bytes},

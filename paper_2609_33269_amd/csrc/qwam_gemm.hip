@@ -139,6 +139,9 @@ __device__ __forceinline__ v32f scale_outer(float sx, float sw) {
 
 // Tile of workgroup `bid`: XCD-major remap (hardware places workgroup b on XCD
 // b % 8), then bands of BAND tile-rows, columns fastest inside a band-column.
+// (An XCD owning a range of whole tile-columns instead, so that its weight
+// panel stays in its L2, fetched twice the bytes: a 2.7 MB panel plus the
+// streaming activation tiles and the output does not stay in a 4 MB L2.)
 __device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
   const int total = tiles_m * tiles_n;
   const int per = total / 8, rem = total % 8;
