@@ -15,9 +15,10 @@
 //       Y = s H diag(lambda) W        (fixed-order sum of the K splits, row transform)
 //     A is d x d and read once per product (HBM-bound); the block is p x d
 //     and stays in L2;
-//   * orthonormalisation by CholeskyQR2: Gram matrix in float64 (fixed-order
-//     sum of per-chunk partials), Cholesky and triangular inverse in one
-//     workgroup, then V = W R^-1;
+//   * orthonormalisation by CholeskyQR2: Gram matrix in float64 (per-chunk
+//     partials, then a fixed-order sum in a kernel of its own), Cholesky and
+//     triangular inverse in one wave with the matrix in registers, then
+//     V = W R^-1 (tiled, float64 sums);
 //   * Rayleigh-Ritz: T = V^T G~ V (p x p, float64), parallel cyclic Jacobi in
 //     one workgroup (disjoint rotation pairs by the circle method), Ritz
 //     vectors V Q sorted by eigenvalue, descending; the largest-magnitude entry
@@ -37,6 +38,7 @@ namespace {
 constexpr int P = kEigBlock;     // block width (64)
 constexpr int NT = 256;
 constexpr int GCH = 64;          // columns per Gram partial
+constexpr int AT = 32;           // columns (rows of V) per workgroup of the basis update and Ritz step
 
 typedef float v16f __attribute__((ext_vector_type(16)));
 
@@ -55,43 +57,81 @@ __global__ __launch_bounds__(NT) void eig_init_kernel(float* __restrict__ Vt, in
   Vt[i] = static_cast<float>(static_cast<int64_t>(z >> 40) - (int64_t(1) << 23)) * 0x1p-23f;
 }
 
-// One row (a block vector) per workgroup, in LDS:
+// Largest segment length L (a multiple of the Hadamard block B, at most 1024,
+// dividing d) handled by one workgroup of the row transforms
+int row_segment(int d, int B) {
+  int L = B > 1 ? B : 64;
+  while (L * 2 <= 1024 && d % (L * 2) == 0) L *= 2;
+  return L;
+}
+
+// One segment of L entries of one block row per workgroup (grid: d / L
+// segments x P rows), in LDS:
 //   PRE : out = diag(lam) H in
 //   POST: out = scale * H diag(lam) (sum over `nparts` parts of in, in order)
 // H: fast Walsh-Hadamard transform of every block of B entries (B = 0: none),
-// normalised by 1 / sqrt(B).
+// normalised by 1 / sqrt(B); L is a multiple of B, so every block lies in one
+// segment.
 template <bool POST>
 __global__ __launch_bounds__(NT) void eig_row_kernel(const float* __restrict__ in, int nparts, int64_t part_stride,
                                                      float* __restrict__ out, const float* __restrict__ lam, int B,
-                                                     float scale, int d) {
-  extern __shared__ float row[];
-  const int j = blockIdx.x;
+                                                     float scale, int d, int L) {
+  extern __shared__ float seg[];
+  const int c0 = blockIdx.x * L;
+  const int64_t base = static_cast<int64_t>(blockIdx.y) * d + c0;
   const int tid = threadIdx.x;
-  for (int i = tid; i < d; i += NT) {
-    float v = 0.0f;
-    for (int s = 0; s < nparts; ++s) v += in[s * part_stride + static_cast<int64_t>(j) * d + i];
-    if (POST && lam != nullptr) v *= lam[i];
-    row[i] = v;
+  for (int i4 = tid; i4 < L / 4; i4 += NT) {
+    float4 v = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    for (int s = 0; s < nparts; ++s) {
+      const float4 p = *reinterpret_cast<const float4*>(in + s * part_stride + base + 4 * i4);
+      v.x += p.x;
+      v.y += p.y;
+      v.z += p.z;
+      v.w += p.w;
+    }
+    if (POST && lam != nullptr) {
+      const float4 l = *reinterpret_cast<const float4*>(lam + c0 + 4 * i4);
+      v.x *= l.x;
+      v.y *= l.y;
+      v.z *= l.z;
+      v.w *= l.w;
+    }
+    *reinterpret_cast<float4*>(seg + 4 * i4) = v;
   }
   __syncthreads();
   float norm = 1.0f;
   if (B > 1) {
     for (int h = 1; h < B; h <<= 1) {
-      for (int q = tid; q < d / 2; q += NT) {
-        const int i = (q / h) * 2 * h + (q % h);
-        const float a = row[i], b = row[i + h];
-        row[i] = a + b;
-        row[i + h] = a - b;
+      for (int q = tid; q < L / 2; q += NT) {
+        const int i = ((q & ~(h - 1)) << 1) | (q & (h - 1));
+        const float a = seg[i], b = seg[i + h];
+        seg[i] = a + b;
+        seg[i + h] = a - b;
       }
       __syncthreads();
     }
     norm = 1.0f / __builtin_sqrtf(static_cast<float>(B));
   }
-  for (int i = tid; i < d; i += NT) {
-    float v = row[i] * norm;
-    if (!POST && lam != nullptr) v *= lam[i];
-    if (POST) v *= scale;
-    out[static_cast<int64_t>(j) * d + i] = v;
+  for (int i4 = tid; i4 < L / 4; i4 += NT) {
+    float4 v = *reinterpret_cast<const float4*>(seg + 4 * i4);
+    v.x *= norm;
+    v.y *= norm;
+    v.z *= norm;
+    v.w *= norm;
+    if (!POST && lam != nullptr) {
+      const float4 l = *reinterpret_cast<const float4*>(lam + c0 + 4 * i4);
+      v.x *= l.x;
+      v.y *= l.y;
+      v.z *= l.z;
+      v.w *= l.w;
+    }
+    if (POST) {
+      v.x *= scale;
+      v.y *= scale;
+      v.z *= scale;
+      v.w *= scale;
+    }
+    *reinterpret_cast<float4*>(out + base + 4 * i4) = v;
   }
 }
 
@@ -101,7 +141,9 @@ __global__ __launch_bounds__(NT) void eig_row_kernel(const float* __restrict__ i
 // 32 wn..) on v_mfma_f32_32x32x2_f32.  Lane l supplies row / column l % 32;
 // within a step of 8 channels, lane half h supplies channels 4h .. 4h+3 to
 // the four MFMAs (the same channel order on both operands), so each lane
-// reads 16 contiguous bytes of a row of Xt and of A.
+// reads 16 contiguous bytes of a row of Xt and of A.  Software pipeline over
+// batches of eight steps: the loads of the next batch are issued before the
+// products of this one (kchunk % 64 == 0).
 __global__ __launch_bounds__(NT) void eig_gemm_kernel(const float* __restrict__ Xt, const float* __restrict__ A,
                                                       float* __restrict__ part, int d, int kchunk) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -114,13 +156,36 @@ __global__ __launch_bounds__(NT) void eig_gemm_kernel(const float* __restrict__ 
   const float4* xp = reinterpret_cast<const float4*>(Xt + static_cast<int64_t>(jrow) * d + k0);
   const float4* ap = reinterpret_cast<const float4*>(A + static_cast<int64_t>(nrow) * d + k0);
   v16f acc = {};
-  for (int k = 0; k < kchunk; k += 8) {
-    const float4 x = xp[k / 4];
-    const float4 a = ap[k / 4];
-    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x.x, a.x, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x.y, a.y, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x.z, a.z, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x.w, a.w, acc, 0, 0, 0);
+  const int kc4 = kchunk / 4;
+  float4 x[8], a[8];
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    x[u] = xp[2 * u];
+    a[u] = ap[2 * u];
+  }
+  for (int k4 = 0; k4 < kc4; k4 += 16) {
+    // the next eight steps' operands are in flight while these are multiplied
+    // (the last batch reloads itself)
+    const int nk = k4 + 16 < kc4 ? k4 + 16 : k4;
+    float4 xn[8], an[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      xn[u] = xp[nk + 2 * u];
+      an[u] = ap[nk + 2 * u];
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x[u].x, a[u].x, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x[u].y, a[u].y, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x[u].z, a[u].z, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x[u].w, a[u].w, acc, 0, 0, 0);
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      x[u] = xn[u];
+      a[u] = an[u];
+    }
   }
   // result layout: lane l holds column l % 32, rows 8 (v / 4) + 4 (l / 32) + v % 4
   float* out = part + static_cast<int64_t>(s) * P * d;
@@ -131,166 +196,218 @@ __global__ __launch_bounds__(NT) void eig_gemm_kernel(const float* __restrict__ 
   }
 }
 
-// gpart[c][a][b] = sum over the GCH columns n of chunk c of U[a][n] W[b][n], float64
+// gpart[c][a][b] = sum over the GCH columns n of chunk c of U[a][n] W[b][n],
+// float64, n ascending.  Thread (ta, tb) = (tid / 16, tid % 16) owns the 16
+// entries a = ta + 16 p, b = tb + 16 q; the chunk passes through LDS in two
+// halves of 32 columns, converted to float64 (row stride 34 doubles: the 16
+// rows b of one read fall in distinct banks).
 __global__ __launch_bounds__(NT) void eig_gram_kernel(const float* __restrict__ Ut, const float* __restrict__ Wt,
                                                       double* __restrict__ gpart, int d) {
-  __shared__ float us[P][GCH + 1], ws[P][GCH + 1];
+  constexpr int HW = 32, RS = HW + 2;
+  __shared__ __attribute__((aligned(16))) double us[P][RS], ws[P][RS];
   const int c = blockIdx.x, tid = threadIdx.x;
-  for (int e = tid; e < P * GCH; e += NT) {
-    const int a = e / GCH, n = e % GCH;
-    us[a][n] = Ut[static_cast<int64_t>(a) * d + c * GCH + n];
-    ws[a][n] = Wt[static_cast<int64_t>(a) * d + c * GCH + n];
-  }
-  __syncthreads();
-  const int a = tid >> 2, b0 = (tid & 3) * 16;
-  double acc[16];
+  const int ta = tid >> 4, tb = tid & 15;
+  double acc[4][4];
 #pragma unroll
-  for (int i = 0; i < 16; ++i) acc[i] = 0.0;
-  for (int n = 0; n < GCH; ++n) {
-    const double u = us[a][n];
+  for (int p = 0; p < 4; ++p)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) acc[i] = __builtin_fma(u, static_cast<double>(ws[b0 + i][n]), acc[i]);
-  }
-  double* out = gpart + static_cast<int64_t>(c) * P * P + a * P + b0;
+    for (int q = 0; q < 4; ++q) acc[p][q] = 0.0;
+  for (int h = 0; h < GCH; h += HW) {
 #pragma unroll
-  for (int i = 0; i < 16; ++i) out[i] = acc[i];
-}
-
-// sum of the Gram partials in chunk order, symmetrised, into g[P][P] (LDS)
-__device__ void gram_sum(const double* __restrict__ gpart, int nch, double (*g)[P + 1]) {
-  const int tid = threadIdx.x;
-  for (int e = tid; e < P * P; e += NT) {
-    double v = 0.0;
-    for (int c = 0; c < nch; ++c) v += gpart[static_cast<int64_t>(c) * P * P + e];
-    g[e / P][e % P] = v;
-  }
-  __syncthreads();
-  for (int e = tid; e < P * P; e += NT) {
-    const int a = e / P, b = e % P;
-    if (a < b) {
-      const double v = 0.5 * (g[a][b] + g[b][a]);
-      g[a][b] = v;
-      g[b][a] = v;
+    for (int v = 0; v < 2; ++v) {
+      const int e4 = tid + NT * v;            // 512 float4 per array
+      const int a = e4 >> 3, c4 = e4 & 7;
+      const int64_t g = static_cast<int64_t>(a) * d + c * GCH + h + 4 * c4;
+      const float4 u = *reinterpret_cast<const float4*>(Ut + g);
+      const float4 w = *reinterpret_cast<const float4*>(Wt + g);
+      *reinterpret_cast<double2*>(&us[a][4 * c4]) = make_double2(u.x, u.y);
+      *reinterpret_cast<double2*>(&us[a][4 * c4 + 2]) = make_double2(u.z, u.w);
+      *reinterpret_cast<double2*>(&ws[a][4 * c4]) = make_double2(w.x, w.y);
+      *reinterpret_cast<double2*>(&ws[a][4 * c4 + 2]) = make_double2(w.z, w.w);
     }
+    __syncthreads();
+#pragma unroll 4
+    for (int n = 0; n < HW; n += 2) {
+      double2 u[4], w[4];
+#pragma unroll
+      for (int p = 0; p < 4; ++p) u[p] = *reinterpret_cast<const double2*>(&us[ta + 16 * p][n]);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) w[q] = *reinterpret_cast<const double2*>(&ws[tb + 16 * q][n]);
+#pragma unroll
+      for (int p = 0; p < 4; ++p)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          acc[p][q] = __builtin_fma(u[p].x, w[q].x, acc[p][q]);
+          acc[p][q] = __builtin_fma(u[p].y, w[q].y, acc[p][q]);
+        }
+    }
+    __syncthreads();
   }
-  __syncthreads();
+  double* out = gpart + static_cast<int64_t>(c) * P * P;
+#pragma unroll
+  for (int p = 0; p < 4; ++p)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) out[(ta + 16 * p) * P + tb + 16 * q] = acc[p][q];
 }
 
-// One workgroup: C = sum of the Gram partials; C = R^T R (Cholesky, R upper);
-// Rinv = R^-1 (upper) to global memory.  A pivot below 1e-13 of the largest
-// diagonal entry (a block of lower rank) is raised to that floor, so the
-// inverse stays finite; the next iterations refill such a direction.
-__global__ __launch_bounds__(NT) void eig_chol_kernel(const double* __restrict__ gpart, int nch,
-                                                      double* __restrict__ Rinv) {
-  __shared__ double c[P][P + 1], r[P][P + 1];
-  __shared__ double floor_v;
-  const int tid = threadIdx.x;
-  gram_sum(gpart, nch, c);
-  if (tid == 0) {
-    double m = 0.0;
-    for (int a = 0; a < P; ++a) m = c[a][a] > m ? c[a][a] : m;
-    floor_v = m > 0.0 ? 1e-13 * m : 1e-300;
-  }
-  for (int e = tid; e < P * P; e += NT) r[e / P][e % P] = 0.0;
+// C[e] = sum of the nch Gram partials of entry e, in chunk order: four
+// threads sum consecutive quarters of the chunks, the quarters are added in
+// order.  Grid: P * P / 64 workgroups of 64 entries.
+__global__ __launch_bounds__(NT) void eig_gsum_kernel(const double* __restrict__ gpart, int nch,
+                                                      double* __restrict__ C) {
+  __shared__ double red[4][64];
+  const int t = threadIdx.x & 63, qtr = threadIdx.x >> 6;
+  const int e = blockIdx.x * 64 + t;
+  const int c0 = (nch * qtr) / 4, c1 = (nch * (qtr + 1)) / 4;
+  double v = 0.0;
+#pragma unroll 8
+  for (int c = c0; c < c1; ++c) v += gpart[static_cast<int64_t>(c) * P * P + e];
+  red[qtr][t] = v;
   __syncthreads();
+  if (qtr == 0) C[e] = ((red[0][t] + red[1][t]) + red[2][t]) + red[3][t];
+}
+
+__device__ __forceinline__ double readlane_f64(double v, int l) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, v);
+  const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(u)), l));
+  const uint32_t hi =
+      static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(u >> 32)), l));
+  return __builtin_bit_cast(double, (static_cast<uint64_t>(hi) << 32) | lo);
+}
+
+// One wave: C = R^T R (Cholesky, R upper) and Rinv = R^-1 (upper, its lower
+// part exact zeros) to global memory.  Lane j keeps column j of C in
+// registers; step k takes the pivot from lane k, lane j forms R[k][j], the
+// row R[k][.] goes through LDS and every lane updates its column's trailing
+// part (right-looking).  Only the upper triangle of C is read.  A pivot below
+// 1e-13 of the largest diagonal entry (a block of lower rank) is raised to
+// that floor, so the inverse stays finite; the next iterations refill such a
+// direction.  Column j of R^-1 is then lane j's back substitution R z = e_j
+// over the rows of R in LDS.
+__global__ __launch_bounds__(64) void eig_chol_kernel(const double* __restrict__ C, double* __restrict__ Rinv) {
+  __shared__ __attribute__((aligned(16))) double rl[P][P + 2];
+  __shared__ double dinv[P];
+  const int lane = threadIdx.x;
+  double cc[P];
+#pragma unroll
+  for (int i = 0; i < P; ++i) cc[i] = C[i * P + lane];
+  double m = C[lane * (P + 1)];
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const double t = __shfl_xor(m, o);
+    m = t > m ? t : m;
+  }
+  const double fl = m > 0.0 ? 1e-13 * m : 1e-300;
+#pragma unroll
   for (int k = 0; k < P; ++k) {
-    if (tid == 0) {
-      const double piv = c[k][k] > floor_v ? c[k][k] : floor_v;
-      r[k][k] = __builtin_sqrt(piv);
-    }
+    const double ckk = readlane_f64(cc[k], k);
+    const double piv = ckk > fl ? ckk : fl;
+    const double rkk = __builtin_sqrt(piv);
+    const double inv = 1.0 / rkk;
+    const double rk = lane > k ? cc[k] * inv : (lane == k ? rkk : 0.0);
+    rl[k][lane] = rk;
+    if (lane == 0) dinv[k] = inv;
     __syncthreads();
-    for (int j = k + 1 + tid; j < P; j += NT) r[k][j] = c[k][j] / r[k][k];
-    __syncthreads();
-    for (int e = tid; e < P * P; e += NT) {
-      const int i = e / P, j = e % P;
-      if (i > k && j >= i) {
-        const double v = c[i][j] - r[k][i] * r[k][j];
-        c[i][j] = v;
-        c[j][i] = v;
-      }
-    }
-    __syncthreads();
+#pragma unroll
+    for (int i = k + 1; i < P; ++i) cc[i] = __builtin_fma(-rl[k][i], rk, cc[i]);
   }
-  // column col of R^-1 by back substitution (R x = e_col), one thread per
-  // column, into c (no longer needed): thread col only touches column col
-  if (tid < P) {
-    const int col = tid;
-    for (int i = P - 1; i >= 0; --i) {
-      double v = 0.0;
-      if (i <= col) {
-        v = (i == col) ? 1.0 : 0.0;
-        for (int k = i + 1; k <= col; ++k) v -= r[i][k] * c[k][col];
-        v /= r[i][i];
-      }
-      c[i][col] = v;
-    }
+  double z[P];
+#pragma unroll
+  for (int i = P - 1; i >= 0; --i) {
+    double v = (i == lane) ? 1.0 : 0.0;
+#pragma unroll
+    for (int k = i + 1; k < P; ++k) v = __builtin_fma(-rl[i][k], z[k], v);
+    z[i] = v * dinv[i];
   }
-  __syncthreads();
-  for (int e = tid; e < P * P; e += NT) Rinv[e] = c[e / P][e % P];
+#pragma unroll
+  for (int i = 0; i < P; ++i) Rinv[i * P + lane] = z[i];
 }
 
-// Vt[i][n] = sum_{k <= i} Rinv[k][i] W[k][n]  (V = W R^-1), one thread per column n
+// Vt[i][n] = sum over k of Rinv[k][i] Wt[k][n] (V = W R^-1; Rinv is zero below
+// its diagonal), k ascending, float64, for the AT columns n of the workgroup.
+// Thread (ti, tn) = (tid / 16, tid % 16) owns rows 4 ti .. 4 ti + 3 and columns
+// 2 tn, 2 tn + 1.
 __global__ __launch_bounds__(NT) void eig_apply_kernel(const float* __restrict__ Wt, const double* __restrict__ Rinv,
                                                        float* __restrict__ Vt, int d) {
-  __shared__ double ri[P * P];
-  for (int e = threadIdx.x; e < P * P; e += NT) ri[e] = Rinv[e];
-  __syncthreads();
-  const int n = blockIdx.x * NT + threadIdx.x;
-  if (n >= d) return;
-  double w[P];
-#pragma unroll
-  for (int k = 0; k < P; ++k) w[k] = Wt[static_cast<int64_t>(k) * d + n];
-#pragma unroll
-  for (int i = 0; i < P; ++i) {
-    double v = 0.0;
-#pragma unroll
-    for (int k = 0; k <= i; ++k) v = __builtin_fma(ri[k * P + i], w[k], v);
-    Vt[static_cast<int64_t>(i) * d + n] = static_cast<float>(v);
+  __shared__ __attribute__((aligned(16))) double rs[P][P];
+  __shared__ __attribute__((aligned(16))) double wsd[P][AT + 2];
+  const int tid = threadIdx.x;
+  const int n0 = blockIdx.x * AT;
+  for (int e = tid; e < P * P / 2; e += NT)
+    *reinterpret_cast<double2*>(&rs[0][2 * e]) = reinterpret_cast<const double2*>(Rinv)[e];
+  for (int e = tid; e < P * AT / 4; e += NT) {
+    const int k = e / (AT / 4), c4 = e % (AT / 4);
+    const float4 w = *reinterpret_cast<const float4*>(Wt + static_cast<int64_t>(k) * d + n0 + 4 * c4);
+    *reinterpret_cast<double2*>(&wsd[k][4 * c4]) = make_double2(w.x, w.y);
+    *reinterpret_cast<double2*>(&wsd[k][4 * c4 + 2]) = make_double2(w.z, w.w);
   }
+  __syncthreads();
+  const int ti = tid >> 4, tn = tid & 15;
+  double acc[4][2];
+#pragma unroll
+  for (int p = 0; p < 4; ++p) acc[p][0] = acc[p][1] = 0.0;
+#pragma unroll 8
+  for (int k = 0; k < P; ++k) {
+    const double2 r01 = *reinterpret_cast<const double2*>(&rs[k][4 * ti]);
+    const double2 r23 = *reinterpret_cast<const double2*>(&rs[k][4 * ti + 2]);
+    const double2 w = *reinterpret_cast<const double2*>(&wsd[k][2 * tn]);
+    const double r[4] = {r01.x, r01.y, r23.x, r23.y};
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      acc[p][0] = __builtin_fma(r[p], w.x, acc[p][0]);
+      acc[p][1] = __builtin_fma(r[p], w.y, acc[p][1]);
+    }
+  }
+#pragma unroll
+  for (int p = 0; p < 4; ++p)
+    *reinterpret_cast<float2*>(Vt + static_cast<int64_t>(4 * ti + p) * d + n0 + 2 * tn) =
+        make_float2(static_cast<float>(acc[p][0]), static_cast<float>(acc[p][1]));
 }
 
-// One workgroup: T = sum of the partials of V^T (G~ V), symmetrised; cyclic
-// Jacobi with the 32 disjoint pairs of each round of the circle method (index 0
-// fixed, 1 .. 63 rotating), a sweep being 63 rounds; the rotation of each pair
-// zeroes T[a][b] (Golub and Van Loan's symmetric 2 x 2 Schur step); stops when
-// the off-diagonal mass is below 1e-26 of the diagonal's, or after 30 sweeps.
-// Out: theta (eigenvalues, descending), Q (its columns the eigenvectors of T in
-// that order), both float64.
-__global__ __launch_bounds__(NT) void eig_jacobi_kernel(const double* __restrict__ gpart, int nch,
-                                                        double* __restrict__ Qout, double* __restrict__ theta) {
+// One workgroup: T = the summed V^T (G~ V), symmetrised; cyclic Jacobi with
+// the 32 disjoint pairs of each round of the circle method (index 0 fixed,
+// 1 .. 63 rotating), a sweep being 63 rounds; the rotation of each pair zeroes
+// T[a][b] (Golub and Van Loan's symmetric 2 x 2 Schur step).  The pairs of a
+// round are disjoint and cover every index, so T <- J^T T J splits into the
+// 32 x 32 independent 2 x 2 blocks (rows of pair k, columns of pair m), each
+// updated in one pass (rows, then columns), and Q <- Q J into 64 x 32
+// independent row pairs.  Stops when the off-diagonal mass is below 1e-26 of
+// the diagonal's, or after 30 sweeps.  Out: theta (eigenvalues, descending),
+// Q (its columns the eigenvectors of T in that order), both float64.
+__global__ __launch_bounds__(NT) void eig_jacobi_kernel(const double* __restrict__ C, double* __restrict__ Qout,
+                                                        double* __restrict__ theta) {
   __shared__ double t[P][P + 1], q[P][P + 1];
-  __shared__ double rc[P / 2], rs[P / 2];
-  __shared__ int ra[P / 2], rb[P / 2];
-  __shared__ double red[NT];
+  __shared__ double2 rot[P / 2];
+  __shared__ int2 prs[P / 2];
+  __shared__ double red[2][NT];
   __shared__ int order[P];
   __shared__ int done;
   const int tid = threadIdx.x;
-  gram_sum(gpart, nch, t);
-  for (int e = tid; e < P * P; e += NT) q[e / P][e % P] = (e / P == e % P) ? 1.0 : 0.0;
-  if (tid == 0) done = 0;
+  for (int e = tid; e < P * P; e += NT) {
+    const int a = e / P, b = e % P;
+    t[a][b] = a == b ? C[e] : 0.5 * (C[a * P + b] + C[b * P + a]);
+    q[a][b] = a == b ? 1.0 : 0.0;
+  }
   __syncthreads();
+  const int bk = tid >> 3, bm0 = tid & 7;      // T blocks (bk, bm0 + 8 j)
+  const int qm = tid & 31, qi0 = tid >> 5;     // Q rows qi0 + 8 u of pair qm
   for (int sweep = 0; sweep < 30; ++sweep) {
-    // convergence test
     double off = 0.0, dia = 0.0;
     for (int e = tid; e < P * P; e += NT) {
       const double v = t[e / P][e % P];
       if (e / P == e % P) dia += v * v; else off += v * v;
     }
-    red[tid] = off;
+    red[0][tid] = off;
+    red[1][tid] = dia;
     __syncthreads();
     for (int w = NT / 2; w > 0; w >>= 1) {
-      if (tid < w) red[tid] += red[tid + w];
+      if (tid < w) {
+        red[0][tid] += red[0][tid + w];
+        red[1][tid] += red[1][tid + w];
+      }
       __syncthreads();
     }
-    const double off_all = red[0];
-    __syncthreads();
-    red[tid] = dia;
-    __syncthreads();
-    for (int w = NT / 2; w > 0; w >>= 1) {
-      if (tid < w) red[tid] += red[tid + w];
-      __syncthreads();
-    }
-    if (tid == 0) done = !(off_all > 1e-26 * red[0]);
+    if (tid == 0) done = !(red[0][0] > 1e-26 * red[1][0]);
     __syncthreads();
     if (done) break;
     for (int round = 0; round < P - 1; ++round) {
@@ -307,33 +424,35 @@ __global__ __launch_bounds__(NT) void eig_jacobi_kernel(const double* __restrict
           c = 1.0 / __builtin_sqrt(1.0 + tt * tt);
           s = tt * c;
         }
-        ra[k] = a;
-        rb[k] = b;
-        rc[k] = c;
-        rs[k] = s;
+        prs[k] = make_int2(a, b);
+        rot[k] = make_double2(c, s);
       }
       __syncthreads();
-      // rows: T <- J^T T
-      for (int e = tid; e < (P / 2) * P; e += NT) {
-        const int k = e / P, j = e % P;
-        const int a = ra[k], b = rb[k];
-        const double c = rc[k], s = rs[k];
-        const double ta = t[a][j], tb = t[b][j];
-        t[a][j] = c * ta - s * tb;
-        t[b][j] = s * ta + c * tb;
-      }
-      __syncthreads();
-      // columns: T <- T J, Q <- Q J
-      for (int e = tid; e < (P / 2) * P; e += NT) {
-        const int k = e / P, i = e % P;
-        const int a = ra[k], b = rb[k];
-        const double c = rc[k], s = rs[k];
-        const double ta = t[i][a], tb = t[i][b];
-        t[i][a] = c * ta - s * tb;
-        t[i][b] = s * ta + c * tb;
-        const double qa = q[i][a], qb = q[i][b];
-        q[i][a] = c * qa - s * qb;
-        q[i][b] = s * qa + c * qb;
+      {
+        const int2 ab = prs[bk];
+        const double2 cs = rot[bk];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int bm = bm0 + 8 * j;
+          const int2 ef = prs[bm];
+          const double2 cs2 = rot[bm];
+          const double xae = t[ab.x][ef.x], xaf = t[ab.x][ef.y], xbe = t[ab.y][ef.x], xbf = t[ab.y][ef.y];
+          const double yae = cs.x * xae - cs.y * xbe, yaf = cs.x * xaf - cs.y * xbf;
+          const double ybe = cs.y * xae + cs.x * xbe, ybf = cs.y * xaf + cs.x * xbf;
+          t[ab.x][ef.x] = cs2.x * yae - cs2.y * yaf;
+          t[ab.x][ef.y] = cs2.y * yae + cs2.x * yaf;
+          t[ab.y][ef.x] = cs2.x * ybe - cs2.y * ybf;
+          t[ab.y][ef.y] = cs2.y * ybe + cs2.x * ybf;
+        }
+        const int2 gh = prs[qm];
+        const double2 cq = rot[qm];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int i = qi0 + 8 * u;
+          const double qa = q[i][gh.x], qb = q[i][gh.y];
+          q[i][gh.x] = cq.x * qa - cq.y * qb;
+          q[i][gh.y] = cq.y * qa + cq.x * qb;
+        }
       }
       __syncthreads();
     }
@@ -356,59 +475,66 @@ __global__ __launch_bounds__(NT) void eig_jacobi_kernel(const double* __restrict
   }
 }
 
-// V[n][i] = sum_j Vt[j][n] Q[j][i] for i < r (Ritz vectors, float64 sums), and
-// per workgroup and column the entry of largest magnitude (the first row on
-// ties): its signed value and its row
+// V[n][i] = sum over j of Vt[j][n] Q[j][i] for i < r (Ritz vectors, float64
+// sums, j ascending) over the AT rows n of the workgroup; then per column the
+// entry of largest magnitude among those rows (the first row on ties): its
+// signed value and its row.  Thread (tn, ti0) = (tid % 32, tid / 32) owns
+// row n0 + tn, columns ti0 + 8 u.
 __global__ __launch_bounds__(NT) void eig_ritz_kernel(const float* __restrict__ Vt, const double* __restrict__ Q,
                                                       float* __restrict__ V, float* __restrict__ cmax,
                                                       int* __restrict__ cidx, int d, int r) {
-  __shared__ double qs[P * kEigMaxRank];
-  __shared__ float bm[NT], bv[NT];
-  __shared__ int bi[NT];
-  for (int e = threadIdx.x; e < P * r; e += NT) qs[e] = Q[(e / r) * P + (e % r)];
+  __shared__ double qs[P][kEigMaxRank];
+  __shared__ double vs[P][AT + 1];
+  __shared__ float out[AT][kEigMaxRank + 1];
+  const int tid = threadIdx.x;
+  const int n0 = blockIdx.x * AT;
+  for (int e = tid; e < P * r; e += NT) qs[e / r][e % r] = Q[(e / r) * P + (e % r)];
+  for (int e = tid; e < P * AT; e += NT) {
+    const int k = e / AT, c = e % AT;
+    vs[k][c] = Vt[static_cast<int64_t>(k) * d + n0 + c];
+  }
   __syncthreads();
-  const int n = blockIdx.x * NT + threadIdx.x;
-  double w[P];
+  const int tn = tid & 31, ti0 = tid >> 5;
+  constexpr int U = kEigMaxRank / 8;
+  double acc[U];
 #pragma unroll
-  for (int k = 0; k < P; ++k) w[k] = (n < d) ? Vt[static_cast<int64_t>(k) * d + n] : 0.0f;
-  for (int i = 0; i < r; ++i) {
-    double v = 0.0;
-    for (int k = 0; k < P; ++k) v = __builtin_fma(w[k], qs[k * r + i], v);
-    const float f = static_cast<float>(v);
-    if (n < d) V[static_cast<int64_t>(n) * r + i] = f;
-    bm[threadIdx.x] = (n < d) ? __builtin_fabsf(f) : -1.0f;
-    bv[threadIdx.x] = f;
-    bi[threadIdx.x] = n;
-    __syncthreads();
-    for (int s = NT / 2; s > 0; s >>= 1) {
-      if (threadIdx.x < s) {
-        const float o = bm[threadIdx.x + s];
-        const int oi = bi[threadIdx.x + s];
-        if (o > bm[threadIdx.x] || (o == bm[threadIdx.x] && oi < bi[threadIdx.x])) {
-          bm[threadIdx.x] = o;
-          bv[threadIdx.x] = bv[threadIdx.x + s];
-          bi[threadIdx.x] = oi;
-        }
+  for (int u = 0; u < U; ++u) acc[u] = 0.0;
+  for (int k = 0; k < P; ++k) {
+    const double v = vs[k][tn];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (ti0 + 8 * u < r) acc[u] = __builtin_fma(v, qs[k][ti0 + 8 * u], acc[u]);
+  }
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+    if (ti0 + 8 * u < r) out[tn][ti0 + 8 * u] = static_cast<float>(acc[u]);
+  __syncthreads();
+  for (int e = tid; e < AT * r; e += NT) V[static_cast<int64_t>(n0) * r + e] = out[e / r][e % r];
+  if (tid < r) {
+    float best = -1.0f, bval = 0.0f;
+    int bidx = 0;
+    for (int c = 0; c < AT; ++c) {
+      const float f = out[c][tid];
+      if (__builtin_fabsf(f) > best) {
+        best = __builtin_fabsf(f);
+        bval = f;
+        bidx = n0 + c;
       }
-      __syncthreads();
     }
-    if (threadIdx.x == 0) {
-      cmax[blockIdx.x * r + i] = bv[0];
-      cidx[blockIdx.x * r + i] = bi[0];
-    }
-    __syncthreads();
+    cmax[blockIdx.x * r + tid] = bval;
+    cidx[blockIdx.x * r + tid] = bidx;
   }
 }
 
 // Each workgroup finds, for every column, the entry of largest magnitude (the
-// first row on ties) among the per-workgroup maxima, and flips its own rows
+// first row on ties) among the per-workgroup maxima, and flips its own AT rows
 // of the column if that entry is negative (only the maxima written by the
 // previous launch are read, never another workgroup's rows); workgroup 0
 // writes the r eigenvalues.
 __global__ __launch_bounds__(NT) void eig_sign_kernel(float* __restrict__ V, const float* __restrict__ cmax,
                                                       const int* __restrict__ cidx, int nblk,
                                                       const double* __restrict__ theta, float* __restrict__ evals,
-                                                      int d, int r) {
+                                                      int r) {
   __shared__ float sgn[kEigMaxRank];
   if (threadIdx.x < r) {
     const int i = threadIdx.x;
@@ -428,21 +554,20 @@ __global__ __launch_bounds__(NT) void eig_sign_kernel(float* __restrict__ V, con
     if (blockIdx.x == 0) evals[i] = static_cast<float>(theta[i]);
   }
   __syncthreads();
-  const int n = blockIdx.x * NT + threadIdx.x;
-  if (n < d)
-    for (int i = 0; i < r; ++i) V[static_cast<int64_t>(n) * r + i] *= sgn[i];
+  float* tile = V + static_cast<int64_t>(blockIdx.x) * AT * r;
+  for (int e = threadIdx.x; e < AT * r; e += NT) tile[e] *= sgn[e % r];
 }
 
 int gemm_splits(int d) {
   int s = d / 512;
   s = s < 1 ? 1 : (s > 8 ? 8 : s);
-  while (s > 1 && (d % s != 0 || (d / s) % 8 != 0)) --s;
+  while (s > 1 && (d % s != 0 || (d / s) % 64 != 0)) --s;
   return s;
 }
 
 struct EigWs {
   float *Vt, *Wt, *Xt, *part;
-  double *gpart, *Rinv, *Q, *theta;
+  double *gpart, *C, *Rinv, *Q, *theta;
   float* cmax;
   int* cidx;
 };
@@ -452,7 +577,7 @@ int64_t align256(int64_t b) { return (b + 255) & ~int64_t(255); }
 int64_t layout(int d, int r, char* base, EigWs* w) {
   const int S = gemm_splits(d);
   const int64_t blk = static_cast<int64_t>(P) * d * 4;
-  const int nblk = (d + NT - 1) / NT;
+  const int nblk = d / AT;
   int64_t off = 0;
   auto take = [&](int64_t bytes) {
     char* p = base ? base + off : nullptr;
@@ -464,6 +589,7 @@ int64_t layout(int d, int r, char* base, EigWs* w) {
   char* xt = take(blk);
   char* part = take(blk * S);
   char* gp = take(static_cast<int64_t>(d / GCH) * P * P * 8);
+  char* cs = take(P * P * 8);
   char* ri = take(P * P * 8);
   char* q = take(P * P * 8);
   char* th = take(P * 8);
@@ -475,6 +601,7 @@ int64_t layout(int d, int r, char* base, EigWs* w) {
     w->Xt = reinterpret_cast<float*>(xt);
     w->part = reinterpret_cast<float*>(part);
     w->gpart = reinterpret_cast<double*>(gp);
+    w->C = reinterpret_cast<double*>(cs);
     w->Rinv = reinterpret_cast<double*>(ri);
     w->Q = reinterpret_cast<double*>(q);
     w->theta = reinterpret_cast<double*>(th);
@@ -494,26 +621,32 @@ hipError_t launch_aog_eig(int d, int r, int iters, const float* A, float scale, 
   layout(d, r, static_cast<char*>(workspace), &w);
   const int S = gemm_splits(d);
   const int nch = d / GCH;
-  const int nblk = (d + NT - 1) / NT;
-  const size_t row_lds = static_cast<size_t>(d) * sizeof(float);
+  const int nblk = d / AT;
+  const int L = row_segment(d, B);
+  const size_t seg_lds = static_cast<size_t>(L) * sizeof(float);
   const bool pre = (lam != nullptr) || B > 1;
 
   // block -> block: G~ applied to the rows of `in` (p x d), into `out`
   auto apply_op = [&](const float* in, float* out) {
     const float* x = in;
     if (pre) {
-      hipLaunchKernelGGL(eig_row_kernel<false>, dim3(P), dim3(NT), row_lds, st, in, 1, int64_t(0), w.Xt, lam, B,
-                         1.0f, d);
+      hipLaunchKernelGGL(eig_row_kernel<false>, dim3(d / L, P), dim3(NT), seg_lds, st, in, 1, int64_t(0), w.Xt,
+                         lam, B, 1.0f, d, L);
       x = w.Xt;
     }
     hipLaunchKernelGGL(eig_gemm_kernel, dim3(d / 64, S), dim3(NT), 0, st, x, A, w.part, d, d / S);
-    hipLaunchKernelGGL(eig_row_kernel<true>, dim3(P), dim3(NT), row_lds, st, w.part, S,
-                       static_cast<int64_t>(P) * d, out, lam, B, scale, d);
+    hipLaunchKernelGGL(eig_row_kernel<true>, dim3(d / L, P), dim3(NT), seg_lds, st, w.part, S,
+                       static_cast<int64_t>(P) * d, out, lam, B, scale, d, L);
+  };
+  // C = U W^T (float64) from the block rows of U and W
+  auto gram = [&](const float* u, const float* wv) {
+    hipLaunchKernelGGL(eig_gram_kernel, dim3(nch), dim3(NT), 0, st, u, wv, w.gpart, d);
+    hipLaunchKernelGGL(eig_gsum_kernel, dim3(P * P / 64), dim3(NT), 0, st, w.gpart, nch, w.C);
   };
   // rows of `src` orthonormalised into `dst` (one CholeskyQR pass)
   auto orth = [&](const float* src, float* dst) {
-    hipLaunchKernelGGL(eig_gram_kernel, dim3(nch), dim3(NT), 0, st, src, src, w.gpart, d);
-    hipLaunchKernelGGL(eig_chol_kernel, dim3(1), dim3(NT), 0, st, w.gpart, nch, w.Rinv);
+    gram(src, src);
+    hipLaunchKernelGGL(eig_chol_kernel, dim3(1), dim3(64), 0, st, w.C, w.Rinv);
     hipLaunchKernelGGL(eig_apply_kernel, dim3(nblk), dim3(NT), 0, st, src, w.Rinv, dst, d);
   };
 
@@ -531,10 +664,10 @@ hipError_t launch_aog_eig(int d, int r, int iters, const float* A, float scale, 
   }
   // Rayleigh-Ritz on the final block
   apply_op(w.Vt, w.Wt);
-  hipLaunchKernelGGL(eig_gram_kernel, dim3(nch), dim3(NT), 0, st, w.Vt, w.Wt, w.gpart, d);
-  hipLaunchKernelGGL(eig_jacobi_kernel, dim3(1), dim3(NT), 0, st, w.gpart, nch, w.Q, w.theta);
+  gram(w.Vt, w.Wt);
+  hipLaunchKernelGGL(eig_jacobi_kernel, dim3(1), dim3(NT), 0, st, w.C, w.Q, w.theta);
   hipLaunchKernelGGL(eig_ritz_kernel, dim3(nblk), dim3(NT), 0, st, w.Vt, w.Q, V, w.cmax, w.cidx, d, r);
-  hipLaunchKernelGGL(eig_sign_kernel, dim3(nblk), dim3(NT), 0, st, V, w.cmax, w.cidx, nblk, w.theta, evals, d, r);
+  hipLaunchKernelGGL(eig_sign_kernel, dim3(nblk), dim3(NT), 0, st, V, w.cmax, w.cidx, nblk, w.theta, evals, r);
   return hipGetLastError();
 }
 

@@ -34,9 +34,10 @@ def test_reduce_counters_scales_each_counter_by_the_copy_probe(tmp_path):
     # a 256 MiB probe whose FETCH_SIZE reads half its bytes (factor 2) and
     # whose WRITE_SIZE reads them exactly (factor 1); three GEMM dispatches
     g = f"void qwam::{bench.GEMM_KERNEL}(unsigned char const*, ...)"
-    c = f"void at::native::{bench.COPY_KERNEL}<float>(...)"
+    c = f"{bench.COPY_KERNEL}HIP_vector_type<unsigned int, 4u> const*, ...)"
+    torch_copy = "void at::native::vectorized_elementwise_kernel<4, copy_kernel(...)"
     fetch, write = tmp_path / "f.csv", tmp_path / "w.csv"
-    _write_counters(fetch, [(g, 1000.0), (c, 131072.0), (g, 1100.0), (g, 900.0)])
+    _write_counters(fetch, [(g, 1000.0), (c, 131072.0), (torch_copy, 7.0), (g, 1100.0), (g, 900.0)])
     _write_counters(write, [(c, 262144.0), (g, 500.0), (g, 500.0), (g, 500.0)])
     rec = bench.reduce_counters(str(fetch), str(write), 256)
     assert rec["fetch_factor"] == pytest.approx(2.0)
