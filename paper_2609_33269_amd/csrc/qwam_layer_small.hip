@@ -2,7 +2,11 @@
 // one launch: the activation step of qwam_quantize_act and the GEMM of
 // qwam_asp_linear, fused.  With so few tokens both steps are latency-bound
 // (a launch floor of ~1.5 us each and a dependent memory round trip in
-// between), so every workgroup quantizes the tokens it needs itself.
+// between), so every workgroup quantizes the tokens it needs itself.  That
+// quantization is the bulk of a workgroup's vector work and is repeated by
+// every workgroup of a token block, so a CU is best given one workgroup:
+// the 16-token form (the second kernel below, 16 x 16 NB outputs) runs when
+// at most 256 workgroups cover y, the 32-token form otherwise:
 //
 //   * a workgroup owns a 32 x 32 block of y (32 tokens x 32 output channels)
 //     and all of K; its 8 waves split the 64-channel spans into contiguous
@@ -262,22 +266,27 @@ __global__ __launch_bounds__(64 * LW) void asp_layer_small_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// The same layer for at most 16 tokens.  A 32-token block would be half
-// padding, so the workgroup owns 16 tokens x 16 output channels and runs the
-// integer partials on v_mfma_scale_f32_16x16x128_f8f6f4: lane l holds token
-// (or output channel) l % 16 and channels 32*(l/16) .. +31 of a 128-channel
+// The same layer in 16-token blocks.  The workgroup owns 16 tokens x 16 NB
+// output channels (NB = 1, 2 or 4 blocks of 16) and runs the integer
+// partials on v_mfma_scale_f32_16x16x128_f8f6f4: lane l holds token (or
+// output channel) l % 16 and channels 32*(l/16) .. +31 of a 128-channel
 // step, i.e. two 64-channel spans, lane groups 0-1 the first and 2-3 the
 // second.  Each span's partial is its own instruction, with the other span's
 // lane scales at 2^-127 on both operands (their products underflow to zero).
 // Per lane and step this quantizes 32 real channels (the 32-token form
-// quantizes 32 channels for two tokens of which one is padding at M <= 16).
+// quantizes 32 channels for two tokens), and the NB weight blocks reuse the
+// quantized operand.  Every workgroup quantizes its 16 tokens itself, so the
+// quantization is repeated once per workgroup of a token block; the launcher
+// takes this form when it fits one workgroup per CU (at most 256 workgroups
+// with NB <= 4), the 32-token form above otherwise.  With NB = 4 (only for
+// K <= 1024, one step per wave) there is no prefetch buffer.
 //
 // The K split (eight waves, contiguous ranges of spans), the order of the
 // per-span scaling and of the sum over the waves, and the epilogue's
 // v_mfma_f32_32x32x16_bf16 (rows 16-31 zero) are those of the few-token
 // GEMM, so the two paths give the same y from the same codes, scales and t.
 // ---------------------------------------------------------------------------
-template <int RANK>
+template <int RANK, int NB>
 __global__ __launch_bounds__(64 * LW) void asp_layer_tiny_kernel(
     const uint16_t* __restrict__ x, const float* __restrict__ inv_smooth, const uint16_t* __restrict__ L1t,
     const uint8_t* __restrict__ wq, const float* __restrict__ ws, const uint16_t* __restrict__ L2t,
@@ -289,16 +298,20 @@ __global__ __launch_bounds__(64 * LW) void asp_layer_tiny_kernel(
   // dynamic LDS: partial acc [LW][16][16] | partial t [LW][16][RANK] | t bf16 [16][RANK] | 1/lambda [K]
   // and 128 floats that a second span past K reads (its values are discarded)
   extern __shared__ __attribute__((aligned(16))) float lds[];
+  constexpr int BN = TBK * NB;            // output channels of the workgroup
   float* red_acc = lds;
-  float* red_t = red_acc + LW * TBK * TBK;
+  float* red_t = red_acc + LW * TBK * BN;
   uint16_t* t_l = reinterpret_cast<uint16_t*>(red_t + LW * TBK * RANK);
   float* inv_l = red_t + LW * TBK * RANK + TBK * RANK / 2;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int n0 = blockIdx.x * TBK;
-  const bool write_act = xq_out != nullptr && blockIdx.x == 0;
+  const int ncb = (N + BN - 1) / BN;
+  const int n0 = (blockIdx.x % ncb) * BN;
+  const int m0 = (blockIdx.x / ncb) * TBK;
+  const int rows = min(TBK, M - m0);
+  const bool write_act = xq_out != nullptr && blockIdx.x % ncb == 0;
   const int G = K / kGroup;
   const int KB = K / 2;
   const int gpw = (G + LW - 1) / LW;
@@ -309,8 +322,8 @@ __global__ __launch_bounds__(64 * LW) void asp_layer_tiny_kernel(
   const int half = grp >> 1;             // span of the step
   // D of a 16x16 block: lane l holds column l%16 and rows 4*(l/16) + i
 
-  const buf_rsrc x_rsrc = make_rsrc(x, static_cast<uint32_t>(M) * K * 2u);
-  const buf_rsrc w_rsrc = make_rsrc(wq + static_cast<int64_t>(n0) * KB, static_cast<uint32_t>(min(TBK, N - n0)) * KB);
+  const buf_rsrc x_rsrc = make_rsrc(x + static_cast<int64_t>(m0) * K, static_cast<uint32_t>(rows) * K * 2u);
+  const buf_rsrc w_rsrc = make_rsrc(wq + static_cast<int64_t>(n0) * KB, static_cast<uint32_t>(min(BN, N - n0)) * KB);
   const buf_rsrc ws_rsrc = make_rsrc(ws, static_cast<uint32_t>(G) * N * 4u);
   const buf_rsrc l1_rsrc = make_rsrc(L1t, static_cast<uint32_t>(RANK) * K * 2u);
   const uint32_t x_off = static_cast<uint32_t>(frow * K + 32 * grp) * 2u;
@@ -323,8 +336,8 @@ __global__ __launch_bounds__(64 * LW) void asp_layer_tiny_kernel(
 
   struct Fetch {
     uint4 x[4];                    // 32 bf16 of x
-    uint4 w;                       // 32 packed weight codes of column n0 + lane%16
-    float sw[2];                   // weight scales of column n0 + lane%16, both spans
+    uint4 w[NB];                   // 32 packed weight codes of column n0 + 16 b + lane%16
+    float sw[NB][2];               // weight scales of those columns, both spans
     v8s l1[RB][4];
   };
   // the step of spans g, g+1 (g+1 only when below g_hi)
@@ -332,9 +345,13 @@ __global__ __launch_bounds__(64 * LW) void asp_layer_tiny_kernel(
     const uint32_t go = static_cast<uint32_t>(g) * kGroup * 2u;
 #pragma unroll
     for (int q = 0; q < 4; ++q) f.x[q] = buf_load16(x_rsrc, x_off + go + 16u * q);
-    f.w = buf_load16(w_rsrc, w_off + static_cast<uint32_t>(g) * 32u);
 #pragma unroll
-    for (int h = 0; h < 2; ++h) f.sw[h] = buf_load4f(ws_rsrc, sw_off + static_cast<uint32_t>(g + h) * N * 4u);
+    for (int nb = 0; nb < NB; ++nb) {
+      f.w[nb] = buf_load16(w_rsrc, w_off + static_cast<uint32_t>(nb * TBK * KB) + static_cast<uint32_t>(g) * 32u);
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        f.sw[nb][h] = buf_load4f(ws_rsrc, sw_off + static_cast<uint32_t>(nb * TBK) * 4u + static_cast<uint32_t>(g + h) * N * 4u);
+    }
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
@@ -343,7 +360,9 @@ __global__ __launch_bounds__(64 * LW) void asp_layer_tiny_kernel(
             v8s, buf_load16(l1_rsrc, l1_off + static_cast<uint32_t>(16 * rb) * K * 2u + go + 16u * j));
   };
 
-  v4f acc = v4f{0.f, 0.f, 0.f, 0.f};
+  v4f acc[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) acc[nb] = v4f{0.f, 0.f, 0.f, 0.f};
   v4f tacc[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) tacc[rb] = v4f{0.f, 0.f, 0.f, 0.f};
@@ -384,25 +403,29 @@ __global__ __launch_bounds__(64 * LW) void asp_layer_tiny_kernel(
     v8i af;          // words 6-7 are not read with FP6 operands and stay unset
 #pragma unroll
     for (int k = 0; k < 6; ++k) af[k] = static_cast<int>(d[k]);
-    if (write_act && frow < M && (half == 0 || two)) {
+    if (write_act && frow < rows && (half == 0 || two)) {
       const uint2 b0 = fp6_code_block(d[0], d[1], d[2]);
       const uint2 b1 = fp6_code_block(d[3], d[4], d[5]);
-      *reinterpret_cast<uint4*>(xq_out + static_cast<int64_t>(frow) * KB + g * 32 + 16 * grp) =
+      *reinterpret_cast<uint4*>(xq_out + static_cast<int64_t>(m0 + frow) * KB + g * 32 + 16 * grp) =
           make_uint4(b0.x, b0.y, b1.x, b1.y);
-      if ((grp & 1) == 0) xs_out[static_cast<int64_t>(g + half) * M + frow] = s;
+      if ((grp & 1) == 0) xs_out[static_cast<int64_t>(g + half) * M + m0 + frow] = s;
     }
     // the spans' exact integer partials, then acc += P * xs * ws, span g first
-    const v8i bf = codes_to_fp6(f.w);
+    float sxs[2][4];
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      if (h == 1 && !two) break;
-      const int sc = half == h ? kE8M0Code : 0;
-      const v4f p = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(af, bf, v4f{}, kFmtFp6, kFmtFp6, 0, sc, 0, sc);
+    for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        // scale of token 4*(l/16) + i for span h: lane (token, 2h)
-        const float sx = __shfl(s, 4 * grp + i + 32 * h);
-        acc[i] = __builtin_fmaf(p[i], sx * f.sw[h], acc[i]);
+      for (int i = 0; i < 4; ++i) sxs[h][i] = __shfl(s, 4 * grp + i + 32 * h);   // token 4*(l/16)+i, span h
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const v8i bf = codes_to_fp6(f.w[nb]);
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        if (h == 1 && !two) break;
+        const int sc = half == h ? kE8M0Code : 0;
+        const v4f p = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(af, bf, v4f{}, kFmtFp6, kFmtFp6, 0, sc, 0, sc);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[nb][i] = __builtin_fmaf(p[i], sxs[h][i] * f.sw[nb][h], acc[nb][i]);
       }
     }
     // t partial: A = bf16(x~) of 8 channels per MFMA, B = the matching L1t slice
@@ -417,20 +440,26 @@ __global__ __launch_bounds__(64 * LW) void asp_layer_tiny_kernel(
     }
   };
 
-  // epilogue operands: the 32x32 MFMA's B (L2t rows of the block's columns,
-  // columns 16-31 zero) and the bias bits (converted only at the end)
+  // epilogue operands: the 32x32 MFMA's B (L2t rows of 32 columns of the
+  // block, columns past BN zero) and the bias bits (converted only at the end)
   constexpr int KSTEPS = RANK / 16;
+  constexpr int EB = (BN + 31) / 32;     // 32-column epilogue blocks
   const int ecol = lane & 31, ehalf = lane >> 5;
-  const int nt = n0 + ecol;
-  const bool col_ok = ecol < TBK && nt < N;
   const buf_rsrc l2_rsrc = make_rsrc(L2t + static_cast<int64_t>(n0) * RANK,
-                                     static_cast<uint32_t>(min(TBK, N - n0)) * RANK * 2u);
-  v8s lv[KSTEPS];
-#pragma unroll
-  for (int k = 0; k < KSTEPS; ++k)
-    lv[k] = __builtin_bit_cast(v8s, buf_load16(l2_rsrc, static_cast<uint32_t>(ecol * RANK + k * 16 + ehalf * 8) * 2u));
+                                     static_cast<uint32_t>(min(BN, N - n0)) * RANK * 2u);
   const buf_rsrc b_rsrc = make_rsrc(bias, bias != nullptr ? static_cast<uint32_t>(N) * 2u : 0u);
-  const uint32_t bbits = __builtin_amdgcn_raw_buffer_load_b16(b_rsrc, static_cast<uint32_t>(col_ok ? nt : N) * 2u, 0, 0);
+  v8s lv[EB][KSTEPS];
+  uint32_t bbits[EB];
+#pragma unroll
+  for (int eb = 0; eb < EB; ++eb) {
+    const int c = 32 * eb + ecol;
+    const bool ok = c < BN && n0 + c < N;
+#pragma unroll
+    for (int k = 0; k < KSTEPS; ++k)
+      lv[eb][k] = c < BN ? __builtin_bit_cast(v8s, buf_load16(l2_rsrc, static_cast<uint32_t>(c * RANK + k * 16 + ehalf * 8) * 2u))
+                         : v8s{0, 0, 0, 0, 0, 0, 0, 0};
+    bbits[eb] = __builtin_amdgcn_raw_buffer_load_b16(b_rsrc, static_cast<uint32_t>(ok ? n0 + c : N) * 2u, 0, 0);
+  }
 
   // the wave's slice of 1/lambda to LDS, then the first steps; all of it is
   // waited for before the first step is used
@@ -441,7 +470,15 @@ __global__ __launch_bounds__(64 * LW) void asp_layer_tiny_kernel(
       if (c + 4 * lane < nfl)
         buf_load16_lds(i_rsrc, static_cast<uint32_t>(g_lo * kGroup + c + 4 * lane) * 4u, inv_l + g_lo * kGroup + c);
   }
-  if (g_lo < g_hi) {
+  if constexpr (NB == 4) {
+    // one step per wave (K <= 1024, chosen by the launcher): no prefetch buffer
+    if (g_lo < g_hi) {
+      Fetch fa;
+      fetch(g_lo, fa);
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the 1/lambda copies have landed
+      work(g_lo, fa);
+    }
+  } else if (g_lo < g_hi) {
     Fetch fa, fb;
     fetch(g_lo, fa);
     int g = g_lo;
@@ -459,7 +496,8 @@ __global__ __launch_bounds__(64 * LW) void asp_layer_tiny_kernel(
   // partial blocks -> LDS: acc as [wave][token][column], t as [wave][token][column]
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    red_acc[(wave * TBK + 4 * grp + i) * TBK + frow] = acc[i];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) red_acc[(wave * TBK + 4 * grp + i) * BN + nb * TBK + frow] = acc[nb][i];
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) red_t[(wave * TBK + 4 * grp + i) * RANK + 16 * rb + frow] = tacc[rb][i];
   }
@@ -472,42 +510,57 @@ __global__ __launch_bounds__(64 * LW) void asp_layer_tiny_kernel(
     for (int w = 0; w < LW; ++w) sum += red_t[(w * TBK + tok) * RANK + j];
     const uint16_t b = static_cast<uint16_t>(f32_to_bf16_rne(sum));
     t_l[tok * RANK + j] = b;
-    if (write_act && tok < M) t_out[static_cast<int64_t>(tok) * RANK + j] = b;
+    if (write_act && tok < rows) t_out[static_cast<int64_t>(m0 + tok) * RANK + j] = b;
   }
-  // this wave's result register of the 32x32 epilogue block: v = wave (rows
-  // below 16), token 8(v/4) + 4(l/32) + v%4, column l%32
+  // this wave's result register of the 32x32 epilogue blocks: v = wave (rows
+  // below 16), token 8(v/4) + 4(l/32) + v%4, column 32 eb + l%32
   const int v0 = wave;
   const int tok = 8 * (v0 >> 2) + 4 * ehalf + (v0 & 3);
-  float c2 = 0.0f;
+  float c2[EB];
 #pragma unroll
-  for (int w = 0; w < LW; ++w) c2 += ecol < TBK ? red_acc[(w * TBK + tok) * TBK + ecol] : 0.0f;
+  for (int eb = 0; eb < EB; ++eb) {
+    const int c = 32 * eb + ecol;
+    c2[eb] = 0.0f;
+#pragma unroll
+    for (int w = 0; w < LW; ++w) c2[eb] += c < BN ? red_acc[(w * TBK + tok) * BN + c] : 0.0f;
+  }
   __syncthreads();                      // t_l complete
-  v16f c;
-#pragma unroll
-  for (int v = 0; v < 16; ++v) c[v] = v == v0 ? c2 : 0.0f;
   const int arow = lane & 31;           // A operand: token l%32 (rows 16-31 zero)
 #pragma unroll
-  for (int k = 0; k < KSTEPS; ++k) {
-    v8s tv = v8s{0, 0, 0, 0, 0, 0, 0, 0};
-    if (arow < TBK) tv = *reinterpret_cast<const v8s*>(t_l + arow * RANK + k * 16 + ehalf * 8);
-    c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, tv), __builtin_bit_cast(v8bf, lv[k]), c, 0,
-                                                0, 0);
-  }
-  float yv = 0.0f;
+  for (int eb = 0; eb < EB; ++eb) {
+    v16f c;
 #pragma unroll
-  for (int v = 0; v < 16; ++v)
-    if (v == v0) yv = c[v];
-  if (tok < M && col_ok)
-    y[static_cast<int64_t>(tok) * N + nt] = static_cast<uint16_t>(f32_to_bf16_rne(yv + bf16_to_f32(bbits)));
+    for (int v = 0; v < 16; ++v) c[v] = v == v0 ? c2[eb] : 0.0f;
+#pragma unroll
+    for (int k = 0; k < KSTEPS; ++k) {
+      v8s tv = v8s{0, 0, 0, 0, 0, 0, 0, 0};
+      if (arow < TBK) tv = *reinterpret_cast<const v8s*>(t_l + arow * RANK + k * 16 + ehalf * 8);
+      c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, tv), __builtin_bit_cast(v8bf, lv[eb][k]), c,
+                                                  0, 0, 0);
+    }
+    float yv = 0.0f;
+#pragma unroll
+    for (int v = 0; v < 16; ++v)
+      if (v == v0) yv = c[v];
+    const int col = 32 * eb + ecol;
+    if (tok < rows && col < BN && n0 + col < N)
+      y[static_cast<int64_t>(m0 + tok) * N + n0 + col] =
+          static_cast<uint16_t>(f32_to_bf16_rne(yv + bf16_to_f32(bbits[eb])));
+  }
 }
 
 hipError_t launch_asp_layer_small(int M, int N, int K, int r, const uint16_t* x, const float* inv_smooth,
                                   const uint16_t* L1t, const uint8_t* wq, const float* ws, const uint16_t* L2t,
                                   const uint16_t* bias, uint16_t* y, uint8_t* xq, float* xs, uint16_t* t,
                                   hipStream_t stream) {
-  const bool tiny = M <= 16;
-  const dim3 grid(tiny ? (N + 15) / 16 : ((M + LB - 1) / LB) * ((N + LB - 1) / LB)), block(64 * LW);
-  const size_t lds = tiny ? static_cast<size_t>(LW) * 16 * (16 + r) * 4 + 16 * r * 2 + static_cast<size_t>(K + 128) * 4
+  const int units = ((M + 15) / 16) * ((N + 15) / 16);
+  int nb = 1;
+  const int maxnb = K <= 1024 ? 4 : 2;
+  while (nb < maxnb && units > 256 * nb) nb *= 2;
+  const bool tiny = M <= 16 || units <= 256 * nb;
+  const dim3 grid(tiny ? ((M + 15) / 16) * ((N + 16 * nb - 1) / (16 * nb)) : ((M + LB - 1) / LB) * ((N + LB - 1) / LB)),
+      block(64 * LW);
+  const size_t lds = tiny ? static_cast<size_t>(LW) * 16 * (16 * nb + r) * 4 + 16 * r * 2 + static_cast<size_t>(K + 128) * 4
                           : static_cast<size_t>(2) * LW * 16 * 64 * 4 + LB * r * 2 + static_cast<size_t>(K) * 4;
   auto go = [&](auto kernel) {
     if (lds > 64 * 1024) {
@@ -519,9 +572,13 @@ hipError_t launch_asp_layer_small(int M, int N, int K, int r, const uint16_t* x,
                        K);
     return hipGetLastError();
   };
+  auto pick = [&](auto k1, auto k2, auto k4, auto ksmall) {
+    if (!tiny) return go(ksmall);
+    return nb == 1 ? go(k1) : (nb == 2 ? go(k2) : go(k4));
+  };
   switch (r) {
-    case 16: return tiny ? go(asp_layer_tiny_kernel<16>) : go(asp_layer_small_kernel<16>);
-    case 32: return tiny ? go(asp_layer_tiny_kernel<32>) : go(asp_layer_small_kernel<32>);
+    case 16: return pick(asp_layer_tiny_kernel<16, 1>, asp_layer_tiny_kernel<16, 2>, asp_layer_tiny_kernel<16, 4>, asp_layer_small_kernel<16>);
+    case 32: return pick(asp_layer_tiny_kernel<32, 1>, asp_layer_tiny_kernel<32, 2>, asp_layer_tiny_kernel<32, 4>, asp_layer_small_kernel<32>);
     default: return hipErrorInvalidValue;
   }
 }

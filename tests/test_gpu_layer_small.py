@@ -1,5 +1,6 @@
 """GPU parity of the fused few-token layer (qwam_asp_layer, M <= 64): the
-activation step and the GEMM in one launch.
+activation step and the GEMM in one launch, in both of its forms (16-token
+blocks with one, two or four weight blocks per workgroup; 32-token blocks).
 
 Bit-exact: the codes, packed bytes and scales it reports (the activation
 step's arithmetic is the activation kernel's).  t within its rounding bound
@@ -74,6 +75,13 @@ def test_fused_action_expert_layers(M, N):
     # largest K
     (16, 4160, 80, 32, True),
     (3, 16384, 48, 16, False),
+    # 16-token blocks with two or four weight blocks per workgroup (ragged
+    # last token block and last column block), and the 32-token form once
+    # more than 256 workgroups would be needed
+    (48, 1024, 4160, 32, False),
+    (32, 2048, 4096, 32, True),
+    (64, 2048, 2304, 16, True),
+    (64, 1024, 8192, 16, False),
 ])
 def test_fused_edge_shapes(M, K, N, r, bias):
     d = I.custom(M=M, K=K, N=N, r=r, seed=M * 23 + K, n_outliers=max(1, K // 100), with_bias=bias)
