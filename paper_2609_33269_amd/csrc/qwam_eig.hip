@@ -15,10 +15,11 @@
 //       Y = s H diag(lambda) W        (fixed-order sum of the K splits, row transform)
 //     A is d x d and read once per product (HBM-bound); the block is p x d
 //     and stays in L2;
-//   * orthonormalisation by CholeskyQR2: Gram matrix in float64 (per-chunk
+//   * orthonormalisation by CholeskyQR: Gram matrix in float64 (per-chunk
 //     partials, then a fixed-order sum in a kernel of its own), Cholesky and
 //     triangular inverse in one wave with the matrix in registers, then
-//     V = W R^-1 (tiled, float64 sums);
+//     V = W R^-1 (tiled, float64 sums); one pass per iteration, two (i.e.
+//     CholeskyQR2) on the block that enters Rayleigh-Ritz;
 //   * Rayleigh-Ritz: T = V^T G~ V (p x p, float64), parallel cyclic Jacobi in
 //     one workgroup (disjoint rotation pairs by the circle method), Ritz
 //     vectors V Q sorted by eigenvalue, descending; the largest-magnitude entry
@@ -39,6 +40,7 @@ constexpr int P = kEigBlock;     // block width (64)
 constexpr int NT = 256;
 constexpr int GCH = 64;          // columns per Gram partial
 constexpr int AT = 32;           // columns (rows of V) per workgroup of the basis update and Ritz step
+constexpr int JT = 512;          // threads of the Jacobi workgroup
 
 typedef float v16f __attribute__((ext_vector_type(16)));
 
@@ -282,10 +284,11 @@ __device__ __forceinline__ double readlane_f64(double v, int l) {
 // part (right-looking).  Only the upper triangle of C is read.  A pivot below
 // 1e-13 of the largest diagonal entry (a block of lower rank) is raised to
 // that floor, so the inverse stays finite; the next iterations refill such a
-// direction.  Column j of R^-1 is then lane j's back substitution R z = e_j
-// over the rows of R in LDS.
+// direction.  Column j of R^-1 is then lane j's back substitution R z = e_j,
+// column by column over R in LDS.
 __global__ __launch_bounds__(64) void eig_chol_kernel(const double* __restrict__ C, double* __restrict__ Rinv) {
-  __shared__ __attribute__((aligned(16))) double rl[P][P + 2];
+  __shared__ __attribute__((aligned(16))) double rl[P][P + 2];    // rows of R
+  __shared__ __attribute__((aligned(16))) double rc[P][P + 2];    // columns of R: rc[j][k] = R[k][j]
   __shared__ double dinv[P];
   const int lane = threadIdx.x;
   double cc[P];
@@ -298,26 +301,43 @@ __global__ __launch_bounds__(64) void eig_chol_kernel(const double* __restrict__
     m = t > m ? t : m;
   }
   const double fl = m > 0.0 ? 1e-13 * m : 1e-300;
+  // software pipeline: the pivot of step k + 1 is taken as soon as its
+  // column is updated, so its square root and division overlap the rest of
+  // step k's update (both lie between the same two barriers)
+  auto pivot = [&](double ckk, double& rkk, double& inv) __attribute__((always_inline)) {
+    const double piv = ckk > fl ? ckk : fl;
+    rkk = __builtin_sqrt(piv);
+    inv = 1.0 / rkk;
+  };
+  double rkk, inv;
+  pivot(readlane_f64(cc[0], 0), rkk, inv);
 #pragma unroll
   for (int k = 0; k < P; ++k) {
-    const double ckk = readlane_f64(cc[k], k);
-    const double piv = ckk > fl ? ckk : fl;
-    const double rkk = __builtin_sqrt(piv);
-    const double inv = 1.0 / rkk;
     const double rk = lane > k ? cc[k] * inv : (lane == k ? rkk : 0.0);
     rl[k][lane] = rk;
+    rc[lane][k] = rk;
     if (lane == 0) dinv[k] = inv;
     __syncthreads();
+    double rkk_n = 0.0, inv_n = 0.0;
+    if (k + 1 < P) {
+      cc[k + 1] = __builtin_fma(-rl[k][k + 1], rk, cc[k + 1]);
+      pivot(readlane_f64(cc[k + 1], k + 1), rkk_n, inv_n);
+    }
 #pragma unroll
-    for (int i = k + 1; i < P; ++i) cc[i] = __builtin_fma(-rl[k][i], rk, cc[i]);
+    for (int i = k + 2; i < P; ++i) cc[i] = __builtin_fma(-rl[k][i], rk, cc[i]);
+    rkk = rkk_n;
+    inv = inv_n;
   }
+  // column-oriented: z_i = b_i / R[i][i], then b_k -= R[k][i] z_i for k < i,
+  // so the dependent chain is one multiply and one FMA per row
   double z[P];
 #pragma unroll
-  for (int i = P - 1; i >= 0; --i) {
-    double v = (i == lane) ? 1.0 : 0.0;
+  for (int i = 0; i < P; ++i) z[i] = (i == lane) ? 1.0 : 0.0;
 #pragma unroll
-    for (int k = i + 1; k < P; ++k) v = __builtin_fma(-rl[i][k], z[k], v);
-    z[i] = v * dinv[i];
+  for (int i = P - 1; i >= 0; --i) {
+    z[i] *= dinv[i];
+#pragma unroll
+    for (int k = 0; k < i; ++k) z[k] = __builtin_fma(-rc[i][k], z[i], z[k]);
   }
 #pragma unroll
   for (int i = 0; i < P; ++i) Rinv[i * P + lane] = z[i];
@@ -374,33 +394,33 @@ __global__ __launch_bounds__(NT) void eig_apply_kernel(const float* __restrict__
 // independent row pairs.  Stops when the off-diagonal mass is below 1e-26 of
 // the diagonal's, or after 30 sweeps.  Out: theta (eigenvalues, descending),
 // Q (its columns the eigenvectors of T in that order), both float64.
-__global__ __launch_bounds__(NT) void eig_jacobi_kernel(const double* __restrict__ C, double* __restrict__ Qout,
+__global__ __launch_bounds__(JT) void eig_jacobi_kernel(const double* __restrict__ C, double* __restrict__ Qout,
                                                         double* __restrict__ theta) {
   __shared__ double t[P][P + 1], q[P][P + 1];
   __shared__ double2 rot[P / 2];
   __shared__ int2 prs[P / 2];
-  __shared__ double red[2][NT];
+  __shared__ double red[2][JT];
   __shared__ int order[P];
   __shared__ int done;
   const int tid = threadIdx.x;
-  for (int e = tid; e < P * P; e += NT) {
+  for (int e = tid; e < P * P; e += JT) {
     const int a = e / P, b = e % P;
     t[a][b] = a == b ? C[e] : 0.5 * (C[a * P + b] + C[b * P + a]);
     q[a][b] = a == b ? 1.0 : 0.0;
   }
   __syncthreads();
-  const int bk = tid >> 3, bm0 = tid & 7;      // T blocks (bk, bm0 + 8 j)
-  const int qm = tid & 31, qi0 = tid >> 5;     // Q rows qi0 + 8 u of pair qm
+  const int bk = tid >> 4, bm0 = tid & 15;     // T blocks (bk, bm0 + 16 j)
+  const int qm = tid & 31, qi0 = tid >> 5;     // Q rows qi0 + 16 u of pair qm
   for (int sweep = 0; sweep < 30; ++sweep) {
     double off = 0.0, dia = 0.0;
-    for (int e = tid; e < P * P; e += NT) {
+    for (int e = tid; e < P * P; e += JT) {
       const double v = t[e / P][e % P];
       if (e / P == e % P) dia += v * v; else off += v * v;
     }
     red[0][tid] = off;
     red[1][tid] = dia;
     __syncthreads();
-    for (int w = NT / 2; w > 0; w >>= 1) {
+    for (int w = JT / 2; w > 0; w >>= 1) {
       if (tid < w) {
         red[0][tid] += red[0][tid + w];
         red[1][tid] += red[1][tid + w];
@@ -432,8 +452,8 @@ __global__ __launch_bounds__(NT) void eig_jacobi_kernel(const double* __restrict
         const int2 ab = prs[bk];
         const double2 cs = rot[bk];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int bm = bm0 + 8 * j;
+        for (int j = 0; j < 2; ++j) {
+          const int bm = bm0 + 16 * j;
           const int2 ef = prs[bm];
           const double2 cs2 = rot[bm];
           const double xae = t[ab.x][ef.x], xaf = t[ab.x][ef.y], xbe = t[ab.y][ef.x], xbf = t[ab.y][ef.y];
@@ -447,8 +467,8 @@ __global__ __launch_bounds__(NT) void eig_jacobi_kernel(const double* __restrict
         const int2 gh = prs[qm];
         const double2 cq = rot[qm];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int i = qi0 + 8 * u;
+        for (int u = 0; u < 4; ++u) {
+          const int i = qi0 + 16 * u;
           const double qa = q[i][gh.x], qb = q[i][gh.y];
           q[i][gh.x] = cq.x * qa - cq.y * qb;
           q[i][gh.y] = cq.y * qa + cq.x * qb;
@@ -469,7 +489,7 @@ __global__ __launch_bounds__(NT) void eig_jacobi_kernel(const double* __restrict
   }
   __syncthreads();
   if (tid < P) theta[tid] = t[order[tid]][order[tid]];
-  for (int e = tid; e < P * P; e += NT) {
+  for (int e = tid; e < P * P; e += JT) {
     const int i = e / P, col = e % P;
     Qout[i * P + col] = q[i][order[col]];
   }
@@ -530,32 +550,54 @@ __global__ __launch_bounds__(NT) void eig_ritz_kernel(const float* __restrict__ 
 // first row on ties) among the per-workgroup maxima, and flips its own AT rows
 // of the column if that entry is negative (only the maxima written by the
 // previous launch are read, never another workgroup's rows); workgroup 0
-// writes the r eigenvalues.
+// writes the r eigenvalues.  The scan: thread (part, column) takes every
+// (NT / r)-th block maximum, the parts are merged in LDS.
+__device__ __forceinline__ bool better_max(float am, int mi, float best, int bidx) {
+  return am > best || (am == best && mi < bidx);
+}
+
 __global__ __launch_bounds__(NT) void eig_sign_kernel(float* __restrict__ V, const float* __restrict__ cmax,
                                                       const int* __restrict__ cidx, int nblk,
                                                       const double* __restrict__ theta, float* __restrict__ evals,
                                                       int r) {
   __shared__ float sgn[kEigMaxRank];
-  if (threadIdx.x < r) {
-    const int i = threadIdx.x;
-    float best = -1.0f, bval = 0.0f;
-    int bidx = 0;
-    for (int b = 0; b < nblk; ++b) {
+  __shared__ float pbest[NT], pval[NT];
+  __shared__ int pidx[NT];
+  const int tid = threadIdx.x;
+  const int parts = NT / r;
+  const int i = tid % r, part = tid / r;
+  float best = -1.0f, bval = 0.0f;
+  int bidx = 0x7fffffff;
+  if (part < parts) {
+    for (int b = part; b < nblk; b += parts) {
       const float m = cmax[b * r + i];
       const int mi = cidx[b * r + i];
-      const float am = __builtin_fabsf(m);
-      if (am > best || (am == best && mi < bidx)) {
-        best = am;
+      if (better_max(__builtin_fabsf(m), mi, best, bidx)) {
+        best = __builtin_fabsf(m);
         bval = m;
         bidx = mi;
       }
     }
-    sgn[i] = bval < 0.0f ? -1.0f : 1.0f;
-    if (blockIdx.x == 0) evals[i] = static_cast<float>(theta[i]);
+  }
+  pbest[tid] = best;
+  pval[tid] = bval;
+  pidx[tid] = bidx;
+  __syncthreads();
+  if (tid < r) {
+    for (int q = 1; q < parts; ++q) {
+      const int o = q * r + tid;
+      if (better_max(pbest[o], pidx[o], best, bidx)) {
+        best = pbest[o];
+        bval = pval[o];
+        bidx = pidx[o];
+      }
+    }
+    sgn[tid] = bval < 0.0f ? -1.0f : 1.0f;
+    if (blockIdx.x == 0) evals[tid] = static_cast<float>(theta[tid]);
   }
   __syncthreads();
   float* tile = V + static_cast<int64_t>(blockIdx.x) * AT * r;
-  for (int e = threadIdx.x; e < AT * r; e += NT) tile[e] *= sgn[e % r];
+  for (int e = tid; e < AT * r; e += NT) tile[e] *= sgn[e % r];
 }
 
 int gemm_splits(int d) {
@@ -652,20 +694,19 @@ hipError_t launch_aog_eig(int d, int r, int iters, const float* A, float scale, 
 
   hipLaunchKernelGGL(eig_init_kernel, dim3((P * d + NT - 1) / NT), dim3(NT), 0, st, w.Vt, d,
                      static_cast<uint64_t>(0x51ED2701ull));
+  // one CholeskyQR pass per iteration (the next product only needs a
+  // well-conditioned block); the block that enters Rayleigh-Ritz gets the
+  // second pass of CholeskyQR2
   orth(w.Vt, w.Wt);
-  orth(w.Wt, w.Vt);
   for (int it = 0; it < iters; ++it) {
-    apply_op(w.Vt, w.Wt);
-    orth(w.Wt, w.Vt);
+    apply_op(w.Wt, w.Vt);
     orth(w.Vt, w.Wt);
-    float* tmp = w.Vt;   // the orthonormal block is now in Wt
-    w.Vt = w.Wt;
-    w.Wt = tmp;
   }
+  orth(w.Wt, w.Vt);
   // Rayleigh-Ritz on the final block
   apply_op(w.Vt, w.Wt);
   gram(w.Vt, w.Wt);
-  hipLaunchKernelGGL(eig_jacobi_kernel, dim3(1), dim3(NT), 0, st, w.C, w.Q, w.theta);
+  hipLaunchKernelGGL(eig_jacobi_kernel, dim3(1), dim3(JT), 0, st, w.C, w.Q, w.theta);
   hipLaunchKernelGGL(eig_ritz_kernel, dim3(nblk), dim3(NT), 0, st, w.Vt, w.Q, V, w.cmax, w.cidx, d, r);
   hipLaunchKernelGGL(eig_sign_kernel, dim3(nblk), dim3(NT), 0, st, V, w.cmax, w.cidx, nblk, w.theta, evals, r);
   return hipGetLastError();
