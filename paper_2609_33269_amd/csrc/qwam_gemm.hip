@@ -409,7 +409,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
       }
   }
 
-  if constexpr (GS == 32) {
+  if constexpr (GS == 32 && PARTIALS) {
     int s = 0;
     for (; s + 1 < S_full; s += 2) {
       stage_step(s, st0, st1, KC);
@@ -423,6 +423,18 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
     } else if (s < S) {
       stage_step(s, st0, st1, G - s * KC);
     }
+  } else if constexpr (GS == 32) {
+    // every stage runs all KC spans: a span past K reads finite FP6 codes (the
+    // next row's, or zeros past the buffer) with scales of zero (its scale
+    // groups lie past the scale arrays, where the buffer loads return zero),
+    // so it adds exactly zero; the single loop body keeps the registers of a
+    // partial-stage tail out of the kernel
+    int s = 0;
+    for (; s + 1 < S; s += 2) {
+      stage_step(s, st0, st1, KC);
+      stage_step(s + 1, st1, st0, KC);
+    }
+    if (s < S) stage_step(s, st0, st1, KC);
   } else {
     // Group 64: a software pipeline across groups.  The matrix core runs one
     // MFMA at a time and a wave that issues an MFMA while the previous one is
