@@ -30,6 +30,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "qwam_device.h"
 #include "qwam_internal.h"
 
 namespace qwam {
@@ -140,53 +141,77 @@ __global__ __launch_bounds__(NT) void eig_row_kernel(const float* __restrict__ i
 // part[s][j][n] = sum over k in split s of Xt[j][k] A[n][k]  (A symmetric, so
 // this is (A X)[n][j]).  Workgroup: 64 columns n x the 64 block rows j, one
 // K split; wave (wm, wn) owns the 32 x 32 block (rows 32 wm.., columns
-// 32 wn..) on v_mfma_f32_32x32x2_f32.  Lane l supplies row / column l % 32;
-// within a step of 8 channels, lane half h supplies channels 4h .. 4h+3 to
-// the four MFMAs (the same channel order on both operands), so each lane
-// reads 16 contiguous bytes of a row of Xt and of A.  Software pipeline over
-// batches of eight steps: the loads of the next batch are issued before the
-// products of this one (kchunk % 64 == 0).
+// 32 wn..) on v_mfma_f32_32x32x2_f32.
+//   * Steps of GK = 64 channels: the 64 x 64 tiles of A and Xt are copied
+//     straight into LDS (buffer_load ... lds, 16 bytes per lane, one copy
+//     instruction filling 4 rows of 256 bytes, i.e. whole cache lines).  Row r
+//     keeps its 16-byte chunk c at slot c ^ (r & 15), so the fragment reads
+//     (rows r .. r + 15, one chunk) hit distinct banks.  Two stages: the copy
+//     of step t + 1 runs during the MFMAs of step t.
+//   * Within a step of 8 channels, lane l supplies row / column l % 32 and
+//     lane half h channels 4h .. 4h + 3 to four MFMAs (the same channel order
+//     on both operands).  Even and odd 8-channel steps go to two accumulators
+//     (so consecutive MFMAs of a wave do not wait on each other), added at the
+//     end.
+constexpr int GK = 64;
+
 __global__ __launch_bounds__(NT) void eig_gemm_kernel(const float* __restrict__ Xt, const float* __restrict__ A,
                                                       float* __restrict__ part, int d, int kchunk) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __shared__ __attribute__((aligned(16))) float la0[64 * GK], lx0[64 * GK];
+  __shared__ __attribute__((aligned(16))) float la1[64 * GK], lx1[64 * GK];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = wave >> 1, wn = wave & 1;
   const int n0 = blockIdx.x * 64;
   const int s = blockIdx.y;
-  const int jrow = wm * 32 + (lane & 31);
-  const int nrow = n0 + wn * 32 + (lane & 31);
-  const int64_t k0 = static_cast<int64_t>(s) * kchunk + 4 * (lane >> 5);
-  const float4* xp = reinterpret_cast<const float4*>(Xt + static_cast<int64_t>(jrow) * d + k0);
-  const float4* ap = reinterpret_cast<const float4*>(A + static_cast<int64_t>(nrow) * d + k0);
-  v16f acc = {};
-  const int kc4 = kchunk / 4;
-  float4 x[8], a[8];
+  const int k0 = s * kchunk;
+  const int nsteps = kchunk / GK;
+  const uint32_t rowb = static_cast<uint32_t>(d) * 4u;
+  const buf_rsrc a_rsrc = make_rsrc(A + static_cast<int64_t>(n0) * d, 64u * rowb);
+  const buf_rsrc x_rsrc = make_rsrc(Xt, 64u * rowb);
+  // copy i of this wave: rows 4 (4 wave + i) + lane / 16, slot lane % 16
+  uint32_t c_off[4];
 #pragma unroll
-  for (int u = 0; u < 8; ++u) {
-    x[u] = xp[2 * u];
-    a[u] = ap[2 * u];
+  for (int i = 0; i < 4; ++i) {
+    const int r = 4 * (4 * wave + i) + (lane >> 4);
+    const int c = (lane & 15) ^ (r & 15);
+    c_off[i] = static_cast<uint32_t>(r) * rowb + static_cast<uint32_t>(k0 + 4 * c) * 4u;
   }
-  for (int k4 = 0; k4 < kc4; k4 += 16) {
-    // the next eight steps' operands are in flight while these are multiplied
-    // (the last batch reloads itself)
-    const int nk = k4 + 16 < kc4 ? k4 + 16 : k4;
-    float4 xn[8], an[8];
+  auto issue = [&](int t, float* la, float* lx) __attribute__((always_inline)) {
+    const uint32_t ko = static_cast<uint32_t>(t) * GK * 4u;
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      xn[u] = xp[nk + 2 * u];
-      an[u] = ap[nk + 2 * u];
+    for (int i = 0; i < 4; ++i) {
+      buf_load16_lds(a_rsrc, c_off[i] + ko, la + (4 * wave + i) * 4 * GK);
+      buf_load16_lds(x_rsrc, c_off[i] + ko, lx + (4 * wave + i) * 4 * GK);
     }
-    __builtin_amdgcn_sched_barrier(0);
+  };
+  const int ra = wn * 32 + (lane & 31), rx = wm * 32 + (lane & 31);
+  const int h = lane >> 5;
+  v16f acc0 = {}, acc1 = {};
+  auto compute = [&](const float* la, const float* lx) __attribute__((always_inline)) {
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x[u].x, a[u].x, acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x[u].y, a[u].y, acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x[u].z, a[u].z, acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x[u].w, a[u].w, acc, 0, 0, 0);
+    for (int t = 0; t < GK / 8; ++t) {
+      const int c = 2 * t + h;
+      const float4 a = *reinterpret_cast<const float4*>(la + ra * GK + 4 * (c ^ (ra & 15)));
+      const float4 x = *reinterpret_cast<const float4*>(lx + rx * GK + 4 * (c ^ (rx & 15)));
+      v16f& acc = (t & 1) ? acc1 : acc0;
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x.x, a.x, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x.y, a.y, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x.z, a.z, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x.w, a.w, acc, 0, 0, 0);
     }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      x[u] = xn[u];
-      a[u] = an[u];
+  };
+  issue(0, la0, lx0);
+  for (int t = 0; t < nsteps; t += 2) {
+    wait_vmcnt<0>();             // this thread's copies of step t have landed
+    lds_barrier();               // ... and every thread's; step t - 1's stage is free
+    if (t + 1 < nsteps) issue(t + 1, la1, lx1);
+    compute(la0, lx0);
+    if (t + 1 < nsteps) {
+      wait_vmcnt<0>();
+      lds_barrier();
+      if (t + 2 < nsteps) issue(t + 2, la0, lx0);
+      compute(la1, lx1);
     }
   }
   // result layout: lane l holds column l % 32, rows 8 (v / 4) + 4 (l / 32) + v % 4
@@ -194,7 +219,7 @@ __global__ __launch_bounds__(NT) void eig_gemm_kernel(const float* __restrict__ 
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
     const int j = wm * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-    out[static_cast<int64_t>(j) * d + n0 + wn * 32 + (lane & 31)] = acc[v];
+    out[static_cast<int64_t>(j) * d + n0 + wn * 32 + (lane & 31)] = acc0[v] + acc1[v];
   }
 }
 
