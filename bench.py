@@ -540,6 +540,15 @@ def aog_report(args):
         reps += 1
     dt = time.perf_counter() - t0
     cpu_tflops = float(cols) * d * (d + 1) * reps / dt / 1e12
+    # the oracle's eigensolve (numpy eigh in float64) of the same rotated estimate, one call
+    eig_cpu = None
+    if not args.no_cpu_baseline:
+        Gt = O.rotated_aog(O.aog_estimate(accs[0].double().cpu().numpy(), n, 1), lam.double().cpu().numpy(), 1024)
+        t0 = time.perf_counter()
+        O.protected_basis_eigh(Gt, r_eig)
+        eig_cpu = {"seconds": round(time.perf_counter() - t0, 2), "kind": "oracle (numpy eigh, float64)",
+                   "cores": os.cpu_count(), "sample": f"one call at d = {d}"}
+        del Gt
     print(json.dumps({
         "metric": "AOG accumulation A += gT gT^T: TFLOP/s", "value": round(tflops, 1), "unit": "TFLOP/s",
         "n_gpus": 1, "steps": steps, "warmup": args.warmup, "ms_per_step": round(us / 1e3, 5),
@@ -553,7 +562,8 @@ def aog_report(args):
         "eigensolve": {"kernel": "qwam_aog_protected_basis", "d": d, "r": r_eig, "iters": iters, "block": 64,
                        "hadamard": 1024, "us": round(eig_us, 1),
                        "A_bytes_read": eig_bytes, "hbm_GBs": round(eig_bytes / (eig_us * 1e-6) / 1e9, 1),
-                       "frac_of_hbm_peak": round(eig_bytes / (eig_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)},
+                       "frac_of_hbm_peak": round(eig_bytes / (eig_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                       "cpu_oracle": eig_cpu},
         "cpu_baseline": {"value": round(cpu_tflops, 5), "unit": "TFLOP/s", "cores": os.cpu_count(), "kind": "oracle",
                          "sample": f"{reps} calls of the oracle on {cols} of the {n} VJPs (all {d} channels) in "
                                    f"{dt:.1f} s; value = cols*d*(d+1)*calls/time"}}), flush=True)
