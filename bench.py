@@ -529,6 +529,7 @@ def aog_report(args):
     eig_us = e0.elapsed_time(e1) * 1e3 / 5
     eig_bytes = (iters + 1) * d * d * 4
     # the CPU oracle (float64 rank-k update) on column samples of the same batch
+    print("[bench] oracle accumulation (host)", file=sys.stderr, flush=True)
     from oracle import qwam_oracle as O
     g_bits = gts[0].view(torch.int16).cpu().numpy().view(np.uint16)
     cols = 256
@@ -540,14 +541,17 @@ def aog_report(args):
         reps += 1
     dt = time.perf_counter() - t0
     cpu_tflops = float(cols) * d * (d + 1) * reps / dt / 1e12
-    # the oracle's eigensolve (numpy eigh in float64) of the same rotated estimate, one call
+    # the oracle's eigensolve (numpy eigh in float64), one call on the smoothed
+    # estimate diag(lam) G^ diag(lam); the oracle's dense block rotation of a
+    # 4096 x 4096 matrix alone takes minutes on the host, so the sample leaves it out
     eig_cpu = None
     if not args.no_cpu_baseline:
-        Gt = O.rotated_aog(O.aog_estimate(accs[0].double().cpu().numpy(), n, 1), lam.double().cpu().numpy(), 1024)
+        print("[bench] oracle eigensolve (host, one call)", file=sys.stderr, flush=True)
+        Gt = O.rotated_aog(O.aog_estimate(accs[0].double().cpu().numpy(), n, 1), lam.double().cpu().numpy(), 0)
         t0 = time.perf_counter()
         O.protected_basis_eigh(Gt, r_eig)
         eig_cpu = {"seconds": round(time.perf_counter() - t0, 2), "kind": "oracle (numpy eigh, float64)",
-                   "cores": os.cpu_count(), "sample": f"one call at d = {d}"}
+                   "cores": os.cpu_count(), "sample": f"one call at d = {d}, smoothed estimate without the rotation"}
         del Gt
     print(json.dumps({
         "metric": "AOG accumulation A += gT gT^T: TFLOP/s", "value": round(tflops, 1), "unit": "TFLOP/s",

@@ -17,7 +17,7 @@
 //     and stays in L2;
 //   * orthonormalisation by CholeskyQR: Gram matrix in float64 (per-chunk
 //     partials, then a fixed-order sum in a kernel of its own), Cholesky and
-//     triangular inverse in one wave with the matrix in registers, then
+//     triangular inverse by blocks of 16 rows in one workgroup, then
 //     V = W R^-1 (tiled, float64 sums); one pass per iteration, two (i.e.
 //     CholeskyQR2) on the block that enters Rayleigh-Ritz;
 //   * Rayleigh-Ritz: T = V^T G~ V (p x p, float64), parallel cyclic Jacobi in
@@ -294,6 +294,28 @@ __global__ __launch_bounds__(NT) void eig_gsum_kernel(const double* __restrict__
   if (qtr == 0) C[e] = ((red[0][t] + red[1][t]) + red[2][t]) + red[3][t];
 }
 
+// 1/sqrt(x) for x > 0: the hardware estimate refined by two Newton steps
+// y <- y + y (1 - x y^2) / 2 (quadratic convergence from its ~2^-22 relative
+// error, so the result is within an ulp or two); no division on the chain
+__device__ __forceinline__ double rsqrt_f64(double x) {
+  double y = __builtin_amdgcn_rsq(x);
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const double e = __builtin_fma(-x * y, y, 1.0);
+    y = __builtin_fma(0.5 * y, e, y);
+  }
+  return y;
+}
+
+// 1/x for finite x != 0 (|x| below ~1e300): the hardware estimate refined by
+// two Newton steps y <- y + y (1 - x y)
+__device__ __forceinline__ double rcp_f64(double x) {
+  double y = __builtin_amdgcn_rcp(x);
+#pragma unroll
+  for (int i = 0; i < 2; ++i) y = __builtin_fma(y, __builtin_fma(-x, y, 1.0), y);
+  return y;
+}
+
 __device__ __forceinline__ double readlane_f64(double v, int l) {
   const uint64_t u = __builtin_bit_cast(uint64_t, v);
   const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(u)), l));
@@ -302,23 +324,37 @@ __device__ __forceinline__ double readlane_f64(double v, int l) {
   return __builtin_bit_cast(double, (static_cast<uint64_t>(hi) << 32) | lo);
 }
 
-// One wave: C = R^T R (Cholesky, R upper) and Rinv = R^-1 (upper, its lower
-// part exact zeros) to global memory.  Lane j keeps column j of C in
-// registers; step k takes the pivot from lane k, lane j forms R[k][j], the
-// row R[k][.] goes through LDS and every lane updates its column's trailing
-// part (right-looking).  Only the upper triangle of C is read.  A pivot below
-// 1e-13 of the largest diagonal entry (a block of lower rank) is raised to
-// that floor, so the inverse stays finite; the next iterations refill such a
-// direction.  Column j of R^-1 is then lane j's back substitution R z = e_j,
-// column by column over R in LDS.
-__global__ __launch_bounds__(64) void eig_chol_kernel(const double* __restrict__ C, double* __restrict__ Rinv) {
+// C = R^T R (Cholesky, R upper) and Rinv = R^-1 (upper, its lower part exact
+// zeros) to global memory, in one workgroup of four waves.  Lane j holds
+// column j; wave q holds rows 16 q .. 16 q + 15 of it in registers (blocks of
+// 16 rows).  Only the upper triangle of C is read.
+//   * Factorisation, right-looking by blocks: the wave that owns diagonal
+//     block b factors its 16 rows alone (step k: the pivot from lane k, lane
+//     j forms R[k][j], the row goes to LDS and the wave updates its remaining
+//     rows of the block); one workgroup barrier; then every wave below the
+//     block subtracts the block's rank-16 product from its rows.
+//   * A pivot below 1e-13 of the largest diagonal entry (a block of lower
+//     rank) is raised to that floor, so the inverse stays finite; the next
+//     iterations refill such a direction.
+//   * Inverse, R z = e_j for column j, by blocks from the last: the owner wave
+//     solves its 16 rows (column-oriented within the block), its rows of z go
+//     to LDS, one barrier, and every wave above the block subtracts the
+//     block's contribution from its rows.
+// Inside a block the row of R reaches the wave's other lanes by cross-lane
+// reads (no LDS round trip on the chain of pivots).
+constexpr int CB = 16;          // rows per block (and per wave)
+
+__global__ __launch_bounds__(NT) void eig_chol_kernel(const double* __restrict__ C, double* __restrict__ Rinv) {
   __shared__ __attribute__((aligned(16))) double rl[P][P + 2];    // rows of R
   __shared__ __attribute__((aligned(16))) double rc[P][P + 2];    // columns of R: rc[j][k] = R[k][j]
+  __shared__ __attribute__((aligned(16))) double zl[P][P + 2];    // rows of R^-1 as they are solved
   __shared__ double dinv[P];
-  const int lane = threadIdx.x;
-  double cc[P];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r0 = CB * wave;
+  double c[CB];
 #pragma unroll
-  for (int i = 0; i < P; ++i) cc[i] = C[i * P + lane];
+  for (int i = 0; i < CB; ++i) c[i] = C[(r0 + i) * P + lane];
   double m = C[lane * (P + 1)];
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
@@ -326,46 +362,68 @@ __global__ __launch_bounds__(64) void eig_chol_kernel(const double* __restrict__
     m = t > m ? t : m;
   }
   const double fl = m > 0.0 ? 1e-13 * m : 1e-300;
-  // software pipeline: the pivot of step k + 1 is taken as soon as its
-  // column is updated, so its square root and division overlap the rest of
-  // step k's update (both lie between the same two barriers)
-  auto pivot = [&](double ckk, double& rkk, double& inv) __attribute__((always_inline)) {
-    const double piv = ckk > fl ? ckk : fl;
-    rkk = __builtin_sqrt(piv);
-    inv = 1.0 / rkk;
-  };
-  double rkk, inv;
-  pivot(readlane_f64(cc[0], 0), rkk, inv);
+
 #pragma unroll
-  for (int k = 0; k < P; ++k) {
-    const double rk = lane > k ? cc[k] * inv : (lane == k ? rkk : 0.0);
-    rl[k][lane] = rk;
-    rc[lane][k] = rk;
-    if (lane == 0) dinv[k] = inv;
-    __syncthreads();
-    double rkk_n = 0.0, inv_n = 0.0;
-    if (k + 1 < P) {
-      cc[k + 1] = __builtin_fma(-rl[k][k + 1], rk, cc[k + 1]);
-      pivot(readlane_f64(cc[k + 1], k + 1), rkk_n, inv_n);
+  for (int b = 0; b < P / CB; ++b) {
+    if (wave == b) {
+#pragma unroll
+      for (int kk = 0; kk < CB; ++kk) {
+        const int k = CB * b + kk;
+        const double ckk = readlane_f64(c[kk], k);
+        const double piv = ckk > fl ? ckk : fl;
+        const double inv = rsqrt_f64(piv);              // 1 / R[k][k]
+        const double rkk = piv * inv;                   // R[k][k]
+        const double rk = lane > k ? c[kk] * inv : (lane == k ? rkk : 0.0);
+        c[kk] = rk;
+        rl[k][lane] = rk;
+        rc[lane][k] = rk;
+        if (lane == 0) dinv[k] = inv;
+        // R[k][i] of the block's later rows i from lane i (the next pivot's
+        // row first)
+#pragma unroll
+        for (int ii = kk + 1; ii < CB; ++ii) c[ii] = __builtin_fma(-readlane_f64(rk, CB * b + ii), rk, c[ii]);
+      }
     }
+    __syncthreads();
+    if (wave > b) {
 #pragma unroll
-    for (int i = k + 2; i < P; ++i) cc[i] = __builtin_fma(-rl[k][i], rk, cc[i]);
-    rkk = rkk_n;
-    inv = inv_n;
+      for (int kk = 0; kk < CB; ++kk) {
+        const int k = CB * b + kk;
+        const double rkj = rl[k][lane];
+#pragma unroll
+        for (int ii = 0; ii < CB; ++ii) c[ii] = __builtin_fma(-rl[k][r0 + ii], rkj, c[ii]);
+      }
+    }
   }
-  // column-oriented: z_i = b_i / R[i][i], then b_k -= R[k][i] z_i for k < i,
-  // so the dependent chain is one multiply and one FMA per row
-  double z[P];
+
+  double z[CB];
 #pragma unroll
-  for (int i = 0; i < P; ++i) z[i] = (i == lane) ? 1.0 : 0.0;
+  for (int i = 0; i < CB; ++i) z[i] = (r0 + i == lane) ? 1.0 : 0.0;
 #pragma unroll
-  for (int i = P - 1; i >= 0; --i) {
-    z[i] *= dinv[i];
+  for (int b = P / CB - 1; b >= 0; --b) {
+    if (wave == b) {
 #pragma unroll
-    for (int k = 0; k < i; ++k) z[k] = __builtin_fma(-rc[i][k], z[i], z[k]);
+      for (int ii = CB - 1; ii >= 0; --ii) {
+        const int i = CB * b + ii;
+        z[ii] *= dinv[i];
+        zl[i][lane] = z[ii];
+#pragma unroll
+        for (int kk = 0; kk < ii; ++kk) z[kk] = __builtin_fma(-rc[i][CB * b + kk], z[ii], z[kk]);
+      }
+    }
+    __syncthreads();
+    if (wave < b) {
+#pragma unroll
+      for (int ii = 0; ii < CB; ++ii) {
+        const int i = CB * b + ii;
+        const double zi = zl[i][lane];
+#pragma unroll
+        for (int kk = 0; kk < CB; ++kk) z[kk] = __builtin_fma(-rc[i][r0 + kk], zi, z[kk]);
+      }
+    }
   }
 #pragma unroll
-  for (int i = 0; i < P; ++i) Rinv[i * P + lane] = z[i];
+  for (int i = 0; i < CB; ++i) Rinv[(r0 + i) * P + lane] = z[i];
 }
 
 // Vt[i][n] = sum over k of Rinv[k][i] Wt[k][n] (V = W R^-1; Rinv is zero below
@@ -464,9 +522,22 @@ __global__ __launch_bounds__(JT) void eig_jacobi_kernel(const double* __restrict
         double c = 1.0, s = 0.0;
         const double apq = t[a][b];
         if (apq != 0.0) {
-          const double tau = (t[b][b] - t[a][a]) / (2.0 * apq);
-          const double tt = (tau >= 0.0 ? 1.0 : -1.0) / (__builtin_fabs(tau) + __builtin_sqrt(1.0 + tau * tau));
-          c = 1.0 / __builtin_sqrt(1.0 + tt * tt);
+          // tau = (T_bb - T_aa) / (2 T_ab); tt = sign(tau) / (|tau| + sqrt(1 + tau^2)),
+          // the smaller root of tt^2 + 2 tau tt - 1 = 0; c = 1 / sqrt(1 + tt^2).
+          // Reciprocals and square roots by refined hardware estimates; a
+          // |tau| beyond 1e100 (tau^2 would overflow) takes tt = 1 / (2 tau)
+          const double diff = t[b][b] - t[a][a];
+          const double aa = __builtin_fabs(apq);
+          double tt;
+          if (__builtin_fabs(diff) > 1e100 * aa) {
+            tt = 0.5 * apq / diff;
+          } else {
+            const double tau = diff * rcp_f64(2.0 * apq);
+            const double q = 1.0 + tau * tau;
+            const double root = q * rsqrt_f64(q);
+            tt = (tau >= 0.0 ? 1.0 : -1.0) * rcp_f64(__builtin_fabs(tau) + root);
+          }
+          c = rsqrt_f64(1.0 + tt * tt);
           s = tt * c;
         }
         prs[k] = make_int2(a, b);
@@ -713,7 +784,7 @@ hipError_t launch_aog_eig(int d, int r, int iters, const float* A, float scale, 
   // rows of `src` orthonormalised into `dst` (one CholeskyQR pass)
   auto orth = [&](const float* src, float* dst) {
     gram(src, src);
-    hipLaunchKernelGGL(eig_chol_kernel, dim3(1), dim3(64), 0, st, w.C, w.Rinv);
+    hipLaunchKernelGGL(eig_chol_kernel, dim3(1), dim3(NT), 0, st, w.C, w.Rinv);
     hipLaunchKernelGGL(eig_apply_kernel, dim3(nblk), dim3(NT), 0, st, src, w.Rinv, dst, d);
   };
 
