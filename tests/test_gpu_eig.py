@@ -126,3 +126,63 @@ def test_deterministic_and_workspace_reuse():
     assert torch.equal(V1, V2) and torch.equal(e1, e2)
     V0 = V0.cpu().double().numpy()
     assert np.abs(V0.T @ V0 - np.eye(r)).max() <= 1e-5
+
+
+def test_max_size_known_spectrum():
+    """The largest size the entry point takes (d = 16384, r = 48), on a matrix
+    whose eigenpairs are known in closed form: A = U diag(e) U^T + 1e-3 I with
+    U orthonormal (QR of a seeded Gaussian d x 64 block, each column's
+    largest-magnitude entry made positive) and e_i = 2^(-i/8).  Its top-48
+    eigenvectors are U's first columns and its eigenvalues e_i + 1e-3 (the
+    float32 rounding of A moves them by ~1e-7, far inside the tolerances)."""
+    d, r, p = 16384, 48, 64
+    log(f"  eigensolve at the maximum size d={d} r={r} (known spectrum)")
+    U, _ = np.linalg.qr(np.random.default_rng(16384).standard_normal((d, p)))
+    idx = np.argmax(np.abs(U), axis=0)
+    U = U * np.sign(U[idx, np.arange(p)])[None, :]
+    e = 2.0 ** (-np.arange(p) / 8.0)
+    Ud = torch.from_numpy(U).to("cuda:0")
+    A64 = (Ud * torch.from_numpy(e).to("cuda:0")[None, :]) @ Ud.T.contiguous()
+    A64.diagonal().add_(1e-3)
+    A = A64.float().contiguous()
+    del A64
+    V, ev = Q.aog_protected_basis(A, r, iters=10)
+    torch.cuda.synchronize()
+    # Ky Fan on the GPU in float64: tr(V^T A V)
+    Vd = V.double()
+    kyfan = float(torch.trace(Vd.T @ (A.double() @ Vd)))
+    del A
+    V = V.cpu().numpy().astype(np.float64)
+    ev = ev.cpu().numpy().astype(np.float64)
+    top = e[:r] + 1e-3
+    overlap = float(np.linalg.norm(V.T @ U[:, :r]) ** 2 / r)
+    orth = float(np.abs(V.T @ V - np.eye(r)).max())
+    dots = np.einsum("ij,ij->j", V, U[:, :r])
+    log(f"    overlap 1 - {1 - overlap:.2e}, Ky Fan rel {abs(kyfan - top.sum()) / top.sum():.2e}, "
+        f"eigenvalue rel {np.abs(ev - top).max() / top[0]:.2e}, min |v.u| {np.abs(dots).min():.8f}, "
+        f"orthonormality {orth:.2e}")
+    assert overlap >= 1 - 1e-6
+    assert abs(kyfan - top.sum()) <= 1e-6 * top.sum()
+    assert np.abs(ev - top).max() <= 1e-5 * top[0]
+    assert (np.diff(ev) <= 0).all()
+    assert orth <= 1e-5
+    assert (dots >= 1 - 1e-5).all(), "each eigenvector, with the sign of the largest entry"
+    idx = np.argmax(np.abs(V), axis=0)
+    assert (V[idx, np.arange(r)] > 0).all()
+
+
+def test_small_hadamard_block_and_largest_rank():
+    """r = 48 (the largest rank) with the smallest rotation block (B = 16) and
+    smoothing, against the oracle's eigh of the same G~.  The rank-80 stand-in
+    decays slowly (lambda_65 / lambda_48 = 0.76 here), and subspace iteration
+    with a 64-vector block converges by that factor per product, so this case
+    takes 30 iterations (12 leave ~1e-4 in the overlap, in exact arithmetic
+    as well)."""
+    d, r, B = 1024, 48, 16
+    rng = np.random.default_rng(48)
+    G = _stand_in(d, width=80, seed=48)
+    lam = np.exp(rng.uniform(-0.7, 0.7, size=d)).astype(np.float32)
+    Gf = G.astype(np.float32).astype(np.float64)
+    log(f"  eigensolve d={d} r={r} B={B} with smoothing")
+    V, ev = _run(Gf, r, iters=30, scale=0.5, lam=lam, B=B)
+    _check_basis(V, ev, O.rotated_aog(0.5 * Gf, lam, B), r)
