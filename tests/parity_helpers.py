@@ -137,7 +137,7 @@ def check_y_elements(y_gpu_bits, y_ref, abs_terms, n_groups, rank, min_identical
     yg = O.bf16_bits_to_f64(y_gpu_bits)
     yr = O.round_to_bf16(y_ref)
     ulp = np.maximum(bf16_ulp(yr), bf16_ulp(yg))
-    bound = ulp + (2.0 ** -15 + (n_groups + rank + 2) * U32) * abs_terms
+    bound = ulp + y_float32_bound(abs_terms, n_groups, rank)
     diff = np.abs(yg - yr)
     bad = np.argwhere(diff > bound)
     assert bad.size == 0, f"y outside one ulp + float32 bound at {bad[:5].tolist()}"
@@ -147,14 +147,35 @@ def check_y_elements(y_gpu_bits, y_ref, abs_terms, n_groups, rank, min_identical
     return same
 
 
-def check_y_per_token(y_gpu_bits, y_ref):
-    """Relative Frobenius error of every token's output row within the tolerance."""
+def y_float32_bound(abs_terms, n_groups, rank) -> np.ndarray:
+    """Per-element bound on the kernel's float32 result before its bf16
+    rounding: the two-piece bf16 splits of the scales (within 2^-15 of
+    sx * sw) and the G + r + 2 float32 roundings of the accumulation."""
+    return (2.0 ** -15 + (n_groups + rank + 2) * U32) * np.asarray(abs_terms, dtype=np.float64)
+
+
+def check_y_per_token(y_gpu_bits, y_ref, abs_terms, n_groups, rank):
+    """Relative Frobenius error of every token's output row within its
+    tolerance: 2e-3, or, where larger, the row's error when each element takes
+    the farther of the bf16 values that a float32 result within the kernel's
+    accumulation bound of y_ref can round to (+1e-4).  An element whose bound
+    interval does not contain a bf16 rounding midpoint can only take the
+    correctly rounded value, so for most rows that is the row's own bf16
+    rounding error; a row of few outputs with one element next to a midpoint
+    may need more than 2e-3."""
     yg = O.bf16_bits_to_f64(y_gpu_bits)
-    errs = [rel_fro(yg[i], y_ref[i]) for i in range(y_ref.shape[0])]
-    tols = [y_tolerance(y_ref[i]) for i in range(y_ref.shape[0])]
-    worst = int(np.argmax(np.array(errs) / np.array(tols)))
-    log(f"    worst token error {errs[worst]:.3e} (tolerance {tols[worst]:.3e})")
-    assert all(e <= t for e, t in zip(errs, tols)), "a token's output exceeds the tolerance"
+    y_ref = np.asarray(y_ref, dtype=np.float64)
+    eb = y_float32_bound(abs_terms, n_groups, rank)
+    worst = np.maximum(np.abs(O.round_to_bf16(y_ref - eb) - y_ref), np.abs(O.round_to_bf16(y_ref + eb) - y_ref))
+    nref = np.linalg.norm(y_ref, axis=1)
+    nref = np.where(nref > 0, nref, 1.0)
+    errs = np.linalg.norm(yg - y_ref, axis=1) / nref
+    tols = np.maximum(Y_TOL, np.linalg.norm(worst, axis=1) / nref + 1e-4)
+    worst_row = int(np.argmax(errs / tols))
+    log(f"    worst token error {errs[worst_row]:.3e} (tolerance {tols[worst_row]:.3e}); "
+        f"{int(np.sum(tols > Y_TOL))} of {len(tols)} rows above 2e-3 by rounding")
+    bad = np.flatnonzero(errs > tols)
+    assert bad.size == 0, f"tokens {bad[:8].tolist()} exceed their tolerance"
 
 
 def sample_rows(M: int, seed: int, extra: int = 64) -> np.ndarray:
@@ -169,20 +190,23 @@ def sample_rows(M: int, seed: int, extra: int = 64) -> np.ndarray:
     return np.array(sorted(rows))
 
 
-def check_sampled_rows(layer, xq, y, xq_ref, sx_ref, t_ref, wq, sw, L2_bits, rows, bias_bits=None):
+def check_sampled_rows(layer, xq, y, xq_ref, sx_ref, t_bits, wq, sw, L2_bits, rows, bias_bits=None):
     """y and the int32 group partials of sampled tokens of a large layer against
-    the oracle computed from the same codes: Frobenius error over the sample,
-    every token's own error, every element (check_y_elements), and the
-    partials bit for bit through the debug entry point on the sampled rows."""
+    the oracle computed from the same codes and scales and the t the GEMM ran
+    with (t_bits: the GPU's own, checked against the oracle's by the caller):
+    Frobenius error over the sample, every token's own error, every element
+    (check_y_elements), and the partials bit for bit through the debug entry
+    point on the sampled rows."""
+    t_ref = t_bits
     y_ref, P_ref = O.asp_output_rows(xq_ref[rows], sx_ref[rows], t_ref[rows], wq, sw, L2_bits, bias_bits)
     sel = torch.from_numpy(rows).cuda()
     yb = bits(y[sel])
     err = rel_fro(O.bf16_bits_to_f64(yb), y_ref)
     log(f"    y rel Frobenius error on {len(rows)} sampled tokens {err:.3e}")
     assert err <= y_tolerance(y_ref)
-    check_y_per_token(yb, y_ref)
-    check_y_elements(yb, y_ref, y_abs_terms(sx_ref[rows], sw, P_ref, t_ref[rows], L2_bits, bias_bits),
-                     P_ref.shape[2], np.asarray(L2_bits).shape[0])
+    at = y_abs_terms(sx_ref[rows], sw, P_ref, t_ref[rows], L2_bits, bias_bits)
+    check_y_per_token(yb, y_ref, at, P_ref.shape[2], np.asarray(L2_bits).shape[0])
+    check_y_elements(yb, y_ref, at, P_ref.shape[2], np.asarray(L2_bits).shape[0])
     P = Q.debug_group_partials(layer, xq[sel].contiguous())
     torch.cuda.synchronize()
     assert (P.cpu().numpy() == P_ref).all(), "int32 group partials of sampled tokens"

@@ -96,6 +96,6 @@ def test_group32_full_size_sampled():
     assert (bits(t) == t_ref).all(), "t"
     assert (xq.cpu().numpy() == xq_ref).all(), "packed activation bytes"
     assert (xs.cpu().numpy() == sx_ref.T).all(), "activation scales"
-    check_sampled_rows(layer, xq, y, xq_ref, sx_ref, t_ref, wq, sw, f["L2"], sample_rows(M, seed=M + 32))
+    check_sampled_rows(layer, xq, y, xq_ref, sx_ref, bits(t), wq, sw, f["L2"], sample_rows(M, seed=M + 32))
     del x, xq, xs, t, y, layer
     torch.cuda.empty_cache()

@@ -82,6 +82,8 @@ def test_fused_action_expert_layers(M, N):
     (32, 2048, 4096, 32, True),
     (64, 2048, 2304, 16, True),
     (64, 1024, 8192, 16, False),
+    # N at the largest size the entry point takes
+    (1, 64, 1 << 20, 16, False),
 ])
 def test_fused_edge_shapes(M, K, N, r, bias):
     d = I.custom(M=M, K=K, N=N, r=r, seed=M * 23 + K, n_outliers=max(1, K // 100), with_bias=bias)

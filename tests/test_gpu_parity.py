@@ -46,9 +46,13 @@ def _full_parity(draws, factors, bias_bits=None, check_partials=True):
         P = Q.debug_group_partials(layer, xq)
         torch.cuda.synchronize()
         assert (P.cpu().numpy() == ref["P"]).all(), "int32 group partials"
-    check_y_per_token(bits(y), ref["y"])
-    check_y_elements(bits(y), ref["y"], y_abs_terms(ref["sx"], ref["sw"], ref["P"], ref["t"], factors["L2"], bias_bits),
-                     ref["P"].shape[2], factors["L1"].shape[1])
+    # token by token and element by element against the oracle's output for the
+    # t the GEMM ran with (t itself is checked above): y_ref + (t_gpu - t_ref) L2
+    tg = bits(t)
+    y_t = ref["y"] + (O.bf16_bits_to_f64(tg) - O.bf16_bits_to_f64(ref["t"])) @ O.bf16_bits_to_f64(factors["L2"])
+    at = y_abs_terms(ref["sx"], ref["sw"], ref["P"], tg, factors["L2"], bias_bits)
+    check_y_per_token(bits(y), y_t, at, ref["P"].shape[2], factors["L1"].shape[1])
+    check_y_elements(bits(y), y_t, at, ref["P"].shape[2], factors["L1"].shape[1])
     return check_y(bits(y), ref["y"])
 
 
@@ -68,6 +72,10 @@ EDGE_SHAPES = [
     (130, 1024, 1040, 16, True),
     (257, 640, 256, 32, False),
     (33, 16448, 64, 32, False),      # K > 16384: 1/lambda read from global memory
+    # the largest sizes the entry points take
+    (130, 65536, 64, 16, True),      # K = 65536, the large-tile GEMM
+    (1, 64, 1 << 20, 16, False),     # N = 2^20, one token
+    (1 << 20, 64, 16, 16, False),    # M = 2^20
 ]
 
 
@@ -136,7 +144,7 @@ def _large_parity(draws, extra_rows=64):
     assert (wq[wrows] == O.pack_codes(qw[wrows], O.quantize_groups_signed(f["R"][wrows])[2])).all(), \
         "packed weight bytes"
     rows = sample_rows(M, seed=M + N, extra=extra_rows)
-    check_sampled_rows(layer, xq, y, xq_ref, sx_ref, t_ref, wq, sw, f["L2"], rows)
+    check_sampled_rows(layer, xq, y, xq_ref, sx_ref, bits(t), wq, sw, f["L2"], rows)
     del x, xq, xs, t, y, layer
     torch.cuda.empty_cache()
 

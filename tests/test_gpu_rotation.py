@@ -143,7 +143,7 @@ def test_rotated_full_size(deflate):
         assert (bits(t) == t_ref).all(), "t"
     else:
         check_t(bits(t), t_ref, O.transformed_activations(draws.x, inv_lam, f["hadamard"]), f["L1"])
-    check_sampled_rows(layer, xq, y, xq_ref, sx_ref, t_ref, wq, sw, f["L2"], sample_rows(M, seed=M + 7))
+    check_sampled_rows(layer, xq, y, xq_ref, sx_ref, bits(t), wq, sw, f["L2"], sample_rows(M, seed=M + 7))
     del x, xq, xs, t, y, layer
     torch.cuda.empty_cache()
 
