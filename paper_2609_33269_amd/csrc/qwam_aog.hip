@@ -8,9 +8,13 @@
 //
 // an NT matrix product whose two operands are both K-contiguous rows of gT.
 //
-//   * only the tiles (I, J) with I <= J are computed (TB x TB, four waves of
-//     TB/2 x TB/2 = BW x BW blocks of v_mfma_f32_32x32x16_bf16); each is added
-//     to A[I][J] and, transposed, to A[J][I].  On a diagonal tile the upper
+//   * only the tiles (I, J) with I <= J are computed (TB x TB); each is added
+//     to A[I][J] and, transposed, to A[J][I].  Eight waves, two per SIMD: wave
+//     w owns the TB/2 x TB/2 block (w%4)/2, w%2 of the tile (BW x BW blocks of
+//     v_mfma_f32_32x32x16_bf16) for half w/4 of every stage's k-steps, so that
+//     one wave's matrix-core work covers the other's LDS reads; the two
+//     partial blocks are summed once, after the last stage (the half with the
+//     later k-steps added to the other, in that fixed order).  On a diagonal tile the upper
 //     triangle comes from the normal write and the strict lower triangle from
 //     the transposed one, so A stays exactly symmetric;
 //   * products of two bf16 values are exact in float32; the sums are float32
@@ -20,11 +24,10 @@
 //     buffer_load ... lds (rows past d read as zero), with the chunk swizzle of
 //     the ASP GEMM so that the fragment loads are bank-conflict free; one
 //     barrier per stage, one workgroup per CU;
-//   * the copies into LDS, not the matrix cores, bound the main loop (about
-//     50 GB/s per CU measured), so the tile is as large as one round of
-//     workgroups allows: TB = 192 when the 192-tile triangle fits on the 256
-//     CUs and the 128-tile one does not (d = 2817 .. 4224, the paper's layer
-//     widths up to 4096), TB = 128 otherwise.  Three stages of 48 KB (192) or
+//   * the tile is as large as one round of workgroups allows (LDS traffic per
+//     product falls with the tile edge): TB = 192 when the 192-tile triangle
+//     fits on the 256 CUs and the 128-tile one does not (d = 2817 .. 4224, the
+//     paper's layer widths up to 4096), TB = 128 otherwise.  Three stages of 48 KB (192) or
 //     four of 32 KB (128) keep 96 KB in flight per CU;
 //   * the tile goes through LDS (C, then C^T) so that both read-modify-write
 //     passes move 16 bytes per lane along rows of A; with TB = 128 the reads
@@ -39,7 +42,7 @@ namespace qwam {
 
 namespace {
 
-constexpr int NWAVES_S = 4;
+constexpr int NWAVES_S = 8;
 constexpr int NT_S = 64 * NWAVES_S;
 constexpr int KS = 64;             // values of n per ring stage (one 128-byte line per row)
 constexpr int ROWB_S = KS * 2;
@@ -52,7 +55,7 @@ struct SyrkCfg {
   static constexpr int BW = TB / 64;                       // 32x32 blocks per wave edge
   static constexpr int NST = TB == 128 ? 4 : 3;            // ring stages
   static constexpr int STAGE_B = 2 * TB * ROWB_S;          // A tile, then B tile ([row][8 swizzled chunk slots])
-  static constexpr int CPW = TB / 32;                      // 1 KB copies per operand, stage and wave
+  static constexpr int CPW = TB / (8 * NWAVES_S);          // 1 KB copies per operand, stage and wave
   static constexpr int IPS = 2 * CPW;                      // copies per stage and wave
   static constexpr int LDC = TB + 4;                       // float row stride of the epilogue tile
   static constexpr int F4 = TB * TB / 4 / NT_S;            // float4 of a tile per thread
@@ -148,7 +151,8 @@ __global__ __launch_bounds__(NT_S, 1) void aog_syrk_kernel(const uint16_t* __res
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = (wave >> 1) & 1, wn = wave & 1;       // block of the tile
+  const int kh = wave >> 2;                            // half of the k-steps of a stage
   const int T = (d + TB - 1) / TB;
   int ti, tj;
   triangle_tile(blockIdx.x, T, ti, tj);
@@ -242,7 +246,7 @@ __global__ __launch_bounds__(NT_S, 1) void aog_syrk_kernel(const uint16_t* __res
     lds_barrier();
     if (s + NST - 1 < S) issue(s + NST - 1, (k + NST - 1) % NST);
     if (pref && s == S - NST) load_block(m0, n0, pn);
-    // fragments of k-step q + 1 are read while step q multiplies
+    // fragments of the wave's next k-step are read while the current one multiplies
     const uint32_t a_base = lds_addr(stage_a(k)) + (wm * (TB / 2)) * ROWB_S + frow_off;
     const uint32_t b_base = lds_addr(stage_b(k)) + (wn * (TB / 2)) * ROWB_S + frow_off;
     v4i fr[2][2 * BW];
@@ -253,12 +257,14 @@ __global__ __launch_bounds__(NT_S, 1) void aog_syrk_kernel(const uint16_t* __res
 #pragma unroll
       for (int j = 0; j < BW; ++j) f[BW + j] = lds_read16(b_base + so + j * 32 * ROWB_S);
     };
-    read_step(0, fr[0]);
+    // this wave's k-steps of the stage: KH consecutive 16-wide steps from kh * KH
+    constexpr int KH = KS / 16 / 2;
+    read_step(kh * KH, fr[0]);
 #pragma unroll
-    for (int q = 0; q < KS / 16; ++q) {
+    for (int q = 0; q < KH; ++q) {
       v4i(&f)[2 * BW] = fr[q & 1];
-      if (q + 1 < KS / 16) {
-        read_step(q + 1, fr[(q + 1) & 1]);
+      if (q + 1 < KH) {
+        read_step(kh * KH + q + 1, fr[(q + 1) & 1]);
         lgkm_wait_for<2 * BW>(f);
       } else {
         lgkm_wait_for<0>(f);
@@ -286,16 +292,17 @@ __global__ __launch_bounds__(NT_S, 1) void aog_syrk_kernel(const uint16_t* __res
     if (s + k < S) stage_step(s + k, k);
 
   // ---- epilogue: A[I][J] += C, then A[J][I] += C^T, through LDS ----
-  // Each pass stages its tile in LDS ([row][LDC] floats) and moves 16 bytes
-  // per lane along rows of A; the reads of A are issued before the tile is
-  // staged.  A diagonal tile (I = J) is one pass over its block: element
-  // (r, c) gets C[r][c] for r <= c and C[c][r] below the diagonal.  Blocks
-  // past d are skipped float4 by float4 (d % 16 == 0, so a float4 is all in
-  // or all out).
+  // C is staged in LDS ([row][LDC] floats), then transposed in place, and
+  // each pass moves 16 bytes per lane along rows of A.  A diagonal tile
+  // (I = J) is one pass over its block: element (r, c) gets C[r][c] for
+  // r <= c and C[c][r] below the diagonal.  Blocks past d are skipped float4
+  // by float4 (d % 16 == 0, so a float4 is all in or all out).
   float* C = reinterpret_cast<float*>(smem);
   // result layout of a 32x32 block: lane l holds column l%32 and rows
   // 8*(v/4) + 4*(l/32) + v%4, v = 0..15
-  auto stage_tile = [&](bool transposed) __attribute__((always_inline)) {
+  // with `add`, the block already in C (the other k-half's, same element
+  // positions) is first added to the accumulators
+  auto stage_tile = [&](bool add) __attribute__((always_inline)) {
 #pragma unroll
     for (int i = 0; i < BW; ++i)
 #pragma unroll
@@ -304,7 +311,9 @@ __global__ __launch_bounds__(NT_S, 1) void aog_syrk_kernel(const uint16_t* __res
         for (int v = 0; v < 16; ++v) {
           const int r = wm * (TB / 2) + i * 32 + 8 * (v >> 2) + 4 * fhalf + (v & 3);
           const int c = wn * (TB / 2) + j * 32 + frow;
-          C[transposed ? c * LDC + r : r * LDC + c] = acc[i][j][v];
+          float* e = &C[r * LDC + c];
+          if (add) acc[i][j][v] += *e;
+          *e = acc[i][j][v];
         }
   };
   auto in_range = [&](int r0, int c0, int q) __attribute__((always_inline)) {
@@ -340,17 +349,49 @@ __global__ __launch_bounds__(NT_S, 1) void aog_syrk_kernel(const uint16_t* __res
     }
   };
 
-  if (!pref) load_ranged(m0, n0, pn);
   lds_barrier();                                   // every wave is past the ring
-  stage_tile(false);
+  // C = first k-half + second k-half: the second half's waves stage their
+  // blocks, then each first-half thread adds the elements it owns (the same
+  // positions) into its accumulators and stores the sums in their place.
+  // Every thread then requests its share of both blocks of A, so that the
+  // reads of A[J][I] overlap the first pass.
+  if (kh == 1) stage_tile(false);
+  __syncthreads();
+  if (kh == 0) stage_tile(true);
+  asm volatile("" ::: "memory");                 // the reads of A stay after the staging
+  float4 pt[F4];
+  if (!pref) load_ranged(m0, n0, pn);
+  if (!diag) load_ranged(n0, m0, pt);
   __syncthreads();
   add_store(m0, n0, pn);
   if (diag) return;
-  load_ranged(n0, m0, pn);                         // the transposed block's current values
-  __syncthreads();                                 // every thread is done with C
-  stage_tile(true);
+  // C transposed in place: each thread takes half of the elements of its
+  // block positions (the k-half picks the half), all read before any is
+  // written back at its transposed position
+  float tv[BW][BW][8];
+#pragma unroll
+  for (int i = 0; i < BW; ++i)
+#pragma unroll
+    for (int j = 0; j < BW; ++j)
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int v = 8 * kh + u;
+        const int r = wm * (TB / 2) + i * 32 + 8 * (v >> 2) + 4 * fhalf + (v & 3);
+        tv[i][j][u] = C[r * LDC + wn * (TB / 2) + j * 32 + frow];
+      }
+  __syncthreads();                                 // every thread is done reading C
+#pragma unroll
+  for (int i = 0; i < BW; ++i)
+#pragma unroll
+    for (int j = 0; j < BW; ++j)
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int v = 8 * kh + u;
+        const int r = wm * (TB / 2) + i * 32 + 8 * (v >> 2) + 4 * fhalf + (v & 3);
+        C[(wn * (TB / 2) + j * 32 + frow) * LDC + r] = tv[i][j][u];
+      }
   __syncthreads();
-  add_store(n0, m0, pn);
+  add_store(n0, m0, pt);
 }
 
 static int syrk_tiles(int d, int tb) {
