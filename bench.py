@@ -447,21 +447,26 @@ def denoise_step_report(args):
             qwam.asp_linear(L, xq, xs, t, out=y)
 
     stream = torch.cuda.current_stream()
-    step()
-    torch.cuda.synchronize()
-    steps = max(1, min(args.steps, 5))
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
+    # warm up by time (clocks settle), then the median of 5 steps, each
+    # bracketed by its own events
+    settle = settle_clocks(lambda _: step(), min_seconds=1.0, window=1, max_seconds=6.0)
+    steps = 5
+    per = []
     for _ in range(steps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
         step()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / steps
+        e1.record(stream)
+        torch.cuda.synchronize()
+        per.append(e0.elapsed_time(e1))
+    ms = float(np.median(per))
     print(json.dumps({
         "workload": "denoise_step", "blocks": inputs.DENOISE_BLOCKS, "layers": len(layers), "M": Ms, "r": rr,
         "layer_shapes": [[n, k, nn] for n, k, nn in inputs.DENOISE_BLOCK],
         "ms_per_step": round(ms, 3), "effective_TOPS": round(flops / (ms * 1e-3) / 1e12, 1),
         "frac_of_5P_peak": round(flops / (ms * 1e-3) / 1e12 / MFMA_PEAK, 4), "steps": steps,
+        "timing": "median of 5 steps, each between two events, after a time-based warm-up",
+        "step_ms": [round(v, 3) for v in per], "clock_settle": settle,
         "dense_equivalent_ops": flops, "data": "synthetic, drawn on the GPU"}), flush=True)
 
 
