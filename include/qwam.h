@@ -254,8 +254,10 @@ qwam_status qwam_aog_accumulate(int32_t d, int32_t n, const uint16_t *gT, float 
  * scale = 1 / (N P) for N inputs and P probes, lam the smoothing factors, H
  * the orthonormal block Hadamard matrix of block `hadamard` (the identity for
  * 0).  By blocked subspace iteration (a block of 64 vectors, `iters` products
- * with G~, each followed by a CholeskyQR2 orthonormalisation in float64) and a
- * Rayleigh-Ritz step; products with A on the float32 matrix cores.  The
+ * with G~, each followed by a CholeskyQR orthonormalisation, the last block by
+ * CholeskyQR2; Gram sums and Cholesky factors in float64) and a Rayleigh-Ritz
+ * step (cyclic Jacobi in float64); products with A on the float32 matrix
+ * cores.  The
  * result is deterministic.  Column i of V is the eigenvector of the i-th
  * largest eigenvalue, its largest-magnitude entry made positive.
  *   d       in   channels, d % 64 == 0, 128 <= d <= 16384
