@@ -115,3 +115,27 @@ def test_aog_full_size_sampled():
     assert (np.abs(got - ref) <= bound).all()
     del A, gT
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("d,n", [(16384, 64), (4096, 16384)])
+def test_aog_largest_sizes(d, n):
+    """The largest accumulator the entry point takes (d = 16384: a 1 GiB
+    float32 A, 8256 tiles of 128 rows over many rounds) and a long batch
+    (n = 16384: 256 stages per tile): exact symmetry everywhere, the float32
+    bound on sampled rows (the first and last row of tiles, and random ones)."""
+    log(f"  aog accumulate at d={d} n={n}")
+    gb = _vjp_batch(d, n, seed=d + 3 * n)
+    A = torch.zeros((d, d), dtype=torch.float32, device="cuda:0")
+    gT = torch.from_numpy(gb.view(np.int16)).view(torch.bfloat16).cuda()
+    Q.aog_accumulate(gT, A)
+    torch.cuda.synchronize()
+    assert torch.equal(A, A.t()), "symmetry"
+    rng = np.random.default_rng(d + n)
+    rows = np.array(sorted({0, 127, 128, 191, 192, d - 129, d - 1} | set(int(v) for v in rng.choice(d, 16, replace=False))))
+    g = O.bf16_bits_to_f64(gb)
+    got = A[torch.from_numpy(rows).cuda()].cpu().numpy().astype(np.float64)
+    ref = g[rows] @ g.T
+    bound = (n + 1) * 2.0 ** -24 * (np.abs(g[rows]) @ np.abs(g).T) + 2.0 ** -149
+    assert (np.abs(got - ref) <= bound).all(), np.argwhere(np.abs(got - ref) > bound)[:5].tolist()
+    del A, gT
+    torch.cuda.empty_cache()
