@@ -63,6 +63,9 @@ DEFLATED_SHAPES = [
     (130, 1024, 1040, 16, True),
     (33, 16448, 64, 32, False),      # K > 16384: 1/lambda read from global memory
     (20, 16448, 32, 64, True),
+    # the largest K the entry points take
+    (33, 65536, 64, 64, True),
+    (130, 65536, 32, 16, False),
 ]
 
 

@@ -66,6 +66,7 @@ ROTATED_SHAPES = [
     (40, 640, 96, 32, False),   # B 128, T 640
     (33, 3072, 64, 32, True),   # B 1024, three tiles
     (20, 16448, 32, 64, False),  # B 64, T 64, 257 tiles
+    (33, 65536, 64, 64, True),   # B 1024, 64 tiles: the largest K
 ]
 
 # block sizes below App. B.1's choice, which the ABI also accepts: the first
