@@ -66,6 +66,7 @@ DEFLATED_SHAPES = [
     # the largest K the entry points take
     (33, 65536, 64, 64, True),
     (130, 65536, 32, 16, False),
+    (1 << 20, 64, 16, 16, False),    # the largest M
 ]
 
 

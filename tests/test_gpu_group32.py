@@ -65,6 +65,7 @@ G32_SHAPES = [
     (200, 320, 400, 32, True),
     (257, 640, 256, 32, False),
     (130, 65536, 64, 16, True),      # the largest K, large-tile GEMM
+    (1 << 20, 64, 16, 16, False),    # the largest M
 ]
 
 

@@ -69,6 +69,12 @@ ROTATED_SHAPES = [
     (33, 65536, 64, 64, True),   # B 1024, 64 tiles: the largest K
 ]
 
+def test_rotated_largest_m():
+    """M = 2^20, the largest M the entry points take (B = 64)."""
+    d = I.custom(M=1 << 20, K=64, N=16, r=16, seed=29, n_outliers=1)
+    _rotated_parity(d, oracle_factors(d, 16, hadamard=True))
+
+
 # block sizes below App. B.1's choice, which the ABI also accepts: the first
 # butterfly stages stay inside a lane, or end at the lane-pair exchange
 SMALL_BLOCK_SHAPES = [
