@@ -66,6 +66,7 @@ G32_SHAPES = [
     (257, 640, 256, 32, False),
     (130, 65536, 64, 16, True),      # the largest K, large-tile GEMM
     (1 << 20, 64, 16, 16, False),    # the largest M
+    (65, 64, 1 << 20, 16, False),    # the largest N, large-tile GEMM
 ]
 
 

@@ -76,6 +76,7 @@ EDGE_SHAPES = [
     (130, 65536, 64, 16, True),      # K = 65536, the large-tile GEMM
     (1, 64, 1 << 20, 16, False),     # N = 2^20, one token
     (1 << 20, 64, 16, 16, False),    # M = 2^20
+    (65, 64, 1 << 20, 16, False),    # N = 2^20 on the large-tile GEMM
 ]
 
 
