@@ -4,8 +4,10 @@ The compute lives in libqwam.so (hand-written HIP kernels for gfx950 behind a
 C ABI, include/qwam.h).  `qwam` is its thin ctypes binding, `calib` builds a
 layer's factors offline, `inputs` draws the seeded synthetic workloads.
 """
-from .qwam import (PackedLayer, QwamError, asp_linear, debug_group_partials, forward,  # noqa: F401
-                   lib, make_layer, pack_weights, quantize_act)
+from .qwam import (PackedLayer, QwamError, aog_accumulate, aog_protected_basis,  # noqa: F401
+                   aog_protected_basis_workspace, asp_layer, asp_linear, debug_group_partials, forward, lib,
+                   make_layer, pack_weights, quantize_act, quantize_act_deflated)
 
-__all__ = ["PackedLayer", "QwamError", "asp_linear", "debug_group_partials", "forward", "lib",
-           "make_layer", "pack_weights", "quantize_act"]
+__all__ = ["PackedLayer", "QwamError", "aog_accumulate", "aog_protected_basis", "aog_protected_basis_workspace",
+           "asp_layer", "asp_linear", "debug_group_partials", "forward", "lib", "make_layer", "pack_weights",
+           "quantize_act", "quantize_act_deflated"]
