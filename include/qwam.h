@@ -63,6 +63,7 @@
  *   xq   uint8   [M][K/2]    packed activation codes (code blocks, below)
  *   xs   float   [G][M]      activation scales, group-major
  *   L1t  bf16    [r][K]      L1 transposed: row j is the j-th protected direction
+ *   L1   bf16    [K][r]      L1 itself (row k: channel k of every direction), for the deflation
  *   L2t  bf16    [N][r]      L2 transposed: row n holds (V^T W~)[:, n]
  *   t    bf16    [M][r]      t = bf16(sum_k bf16(x~_k) L1[k, j]), float32 accumulation
  *   bias bf16    [N]         optional
@@ -104,7 +105,7 @@
 extern "C" {
 #endif
 
-#define QWAM_ABI_VERSION 10
+#define QWAM_ABI_VERSION 11
 #define QWAM_GROUP 64
 
 typedef enum {
@@ -129,6 +130,9 @@ typedef struct qwam_layer {
     const uint16_t *L1t;        /* [r][K]    bf16                                    */
     const uint16_t *L2t;        /* [N][r]    bf16                                    */
     const uint16_t *bias;       /* [N]       bf16, or NULL for no bias               */
+    const uint16_t *L1;         /* [K][r]    bf16, the same factor as L1t row by row; */
+                                /* read by qwam_quantize_act_deflated only (may be    */
+                                /* NULL for a layer that is never deflated)           */
 } qwam_layer;
 
 /*
@@ -179,7 +183,9 @@ qwam_status qwam_quantize_act(const qwam_layer *L, int32_t M, const uint16_t *x,
  *             x~_perp <- fl32(x~_perp - t_j L1[:, j])   (exact products)
  *   xq, xs  = group quantization (Eq. 2) and code blocks of x~_perp
  * The outputs feed qwam_asp_linear unchanged: y = Q4(x~_perp) Q4(R)^T + t L2.
- * Arguments, layouts, ownership and errors as for qwam_quantize_act.
+ * Arguments, layouts, ownership and errors as for qwam_quantize_act; it also
+ * reads L->L1 (the deflation takes each channel's row of L1 whole), which
+ * must be set and 16-byte aligned (QWAM_ERR_INVALID_ARG / QWAM_ERR_MISALIGNED).
  */
 qwam_status qwam_quantize_act_deflated(const qwam_layer *L, int32_t M, const uint16_t *x,
                                        uint8_t *xq, float *xs, uint16_t *t, void *stream);

@@ -143,13 +143,20 @@ __device__ __forceinline__ int deflate_channel(int lane) {
   return 16 * ((lane >> 2) & 3) + 4 * (lane >> 4) + (lane & 3);
 }
 
+// The lane's row L1[ch][0 .. RANK-1] of L1 ([K][RANK] bf16, 16-byte aligned):
+// RANK/8 loads of 16 contiguous bytes; word j/2 holds columns j (low half)
+// and j+1.
 template <int RANK>
-__device__ __forceinline__ void load_l1_column(const uint16_t* __restrict__ L1t, int K, int ch,
-                                               uint32_t (&l1w)[RANK / 2]) {
-  const uint16_t* lp = L1t + ch;
+__device__ __forceinline__ void load_l1_row(const uint16_t* __restrict__ L1, int ch, uint32_t (&l1w)[RANK / 2]) {
+  const uint4* lp = reinterpret_cast<const uint4*>(L1 + static_cast<int64_t>(ch) * RANK);
 #pragma unroll
-  for (int j = 0; j < RANK; j += 2)
-    l1w[j / 2] = static_cast<uint32_t>(lp[j * K]) | (static_cast<uint32_t>(lp[(j + 1) * K]) << 16);
+  for (int i = 0; i < RANK / 8; ++i) {
+    const uint4 w = lp[i];
+    l1w[4 * i] = w.x;
+    l1w[4 * i + 1] = w.y;
+    l1w[4 * i + 2] = w.z;
+    l1w[4 * i + 3] = w.w;
+  }
 }
 
 // x~_perp = x~ - L1 t: r rank-1 updates on the FP32 matrix cores, K = 1 each,

@@ -169,7 +169,7 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_kernel(
 template <int RANK, bool INV_LDS>
 __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_deflated_kernel(
     const uint16_t* __restrict__ x, const float* __restrict__ inv_smooth,
-    const uint16_t* __restrict__ L1t, uint8_t* __restrict__ xq, float* __restrict__ xs,
+    const uint16_t* __restrict__ L1t, const uint16_t* __restrict__ L1, uint8_t* __restrict__ xq, float* __restrict__ xs,
     uint16_t* __restrict__ t, int M, int K, int groups_per_wave, int g32) {
   constexpr int RB = RANK / 16;
   // dynamic LDS: [nwaves][16][RANK] double partial t | [16][RANK] float -t |
@@ -242,7 +242,7 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_deflated_
     const uint32_t go = static_cast<uint32_t>(g) * kGroup * 2u;
     f.xa = buf_load16(x_rsrc, x_off + go);
     f.xb = buf_load16(x_rsrc, x_off + go + 16u);
-    load_l1_column<RANK>(L1t, K, g * kGroup + a_ch, f.l1);
+    load_l1_row<RANK>(L1, g * kGroup + a_ch, f.l1);
   };
   const float* tn_row = tneg + row * RANK;
   auto work2 = [&](int g, const DeflFetch<RANK>& f) __attribute__((always_inline)) {
@@ -312,8 +312,8 @@ hipError_t launch_quantize_act(int M, int K, int r, int group, const uint16_t* x
 }
 
 hipError_t launch_quantize_act_deflated(int M, int K, int r, int group, const uint16_t* x,
-                                        const float* inv_smooth, const uint16_t* L1t, uint8_t* xq, float* xs,
-                                        uint16_t* t, hipStream_t stream) {
+                                        const float* inv_smooth, const uint16_t* L1t, const uint16_t* L1,
+                                        uint8_t* xq, float* xs, uint16_t* t, hipStream_t stream) {
   const int g32 = group == 32 ? 1 : 0;
   const int G = K / kGroup;
   const bool inv_lds = K <= 16384;
@@ -329,10 +329,10 @@ hipError_t launch_quantize_act_deflated(int M, int K, int r, int group, const ui
     }
     if (inv_lds)
       hipLaunchKernelGGL(kernel_lds, dim3((M + 15) / 16), dim3(64 * nwaves), lds, stream, x, inv_smooth, L1t,
-                         xq, xs, t, M, K, gpw, g32);
+                         L1, xq, xs, t, M, K, gpw, g32);
     else
       hipLaunchKernelGGL(kernel_global, dim3((M + 15) / 16), dim3(64 * nwaves), lds, stream, x, inv_smooth, L1t,
-                         xq, xs, t, M, K, gpw, g32);
+                         L1, xq, xs, t, M, K, gpw, g32);
     return hipGetLastError();
   };
   switch (r) {

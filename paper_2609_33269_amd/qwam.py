@@ -34,7 +34,7 @@ class QwamLayerC(ctypes.Structure):
     _fields_ = [("K", ctypes.c_int32), ("N", ctypes.c_int32), ("r", ctypes.c_int32),
                 ("group", ctypes.c_int32), ("hadamard", ctypes.c_int32), ("wq", ctypes.c_void_p), ("ws", ctypes.c_void_p),
                 ("inv_smooth", ctypes.c_void_p), ("L1t", ctypes.c_void_p),
-                ("L2t", ctypes.c_void_p), ("bias", ctypes.c_void_p)]
+                ("L2t", ctypes.c_void_p), ("bias", ctypes.c_void_p), ("L1", ctypes.c_void_p)]
 
 
 _LP = ctypes.POINTER(QwamLayerC)
@@ -126,6 +126,7 @@ class PackedLayer:
     bias: Optional[torch.Tensor] = None   # bf16 [N]
     hadamard: int = 0                     # block size of the rotation (Eq. 3), 0 = none
     group: int = GROUP                    # channels per scale: 64, or 32 (App. B.1)
+    L1: Optional[torch.Tensor] = None     # bf16 [K][r] (the deflated activation path reads it)
 
     def c_struct(self) -> QwamLayerC:
         G = self.K // self.group
@@ -137,6 +138,7 @@ class PackedLayer:
         c.L1t = _req(self.L1t, "L1t", torch.bfloat16, (self.r, self.K))
         c.L2t = _req(self.L2t, "L2t", torch.bfloat16, (self.N, self.r))
         c.bias = None if self.bias is None else _req(self.bias, "bias", torch.bfloat16, (self.N,))
+        c.L1 = None if self.L1 is None else _req(self.L1, "L1", torch.bfloat16, (self.K, self.r))
         return c
 
 
@@ -159,13 +161,14 @@ def make_layer(R: torch.Tensor, smooth: torch.Tensor, L1: torch.Tensor, L2: torc
                bias: Optional[torch.Tensor] = None, stream=None, hadamard: int = 0,
                group: int = GROUP) -> PackedLayer:
     """Pack R and lambda and lay out the branch factors: L1 bf16 [K][r] and
-    L2 bf16 [r][N] are stored transposed (L1t [r][K], L2t [N][r]).  With
+    L2 bf16 [r][N] are stored transposed (L1t [r][K], L2t [N][r]), and L1 also
+    as given (the deflated activation path reads its rows).  With
     `hadamard` = B, R, L1 and L2 must be those of the rotated layer (Eq. 3)."""
     N, K = R.shape
     r = L1.shape[1]
     wq, ws, inv = pack_weights(R, smooth, stream, group)
     return PackedLayer(K=K, N=N, r=r, wq=wq, ws=ws, inv_smooth=inv,
-                       L1t=L1.t().contiguous(), L2t=L2.t().contiguous(),
+                       L1t=L1.t().contiguous(), L2t=L2.t().contiguous(), L1=L1.contiguous(),
                        bias=None if bias is None else bias.contiguous(), hadamard=hadamard, group=group)
 
 

@@ -40,7 +40,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == set(Q.SIGNATURES), "binding and header disagree"
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.qwam_abi_version() == 10
+    assert lib.qwam_abi_version() == 11
     assert lib.qwam_status_string(3) == b"QWAM_ERR_MISALIGNED"
 
 
@@ -60,7 +60,7 @@ def test_probe_argument_checks(lib):
 def _layer(K=256, N=256, r=16, group=64, hadamard=0, **ptrs):
     c = Q.QwamLayerC()
     c.K, c.N, c.r, c.group, c.hadamard = K, N, r, group, hadamard
-    for f in ("wq", "ws", "inv_smooth", "L1t", "L2t"):
+    for f in ("wq", "ws", "inv_smooth", "L1t", "L2t", "L1"):
         setattr(c, f, ptrs.get(f, FAKE))
     c.bias = ptrs.get("bias", None)
     return c
@@ -125,6 +125,12 @@ def test_layer_calls_reject_bad_arguments(lib):
     assert _act(lib, _layer(**{"L1t": FAKE + 2}), deflated=True) == MISALIGNED
     assert _act(lib, _layer(), t=None, deflated=True) == INVALID
     assert lib.qwam_last_error().startswith(b"qwam_quantize_act_deflated")
+    # only the deflated call reads L1 ([K][r]): it must be set and aligned there
+    assert _act(lib, _layer(L1=None), deflated=True) == INVALID
+    assert b"L1 is NULL" in lib.qwam_last_error()
+    assert _act(lib, _layer(L1=FAKE + 2), deflated=True) == MISALIGNED
+    assert _act(lib, _layer(L1=None, hadamard=64), deflated=True) == INVALID
+    assert _act(lib, _layer(L1=None)) in (OK, NO_DEVICE)
     # the rotation block: a power of two in [16, 1024] dividing K, or 0
     for B in (8, 2048, 96, 512):        # too small, too large, not a power of two, does not divide K = 256
         assert _act(lib, _layer(hadamard=B)) == INVALID
