@@ -359,6 +359,28 @@ def small_m_report(args):
 
         us = graph_us(call, nrot)
         us_fused = graph_us(lambda i: qwam.asp_layer(layers[i], x0, out=y), nrot)
+        # App. B.1's full setting (group 32, Hadamard rotation, deflation) on
+        # the same shape: the two-call path (the fused layer takes group 64
+        # without rotation only)
+        w0 = torch.from_numpy(d.w.view(np.int16)).view(torch.bfloat16).to(dev)
+        fp = calib.build_layer(x0, w0, calib.protected_basis(torch.from_numpy(d.a), ra), hadamard=True)
+        Lp = qwam.make_layer(fp["R"], fp["lam"], fp["L1"], fp["L2"], hadamard=fp["hadamard"], group=32)
+        del fp, w0
+        players = [Lp] + [qwam.PackedLayer(K=Ka, N=Ns, r=ra, wq=Lp.wq.clone(), ws=Lp.ws.clone(),
+                                           inv_smooth=Lp.inv_smooth.clone(), L1t=Lp.L1t.clone(),
+                                           L2t=Lp.L2t.clone(), L1=Lp.L1.clone(), hadamard=Lp.hadamard,
+                                           group=32) for _ in range(nrot - 1)]
+        xs32 = torch.empty((Ka // 32, Ms), dtype=torch.float32, device=dev)
+
+        def call_paper(i):
+            L = players[i]
+            qwam.quantize_act_deflated(L, x0, out=(xq, xs32, t))
+            qwam.asp_linear(L, xq, xs32, t, out=y)
+
+        us_paper = graph_us(call_paper, nrot)
+        us_paper_act = graph_us(lambda i: qwam.quantize_act_deflated(players[i], x0, out=(xq, xs32, t)), nrot)
+        us_paper_gemm = graph_us(lambda i: qwam.asp_linear(players[i], xq, xs32, t, out=y), nrot)
+        del players, Lp
         us1 = graph_us(lambda i: qwam.quantize_act(layers[i], x0, out=(xq, xs, t)), nrot)
         us2 = graph_us(lambda i: qwam.asp_linear(layers[i], xq, xs, t, out=y), nrot)
         # the bf16 linear it replaces (hipBLASLt through torch), same graph method,
@@ -375,6 +397,9 @@ def small_m_report(args):
             "workload": "action_expert", "M": Ms, "K": Ka, "N": Ns, "r": ra,
             "us_per_call": round(us, 2), "us_quantize_act": round(us1, 2), "us_asp_gemm": round(us2, 2),
             "us_fused_layer": round(us_fused, 2), "fused_GBs": round((b1 + b2) / (us_fused * 1e-6) / 1e9, 1),
+            "us_group32_rotated_deflated_two_call": round(us_paper, 2),
+            "us_group32_rotated_deflated_act": round(us_paper_act, 2),
+            "us_group32_gemm": round(us_paper_gemm, 2),
             "fused_speedup_vs_bf16_linear": round(us_bf16 / us_fused, 3),
             "algorithmic_bytes": b1 + b2, "GBs": round((b1 + b2) / (us * 1e-6) / 1e9, 1),
             "gemm_GBs": round(b2 / (us2 * 1e-6) / 1e9, 1),

@@ -105,8 +105,8 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_rotated_k
   using Acc = std::conditional_t<DEFLATE, double, float>;
   // dynamic LDS: two tiles [16][T + pad] float (tile tb in buffer tb % 2) |
   // partial t [nwaves][16][RANK] Acc at float offset red_off (after the tiles,
-  // or over the second tile when both do not fit) | (DEFLATE) -t [16][RANK]
-  // float after both
+  // or, when both do not fit, over the buffer the last tile does not use) |
+  // (DEFLATE) -t [16][RANK] float after both
   extern __shared__ double lds_raw[];
 
   const int lane = threadIdx.x & 63;
@@ -123,7 +123,7 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_rotated_k
   float* tiles = reinterpret_cast<float*>(lds_raw);
   Acc* red = reinterpret_cast<Acc*>(tiles + red_off);
   float* tneg = reinterpret_cast<float*>(red + nwaves * 16 * RANK);
-  if (red_off < 2 * 16 * TS) tneg = tiles + 2 * 16 * TS;   // red over the second tile
+  if (red_off < 2 * 16 * TS) tneg = tiles + 2 * 16 * TS;   // red over a tile buffer
 
   const buf_rsrc x_rsrc = make_rsrc(x + static_cast<int64_t>(m0) * K, static_cast<uint32_t>(rows) * K * 2u);
   const buf_rsrc q_rsrc = make_rsrc(xq + static_cast<int64_t>(m0) * (K / 2), static_cast<uint32_t>(rows) * (K / 2));
@@ -213,21 +213,32 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_rotated_k
       }
     }
   }
-  if constexpr (DEFLATE) fetch_tile(0, rf);     // the second pass starts over
-  lds_sync();                                   // the partials may overwrite the second tile
+  // the second pass takes the last tile first, still in LDS from the first
+  // pass, then tiles 0 .. ntiles - 2 again; tile 0's x is requested here
+  if constexpr (DEFLATE)
+    if (ntiles > 1) fetch_tile(0, rf);
+  lds_sync();                                   // the partials may overwrite a tile buffer
   store_t_partials<RB>(red, wave, lane, acc);
   lds_sync();
   reduce_t<RANK>(red, nwaves, rows, t + static_cast<int64_t>(m0) * RANK, DEFLATE ? tneg : nullptr);
 
   if constexpr (DEFLATE) {
     lds_sync();
-    // second pass: rotate again, deflate, quantize
+    // second pass: deflate and quantize.  Step 0 reads the last tile where
+    // the first pass left it (buffer Lb; the partial t tiles, if they were
+    // placed over a tile, went to the other buffer); step i >= 1 rotates tile
+    // i - 1 again into buffer (Lb + i) % 2, which every wave last read at
+    // step i - 2, before the previous barrier.
     const int a_ch = deflate_channel(lane);
     const float* tn_row = tneg + row * RANK;
-    for (int tb = 0; tb < ntiles; ++tb) {
-      float* tile = tiles + (tb & 1) * 16 * TS;
-      rotate_tile(rf, tile);
-      if (tb + 1 < ntiles) fetch_tile(tb + 1, rf);
+    const int Lb = (ntiles - 1) & 1;
+    for (int i = 0; i < ntiles; ++i) {
+      const int tb = i == 0 ? ntiles - 1 : i - 1;
+      float* tile = tiles + ((Lb + i) & 1) * 16 * TS;
+      if (i > 0) {
+        rotate_tile(rf, tile);
+        if (i < ntiles - 1) fetch_tile(i, rf);
+      }
       uint32_t l1w[kMaxPerWave][RANK / 2];
 #pragma unroll
       for (int k = 0; k < kMaxPerWave; ++k) {
@@ -269,13 +280,16 @@ hipError_t launch_quantize_act_rotated(int M, int K, int r, int group, int B, bo
   if (T / kGroup > 16) return hipErrorInvalidValue;
   const float hscale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(B)));
   auto go = [&](auto kernel, int nwaves, size_t acc_bytes) {
-    // two tiles, then the partial t tiles, or those over the second tile when
+    // two tiles, then the partial t tiles, or those over a tile buffer when
     // all of it would not fit in LDS (and they fit in a tile)
     const size_t tile_bytes = static_cast<size_t>(16) * (T + kTilePad) * sizeof(float);
     const size_t red_bytes = static_cast<size_t>(nwaves) * 16 * r * acc_bytes;
     const size_t tneg_bytes = deflate ? 16 * r * sizeof(float) : 0;
     const bool over = 2 * tile_bytes + red_bytes + tneg_bytes > 160 * 1024 && red_bytes <= tile_bytes;
-    const int red_off = static_cast<int>((over ? 1 : 2) * tile_bytes / sizeof(float));
+    // over a tile: the buffer the last tile does not use (the deflated
+    // variant's second pass reads that tile again)
+    const int last_buf = (K / T - 1) & 1;
+    const int red_off = static_cast<int>((over ? 1 - last_buf : 2) * tile_bytes / sizeof(float));
     const size_t lds = 2 * tile_bytes + (over ? 0 : red_bytes) + tneg_bytes;
     if (lds > 160 * 1024) return hipErrorInvalidValue;
     if (lds > 64 * 1024) {
