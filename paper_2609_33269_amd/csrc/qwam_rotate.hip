@@ -260,6 +260,180 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_rotated_k
   }
 }
 
+// Few tokens (M <= kFewTokens, K <= KMAX): one 256-thread workgroup per
+// token, so that a call of a few tokens spreads over as many CUs as tokens
+// instead of running on one.  The same arithmetic as above, laid out for one
+// token:
+//   rotate:   wave w < ceil(K / 1024) transforms channels 1024 w + 16 lane ..
+//             +15 in registers (fwht16) into an LDS row of K floats, and
+//             bf16(x~) as doubles into a second row;
+//   t:        thread i sums column j = i % r over its range of CH = KMAX r /
+//             256 consecutive channels in double, from its L1t row segment
+//             (requested at the start); the 256 / r range sums of a column
+//             are then added in range order and rounded once to bf16 (the
+//             sum is exact up to double rounding, as in the oracle's float64
+//             sum);
+//   deflate:  thread i takes channels i, i + 256, .. (CPT = KMAX / 256) and
+//             removes the r directions from them, j ascending, with its L1
+//             rows: cur <- fma(L1[c][j], -t_j, cur) (an exact product, one
+//             rounding: the oracle's step);
+//   quantize: the rotation waves read their 16 channels per lane back and
+//             quantize per group (lanes l, l^1 share a group of 32; l .. l^3
+//             one of 64), one code block per lane.
+constexpr int kFewTokens = 64;
+
+template <int RANK, int KMAX, bool DEFLATE>
+__global__ __launch_bounds__(256) void quantize_act_rotated_few_kernel(
+    const uint16_t* __restrict__ x, const float* __restrict__ inv_smooth, const uint16_t* __restrict__ L1t,
+    const uint16_t* __restrict__ L1, uint8_t* __restrict__ xq, float* __restrict__ xs, uint16_t* __restrict__ t,
+    int M, int K, int logB, float hscale, int group) {
+  constexpr int Q = 256 / RANK;                 // channel ranges per column of t
+  constexpr int CH = KMAX / Q;                  // channels per range
+  constexpr int CPT = KMAX / 256;               // channels per thread in the deflation
+  // LDS: bf16(x~) row [K] double | range sums [Q][RANK] double | x~ row [K] float | -t [RANK] float
+  extern __shared__ double lds_raw[];
+  double* xd = lds_raw;
+  double* sums = xd + K;
+  float* xt = reinterpret_cast<float*>(sums + Q * RANK);
+  float* tn = xt + K;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int m = blockIdx.x;
+  const int npass = (K + 1023) / 1024;
+  const int e = wave * 1024 + 16 * lane;        // first channel of this lane's rotation slice
+  const bool rot_wave = wave < npass;
+  const bool rot_lane = rot_wave && e < K;
+  const int tj = tid % RANK;                    // column of t
+  const int c0 = (tid / RANK) * CH;             // first channel of the range
+
+  // requests: the lane's x and 1/lambda (rotation waves), the thread's L1t
+  // segment and (deflated) its L1 rows
+  const buf_rsrc x_rsrc = make_rsrc(x + static_cast<int64_t>(m) * K, static_cast<uint32_t>(K) * 2u);
+  RotFetch rf{};
+  if (rot_wave) {
+    rf.xa = buf_load16(x_rsrc, static_cast<uint32_t>(e) * 2u);
+    rf.xb = buf_load16(x_rsrc, static_cast<uint32_t>(e) * 2u + 16u);
+    if (rot_lane) {
+      const float4* ip = reinterpret_cast<const float4*>(inv_smooth + e);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) rf.inv[q] = ip[q];
+    }
+  }
+  uint4 lt[CH / 8];
+#pragma unroll
+  for (int k = 0; k < CH / 8; ++k) {
+    lt[k] = make_uint4(0, 0, 0, 0);
+    if (c0 + 8 * k < K) lt[k] = *reinterpret_cast<const uint4*>(L1t + static_cast<int64_t>(tj) * K + c0 + 8 * k);
+  }
+  uint32_t l1w[DEFLATE ? CPT : 1][RANK / 2];
+  if constexpr (DEFLATE) {
+#pragma unroll
+    for (int i = 0; i < CPT; ++i)
+      if (tid + 256 * i < K) load_l1_row<RANK>(L1, tid + 256 * i, l1w[i]);
+  }
+
+  // rotate into the LDS rows (lanes past K stay out of every block: B divides K)
+  if (rot_wave) {
+    float v[16];
+    smooth16_regs(rf.xa, rf.xb, rf.inv, v);
+    fwht16(v, lane, logB);
+    if (rot_lane) {
+      float4* dst = reinterpret_cast<float4*>(xt + e);
+      double2* dd = reinterpret_cast<double2*>(xd + e);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float4 f = make_float4(v[4 * q] * hscale, v[4 * q + 1] * hscale, v[4 * q + 2] * hscale,
+                                     v[4 * q + 3] * hscale);
+        dst[q] = f;
+        dd[2 * q] = make_double2(bf16_to_f32(f32_to_bf16_rne(f.x)), bf16_to_f32(f32_to_bf16_rne(f.y)));
+        dd[2 * q + 1] = make_double2(bf16_to_f32(f32_to_bf16_rne(f.z)), bf16_to_f32(f32_to_bf16_rne(f.w)));
+      }
+    }
+  }
+  __syncthreads();
+
+  // column tj of t over the thread's channel range, in double
+  {
+    double s = 0.0;
+#pragma unroll
+    for (int k = 0; k < CH / 8; ++k) {
+      if (c0 + 8 * k < K) {
+        const uint32_t w[4] = {lt[k].x, lt[k].y, lt[k].z, lt[k].w};
+        const double2* xp = reinterpret_cast<const double2*>(xd + c0 + 8 * k);
+#pragma unroll
+        for (int h = 0; h < 4; ++h) {
+          const double2 a = xp[h];
+          s = __builtin_fma(a.x, static_cast<double>(__uint_as_float(w[h] << 16)), s);
+          s = __builtin_fma(a.y, static_cast<double>(__uint_as_float(w[h] & 0xFFFF0000u)), s);
+        }
+      }
+    }
+    sums[(tid / RANK) * RANK + tj] = s;
+  }
+  __syncthreads();
+  if (tid < RANK) {
+    double s = 0.0;
+    for (int q = 0; q < Q; ++q) s += sums[q * RANK + tid];
+    const uint32_t b = f64_to_bf16_rne(s);
+    t[static_cast<int64_t>(m) * RANK + tid] = static_cast<uint16_t>(b);
+    tn[tid] = -bf16_to_f32(b);
+  }
+
+  if constexpr (DEFLATE) {
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int c = tid + 256 * i;
+      if (c < K) {
+        float v = xt[c];
+#pragma unroll
+        for (int j = 0; j < RANK; j += 2) {
+          const uint32_t w = l1w[i][j / 2];
+          v = __builtin_fmaf(__uint_as_float(w << 16), tn[j], v);
+          v = __builtin_fmaf(__uint_as_float(w & 0xFFFF0000u), tn[j + 1], v);
+        }
+        xt[c] = v;
+      }
+    }
+    __syncthreads();
+  }
+
+  // quantize the lane's 16 channels; one code block per lane
+  if (rot_wave) {
+    float v[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) v[q] = 0.0f;
+    if (rot_lane) {
+      const float4* src = reinterpret_cast<const float4*>(xt + e);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float4 f = src[q];
+        v[4 * q] = f.x; v[4 * q + 1] = f.y; v[4 * q + 2] = f.z; v[4 * q + 3] = f.w;
+      }
+    }
+    float amax = 0.0f;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) amax = __builtin_fmaxf(amax, __builtin_fabsf(v[q]));
+    // lanes of one group: l, l^1 (32 channels), and l^2, l^3 (64)
+    amax = __builtin_fmaxf(amax, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(amax), 0xB1, 0xF, 0xF, false)));
+    if (group == kGroup)
+      amax = __builtin_fmaxf(amax, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(amax), 0x4E, 0xF, 0xF, false)));
+    const float sc = q4_scale(amax);
+    const float inv = q4_inv(sc);
+    float xs16[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) xs16[q] = v[q] * inv;
+    uint32_t d0, d1, d2;
+    codes_fp6_16(xs16, d0, d1, d2);
+    if (rot_lane) {
+      *reinterpret_cast<uint2*>(xq + static_cast<int64_t>(m) * (K / 2) + e / 2) = fp6_code_block(d0, d1, d2);
+      if (e % group == 0) xs[static_cast<int64_t>(e / group) * M + m] = sc;
+    }
+  }
+}
+
 // Tile width: the largest multiple of max(B, 64) that divides K and is at
 // most 1024.
 static int rotate_tile_width(int K, int B) {
@@ -279,6 +453,23 @@ hipError_t launch_quantize_act_rotated(int M, int K, int r, int group, int B, bo
   // a tile has at most 16 passes / groups: per_wave<r>() per wave
   if (T / kGroup > 16) return hipErrorInvalidValue;
   const float hscale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(B)));
+  // few tokens: one workgroup per token (r = 16 up to K = 2048, r = 32 up to K = 1024)
+  if (M <= kFewTokens && (r == 16 || r == 32) && K * r <= 256 * 128) {
+    auto few = [&](auto kernel) {
+      const size_t lds = static_cast<size_t>(K + 256) * sizeof(double) + static_cast<size_t>(K + r) * sizeof(float);
+      hipLaunchKernelGGL(kernel, dim3(M), dim3(256), lds, stream, x, inv_smooth, L1t, L1, xq, xs, t, M, K, logB,
+                         hscale, group);
+      return hipGetLastError();
+    };
+    const int kmax = K <= 256 ? 256 : K <= 512 ? 512 : K <= 1024 ? 1024 : 2048;
+#define QWAM_FEW(R, KM)                                                                             \
+  if (r == R && kmax == KM)                                                                         \
+    return deflate ? few(quantize_act_rotated_few_kernel<R, KM, true>)                              \
+                   : few(quantize_act_rotated_few_kernel<R, KM, false>);
+    QWAM_FEW(16, 256) QWAM_FEW(16, 512) QWAM_FEW(16, 1024) QWAM_FEW(16, 2048)
+    QWAM_FEW(32, 256) QWAM_FEW(32, 512) QWAM_FEW(32, 1024)
+#undef QWAM_FEW
+  }
   auto go = [&](auto kernel, int nwaves, size_t acc_bytes) {
     // two tiles, then the partial t tiles, or those over a tile buffer when
     // all of it would not fit in LDS (and they fit in a tile)

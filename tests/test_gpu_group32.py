@@ -76,7 +76,8 @@ def test_group32_shapes(M, K, N, r, bias):
     _g32_parity(d, oracle_factors(d, r), d.bias)
 
 
-@pytest.mark.parametrize("M,K,N,r", [(33, 256, 96, 32), (130, 1024, 272, 16), (33, 65536, 64, 32)])
+@pytest.mark.parametrize("M,K,N,r", [(33, 256, 96, 32), (130, 1024, 272, 16), (33, 65536, 64, 32),
+                                     (16, 1024, 512, 16), (64, 1024, 96, 32), (5, 1536, 64, 16)])
 @pytest.mark.parametrize("rotated,deflate", [(False, True), (True, False), (True, True)])
 def test_group32_with_deflation_and_rotation(M, K, N, r, rotated, deflate):
     d = I.custom(M=M, K=K, N=N, r=r, seed=M * 19 + K, n_outliers=2)

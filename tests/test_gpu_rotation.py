@@ -100,6 +100,26 @@ def test_rotated_small_blocks(M, K, N, r, bias, B, deflate):
     _rotated_parity(d, oracle_factors(d, r, hadamard=B), d.bias, deflate=deflate)
 
 
+# one workgroup per token (M <= 64, r = 16 up to K = 2048, r = 32 up to K = 1024)
+FEW_TOKEN_SHAPES = [
+    # M, K, N, r, bias          block B, rotation waves
+    (16, 1024, 256, 16, False),  # B 1024, one wave: the action-expert K
+    (64, 1024, 128, 32, True),  # B 1024, the most tokens and the largest K of r = 32
+    (7, 1536, 64, 16, True),    # B 512, the second wave half past K
+    (3, 2048, 48, 16, False),   # B 1024, two waves: the largest K of r = 16
+    (9, 320, 32, 32, False),    # B 64, K below the kernel's channel capacity
+    (2, 192, 32, 16, True),     # B 64
+    (65, 1024, 64, 16, False),  # one token past: the 16-token kernel
+]
+
+
+@pytest.mark.parametrize("deflate", [False, True])
+@pytest.mark.parametrize("M,K,N,r,bias", FEW_TOKEN_SHAPES)
+def test_rotated_few_tokens(M, K, N, r, bias, deflate):
+    d = I.custom(M=M, K=K, N=N, r=r, seed=M * 23 + K, n_outliers=max(1, K // 100), with_bias=bias)
+    _rotated_parity(d, oracle_factors(d, r, hadamard=True), d.bias, deflate=deflate)
+
+
 def test_rotated_one_hot_closed_form():
     """x = e_k (lambda = 1, B = 1024): the rotated token is +-2^-5 on the whole
     block, so every code of that block is +-7 with the sign of row k of H and
