@@ -344,7 +344,7 @@ def small_m_report(args):
         del f, w0
         wbytes = Ns * Ka // 2 + Ns * Ga * 4 + Ns * ra * 2 + Ka * 4 + ra * Ka * 2
         nrot = int(min(1024, max(2, (768 << 20) // wbytes)))        # > the 256 MB Infinity Cache
-        layers = [L0] + [qwam.PackedLayer(K=Ka, N=Ns, r=ra, wq=L0.wq.clone(), ws=L0.ws.clone(),
+        layers = [L0] + [qwam.PackedLayer(K=Ka, N=Ns, r=ra, wq=L0.wq.clone(), ws=L0.ws.clone(), wsp=L0.wsp.clone(),
                                           inv_smooth=L0.inv_smooth.clone(), L1t=L0.L1t.clone(),
                                           L2t=L0.L2t.clone(), L1=L0.L1.clone()) for _ in range(nrot - 1)]
         xq = torch.empty((Ms, Ka // 2), dtype=torch.uint8, device=dev)
@@ -366,7 +366,7 @@ def small_m_report(args):
         fp = calib.build_layer(x0, w0, calib.protected_basis(torch.from_numpy(d.a), ra), hadamard=True)
         Lp = qwam.make_layer(fp["R"], fp["lam"], fp["L1"], fp["L2"], hadamard=fp["hadamard"], group=32)
         del fp, w0
-        players = [Lp] + [qwam.PackedLayer(K=Ka, N=Ns, r=ra, wq=Lp.wq.clone(), ws=Lp.ws.clone(),
+        players = [Lp] + [qwam.PackedLayer(K=Ka, N=Ns, r=ra, wq=Lp.wq.clone(), ws=Lp.ws.clone(), wsp=Lp.wsp.clone(),
                                            inv_smooth=Lp.inv_smooth.clone(), L1t=Lp.L1t.clone(),
                                            L2t=Lp.L2t.clone(), L1=Lp.L1.clone(), hadamard=Lp.hadamard,
                                            group=32) for _ in range(nrot - 1)]
@@ -718,7 +718,7 @@ def main():
     layers, xins, outs = [], [], []
     for i in range(nrot):
         L = layer0 if i == 0 else qwam.PackedLayer(
-            K=K, N=N, r=R_RANK, wq=layer0.wq.clone(), ws=layer0.ws.clone(),
+            K=K, N=N, r=R_RANK, wq=layer0.wq.clone(), ws=layer0.ws.clone(), wsp=layer0.wsp.clone(),
             inv_smooth=layer0.inv_smooth.clone(), L1t=layer0.L1t.clone(), L2t=layer0.L2t.clone(),
             L1=layer0.L1.clone(), hadamard=layer0.hadamard, group=layer0.group)
         layers.append(L)

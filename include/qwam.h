@@ -59,6 +59,7 @@
  *   smooth float [K]         lambda
  *   wq   uint8   [N][K/2]    packed weight codes (code blocks, below)
  *   ws   float   [G][N]      weight scales, group-major
+ *   wsp  uint32  [G][N]      each weight scale as bf16 pieces hi | lo << 16 (qwam_layer)
  *   inv_smooth float [K]     fl32(1 / lambda)
  *   xq   uint8   [M][K/2]    packed activation codes (code blocks, below)
  *   xs   float   [G][M]      activation scales, group-major
@@ -105,7 +106,7 @@
 extern "C" {
 #endif
 
-#define QWAM_ABI_VERSION 11
+#define QWAM_ABI_VERSION 12
 #define QWAM_GROUP 64
 
 typedef enum {
@@ -133,6 +134,11 @@ typedef struct qwam_layer {
     const uint16_t *L1;         /* [K][r]    bf16, the same factor as L1t row by row; */
                                 /* read by qwam_quantize_act_deflated only (may be    */
                                 /* NULL for a layer that is never deflated)           */
+    const uint32_t *wsp;        /* [K/group][N] each ws as two bf16 pieces,          */
+                                /* hi | lo << 16 with hi = bf16(ws) and              */
+                                /* lo = bf16(ws - hi), both rounded to nearest even; */
+                                /* written by qwam_pack_weights, read by             */
+                                /* qwam_asp_linear                                   */
 } qwam_layer;
 
 /*
@@ -141,17 +147,19 @@ typedef struct qwam_layer {
  * of each row of R with the quantizer of Eq. 2 (scale = fl32(absmax / 7); a group with absmax
  * below 7 * 2^-126 gets scale 0 and codes 0), packs the codes into code blocks
  * and writes
- * inv_smooth[k] = fl32(1 / smooth[k]).
+ * inv_smooth[k] = fl32(1 / smooth[k]).  It also writes each scale as the two
+ * bf16 pieces the GEMM's scale products take (wsp, see qwam_layer).
  *   R          in   float [N][K]
  *   smooth     in   float [K], every entry finite and nonzero
  *   wq         out  uint8 [N][K/2]
  *   ws         out  float [K/group][N]
+ *   wsp        out  uint32 [K/group][N]
  *   inv_smooth out  float [K]
  */
 qwam_status qwam_pack_weights(int32_t K, int32_t N, int32_t group,
                               const float *R, const float *smooth,
-                              uint8_t *wq, float *ws, float *inv_smooth,
-                              void *stream);
+                              uint8_t *wq, float *ws, uint32_t *wsp,
+                              float *inv_smooth, void *stream);
 
 /*
  * Activation side of one layer call (the first kernel of App. B.1): for every
@@ -199,9 +207,10 @@ qwam_status qwam_quantize_act_deflated(const qwam_layer *L, int32_t M, const uin
  *     y[m, n] = bf16( sum_g xs ws P + sum_j t[m, j] L2t[n, j] + bias[n] )
  * The scale product xs * ws of a group is formed from two-piece bf16 splits
  * of each scale (hi = bf16(s), lo = bf16(s - hi)), within about 2^-15 of the
- * float32 product; the float32 sum runs in any order (App. B.1 allows the
+ * float32 product: the weight's from L->wsp, the activation's formed in the
+ * kernel; the float32 sum runs in any order (App. B.1 allows the
  * accumulation order to differ).
- *   L   in   packed layer
+ *   L   in   packed layer (L->wsp must be set)
  *   xq, xs, t  in  outputs of qwam_quantize_act for the same M
  *   y   out  bf16 [M][N]
  */

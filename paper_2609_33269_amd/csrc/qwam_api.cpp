@@ -97,7 +97,7 @@ qwam_status launched(const char* fn, hipError_t e) {
 extern "C" {
 
 qwam_status qwam_pack_weights(int32_t K, int32_t N, int32_t group, const float* R, const float* smooth,
-                              uint8_t* wq, float* ws, float* inv_smooth, void* stream) {
+                              uint8_t* wq, float* ws, uint32_t* wsp, float* inv_smooth, void* stream) {
   const char* fn = "qwam_pack_weights";
   qwam_status s = check_kn(fn, K, N, group);
   if (s != QWAM_OK) return s;
@@ -105,9 +105,10 @@ qwam_status qwam_pack_weights(int32_t K, int32_t N, int32_t group, const float* 
   QWAM_REQUIRE_PTR(smooth);
   QWAM_REQUIRE_PTR(wq);
   QWAM_REQUIRE_PTR(ws);
+  QWAM_REQUIRE_PTR(wsp);
   QWAM_REQUIRE_PTR(inv_smooth);
   if ((s = check_device(fn)) != QWAM_OK) return s;
-  return launched(fn, qwam::launch_pack_weights(K, N, group, R, smooth, wq, ws, inv_smooth,
+  return launched(fn, qwam::launch_pack_weights(K, N, group, R, smooth, wq, ws, wsp, inv_smooth,
                                                 static_cast<hipStream_t>(stream)));
 }
 
@@ -161,6 +162,7 @@ qwam_status qwam_asp_linear(const qwam_layer* L, int32_t M, const uint8_t* xq, c
   if ((s = check_m(fn, M)) != QWAM_OK) return s;
   QWAM_REQUIRE_PTR(L->wq);
   QWAM_REQUIRE_PTR(L->ws);
+  QWAM_REQUIRE_PTR(L->wsp);
   QWAM_REQUIRE_PTR(L->L2t);
   if (L->bias != nullptr && !aligned16(L->bias))
     return fail(QWAM_ERR_MISALIGNED, "%s: bias is not 16-byte aligned", fn);
@@ -173,7 +175,7 @@ qwam_status qwam_asp_linear(const qwam_layer* L, int32_t M, const uint8_t* xq, c
       static_cast<int64_t>(L->N) * (L->K / L->group) >= (int64_t(1) << 29))
     return fail(QWAM_ERR_UNSUPPORTED, "%s: M*K/group and N*K/group must be below 2^29", fn);
   if ((s = check_device(fn)) != QWAM_OK) return s;
-  return launched(fn, qwam::launch_asp_gemm(M, L->N, L->K, L->r, L->group, xq, xs, t, L->wq, L->ws, L->L2t,
+  return launched(fn, qwam::launch_asp_gemm(M, L->N, L->K, L->r, L->group, xq, xs, t, L->wq, L->ws, L->wsp, L->L2t,
                                             L->bias, y, static_cast<hipStream_t>(stream)));
 }
 

@@ -26,13 +26,16 @@
 //     rows per half-wave) hit distinct banks;
 //   * wave (wm, wn) owns rows 64*wm.. and columns 64*wn.. as 2 x 2 blocks of
 //     v_mfma_scale_f32_32x32x64_f8f6f4 (FP6 e2m3 operands, one 64-channel
-//     span per instruction, twice the FP8 rate): lane l holds row l%32 and
-//     half l/32 of the span.  A code block (16 codes in two words, qwam.h)
+//     span per instruction, twice the FP8 rate), with the weight rows as the
+//     A operand and the activation rows as the B operand, so that a block's
+//     result holds y transposed (lane l: token l%32, and four consecutive
+//     output columns per result quarter); lane l of an operand holds its row
+//     l%32 and half l/32 of the span.  A code block (16 codes in two words, qwam.h)
 //     turns into three operand words with four ANDs: each 6-bit field is then
 //     sign | |code| in the mantissa field, the e2m3 subnormal code / 8.  The
 //     E8M0 scales (2^3 on each side) cancel the 2^-6, so the float32 result is
 //     the integer partial P itself, exactly (|P| <= 3136);
-//   * the per-output scale products sx[m] * sw[n] of a group are an outer
+//   * the per-output scale products sw[n] * sx[m] of a group are an outer
 //     product: one v_mfma_f32_32x32x4_2b_bf16 over two-piece bf16 splits of
 //     the scales (scale_outer, within about 2^-15 of the float32 product)
 //     gives them for two 32 x 32 blocks at once, in the result layout of the
@@ -47,8 +50,9 @@
 //   * the accumulators start from the bias plus the bf16 branch
 //     (v_mfma_f32_32x32x16_bf16, same result layout as the integer blocks),
 //     computed while the first stage is copied; the epilogue rounds to bf16
-//     (v_cvt_pk_bf16_f32) and stores through LDS so that every lane writes 16
-//     contiguous bytes.
+//     (v_cvt_pk_bf16_f32), and one v_permlane32_swap per pair of result words
+//     gives every lane 8 consecutive columns of its token, so each lane stores
+//     16 contiguous bytes straight from registers (no LDS, no barrier).
 //
 // Group 32 (GS = 32, the paper's setting): the MFMA's K = 64 covers two groups,
 // one per lane half, and each lane's E8M0 scale governs its own 32 values.
@@ -85,7 +89,7 @@ struct StageRef {
   uint8_t* a;
   uint8_t* b;
   float (*sx)[BM];
-  float (*sw)[BN];
+  uint32_t (*sw)[BN];   // the weight scales as bf16 pieces hi | lo << 16
 };
 static_assert(64 * LDY * 2 <= BM * ROWB && BM == BN, "a wave's 64 x 64 bf16 output block must fit in one tile buffer");
 
@@ -110,30 +114,33 @@ __device__ __forceinline__ float lds_load4_volatile(const float* p) {
   typedef const volatile __attribute__((address_space(3))) float lds_f;
   return *(lds_f*)(p);
 }
+__device__ __forceinline__ uint32_t lds_load4_volatile(const uint32_t* p) {
+  typedef const volatile __attribute__((address_space(3))) uint32_t lds_u;
+  return *(lds_u*)(p);
+}
 
 // bf16 bits of (a, b) rounded to nearest even, a in the low half
 __device__ __forceinline__ uint32_t bf16_pair(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(v2f{a, b}, v2bf));
 }
 
-// The scale products sx * sw of two 32 x 32 blocks (lane l: row of sx,
-// column of sw, both l%32, of block l/32), in the result layout of the integer
-// blocks.  Each scale is split into two bf16 pieces, hi = bf16(s) and
-// lo = bf16(s - hi) (the difference is exact in float32), and one
-// v_mfma_f32_32x32x4_2b_bf16 sums the four exact products of
-// [hi, hi, lo, lo] (sx) and [hi, lo, hi, lo] (sw) in float32.  That is the
-// product of the two 16-bit splits, each within 2^-16 of its scale, so the
-// result is within about 2^-15 of sx * sw.  Unlike the float32 outer-product
-// MFMA, the bf16 one lets the SIMD issue VALU work while it runs.
-__device__ __forceinline__ v32f scale_outer(float sx, float sw) {
+// The scale products sw * sx of two 32 x 32 blocks (lane l: sw of the weight
+// row l%32 (A side), sx of the token l%32 of B block l/32), in the result
+// layout of the integer blocks.  Each scale is split into two bf16 pieces,
+// hi = bf16(s) and lo = bf16(s - hi) (the difference is exact in float32), and
+// one v_mfma_f32_32x32x4_2b_bf16 sums the four exact products of
+// [hi, lo, hi, lo] (sw, the packed pieces hi | lo << 16 the weight pack wrote,
+// twice) and [hi, hi, lo, lo] (sx, split here) in float32.  That is the product
+// of the two 16-bit splits, each within 2^-16 of its scale, so the result is
+// within about 2^-15 of sw * sx.  Unlike the float32 outer-product MFMA, the
+// bf16 one lets the SIMD issue VALU work while it runs.
+__device__ __forceinline__ v32f scale_outer(uint32_t wpieces, float sx) {
   typedef short v4s __attribute__((ext_vector_type(4)));
   const uint32_t hx = bf16_pair(sx, sx);
   const float lo_x = sx - __builtin_bit_cast(float, hx << 16);
   const uint32_t lx = bf16_pair(lo_x, lo_x);
-  const uint32_t hw = bf16_pair(sw, sw);
-  const uint32_t w = bf16_pair(sw, sw - __builtin_bit_cast(float, hw << 16));
-  const v4s a = __builtin_bit_cast(v4s, static_cast<uint64_t>(hx) | (static_cast<uint64_t>(lx) << 32));
-  const v4s b = __builtin_bit_cast(v4s, static_cast<uint64_t>(w) | (static_cast<uint64_t>(w) << 32));
+  const v4s a = __builtin_bit_cast(v4s, static_cast<uint64_t>(wpieces) | (static_cast<uint64_t>(wpieces) << 32));
+  const v4s b = __builtin_bit_cast(v4s, static_cast<uint64_t>(hx) | (static_cast<uint64_t>(lx) << 32));
   return __builtin_amdgcn_mfma_f32_32x32x4bf16_1k(a, b, v32f{}, 0, 0, 0);
 }
 
@@ -160,7 +167,7 @@ __device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& 
 template <int RANK, bool PARTIALS, int GS>
 __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
     const uint8_t* __restrict__ xq, const float* __restrict__ xs, const uint16_t* __restrict__ t,
-    const uint8_t* __restrict__ wq, const float* __restrict__ ws, const uint16_t* __restrict__ L2t,
+    const uint8_t* __restrict__ wq, const uint32_t* __restrict__ wsp, const uint16_t* __restrict__ L2t,
     const uint16_t* __restrict__ bias, uint16_t* __restrict__ y, int32_t* __restrict__ P, int M,
     int N, int K) {
   constexpr int NS = kGroup / GS;                               // scale groups per 64-channel span
@@ -168,8 +175,8 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
   typedef StageRef<GPS> Stage;
   __shared__ __attribute__((aligned(16))) uint8_t lds_a0[BM * ROWB], lds_b0[BN * ROWB];
   __shared__ __attribute__((aligned(16))) uint8_t lds_a1[BM * ROWB], lds_b1[BN * ROWB];
-  __shared__ __attribute__((aligned(16))) float lds_sx0[GPS][BM], lds_sw0[GPS][BN];
-  __shared__ __attribute__((aligned(16))) float lds_sx1[GPS][BM], lds_sw1[GPS][BN];
+  __shared__ __attribute__((aligned(16))) float lds_sx0[GPS][BM], lds_sx1[GPS][BM];
+  __shared__ __attribute__((aligned(16))) uint32_t lds_sw0[GPS][BN], lds_sw1[GPS][BN];
   const Stage st0{lds_a0, lds_b0, lds_sx0, lds_sw0};
   const Stage st1{lds_a1, lds_b1, lds_sx1, lds_sw1};
 
@@ -202,12 +209,13 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
     const int row = 8 * (4 * wave + i) + (lane >> 3);
     d_off[i] = static_cast<uint32_t>(row * KB + (((lane & 7) ^ swz(row)) * 16));
   }
-  // scales: waves 0-1 copy xs of the tile's rows, waves 2-3 ws of its columns;
+  // scales: waves 0-1 copy xs of the tile's rows, waves 2-3 the weight-scale
+  // pieces (wsp) of its columns;
   // copy i of such a wave covers scale group (GPS/2 * (w%2) + i/2) of the
   // stage, rows 64*(i%2) .. +63
   const bool s_is_x = wave < 2;
   const buf_rsrc s_rsrc = s_is_x ? make_rsrc(xs, static_cast<uint32_t>(GSC) * M * 4u)
-                                 : make_rsrc(ws, static_cast<uint32_t>(GSC) * N * 4u);
+                                 : make_rsrc(wsp, static_cast<uint32_t>(GSC) * N * 4u);
   const uint32_t s_stride = static_cast<uint32_t>(s_is_x ? M : N) * 4u;
   uint32_t s_off[GPS];
 #pragma unroll
@@ -249,18 +257,16 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
   // swz depends on frow only)
   const int frow_off = frow * ROWB;
   const int fslot = fhalf ^ swz(frow);
-  // activation-scale row of this lane inside a 32-row block: lane 16*rho + v
-  // holds the scale of result register v of lanes in rows rho (v = lane % 16):
-  // row 8*(v/4) + 4*(lane/32) + v%4
-  const int sx_row = 8 * ((lane & 15) >> 2) + 4 * (lane >> 5) + (lane & 3);
 
   // LDS data of one 64-channel span: packed A / B fragments (16 bytes, the
-  // lane's half of the span) and the lane's scales (NS groups): the activation
-  // scale of row l%32 of each row block (A operand of the scale product) and
-  // the weight scale of column l%32 of column block l/32 (B operand).
+  // lane's half of the span: A from the weight tile, B from the activation
+  // tile) and the lane's scales (NS groups): the weight scale of row l%32 of
+  // each A block (A operand of the scale product) and the activation scale of
+  // row l%32 of B block l/32 (B operand).
   struct GroupData {
     uint4 a[2], b[2];
-    float sx[2][NS], sw[NS];
+    uint32_t sa[2][NS];   // weight-scale pieces of the A blocks
+    float sb[NS];         // activation scale of the B-side token
   };
   // Reads group q's data one group ahead of its use.  The loads are volatile
   // and followed by a compiler-only fence, so they are issued here and not
@@ -272,34 +278,35 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
   auto load_group = [&](const Stage& cur, int q) __attribute__((always_inline)) {
     GroupData d;
 #pragma unroll
-    for (int i = 0; i < 2; ++i) d.a[i] = load_frag(cur.a + (wm * 64 + i * 32) * ROWB + frow_off, q);
+    for (int i = 0; i < 2; ++i) d.a[i] = load_frag(cur.b + (wn * 64 + i * 32) * ROWB + frow_off, q);
 #pragma unroll
-    for (int j = 0; j < 2; ++j) d.b[j] = load_frag(cur.b + (wn * 64 + j * 32) * ROWB + frow_off, q);
+    for (int j = 0; j < 2; ++j) d.b[j] = load_frag(cur.a + (wm * 64 + j * 32) * ROWB + frow_off, q);
     if (!PARTIALS) {
 #pragma unroll
       for (int h = 0; h < NS; ++h) {
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
-          const float* p = &cur.sx[NS * q + h][wm * 64 + i * 32 + frow];
-          d.sx[i][h] = GS == 64 ? *p : lds_load4_volatile(p);
+          const uint32_t* p = &cur.sw[NS * q + h][wn * 64 + i * 32 + frow];
+          d.sa[i][h] = GS == 64 ? *p : lds_load4_volatile(p);
         }
-        const float* p = &cur.sw[NS * q + h][wn * 64 + fhalf * 32 + frow];
-        d.sw[h] = GS == 64 ? *p : lds_load4_volatile(p);
+        const float* p = &cur.sx[NS * q + h][wm * 64 + fhalf * 32 + frow];
+        d.sb[h] = GS == 64 ? *p : lds_load4_volatile(p);
       }
     }
     asm volatile("" ::: "memory");
     return d;
   };
 
-  // block (i, j) of group g, scale group h of the span: acc += P * sx * sw
-  // (the partials themselves with PARTIALS).  Result layout of a 32x32 block:
-  // lane l holds column l%32 and rows 8*(v/4) + 4*(l/32) + v%4, v = 0..15.
+  // block (i, j) of group g, scale group h of the span: acc += P * sw * sx
+  // (the partials themselves with PARTIALS).  Result layout of a 32x32 block
+  // (i: weight block, j: activation block): lane l holds token l%32 of block j
+  // and output columns 8*(v/4) + 4*(l/32) + v%4 of block i, v = 0..15.
   auto update = [&](int i, int j, int g, int h, const v16f& p, const v32f& sc) __attribute__((always_inline)) {
     if (PARTIALS) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const int m = m0 + wm * 64 + i * 32 + 8 * (v >> 2) + rsub + (v & 3);
-        const int n = n0 + wn * 64 + j * 32 + frow;
+        const int n = n0 + wn * 64 + i * 32 + 8 * (v >> 2) + rsub + (v & 3);
+        const int m = m0 + wm * 64 + j * 32 + frow;
         if (m < M && n < N) P[(static_cast<int64_t>(m) * N + n) * GSC + NS * g + h] = static_cast<int32_t>(p[v]);
       }
     } else {
@@ -327,7 +334,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
     // scale products of row block i and both column blocks, group h:
     // registers 0-15 belong to column block 0, 16-31 to column block 1
     auto scale_block = [&](int i, int h) __attribute__((always_inline)) {
-      return scale_outer(d.sx[i][h], d.sw[h]);
+      return scale_outer(d.sa[i][h], d.sb[h]);
     };
     // per group h and row block i: the scale products (one MFMA for both
     // column blocks), the two integer blocks, then their updates; each update
@@ -365,34 +372,43 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
 
   issue(0, st0);
   // The accumulators start from the bias and the low-rank branch t . L2
-  // (v_mfma_f32_32x32x16_bf16: lane l holds row / column l%32 and the 8 rank
-  // slots 8*(l/32) .. +7 of a 16-wide rank step, the same slots for t and
-  // L2t).  Its loads overlap the copy of the first stage.
+  // (v_mfma_f32_32x32x16_bf16 with L2t as the A operand and t as the B
+  // operand, the roles of the integer blocks: lane l holds row / column l%32
+  // and the 8 rank slots 8*(l/32) .. +7 of a 16-wide rank step, the same slots
+  // for both).  Result register v of block (i, j) is output column
+  // n0 + 64 wn + 32 i + 8 (v/4) + 4 (l/32) + v%4, so each lane takes the bias
+  // of four consecutive columns per v/4.  These loads overlap the copy of the
+  // first stage.
   if (!PARTIALS) {
     constexpr int KSTEPS = RANK / 16;
     const int kk = fhalf * 8;
     v8s tf[2][KSTEPS], lf[2][KSTEPS];
-    float bv[2];
+    uint2 bv[2][4];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int m = m0 + wm * 64 + i * 32 + frow;
+    for (int j = 0; j < 2; ++j) {
+      const int m = m0 + wm * 64 + j * 32 + frow;
 #pragma unroll
       for (int s = 0; s < KSTEPS; ++s) {
         v8s val = {0, 0, 0, 0, 0, 0, 0, 0};
         if (m < M) val = *reinterpret_cast<const v8s*>(t + static_cast<int64_t>(m) * RANK + s * 16 + kk);
-        tf[i][s] = val;
+        tf[j][s] = val;
       }
     }
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int n = n0 + wn * 64 + j * 32 + frow;
+    for (int i = 0; i < 2; ++i) {
+      const int n = n0 + wn * 64 + i * 32 + frow;
 #pragma unroll
       for (int s = 0; s < KSTEPS; ++s) {
         v8s val = {0, 0, 0, 0, 0, 0, 0, 0};
         if (n < N) val = *reinterpret_cast<const v8s*>(L2t + static_cast<int64_t>(n) * RANK + s * 16 + kk);
-        lf[j][s] = val;
+        lf[i][s] = val;
       }
-      bv[j] = (bias != nullptr && n < N) ? bf16_to_f32(bias[n]) : 0.0f;
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        // N is a multiple of 16: four consecutive columns are all in range or all out
+        const int nb = n0 + wn * 64 + i * 32 + 8 * q4 + rsub;
+        bv[i][q4] = (bias != nullptr && nb < N) ? *reinterpret_cast<const uint2*>(bias + nb) : make_uint2(0u, 0u);
+      }
     }
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -400,11 +416,15 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
       for (int j = 0; j < 2; ++j) {
         v16f c;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) c[v] = bv[j];
+        for (int v = 0; v < 16; ++v) {
+          const uint2 w = bv[i][v >> 2];
+          const uint32_t word = (v & 2) ? w.y : w.x;
+          c[v] = __builtin_bit_cast(float, (v & 1) ? (word & 0xFFFF0000u) : (word << 16));
+        }
 #pragma unroll
         for (int s = 0; s < KSTEPS; ++s)
-          c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, tf[i][s]),
-                                                      __builtin_bit_cast(v8bf, lf[j][s]), c, 0, 0, 0);
+          c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, lf[i][s]),
+                                                      __builtin_bit_cast(v8bf, tf[j][s]), c, 0, 0, 0);
         accf[i][j] = c;
       }
   }
@@ -456,23 +476,24 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
     struct Pipe {
       v8i af0, bf0;        // unpacked A0 / B0 fragments of the current group
       uint4 ra1, rb1;      // packed A1 / B1 fragments of the current group
-      float sx0, sx1, sw;  // its scales
+      uint32_t sa0, sa1;   // its weight-scale pieces
+      float sb;            // and activation scale
       v32f s1;             // scale products and partial of block (1, 1) of
       v16f p11;            // the previous group, updated in slot 1
     };
     auto span_partial = [&](const v8i& a, const v8i& b) __attribute__((always_inline)) {
       return fp6_partial(a, b, kE8M0Code, kE8M0Code);
     };
-    auto scale_products = [&](float sx, float sw) __attribute__((always_inline)) {
+    auto scale_products = [&](uint32_t sa, float sb) __attribute__((always_inline)) {
       if constexpr (PARTIALS) return v32f{};
-      else return scale_outer(sx, sw);
+      else return scale_outer(sa, sb);
     };
     auto start = [&](Pipe& pp, const GroupData& d) __attribute__((always_inline)) {
       pp.af0 = codes_to_fp6(d.a[0]);
       pp.bf0 = codes_to_fp6(d.b[0]);
       pp.ra1 = d.a[1];
       pp.rb1 = d.b[1];
-      if (!PARTIALS) { pp.sx0 = d.sx[0][0]; pp.sx1 = d.sx[1][0]; pp.sw = d.sw[0]; }
+      if (!PARTIALS) { pp.sa0 = d.sa[0][0]; pp.sa1 = d.sa[1][0]; pp.sb = d.sb[0]; }
     };
     // group g at position q (0..7) of two consecutive stages: q < 4 reads
     // st0, q >= 4 st1; the last group of a stage (q % 4 == 3) switches the
@@ -487,7 +508,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
     auto step = [&](auto qc, int g, Pipe& pp, int s_next) __attribute__((always_inline)) {
       constexpr int q = decltype(qc)::value;
       // slot 1: S0 | update (1,1) of g-1, half of A1
-      const v32f s0 = scale_products(pp.sx0, pp.sw);
+      const v32f s0 = scale_products(pp.sa0, pp.sb);
       __builtin_amdgcn_sched_barrier(0);
       if (!PARTIALS || g > 0) update(1, 1, g - 1, 0, pp.p11, pp.s1);
       v8i af1, bf1, af0n, bf0n;
@@ -514,7 +535,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
       update(0, 0, g, 0, p00, s0);
       __builtin_amdgcn_sched_barrier(0);
       // slot 4: S1 | update (0,1), half of A0 of g+1
-      const v32f s1 = scale_products(pp.sx1, pp.sw);
+      const v32f s1 = scale_products(pp.sa1, pp.sb);
       __builtin_amdgcn_sched_barrier(0);
       update(0, 1, g, 0, p01, s0);
       unpack_half(af0n, 0, nd.a[0].x, nd.a[0].y);
@@ -535,7 +556,7 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
       pp.bf0 = bf0n;
       pp.ra1 = nd.a[1];
       pp.rb1 = nd.b[1];
-      if (!PARTIALS) { pp.sx0 = nd.sx[0][0]; pp.sx1 = nd.sx[1][0]; pp.sw = nd.sw[0]; }
+      if (!PARTIALS) { pp.sa0 = nd.sa[0][0]; pp.sa1 = nd.sa[1][0]; pp.sb = nd.sb[0]; }
       pp.s1 = s1;
       pp.p11 = p11;
     };
@@ -580,60 +601,68 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
     if (rest > 6) step(I6{}, g + 6, pp, 0);
     update(1, 1, G - 1, 0, pp.p11, pp.s1);
   }
-  wait_vmcnt<0>();     // the copies issued past the last stage must land
-  __syncthreads();     // before the LDS is reused below
-
+  // the copies issued past the last stage (a stage earlier) must land before
+  // the workgroup's LDS can go to another workgroup
+  wait_vmcnt<0>();
   if (PARTIALS) return;
 
-  // ---- epilogue: round to bf16, staged through LDS so that every lane
-  // stores 16 contiguous bytes; wave w uses the w-th (idle) tile buffer ----
-  uint16_t* ys = reinterpret_cast<uint16_t*>(wave == 0 ? lds_a0 : wave == 1 ? lds_b0 : wave == 2 ? lds_a1 : lds_b1);
+  // ---- epilogue: round to bf16 and store straight from registers.  Lane l
+  // holds, per block (i, j), output row m = m0 + 64 wm + 32 j + l%32 and
+  // columns 8 q + 4 (l/32) .. +3 (q = v/4) of the block: two bf16 pairs per
+  // q.  One v_permlane32_swap per pair of words gives the lower half-wave
+  // columns 16 p .. +7 and the upper half-wave columns 16 p + 8 .. +15 of the
+  // block (p = 0, 1), so every lane stores 16 contiguous bytes and no LDS or
+  // barrier is involved. ----
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < 2; ++j) {
+      const int m = m0 + wm * 64 + j * 32 + frow;
 #pragma unroll
-      for (int v = 0; v < 16; v += 2) {
-        // rows r and r + 1 of column j * 32 + frow
-        const int r = i * 32 + 8 * (v >> 2) + rsub + (v & 3);
-        const v2f pair = {accf[i][j][v], accf[i][j][v + 1]};
-        const uint32_t h = __builtin_bit_cast(uint32_t, __builtin_convertvector(pair, v2bf));
-        ys[r * LDY + j * 32 + frow] = static_cast<uint16_t>(h);
-        ys[(r + 1) * LDY + j * 32 + frow] = static_cast<uint16_t>(h >> 16);
+      for (int p = 0; p < 2; ++p) {
+        // words (q, e): columns 8 q + 4 (l/32) + 2 e, +1 of the block
+        uint32_t w[2][2];
+#pragma unroll
+        for (int qq = 0; qq < 2; ++qq)
+#pragma unroll
+          for (int e = 0; e < 2; ++e) {
+            const int v = 4 * (2 * p + qq) + 2 * e;
+            w[qq][e] = bf16_pair(accf[i][j][v], accf[i][j][v + 1]);
+          }
+        // the upper half-wave's words of q = 2p trade places with the lower
+        // half-wave's words of q = 2p + 1
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          const auto r = __builtin_amdgcn_permlane32_swap(w[0][e], w[1][e], false, false);
+          w[0][e] = r[0];
+          w[1][e] = r[1];
+        }
+        const int n = n0 + wn * 64 + i * 32 + 16 * p + 8 * fhalf;
+        if (m < M && n < N)
+          *reinterpret_cast<uint4*>(y + static_cast<int64_t>(m) * N + n) = make_uint4(w[0][0], w[0][1], w[1][0], w[1][1]);
       }
-  __syncthreads();
-  // the wave's 64 rows x 64 columns: 8 lanes per row, 16 bytes each
-#pragma unroll
-  for (int it = 0; it < 8; ++it) {
-    const int r = it * 8 + (lane >> 3);
-    const int c8 = (lane & 7) * 8;
-    const int m = m0 + wm * 64 + r;
-    const int n = n0 + wn * 64 + c8;
-    if (m < M && n < N)
-      *reinterpret_cast<uint4*>(y + static_cast<int64_t>(m) * N + n) =
-          *reinterpret_cast<const uint4*>(ys + r * LDY + c8);
-  }
+    }
 }
 
 static int gemm_tiles(int M, int N) { return ((M + BM - 1) / BM) * ((N + BN - 1) / BN); }
 
 template <int GS>
 static hipError_t launch_asp_gemm_gs(int M, int N, int K, int r, const uint8_t* xq, const float* xs,
-                                     const uint16_t* t, const uint8_t* wq, const float* ws, const uint16_t* L2t,
-                                     const uint16_t* bias, uint16_t* y, hipStream_t stream) {
+                                     const uint16_t* t, const uint8_t* wq, const uint32_t* wsp,
+                                     const uint16_t* L2t, const uint16_t* bias, uint16_t* y, hipStream_t stream) {
   const dim3 grid(gemm_tiles(M, N)), block(NT);
   switch (r) {
     case 16:
-      hipLaunchKernelGGL((asp_gemm_kernel<16, false, GS>), grid, block, 0, stream, xq, xs, t, wq, ws, L2t, bias, y, nullptr, M, N, K);
+      hipLaunchKernelGGL((asp_gemm_kernel<16, false, GS>), grid, block, 0, stream, xq, xs, t, wq, wsp, L2t, bias, y, nullptr, M, N, K);
       break;
     case 32:
-      hipLaunchKernelGGL((asp_gemm_kernel<32, false, GS>), grid, block, 0, stream, xq, xs, t, wq, ws, L2t, bias, y, nullptr, M, N, K);
+      hipLaunchKernelGGL((asp_gemm_kernel<32, false, GS>), grid, block, 0, stream, xq, xs, t, wq, wsp, L2t, bias, y, nullptr, M, N, K);
       break;
     case 48:
-      hipLaunchKernelGGL((asp_gemm_kernel<48, false, GS>), grid, block, 0, stream, xq, xs, t, wq, ws, L2t, bias, y, nullptr, M, N, K);
+      hipLaunchKernelGGL((asp_gemm_kernel<48, false, GS>), grid, block, 0, stream, xq, xs, t, wq, wsp, L2t, bias, y, nullptr, M, N, K);
       break;
     case 64:
-      hipLaunchKernelGGL((asp_gemm_kernel<64, false, GS>), grid, block, 0, stream, xq, xs, t, wq, ws, L2t, bias, y, nullptr, M, N, K);
+      hipLaunchKernelGGL((asp_gemm_kernel<64, false, GS>), grid, block, 0, stream, xq, xs, t, wq, wsp, L2t, bias, y, nullptr, M, N, K);
       break;
     default:
       return hipErrorInvalidValue;
@@ -641,13 +670,15 @@ static hipError_t launch_asp_gemm_gs(int M, int N, int K, int r, const uint8_t* 
   return hipGetLastError();
 }
 
+// few tokens: the float32 scales (asp_gemm_small_kernel); otherwise the
+// weight-scale pieces
 hipError_t launch_asp_gemm(int M, int N, int K, int r, int group, const uint8_t* xq, const float* xs,
-                           const uint16_t* t, const uint8_t* wq, const float* ws,
+                           const uint16_t* t, const uint8_t* wq, const float* ws, const uint32_t* wsp,
                            const uint16_t* L2t, const uint16_t* bias, uint16_t* y,
                            hipStream_t stream) {
   if (M <= kSmallM) return launch_asp_gemm_small(M, N, K, r, group, xq, xs, t, wq, ws, L2t, bias, y, stream);
-  return group == 32 ? launch_asp_gemm_gs<32>(M, N, K, r, xq, xs, t, wq, ws, L2t, bias, y, stream)
-                     : launch_asp_gemm_gs<64>(M, N, K, r, xq, xs, t, wq, ws, L2t, bias, y, stream);
+  return group == 32 ? launch_asp_gemm_gs<32>(M, N, K, r, xq, xs, t, wq, wsp, L2t, bias, y, stream)
+                     : launch_asp_gemm_gs<64>(M, N, K, r, xq, xs, t, wq, wsp, L2t, bias, y, stream);
 }
 
 hipError_t launch_group_partials(int M, int N, int K, int group, const uint8_t* xq, const uint8_t* wq,

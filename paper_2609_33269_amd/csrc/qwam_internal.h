@@ -6,7 +6,7 @@
 namespace qwam {
 
 hipError_t launch_pack_weights(int K, int N, int group, const float* R, const float* smooth, uint8_t* wq,
-                               float* ws, float* inv_smooth, hipStream_t stream);
+                               float* ws, uint32_t* wsp, float* inv_smooth, hipStream_t stream);
 
 hipError_t launch_quantize_act(int M, int K, int r, int group, const uint16_t* x, const float* inv_smooth,
                                const uint16_t* L1t, uint8_t* xq, float* xs, uint16_t* t,
@@ -25,7 +25,7 @@ hipError_t launch_quantize_act_rotated(int M, int K, int r, int group, int B, bo
                                        uint8_t* xq, float* xs, uint16_t* t, hipStream_t stream);
 
 hipError_t launch_asp_gemm(int M, int N, int K, int r, int group, const uint8_t* xq, const float* xs,
-                           const uint16_t* t, const uint8_t* wq, const float* ws,
+                           const uint16_t* t, const uint8_t* wq, const float* ws, const uint32_t* wsp,
                            const uint16_t* L2t, const uint16_t* bias, uint16_t* y,
                            hipStream_t stream);
 

@@ -1,6 +1,7 @@
 // Weight pack (offline) and the fused activation kernel of the ASP layer.
 //
-//  pack:  R [N][K] f32 -> wq [N][K/2] packed codes, ws [G][N] scales (Eq. 2, App. B.1)
+//  pack:  R [N][K] f32 -> wq [N][K/2] packed codes, ws [G][N] scales (Eq. 2, App. B.1),
+//         and each scale as two bf16 pieces for the GEMM's scale products
 //  act:   x [M][K] bf16 -> x~ = x * (1/lambda) (Eq. 3), per-token group-64
 //         codes xq [M][K/2] and scales xs [G][M] (Eq. 2), and the rank-r
 //         down-projection t = bf16(x~) . L1 on bf16 matrix cores (V^T x~ of
@@ -17,7 +18,8 @@ namespace qwam {
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void pack_weights_kernel(const float* __restrict__ R,
                                                            uint8_t* __restrict__ wq,
-                                                           float* __restrict__ ws, int N, int K, int g32) {
+                                                           float* __restrict__ ws, uint32_t* __restrict__ wsp,
+                                                           int N, int K, int g32) {
   const int G = K / kGroup;
   const int64_t team = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) >> 2;
   const int sub = threadIdx.x & 3;
@@ -52,7 +54,13 @@ __global__ __launch_bounds__(256) void pack_weights_kernel(const float* __restri
   if (active) {
     *reinterpret_cast<uint2*>(wq + static_cast<int64_t>(n) * (K / 2) + g * (kGroup / 2) + sub * 8) =
         fp6_code_block(d0, d1, d2);
-    if (g32 ? (sub & 1) == 0 : sub == 0) ws[static_cast<int64_t>(g32 ? 2 * g + (sub >> 1) : g) * N + n] = s;
+    if (g32 ? (sub & 1) == 0 : sub == 0) {
+      const int64_t at = static_cast<int64_t>(g32 ? 2 * g + (sub >> 1) : g) * N + n;
+      ws[at] = s;
+      // hi = bf16(s), lo = bf16(s - hi): s - hi is exact in float32
+      const uint32_t hi = f32_to_bf16_rne(s);
+      wsp[at] = hi | (f32_to_bf16_rne(s - bf16_to_f32(hi)) << 16);
+    }
   }
 }
 
@@ -268,11 +276,11 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_deflated_
 
 // ---------------------------------------------------------------------------
 hipError_t launch_pack_weights(int K, int N, int group, const float* R, const float* smooth, uint8_t* wq,
-                               float* ws, float* inv_smooth, hipStream_t stream) {
+                               float* ws, uint32_t* wsp, float* inv_smooth, hipStream_t stream) {
   const int64_t teams = static_cast<int64_t>(N) * (K / kGroup);
   const int64_t blocks = (teams * 4 + 255) / 256;
   hipLaunchKernelGGL(pack_weights_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, R,
-                     wq, ws, N, K, group == 32 ? 1 : 0);
+                     wq, ws, wsp, N, K, group == 32 ? 1 : 0);
   hipLaunchKernelGGL(inverse_smoothing_kernel, dim3((K + 255) / 256), dim3(256), 0, stream, smooth,
                      inv_smooth, K);
   return hipGetLastError();

@@ -34,13 +34,14 @@ class QwamLayerC(ctypes.Structure):
     _fields_ = [("K", ctypes.c_int32), ("N", ctypes.c_int32), ("r", ctypes.c_int32),
                 ("group", ctypes.c_int32), ("hadamard", ctypes.c_int32), ("wq", ctypes.c_void_p), ("ws", ctypes.c_void_p),
                 ("inv_smooth", ctypes.c_void_p), ("L1t", ctypes.c_void_p),
-                ("L2t", ctypes.c_void_p), ("bias", ctypes.c_void_p), ("L1", ctypes.c_void_p)]
+                ("L2t", ctypes.c_void_p), ("bias", ctypes.c_void_p), ("L1", ctypes.c_void_p),
+                ("wsp", ctypes.c_void_p)]
 
 
 _LP = ctypes.POINTER(QwamLayerC)
 SIGNATURES = {
     "qwam_pack_weights": (ctypes.c_int, [_i32, _i32, _i32, _c_void_p, _c_void_p, _c_void_p,
-                                         _c_void_p, _c_void_p, _c_void_p]),
+                                         _c_void_p, _c_void_p, _c_void_p, _c_void_p]),
     "qwam_quantize_act": (ctypes.c_int, [_LP, _i32, _c_void_p, _c_void_p, _c_void_p, _c_void_p,
                                          _c_void_p]),
     "qwam_quantize_act_deflated": (ctypes.c_int, [_LP, _i32, _c_void_p, _c_void_p, _c_void_p,
@@ -127,6 +128,7 @@ class PackedLayer:
     hadamard: int = 0                     # block size of the rotation (Eq. 3), 0 = none
     group: int = GROUP                    # channels per scale: 64, or 32 (App. B.1)
     L1: Optional[torch.Tensor] = None     # bf16 [K][r] (the deflated activation path reads it)
+    wsp: Optional[torch.Tensor] = None    # int32 [K/group][N]: ws as bf16 pieces hi | lo << 16 (asp_linear reads it)
 
     def c_struct(self) -> QwamLayerC:
         G = self.K // self.group
@@ -139,22 +141,25 @@ class PackedLayer:
         c.L2t = _req(self.L2t, "L2t", torch.bfloat16, (self.N, self.r))
         c.bias = None if self.bias is None else _req(self.bias, "bias", torch.bfloat16, (self.N,))
         c.L1 = None if self.L1 is None else _req(self.L1, "L1", torch.bfloat16, (self.K, self.r))
+        c.wsp = None if self.wsp is None else _req(self.wsp, "wsp", torch.int32, (G, self.N))
         return c
 
 
 def pack_weights(R: torch.Tensor, smooth: torch.Tensor, stream=None, group: int = GROUP):
     """qwam_pack_weights: R float32 [N][K], smooth float32 [K] ->
-    (wq uint8 [N][K/2], ws float32 [K/group][N], inv_smooth float32 [K])."""
+    (wq uint8 [N][K/2], ws float32 [K/group][N], wsp int32 [K/group][N] (the
+    scales as bf16 pieces hi | lo << 16), inv_smooth float32 [K])."""
     N, K = R.shape
     dev = R.device
     wq = torch.empty((N, K // 2), dtype=torch.uint8, device=dev)
     ws = torch.empty((K // group, N), dtype=torch.float32, device=dev)
+    wsp = torch.empty((K // group, N), dtype=torch.int32, device=dev)
     inv = torch.empty((K,), dtype=torch.float32, device=dev)
     st = lib().qwam_pack_weights(K, N, group, _req(R, "R", torch.float32, (N, K)),
                                  _req(smooth, "smooth", torch.float32, (K,)),
-                                 wq.data_ptr(), ws.data_ptr(), inv.data_ptr(), _stream_ptr(stream))
+                                 wq.data_ptr(), ws.data_ptr(), wsp.data_ptr(), inv.data_ptr(), _stream_ptr(stream))
     _check("qwam_pack_weights", st)
-    return wq, ws, inv
+    return wq, ws, wsp, inv
 
 
 def make_layer(R: torch.Tensor, smooth: torch.Tensor, L1: torch.Tensor, L2: torch.Tensor,
@@ -166,8 +171,8 @@ def make_layer(R: torch.Tensor, smooth: torch.Tensor, L1: torch.Tensor, L2: torc
     `hadamard` = B, R, L1 and L2 must be those of the rotated layer (Eq. 3)."""
     N, K = R.shape
     r = L1.shape[1]
-    wq, ws, inv = pack_weights(R, smooth, stream, group)
-    return PackedLayer(K=K, N=N, r=r, wq=wq, ws=ws, inv_smooth=inv,
+    wq, ws, wsp, inv = pack_weights(R, smooth, stream, group)
+    return PackedLayer(K=K, N=N, r=r, wq=wq, ws=ws, wsp=wsp, inv_smooth=inv,
                        L1t=L1.t().contiguous(), L2t=L2.t().contiguous(), L1=L1.contiguous(),
                        bias=None if bias is None else bias.contiguous(), hadamard=hadamard, group=group)
 

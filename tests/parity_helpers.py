@@ -24,6 +24,22 @@ def bf16_dev(bits: np.ndarray) -> torch.Tensor:
     return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to("cuda:0")
 
 
+def scale_pieces(s: np.ndarray) -> np.ndarray:
+    """The weight scales in the two-piece form the weight pack writes (wsp in
+    include/qwam.h): hi = bf16(s), lo = bf16(s - hi), both to nearest even,
+    packed as hi | lo << 16 (uint32)."""
+    s = np.asarray(s, dtype=np.float32).astype(np.float64)
+    hi = O.f64_to_bf16_bits(s)
+    lo = O.f64_to_bf16_bits(s - O.bf16_bits_to_f64(hi))     # s - hi is exact
+    return hi.astype(np.uint32) | (lo.astype(np.uint32) << np.uint32(16))
+
+
+def check_weight_scales(layer, sw_ref: np.ndarray) -> None:
+    """ws bit-exact against the oracle's [N][G] scales, and wsp their pieces."""
+    assert (layer.ws.cpu().numpy() == sw_ref.T).all(), "weight scales"
+    assert (layer.wsp.cpu().numpy().view(np.uint32) == scale_pieces(sw_ref.T)).all(), "weight-scale pieces"
+
+
 def f32_dev(a: np.ndarray) -> torch.Tensor:
     return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to("cuda:0")
 

@@ -40,7 +40,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == set(Q.SIGNATURES), "binding and header disagree"
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.qwam_abi_version() == 11
+    assert lib.qwam_abi_version() == 12
     assert lib.qwam_status_string(3) == b"QWAM_ERR_MISALIGNED"
 
 
@@ -60,7 +60,7 @@ def test_probe_argument_checks(lib):
 def _layer(K=256, N=256, r=16, group=64, hadamard=0, **ptrs):
     c = Q.QwamLayerC()
     c.K, c.N, c.r, c.group, c.hadamard = K, N, r, group, hadamard
-    for f in ("wq", "ws", "inv_smooth", "L1t", "L2t", "L1"):
+    for f in ("wq", "ws", "wsp", "inv_smooth", "L1t", "L2t", "L1"):
         setattr(c, f, ptrs.get(f, FAKE))
     c.bias = ptrs.get("bias", None)
     return c
@@ -80,13 +80,13 @@ def _lin(lib, layer, M=64, xq=FAKE, xs=FAKE, t=FAKE, y=FAKE):
     (256, 0, 64, INVALID), (-64, 256, 64, INVALID), (131072, 256, 64, UNSUPPORTED),
     (256, 1 << 21, 64, UNSUPPORTED)])
 def test_pack_rejects_bad_shapes(lib, K, N, group, status):
-    assert lib.qwam_pack_weights(K, N, group, FAKE, FAKE, FAKE, FAKE, FAKE, None) == status
+    assert lib.qwam_pack_weights(K, N, group, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == status
     assert lib.qwam_last_error().startswith(b"qwam_pack_weights")
 
 
 def test_pack_rejects_null_and_misaligned(lib):
-    args = [FAKE] * 5
-    for i in range(5):
+    args = [FAKE] * 6
+    for i in range(6):
         a = list(args); a[i] = None
         assert lib.qwam_pack_weights(256, 256, 64, *a, None) == INVALID
         a = list(args); a[i] = FAKE + 4
@@ -106,7 +106,7 @@ def test_layer_calls_reject_bad_arguments(lib):
     for f in ("inv_smooth", "L1t"):
         assert _act(lib, _layer(**{f: None})) == INVALID
         assert _act(lib, _layer(**{f: FAKE + 2})) == MISALIGNED
-    for f in ("wq", "ws", "L2t"):
+    for f in ("wq", "ws", "wsp", "L2t"):
         assert _lin(lib, _layer(**{f: None})) == INVALID
         assert _lin(lib, _layer(**{f: FAKE + 8})) == MISALIGNED
     assert _lin(lib, _layer(bias=FAKE + 2)) == MISALIGNED
@@ -165,7 +165,7 @@ def test_aog_accumulate_rejects_bad_arguments(lib):
 
 @pytest.mark.skipif(torch.cuda.device_count() > 0, reason="a GPU is visible: the no-device path cannot be forced")
 def test_no_device_is_reported_before_any_launch(lib):
-    assert lib.qwam_pack_weights(256, 256, 64, FAKE, FAKE, FAKE, FAKE, FAKE, None) == NO_DEVICE
+    assert lib.qwam_pack_weights(256, 256, 64, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == NO_DEVICE
     assert _act(lib, _layer()) == NO_DEVICE
     assert _act(lib, _layer(), deflated=True) == NO_DEVICE
     assert _lin(lib, _layer()) == NO_DEVICE

@@ -17,7 +17,7 @@ from oracle import qwam_oracle as O
 from paper_2609_33269_amd import inputs as I
 from paper_2609_33269_amd import qwam as Q
 
-from parity_helpers import (bits, check_sampled_rows, check_t, check_y, gpu_layer, log, oracle_factors, rel_fro,
+from parity_helpers import (bits, check_weight_scales, check_sampled_rows, check_t, check_y, gpu_layer, log, oracle_factors, rel_fro,
                             run_gpu, sample_rows, y_tolerance)
 
 pytestmark = pytest.mark.gpu
@@ -40,7 +40,7 @@ def _g32_parity(draws, factors, bias_bits=None, deflate=False):
     assert layer.group == 32 and layer.ws.shape == (K // 32, N)
     x, xq, xs, t, y = run_gpu(layer, draws.x, deflate=deflate)
     assert (layer.wq.cpu().numpy() == ref["wq"]).all(), "packed weight bytes"
-    assert (layer.ws.cpu().numpy() == ref["sw"].T).all(), "weight scales"
+    check_weight_scales(layer, ref["sw"])
     assert (xq.cpu().numpy() == ref["xq"]).all(), "packed activation bytes"
     assert (xs.cpu().numpy() == ref["sx"].T).all(), "activation scales"
     if deflate:
@@ -95,7 +95,8 @@ def test_group32_full_size_sampled():
     wq, sw, inv_lam, _ = O.pack_weights(f["R"], f["lam"], 32)
     layer = gpu_layer(f)
     x, xq, xs, t, y = run_gpu(layer, draws.x, deflate=True)
-    assert (layer.wq.cpu().numpy() == wq).all() and (layer.ws.cpu().numpy() == sw.T).all()
+    assert (layer.wq.cpu().numpy() == wq).all()
+    check_weight_scales(layer, sw)
     xq_ref, sx_ref, t_ref, _, _ = O.quantize_activations_deflated(draws.x, inv_lam, f["L1"], f["hadamard"], 32)
     assert (bits(t) == t_ref).all(), "t"
     assert (xq.cpu().numpy() == xq_ref).all(), "packed activation bytes"

@@ -14,7 +14,7 @@ from oracle import qwam_oracle as O
 from paper_2609_33269_amd import inputs as I
 from paper_2609_33269_amd import qwam as Q
 
-from parity_helpers import (bf16_dev, bits, check_sampled_rows, check_t, check_y, check_y_elements,
+from parity_helpers import (bf16_dev, bits, check_weight_scales, check_sampled_rows, check_t, check_y, check_y_elements,
                             check_y_per_token, gpu_layer, log, oracle_factors, run_gpu, sample_rows, y_abs_terms)
 
 pytestmark = pytest.mark.gpu
@@ -36,7 +36,7 @@ def _full_parity(draws, factors, bias_bits=None, check_partials=True):
     layer = gpu_layer(factors, bias_bits)
     x, xq, xs, t, y = run_gpu(layer, draws.x)
     assert (layer.wq.cpu().numpy() == ref["wq"]).all(), "packed weight bytes"
-    assert (layer.ws.cpu().numpy() == ref["sw"].T).all(), "weight scales"
+    check_weight_scales(layer, ref["sw"])
     assert (layer.inv_smooth.cpu().numpy() == ref["inv_lam"]).all(), "1/lambda"
     assert (xq.cpu().numpy() == ref["xq"]).all(), "packed activation bytes"
     assert (xs.cpu().numpy() == ref["sx"].T).all(), "activation scales"
@@ -134,7 +134,7 @@ def _large_parity(draws, extra_rows=64):
     x, xq, xs, t, y = run_gpu(layer, draws.x)
     wq = layer.wq.cpu().numpy()
     assert (O.unpack_codes(wq) == qw).all(), "weight codes"
-    assert (layer.ws.cpu().numpy() == sw.T).all(), "weight scales"
+    check_weight_scales(layer, sw)
     assert (layer.inv_smooth.cpu().numpy() == inv_lam).all()
     xq_ref, sx_ref, t_ref, qx, xt = O.quantize_activations(draws.x, inv_lam, f["L1"])
     assert (xq.cpu().numpy() == xq_ref).all(), "packed activation bytes"
