@@ -346,7 +346,7 @@ def small_m_report(args):
         nrot = int(min(1024, max(2, (768 << 20) // wbytes)))        # > the 256 MB Infinity Cache
         layers = [L0] + [qwam.PackedLayer(K=Ka, N=Ns, r=ra, wq=L0.wq.clone(), ws=L0.ws.clone(), wsp=L0.wsp.clone(),
                                           inv_smooth=L0.inv_smooth.clone(), L1t=L0.L1t.clone(),
-                                          L2t=L0.L2t.clone(), L1=L0.L1.clone()) for _ in range(nrot - 1)]
+                                          L2t=L0.L2t.clone(), L1=L0.L1.clone(), L1f=L0.L1f.clone()) for _ in range(nrot - 1)]
         xq = torch.empty((Ms, Ka // 2), dtype=torch.uint8, device=dev)
         xs = torch.empty((Ga, Ms), dtype=torch.float32, device=dev)
         t = torch.empty((Ms, ra), dtype=torch.bfloat16, device=dev)
@@ -368,7 +368,7 @@ def small_m_report(args):
         del fp, w0
         players = [Lp] + [qwam.PackedLayer(K=Ka, N=Ns, r=ra, wq=Lp.wq.clone(), ws=Lp.ws.clone(), wsp=Lp.wsp.clone(),
                                            inv_smooth=Lp.inv_smooth.clone(), L1t=Lp.L1t.clone(),
-                                           L2t=Lp.L2t.clone(), L1=Lp.L1.clone(), hadamard=Lp.hadamard,
+                                           L2t=Lp.L2t.clone(), L1=Lp.L1.clone(), L1f=Lp.L1f.clone(), hadamard=Lp.hadamard,
                                            group=32) for _ in range(nrot - 1)]
         xs32 = torch.empty((Ka // 32, Ms), dtype=torch.float32, device=dev)
 
@@ -720,7 +720,7 @@ def main():
         L = layer0 if i == 0 else qwam.PackedLayer(
             K=K, N=N, r=R_RANK, wq=layer0.wq.clone(), ws=layer0.ws.clone(), wsp=layer0.wsp.clone(),
             inv_smooth=layer0.inv_smooth.clone(), L1t=layer0.L1t.clone(), L2t=layer0.L2t.clone(),
-            L1=layer0.L1.clone(), hadamard=layer0.hadamard, group=layer0.group)
+            L1=layer0.L1.clone(), L1f=layer0.L1f.clone(), hadamard=layer0.hadamard, group=layer0.group)
         layers.append(L)
         xins.append(x0 if i == 0 else x0.clone())
         outs.append((torch.empty((M, K // 2), dtype=torch.uint8, device=dev),

@@ -65,6 +65,7 @@
  *   xs   float   [G][M]      activation scales, group-major
  *   L1t  bf16    [r][K]      L1 transposed: row j is the j-th protected direction
  *   L1   bf16    [K][r]      L1 itself (row k: channel k of every direction), for the deflation
+ *   L1f  bf16    [K*r]       L1 in fragment order (qwam_layer), for the down-projection t
  *   L2t  bf16    [N][r]      L2 transposed: row n holds (V^T W~)[:, n]
  *   t    bf16    [M][r]      t = bf16(sum_k bf16(x~_k) L1[k, j]), float32 accumulation
  *   bias bf16    [N]         optional
@@ -106,7 +107,7 @@
 extern "C" {
 #endif
 
-#define QWAM_ABI_VERSION 12
+#define QWAM_ABI_VERSION 13
 #define QWAM_GROUP 64
 
 typedef enum {
@@ -139,6 +140,11 @@ typedef struct qwam_layer {
                                 /* lo = bf16(ws - hi), both rounded to nearest even; */
                                 /* written by qwam_pack_weights, read by             */
                                 /* qwam_asp_linear                                   */
+    const uint16_t *L1f;        /* L1 again, bf16, in the activation kernels'        */
+                                /* fragment order [K/64][r/16][2][64][8]: entry      */
+                                /* (g, b, h, l, e) = L1[64g + 16(l/16) + 8h + e]      */
+                                /*                     [16b + l%16];                 */
+                                /* read by the activation calls                      */
 } qwam_layer;
 
 /*
@@ -169,7 +175,8 @@ qwam_status qwam_pack_weights(int32_t K, int32_t N, int32_t group,
  * down-projection t = V^T x~ of Eq. 9 (bf16 inputs, float32 accumulation,
  * bf16 result), in one pass over x.  With L->hadamard != 0, x~ is also
  * rotated (Eq. 3) before it is quantized and projected.
- *   L   in   layer (reads K, r, group, hadamard, inv_smooth, L1t)
+ *   L   in   layer (reads K, r, group, hadamard, inv_smooth, L1t, L1f;
+ *            L1t and L1f must both be set)
  *   x   in   bf16 [M][K]
  *   xq  out  uint8 [M][K/2]
  *   xs  out  float [K/group][M]

@@ -88,17 +88,19 @@ struct DeflFetch {
   uint32_t l1[RANK / 2];        // L1[a_ch][j], two bf16 per word (j even in the low half)
 };
 
-// L1t fragments of the lane's 16 channels ch0 .. ch0+15 (ch0 = first channel
-// of its group slice) for the RB blocks of 16 columns of t: row rb*16 + l%16.
+// L1 fragments of the lane's 16 channels of 64-channel span g for the RB
+// blocks of 16 columns of t: L1[64 g + 16 (l/16) + 8 h + e][16 rb + l%16],
+// e = 0..7, h = 0, 1.  L1f holds them in exactly this order
+// ([K/64][RB][2][64 lanes][8]), so each of the wave's 2 RB loads reads one
+// contiguous kilobyte.
 template <int RB>
-__device__ __forceinline__ void load_l1_fragments(const uint16_t* __restrict__ L1t, int K, int ch0, int row,
+__device__ __forceinline__ void load_l1_fragments(const uint16_t* __restrict__ L1f, int g, int lane,
                                                   v8s (&l1)[RB][2]) {
 #pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    const uint16_t* lp = L1t + static_cast<int64_t>(rb * 16 + row) * K + ch0;
-    l1[rb][0] = *reinterpret_cast<const v8s*>(lp);
-    l1[rb][1] = *reinterpret_cast<const v8s*>(lp + 8);
-  }
+  for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+      l1[rb][h] = *reinterpret_cast<const v8s*>(L1f + (static_cast<int64_t>((g * RB + rb) * 2 + h) * 64 + lane) * 8);
 }
 
 // t partial on the bf16 matrix cores: A = bf16(x~) of the lane's token and

@@ -123,6 +123,7 @@ qwam_status quantize_act_common(const char* fn, bool deflate, const qwam_layer* 
   if ((s = check_m(fn, M)) != QWAM_OK) return s;
   QWAM_REQUIRE_PTR(L->inv_smooth);
   QWAM_REQUIRE_PTR(L->L1t);
+  QWAM_REQUIRE_PTR(L->L1f);
   if (deflate) QWAM_REQUIRE_PTR(L->L1);
   QWAM_REQUIRE_PTR(x);
   QWAM_REQUIRE_PTR(xq);
@@ -132,12 +133,12 @@ qwam_status quantize_act_common(const char* fn, bool deflate, const qwam_layer* 
   const hipStream_t st = static_cast<hipStream_t>(stream);
   if (L->hadamard != 0)
     return launched(fn, qwam::launch_quantize_act_rotated(M, L->K, L->r, L->group, L->hadamard, deflate, x,
-                                                          L->inv_smooth, L->L1t, deflate ? L->L1 : nullptr, xq,
-                                                          xs, t, st));
+                                                          L->inv_smooth, L->L1t, L->L1f, deflate ? L->L1 : nullptr,
+                                                          xq, xs, t, st));
   if (deflate)
-    return launched(fn, qwam::launch_quantize_act_deflated(M, L->K, L->r, L->group, x, L->inv_smooth, L->L1t, L->L1,
+    return launched(fn, qwam::launch_quantize_act_deflated(M, L->K, L->r, L->group, x, L->inv_smooth, L->L1f, L->L1,
                                                            xq, xs, t, st));
-  return launched(fn, qwam::launch_quantize_act(M, L->K, L->r, L->group, x, L->inv_smooth, L->L1t, xq, xs, t, st));
+  return launched(fn, qwam::launch_quantize_act(M, L->K, L->r, L->group, x, L->inv_smooth, L->L1f, xq, xs, t, st));
 }
 
 }  // namespace

@@ -8,21 +8,24 @@ namespace qwam {
 hipError_t launch_pack_weights(int K, int N, int group, const float* R, const float* smooth, uint8_t* wq,
                                float* ws, uint32_t* wsp, float* inv_smooth, hipStream_t stream);
 
+// L1f: the fragment-ordered copy of L1 (qwam_layer) that the activation
+// kernels' down-projection reads
 hipError_t launch_quantize_act(int M, int K, int r, int group, const uint16_t* x, const float* inv_smooth,
-                               const uint16_t* L1t, uint8_t* xq, float* xs, uint16_t* t,
+                               const uint16_t* L1f, uint8_t* xq, float* xs, uint16_t* t,
                                hipStream_t stream);
 
 // the 4-bit path quantizes the deflated activation x~ - L1 t (Eq. 8 / Eq. 9);
 // L1 is [K][r] bf16 (the deflation's rows), L1t the same factor as [r][K]
 hipError_t launch_quantize_act_deflated(int M, int K, int r, int group, const uint16_t* x,
-                                        const float* inv_smooth, const uint16_t* L1t, const uint16_t* L1,
+                                        const float* inv_smooth, const uint16_t* L1f, const uint16_t* L1,
                                         uint8_t* xq, float* xs, uint16_t* t, hipStream_t stream);
 
 // the same two activation kernels with the block Hadamard rotation of Eq. 3
 // (block B, a power of two with 16 <= B <= 1024 dividing K)
 hipError_t launch_quantize_act_rotated(int M, int K, int r, int group, int B, bool deflate, const uint16_t* x,
-                                       const float* inv_smooth, const uint16_t* L1t, const uint16_t* L1,
-                                       uint8_t* xq, float* xs, uint16_t* t, hipStream_t stream);
+                                       const float* inv_smooth, const uint16_t* L1t, const uint16_t* L1f,
+                                       const uint16_t* L1, uint8_t* xq, float* xs, uint16_t* t,
+                                       hipStream_t stream);
 
 hipError_t launch_asp_gemm(int M, int N, int K, int r, int group, const uint8_t* xq, const float* xs,
                            const uint16_t* t, const uint8_t* wq, const float* ws, const uint32_t* wsp,

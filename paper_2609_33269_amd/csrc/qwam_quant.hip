@@ -77,7 +77,7 @@ __global__ __launch_bounds__(256) void inverse_smoothing_kernel(const float* __r
 // contiguous ranges, in the lane layout of qwam_act.h (lane l: token l % 16,
 // channels 16*(l/16) .. +15 of the current group), so the smoothed values feed
 // the down-projection on the bf16 matrix cores straight from registers.  Each
-// wave prefetches the next group (x, L1t) while it quantizes the current one;
+// wave prefetches the next group (x, L1 fragments) while it quantizes the current one;
 // x is read with buffer loads and the codes / scales are written with buffer
 // stores, so rows past M need no branches.  The per-wave partial t tiles are
 // summed in LDS in wave order (deterministic) and rounded to bf16 once.
@@ -85,7 +85,7 @@ __global__ __launch_bounds__(256) void inverse_smoothing_kernel(const float* __r
 template <int RANK, bool INV_LDS>
 __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_kernel(
     const uint16_t* __restrict__ x, const float* __restrict__ inv_smooth,
-    const uint16_t* __restrict__ L1t, uint8_t* __restrict__ xq, float* __restrict__ xs,
+    const uint16_t* __restrict__ L1f, uint8_t* __restrict__ xq, float* __restrict__ xs,
     uint16_t* __restrict__ t, int M, int K, int groups_per_wave, int g32) {
   constexpr int RB = RANK / 16;
   // dynamic LDS: [nwaves][16][RANK] partial t, then (INV_LDS) [nwaves][groups_per_wave * 64] 1/lambda
@@ -121,7 +121,7 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_kernel(
     const uint32_t go = static_cast<uint32_t>(g) * kGroup * 2u;
     f.xa = buf_load16(x_rsrc, x_off + go);
     f.xb = buf_load16(x_rsrc, x_off + go + 16u);
-    load_l1_fragments<RB>(L1t, K, g * kGroup + chunk * 16, row, f.l1);
+    load_l1_fragments<RB>(L1f, g, lane, f.l1);
   };
 
   v4f acc[RB];
@@ -177,7 +177,7 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_kernel(
 template <int RANK, bool INV_LDS>
 __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_deflated_kernel(
     const uint16_t* __restrict__ x, const float* __restrict__ inv_smooth,
-    const uint16_t* __restrict__ L1t, const uint16_t* __restrict__ L1, uint8_t* __restrict__ xq, float* __restrict__ xs,
+    const uint16_t* __restrict__ L1f, const uint16_t* __restrict__ L1, uint8_t* __restrict__ xq, float* __restrict__ xs,
     uint16_t* __restrict__ t, int M, int K, int groups_per_wave, int g32) {
   constexpr int RB = RANK / 16;
   // dynamic LDS: [nwaves][16][RANK] double partial t | [16][RANK] float -t |
@@ -217,7 +217,7 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_deflated_
     const uint32_t go = static_cast<uint32_t>(g) * kGroup * 2u;
     f.xa = buf_load16(x_rsrc, x_off + go);
     f.xb = buf_load16(x_rsrc, x_off + go + 16u);
-    load_l1_fragments<RB>(L1t, K, g * kGroup + chunk * 16, row, f.l1);
+    load_l1_fragments<RB>(L1f, g, lane, f.l1);
   };
   v4d acc[RB];
 #pragma unroll
@@ -287,7 +287,7 @@ hipError_t launch_pack_weights(int K, int N, int group, const float* R, const fl
 }
 
 hipError_t launch_quantize_act(int M, int K, int r, int group, const uint16_t* x, const float* inv_smooth,
-                               const uint16_t* L1t, uint8_t* xq, float* xs, uint16_t* t,
+                               const uint16_t* L1f, uint8_t* xq, float* xs, uint16_t* t,
                                hipStream_t stream) {
   const int g32 = group == 32 ? 1 : 0;
   const int G = K / kGroup;
@@ -303,10 +303,10 @@ hipError_t launch_quantize_act(int M, int K, int r, int group, const uint16_t* x
       if (e != hipSuccess) return e;
     }
     if (inv_lds)
-      hipLaunchKernelGGL(kernel_lds, dim3((M + 15) / 16), dim3(64 * nwaves), lds, stream, x, inv_smooth, L1t,
+      hipLaunchKernelGGL(kernel_lds, dim3((M + 15) / 16), dim3(64 * nwaves), lds, stream, x, inv_smooth, L1f,
                          xq, xs, t, M, K, gpw, g32);
     else
-      hipLaunchKernelGGL(kernel_global, dim3((M + 15) / 16), dim3(64 * nwaves), lds, stream, x, inv_smooth, L1t,
+      hipLaunchKernelGGL(kernel_global, dim3((M + 15) / 16), dim3(64 * nwaves), lds, stream, x, inv_smooth, L1f,
                          xq, xs, t, M, K, gpw, g32);
     return hipGetLastError();
   };
@@ -320,7 +320,7 @@ hipError_t launch_quantize_act(int M, int K, int r, int group, const uint16_t* x
 }
 
 hipError_t launch_quantize_act_deflated(int M, int K, int r, int group, const uint16_t* x,
-                                        const float* inv_smooth, const uint16_t* L1t, const uint16_t* L1,
+                                        const float* inv_smooth, const uint16_t* L1f, const uint16_t* L1,
                                         uint8_t* xq, float* xs, uint16_t* t, hipStream_t stream) {
   const int g32 = group == 32 ? 1 : 0;
   const int G = K / kGroup;
@@ -336,10 +336,10 @@ hipError_t launch_quantize_act_deflated(int M, int K, int r, int group, const ui
       if (e != hipSuccess) return e;
     }
     if (inv_lds)
-      hipLaunchKernelGGL(kernel_lds, dim3((M + 15) / 16), dim3(64 * nwaves), lds, stream, x, inv_smooth, L1t,
+      hipLaunchKernelGGL(kernel_lds, dim3((M + 15) / 16), dim3(64 * nwaves), lds, stream, x, inv_smooth, L1f,
                          L1, xq, xs, t, M, K, gpw, g32);
     else
-      hipLaunchKernelGGL(kernel_global, dim3((M + 15) / 16), dim3(64 * nwaves), lds, stream, x, inv_smooth, L1t,
+      hipLaunchKernelGGL(kernel_global, dim3((M + 15) / 16), dim3(64 * nwaves), lds, stream, x, inv_smooth, L1f,
                          L1, xq, xs, t, M, K, gpw, g32);
     return hipGetLastError();
   };

@@ -98,7 +98,7 @@ __device__ __forceinline__ void lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)\
 template <int RANK, bool DEFLATE>
 __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_rotated_kernel(
     const uint16_t* __restrict__ x, const float* __restrict__ inv_smooth,
-    const uint16_t* __restrict__ L1t, const uint16_t* __restrict__ L1, uint8_t* __restrict__ xq, float* __restrict__ xs,
+    const uint16_t* __restrict__ L1f, const uint16_t* __restrict__ L1, uint8_t* __restrict__ xq, float* __restrict__ xs,
     uint16_t* __restrict__ t, int M, int K, int logB, int T, float hscale, int g32, int red_off) {
   constexpr int RB = RANK / 16;
   constexpr int kMaxPerWave = per_wave<RANK>();
@@ -195,7 +195,7 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_rotated_k
 #pragma unroll
     for (int k = 0; k < kMaxPerWave; ++k) {
       const int gl = wave + k * nwaves;
-      if (gl < npass) load_l1_fragments<RB>(L1t, K, (tb * npass + gl) * kGroup + chunk * 16, row, l1[k]);
+      if (gl < npass) load_l1_fragments<RB>(L1f, tb * npass + gl, lane, l1[k]);
     }
     lds_sync();
 #pragma unroll
@@ -444,8 +444,9 @@ static int rotate_tile_width(int K, int B) {
 }
 
 hipError_t launch_quantize_act_rotated(int M, int K, int r, int group, int B, bool deflate, const uint16_t* x,
-                                       const float* inv_smooth, const uint16_t* L1t, const uint16_t* L1,
-                                       uint8_t* xq, float* xs, uint16_t* t, hipStream_t stream) {
+                                       const float* inv_smooth, const uint16_t* L1t, const uint16_t* L1f,
+                                       const uint16_t* L1, uint8_t* xq, float* xs, uint16_t* t,
+                                       hipStream_t stream) {
   int logB = 0;
   while ((1 << logB) < B) ++logB;
   if ((1 << logB) != B || B < 16 || B > 1024 || K % B != 0) return hipErrorInvalidValue;
@@ -488,7 +489,7 @@ hipError_t launch_quantize_act_rotated(int M, int K, int r, int group, int B, bo
                                                hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
       if (e != hipSuccess) return e;
     }
-    hipLaunchKernelGGL(kernel, dim3((M + 15) / 16), dim3(64 * nwaves), lds, stream, x, inv_smooth, L1t, L1, xq, xs, t,
+    hipLaunchKernelGGL(kernel, dim3((M + 15) / 16), dim3(64 * nwaves), lds, stream, x, inv_smooth, L1f, L1, xq, xs, t,
                        M, K, logB, T, hscale, group == 32 ? 1 : 0, red_off);
     return hipGetLastError();
   };

@@ -35,7 +35,7 @@ class QwamLayerC(ctypes.Structure):
                 ("group", ctypes.c_int32), ("hadamard", ctypes.c_int32), ("wq", ctypes.c_void_p), ("ws", ctypes.c_void_p),
                 ("inv_smooth", ctypes.c_void_p), ("L1t", ctypes.c_void_p),
                 ("L2t", ctypes.c_void_p), ("bias", ctypes.c_void_p), ("L1", ctypes.c_void_p),
-                ("wsp", ctypes.c_void_p)]
+                ("wsp", ctypes.c_void_p), ("L1f", ctypes.c_void_p)]
 
 
 _LP = ctypes.POINTER(QwamLayerC)
@@ -129,6 +129,7 @@ class PackedLayer:
     group: int = GROUP                    # channels per scale: 64, or 32 (App. B.1)
     L1: Optional[torch.Tensor] = None     # bf16 [K][r] (the deflated activation path reads it)
     wsp: Optional[torch.Tensor] = None    # int32 [K/group][N]: ws as bf16 pieces hi | lo << 16 (asp_linear reads it)
+    L1f: Optional[torch.Tensor] = None    # bf16 [K/64][r/16][2][64][8]: L1 in fragment order (the activation calls read it)
 
     def c_struct(self) -> QwamLayerC:
         G = self.K // self.group
@@ -142,6 +143,8 @@ class PackedLayer:
         c.bias = None if self.bias is None else _req(self.bias, "bias", torch.bfloat16, (self.N,))
         c.L1 = None if self.L1 is None else _req(self.L1, "L1", torch.bfloat16, (self.K, self.r))
         c.wsp = None if self.wsp is None else _req(self.wsp, "wsp", torch.int32, (G, self.N))
+        c.L1f = None if self.L1f is None else _req(self.L1f, "L1f", torch.bfloat16,
+                                                   (self.K // 64, self.r // 16, 2, 64, 8))
         return c
 
 
@@ -162,6 +165,15 @@ def pack_weights(R: torch.Tensor, smooth: torch.Tensor, stream=None, group: int 
     return wq, ws, wsp, inv
 
 
+def l1_fragment_order(L1: torch.Tensor) -> torch.Tensor:
+    """L1 bf16 [K][r] -> the activation kernels' fragment order
+    [K/64][r/16][2][64][8]: entry (g, b, h, l, e) = L1[64 g + 16 (l // 16) + 8 h + e][16 b + l % 16]
+    (a layout change only, like the transposes of L1 and L2)."""
+    K, r = L1.shape
+    v = L1.reshape(K // 64, 4, 2, 8, r // 16, 16)           # [g][c][h][e][b][j], l = 16 c + j
+    return v.permute(0, 4, 2, 1, 5, 3).contiguous().reshape(K // 64, r // 16, 2, 64, 8)
+
+
 def make_layer(R: torch.Tensor, smooth: torch.Tensor, L1: torch.Tensor, L2: torch.Tensor,
                bias: Optional[torch.Tensor] = None, stream=None, hadamard: int = 0,
                group: int = GROUP) -> PackedLayer:
@@ -174,6 +186,7 @@ def make_layer(R: torch.Tensor, smooth: torch.Tensor, L1: torch.Tensor, L2: torc
     wq, ws, wsp, inv = pack_weights(R, smooth, stream, group)
     return PackedLayer(K=K, N=N, r=r, wq=wq, ws=ws, wsp=wsp, inv_smooth=inv,
                        L1t=L1.t().contiguous(), L2t=L2.t().contiguous(), L1=L1.contiguous(),
+                       L1f=l1_fragment_order(L1),
                        bias=None if bias is None else bias.contiguous(), hadamard=hadamard, group=group)
 
 

@@ -40,7 +40,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == set(Q.SIGNATURES), "binding and header disagree"
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.qwam_abi_version() == 12
+    assert lib.qwam_abi_version() == 13
     assert lib.qwam_status_string(3) == b"QWAM_ERR_MISALIGNED"
 
 
@@ -60,7 +60,7 @@ def test_probe_argument_checks(lib):
 def _layer(K=256, N=256, r=16, group=64, hadamard=0, **ptrs):
     c = Q.QwamLayerC()
     c.K, c.N, c.r, c.group, c.hadamard = K, N, r, group, hadamard
-    for f in ("wq", "ws", "wsp", "inv_smooth", "L1t", "L2t", "L1"):
+    for f in ("wq", "ws", "wsp", "inv_smooth", "L1t", "L2t", "L1", "L1f"):
         setattr(c, f, ptrs.get(f, FAKE))
     c.bias = ptrs.get("bias", None)
     return c
@@ -103,7 +103,7 @@ def test_layer_calls_reject_bad_arguments(lib):
         assert _lin(lib, _layer(), M=M) == st
     assert _act(lib, _layer(group=128)) == INVALID
     assert _lin(lib, _layer(K=96)) == INVALID
-    for f in ("inv_smooth", "L1t"):
+    for f in ("inv_smooth", "L1t", "L1f"):
         assert _act(lib, _layer(**{f: None})) == INVALID
         assert _act(lib, _layer(**{f: FAKE + 2})) == MISALIGNED
     for f in ("wq", "ws", "wsp", "L2t"):
@@ -206,3 +206,18 @@ def test_aog_protected_basis_argument_checks(lib):
     assert call(A=FAKE + 4) == MISALIGNED and call(lam=FAKE + 8) == MISALIGNED
     assert call(wsb=need - 1) == INVALID
     assert b"workspace" in lib.qwam_last_error()
+
+
+@pytest.mark.parametrize("K,r", [(64, 16), (192, 32), (128, 48), (64, 64)])
+def test_l1_fragment_order_matches_its_definition(K, r):
+    """The binding's L1f layout against the header's definition, entry by entry:
+    (g, b, h, l, e) = L1[64 g + 16 (l // 16) + 8 h + e][16 b + l % 16]."""
+    L1 = torch.arange(K * r, dtype=torch.float32).reshape(K, r)
+    F = Q.l1_fragment_order(L1)
+    assert F.shape == (K // 64, r // 16, 2, 64, 8)
+    for g in range(K // 64):
+        for b in range(r // 16):
+            for h in range(2):
+                for l in range(64):
+                    for e in range(8):
+                        assert F[g, b, h, l, e] == L1[64 * g + 16 * (l // 16) + 8 * h + e, 16 * b + l % 16]
