@@ -375,58 +375,62 @@ __global__ __launch_bounds__(NT, WG_PER_CU) void asp_gemm_kernel(
   // (v_mfma_f32_32x32x16_bf16 with L2t as the A operand and t as the B
   // operand, the roles of the integer blocks: lane l holds row / column l%32
   // and the 8 rank slots 8*(l/32) .. +7 of a 16-wide rank step, the same slots
-  // for both).  Result register v of block (i, j) is output column
+  // for both).  The tile's rows of t and L2t and its bias come into the
+  // second stage's buffers (idle until stage 1 is copied) by the same LDS DMA
+  // as the codes, alongside stage 0: t rows [128][RANK] over the A tile, L2t
+  // rows over the B tile, the 128 bias values over the activation scales.
+  // Result register v of block (i, j) is output column
   // n0 + 64 wn + 32 i + 8 (v/4) + 4 (l/32) + v%4, so each lane takes the bias
-  // of four consecutive columns per v/4.  These loads overlap the copy of the
-  // first stage.
+  // of four consecutive columns per v/4.
   if (!PARTIALS) {
+    constexpr int RB2 = RANK * 2;                 // bytes of one row of t / L2t
+    const buf_rsrc t_rsrc = make_rsrc(t + static_cast<int64_t>(m0) * RANK,
+                                      static_cast<uint32_t>(min(BM, M - m0)) * RB2);
+    const buf_rsrc l_rsrc = make_rsrc(L2t + static_cast<int64_t>(n0) * RANK,
+                                      static_cast<uint32_t>(min(BN, N - n0)) * RB2);
+    // 128 rows of RB2 bytes = RANK / 16 kilobyte pieces per wave and array
+#pragma unroll
+    for (int c = 0; c < RANK / 16; ++c) {
+      const int piece = wave * (RANK / 16) + c;   // kilobyte of the array
+      const uint32_t src = static_cast<uint32_t>(piece * 1024 + lane * 16);
+      buf_load16_lds(t_rsrc, src, st1.a + piece * 1024);
+      buf_load16_lds(l_rsrc, src, st1.b + piece * 1024);
+    }
+    if (wave == 0) {
+      const buf_rsrc b_rsrc = make_rsrc(bias != nullptr ? bias + n0 : nullptr,
+                                        bias != nullptr ? static_cast<uint32_t>(min(BN, N - n0)) * 2u : 0u);
+      buf_load4_lds(b_rsrc, static_cast<uint32_t>(lane * 4), &st1.sx[0][0]);
+    }
+    wait_vmcnt<0>();
+    lds_wait_barrier();
     constexpr int KSTEPS = RANK / 16;
-    const int kk = fhalf * 8;
-    v8s tf[2][KSTEPS], lf[2][KSTEPS];
-    uint2 bv[2][4];
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int m = m0 + wm * 64 + j * 32 + frow;
-#pragma unroll
-      for (int s = 0; s < KSTEPS; ++s) {
-        v8s val = {0, 0, 0, 0, 0, 0, 0, 0};
-        if (m < M) val = *reinterpret_cast<const v8s*>(t + static_cast<int64_t>(m) * RANK + s * 16 + kk);
-        tf[j][s] = val;
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int n = n0 + wn * 64 + i * 32 + frow;
-#pragma unroll
-      for (int s = 0; s < KSTEPS; ++s) {
-        v8s val = {0, 0, 0, 0, 0, 0, 0, 0};
-        if (n < N) val = *reinterpret_cast<const v8s*>(L2t + static_cast<int64_t>(n) * RANK + s * 16 + kk);
-        lf[i][s] = val;
-      }
-#pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        // N is a multiple of 16: four consecutive columns are all in range or all out
-        const int nb = n0 + wn * 64 + i * 32 + 8 * q4 + rsub;
-        bv[i][q4] = (bias != nullptr && nb < N) ? *reinterpret_cast<const uint2*>(bias + nb) : make_uint2(0u, 0u);
-      }
-    }
+    const int kk = fhalf * 16;                    // byte offset of the lane's 8 rank slots
+    const uint16_t* bias_lds = reinterpret_cast<const uint16_t*>(&st1.sx[0][0]);
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         v16f c;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const uint2 w = bv[i][v >> 2];
-          const uint32_t word = (v & 2) ? w.y : w.x;
-          c[v] = __builtin_bit_cast(float, (v & 1) ? (word & 0xFFFF0000u) : (word << 16));
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const uint2 w = *reinterpret_cast<const uint2*>(bias_lds + wn * 64 + i * 32 + 8 * q4 + rsub);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const uint32_t word = (e & 2) ? w.y : w.x;
+            c[4 * q4 + e] = __builtin_bit_cast(float, (e & 1) ? (word & 0xFFFF0000u) : (word << 16));
+          }
         }
 #pragma unroll
-        for (int s = 0; s < KSTEPS; ++s)
-          c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, lf[i][s]),
-                                                      __builtin_bit_cast(v8bf, tf[j][s]), c, 0, 0, 0);
+        for (int s = 0; s < KSTEPS; ++s) {
+          const v8s lf = *reinterpret_cast<const v8s*>(st1.b + (wn * 64 + i * 32 + frow) * RB2 + s * 32 + kk);
+          const v8s tf = *reinterpret_cast<const v8s*>(st1.a + (wm * 64 + j * 32 + frow) * RB2 + s * 32 + kk);
+          c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, lf), __builtin_bit_cast(v8bf, tf), c,
+                                                      0, 0, 0);
+        }
         accf[i][j] = c;
       }
+    // every wave has read the branch operands before stage 1 is copied over them
+    lds_wait_barrier();
   }
 
   if constexpr (GS == 32 && PARTIALS) {
