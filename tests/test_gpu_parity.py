@@ -69,6 +69,7 @@ EDGE_SHAPES = [
     (17, 192, 144, 48, False),
     (129, 256, 272, 64, True),
     (200, 320, 400, 32, False),
+    (97, 192, 176, 48, True),        # r = 48 on the large-tile GEMM, ragged N, bias
     (130, 1024, 1040, 16, True),
     (257, 640, 256, 32, False),
     (33, 16448, 64, 32, False),      # K > 16384: 1/lambda read from global memory
