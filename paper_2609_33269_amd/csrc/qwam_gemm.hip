@@ -75,7 +75,6 @@ constexpr int BN = 128;
 constexpr int NWAVES = 4;
 constexpr int NT = 64 * NWAVES;
 constexpr int WG_PER_CU = 2;
-constexpr int LDY = 64 + 8;        // LDS row stride (bf16) of the output staging
 constexpr int BAND = 8;            // tile-rows per band of the tile order
 constexpr int KC = 4;              // groups per ring stage
 constexpr int ROWB = KC * 32;      // bytes of one packed row per stage (one cache line)
@@ -91,7 +90,8 @@ struct StageRef {
   float (*sx)[BM];
   uint32_t (*sw)[BN];   // the weight scales as bf16 pieces hi | lo << 16
 };
-static_assert(64 * LDY * 2 <= BM * ROWB && BM == BN, "a wave's 64 x 64 bf16 output block must fit in one tile buffer");
+static_assert(BM == BN && BM * 64 * 2 <= BM * ROWB,
+              "the tile's rows of t and L2t (up to rank 64) must fit in one tile buffer of a stage");
 
 typedef float v2f __attribute__((ext_vector_type(2)));
 typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
