@@ -94,12 +94,13 @@ def gemm_issue_ceiling(group: int = GROUP) -> float:
     Per wave and 64-channel span (a 64 x 64 block of y): 4 FP6 MFMAs of 32 cycles
     each per scale group (the useful work: 128 cycles at group 64), 2 bf16
     outer-product MFMAs of 64 cycles each per scale group, one FMA per output and
-    scale group (64 per lane) plus 12 scale-split instructions per scale group and
+    scale group (64 per lane) plus 4 instructions per scale group for the bf16
+    split of the token scale (the weight scale's pieces come from the pack) and
     32 unpack instructions on the VALU, 4 cycles each for a 64-wide wave.
     """
     ns = 64 // group
     mfma = ns * (4 * 32 + 2 * 64)
-    valu = 4 * (ns * (64 + 12) + 32)
+    valu = 4 * (ns * (64 + 4) + 32)
     return 128 / max(mfma, valu)
 
 
