@@ -789,24 +789,33 @@ def main():
     graph_ms = timed(replay_steps, args.steps)
     graph_med_ms = float(np.median([timed(replay_steps, rep_steps) for _ in range(10)]))
 
-    # per-kernel durations on the launch stream: `rep_steps` launches of one
-    # kernel back to back over the buffer sets, events only at the two ends
-    # (so the mean includes the gaps between consecutive launches); median of 5
-    def act_only(n):
-        for i in range(n):
-            j = i % nrot
-            act_fn(layers[j], xins[j], out=outs[j][:3])
+    # per-kernel durations: one HIP graph per kernel holding one launch on
+    # each buffer set, replayed until at least `rep_steps` launches ran back to
+    # back, events only at the two ends (so the mean includes the gaps between
+    # consecutive launches, but no host time: a launch through the Python
+    # binding costs more host time than the activation kernel takes); median
+    # of 5
+    def act_one(j):
+        act_fn(layers[j], xins[j], out=outs[j][:3])
 
-    def gemm_only(n):
-        for i in range(n):
-            j = i % nrot
-            xq, xs, t, y = outs[j]
-            qwam.asp_linear(layers[j], xq, xs, t, out=y)
+    def gemm_one(j):
+        xq, xs, t, y = outs[j]
+        qwam.asp_linear(layers[j], xq, xs, t, out=y)
 
-    k1_all = [timed(act_only, rep_steps) for _ in range(5)]
-    k2_all = [timed(gemm_only, rep_steps) for _ in range(5)]
+    act_graph = capture_graphs(lambda _: [act_one(j) for j in range(nrot)], 1)[0]
+    gemm_graph = capture_graphs(lambda _: [gemm_one(j) for j in range(nrot)], 1)[0]
+    reps = max(1, -(-rep_steps // nrot))
+
+    def replayed(g):
+        def run(_n):
+            for _ in range(reps):
+                g.replay()
+        return run
+
+    k1_all = [timed(replayed(act_graph), reps * nrot) for _ in range(5)]
+    k2_all = [timed(replayed(gemm_graph), reps * nrot) for _ in range(5)]
     k1_ms, k2_ms = float(np.median(k1_all)), float(np.median(k2_all))
-    del block, singles
+    del block, singles, act_graph, gemm_graph
     print(f"[bench] {args.steps} steps: {ms_step * 1e3:.1f} us/step (median of 10 x {rep_steps}: {med_ms * 1e3:.1f}; "
           f"graph replay {graph_ms * 1e3:.1f}, median {graph_med_ms * 1e3:.1f}); act kernel {k1_ms * 1e3:.1f} us, "
           f"gemm {k2_ms * 1e3:.1f} us", file=sys.stderr, flush=True)
@@ -870,8 +879,8 @@ def main():
                      "traffic": traffic, "algorithmic_bytes": gemm_bytes},
         "layer_frac_int8_peak": round(eff_tops / MFMA_PEAK, 4),
         "kernels_us": {act_name: round(k1_ms * 1e3, 2), "asp_gemm": round(k2_ms * 1e3, 2),
-                       "timing": f"per launch: {rep_steps} back-to-back launches of the kernel between two "
-                                 f"events on its stream, median of 5"},
+                       "timing": f"per launch: a HIP graph of {nrot} launches of the kernel (one per buffer set) "
+                                 f"replayed {reps} times back to back between two events, median of 5"},
         "timing": {"method": f"{args.steps} steps (both kernels) launched back to back on one stream, events "
                              f"only at the two ends",
                    "repeat_median_ms_per_step": round(med_ms, 5), "repeats": f"10 x {rep_steps} steps",

@@ -13,6 +13,13 @@ namespace qwam {
 typedef double v4d __attribute__((ext_vector_type(4)));
 typedef float v16f_t __attribute__((ext_vector_type(16)));
 
+typedef unsigned int v4u_act __attribute__((ext_vector_type(4)));
+
+// 16-byte buffer store (bytes outside the resource are dropped)
+__device__ __forceinline__ void buf_store16(uint4 v, buf_rsrc r, uint32_t off) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u_act, v), r, off, 0, 0);
+}
+
 template <int RANK>
 struct ActFetch {
   uint4 xa, xb;                 // 16 bf16 of x
@@ -53,10 +60,9 @@ __device__ __forceinline__ void smooth16_regs(const uint4& xa, const uint4& xb, 
 // Quantizes the lane's token over one 64-channel span (Eq. 2): with group 64
 // the four lanes l, l^16, l^32, l^48 (16 consecutive channels each) share one
 // scale; with group 32 (g32) the lanes l, l^16 share the scale of channels
-// 0-31 or 32-63 of the span.  Stores the lane's code block (8 bytes) at byte
-// q_off of q_rsrc and, if xs_dst is not null, the lane's group scale.
-__device__ __forceinline__ void quantize_pack_store(const float (&v)[16], buf_rsrc q_rsrc, uint32_t q_off,
-                                                    float* xs_dst, bool g32 = false) {
+// 0-31 or 32-63 of the span.  Returns the lane's code block (8 bytes) and its
+// group scale.
+__device__ __forceinline__ uint2 quantize_block(const float (&v)[16], bool g32, float& scale) {
   float amax = 0.0f;
 #pragma unroll
   for (int j = 0; j < 16; ++j) amax = __builtin_fmaxf(amax, __builtin_fabsf(v[j]));
@@ -70,7 +76,16 @@ __device__ __forceinline__ void quantize_pack_store(const float (&v)[16], buf_rs
   for (int j = 0; j < 16; ++j) x[j] = v[j] * inv;
   uint32_t d0, d1, d2;
   codes_fp6_16(x, d0, d1, d2);
-  buf_store8(fp6_code_block(d0, d1, d2), q_rsrc, q_off);
+  scale = s;
+  return fp6_code_block(d0, d1, d2);
+}
+
+// The same, storing the lane's code block (8 bytes) at byte q_off of q_rsrc
+// and, if xs_dst is not null, the lane's group scale.
+__device__ __forceinline__ void quantize_pack_store(const float (&v)[16], buf_rsrc q_rsrc, uint32_t q_off,
+                                                    float* xs_dst, bool g32 = false) {
+  float s;
+  buf_store8(quantize_block(v, g32, s), q_rsrc, q_off);
   if (xs_dst != nullptr) *xs_dst = s;
 }
 

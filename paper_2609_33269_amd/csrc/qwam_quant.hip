@@ -79,8 +79,14 @@ __global__ __launch_bounds__(256) void inverse_smoothing_kernel(const float* __r
 // the down-projection on the bf16 matrix cores straight from registers.  Each
 // wave prefetches the next group (x, L1 fragments) while it quantizes the current one;
 // x is read with buffer loads and the codes / scales are written with buffer
-// stores, so rows past M need no branches.  The per-wave partial t tiles are
-// summed in LDS in wave order (deterministic) and rounded to bf16 once.
+// stores, so rows past M need no branches.  From K = 4096 on, a wave's code
+// blocks of four consecutive groups (one 128-byte line of each of its 16 rows)
+// are gathered in a 2 KB LDS line buffer of its own and written out as whole
+// lines, 16 bytes per lane and 8 lines per instruction, instead of 32-byte
+// pieces of 16 lines per group (the wave ranges are then whole line chunks);
+// below, the 16 waves keep their ranges and store each group's blocks.  The
+// per-wave partial t tiles are summed in LDS in wave order (deterministic) and
+// rounded to bf16 once.
 // ---------------------------------------------------------------------------
 template <int RANK, bool INV_LDS>
 __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_kernel(
@@ -88,7 +94,8 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_kernel(
     const uint16_t* __restrict__ L1f, uint8_t* __restrict__ xq, float* __restrict__ xs,
     uint16_t* __restrict__ t, int M, int K, int groups_per_wave, int g32) {
   constexpr int RB = RANK / 16;
-  // dynamic LDS: [nwaves][16][RANK] partial t, then (INV_LDS) [nwaves][groups_per_wave * 64] 1/lambda
+  // dynamic LDS: [nwaves][16][RANK] partial t, then (INV_LDS) [nwaves][groups_per_wave * 64] 1/lambda,
+  // then [nwaves][16 rows][128 bytes] code lines
   extern __shared__ float red[];
 
   const int lane = threadIdx.x & 63;
@@ -128,15 +135,43 @@ __global__ __launch_bounds__(64 * act_waves<RANK>()) void quantize_act_kernel(
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) acc[rb] = v4f{0.f, 0.f, 0.f, 0.f};
 
+  uint8_t* line = reinterpret_cast<uint8_t*>(red + nwaves * 16 * RANK + (INV_LDS ? nwaves * groups_per_wave * kGroup : 0)) +
+                  wave * 2048;
+  // the launcher gives whole line chunks per wave from 64 groups on
+  const bool lines = groups_per_wave % 4 == 0;
+  // writes the staged blocks of groups max(g_begin, g & ~3) .. g (one line
+  // chunk): lane l takes row 8h + l/8 and the 16-byte piece l%8 of its line
+  auto flush = [&](int g) __attribute__((always_inline)) {
+    const int q0 = g & ~3;
+    const int p_lo = 2 * (max(g_begin, q0) - q0), p_hi = 2 * (g - q0 + 1);
+    const int piece = lane & 7;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int r = 8 * h + (lane >> 3);
+      if (piece >= p_lo && piece < p_hi) {
+        const uint4 d = *reinterpret_cast<const uint4*>(line + r * 128 + piece * 16);
+        buf_store16(d, q_rsrc, static_cast<uint32_t>(r * (K / 2) + q0 * (kGroup / 2) + piece * 16));
+      }
+    }
+  };
+
   auto work = [&](int g, const ActFetch<RANK>& f) __attribute__((always_inline)) {
     const float4* ip = INV_LDS ? reinterpret_cast<const float4*>(inv_w + (g - g_begin) * kGroup + chunk * 16)
                                : reinterpret_cast<const float4*>(inv_smooth + g * kGroup + chunk * 16);
     float v[16];
     smooth16(f.xa, f.xb, ip, v);
-    // every lane of a row holds the same scale; lanes of row r write it at r
-    quantize_pack_store(v, q_rsrc, q_off + static_cast<uint32_t>(g) * (kGroup / 2),
-                        xs_slot(xs, g, M, m0, row, rows, chunk, g32), g32);
+    float s;
+    const uint2 blk = quantize_block(v, g32, s);
+    // the block goes to the row's line at its group's 32-byte slot (or, when
+    // the wave's range is not made of line chunks, straight out); every lane
+    // of a row (of a 32-channel half with group 32) holds the same scale and
+    // writes it at the row's slot (letting one lane of each write it instead
+    // measured 2-3 us slower at K = 3072)
+    if (lines) *reinterpret_cast<uint2*>(line + row * 128 + (g & 3) * 32 + chunk * 8) = blk;
+    else buf_store8(blk, q_rsrc, q_off + static_cast<uint32_t>(g) * (kGroup / 2));
+    if (float* p = xs_slot(xs, g, M, m0, row, rows, chunk, g32)) *p = s;
     t_step_bf16<RB>(v, f.l1, acc);
+    if (lines && ((g & 3) == 3 || g == g_end - 1)) flush(g);
   };
 
   // software pipeline, two groups per trip so the fetch registers are named statically;
@@ -294,9 +329,15 @@ hipError_t launch_quantize_act(int M, int K, int r, int group, const uint16_t* x
   // 1/lambda is staged in LDS when the slice fits (K <= 16384); larger K reads it from global memory
   const bool inv_lds = K <= 16384;
   auto go = [&](auto kernel_lds, auto kernel_global, int max_waves) {
-    const int nwaves = G < max_waves ? G : max_waves;
-    const int gpw = (G + nwaves - 1) / nwaves;
-    const size_t lds = static_cast<size_t>(nwaves) * (16 * r + (inv_lds ? gpw * kGroup : 0)) * sizeof(float);
+    int nwaves = G < max_waves ? G : max_waves;
+    int gpw = (G + nwaves - 1) / nwaves;
+    if (G >= 64) {   // wave ranges of whole 4-group line chunks (below, the waves keep one group or more each)
+      gpw = (gpw + 3) & ~3;
+      nwaves = (G + gpw - 1) / gpw;
+    }
+    // the code-line buffers (2 KB per wave) only where the kernel uses them
+    const size_t lds = static_cast<size_t>(nwaves) * (16 * r + (inv_lds ? gpw * kGroup : 0)) * sizeof(float) +
+                       (gpw % 4 == 0 ? static_cast<size_t>(nwaves) * 2048 : 0);
     if (lds > 64 * 1024) {   // opt in to more than 64 KB of dynamic LDS
       const void* fn = inv_lds ? reinterpret_cast<const void*>(kernel_lds) : reinterpret_cast<const void*>(kernel_global);
       const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
