@@ -309,33 +309,46 @@ __global__ __launch_bounds__(256) void quantize_act_rotated_few_kernel(
   const int c0 = (tid / RANK) * CH;             // first channel of the range
 
   // requests: the lane's x and 1/lambda (rotation waves), the thread's L1t
-  // segment and (deflated) its L1 rows
+  // segment and (deflated) its L1 rows, all issued unconditionally as buffer
+  // loads (bytes past each array read as zero), so that the rotation waits
+  // for its own two requests only and not for the L1t and L1 ones behind them
   const buf_rsrc x_rsrc = make_rsrc(x + static_cast<int64_t>(m) * K, static_cast<uint32_t>(K) * 2u);
-  RotFetch rf{};
-  if (rot_wave) {
-    rf.xa = buf_load16(x_rsrc, static_cast<uint32_t>(e) * 2u);
-    rf.xb = buf_load16(x_rsrc, static_cast<uint32_t>(e) * 2u + 16u);
-    if (rot_lane) {
-      const float4* ip = reinterpret_cast<const float4*>(inv_smooth + e);
+  const buf_rsrc inv_rsrc = make_rsrc(inv_smooth, static_cast<uint32_t>(K) * 4u);
+  const buf_rsrc lt_rsrc = make_rsrc(L1t, static_cast<uint32_t>(RANK * K) * 2u);
+  RotFetch rf;
+  rf.xa = buf_load16(x_rsrc, static_cast<uint32_t>(e) * 2u);
+  rf.xb = buf_load16(x_rsrc, static_cast<uint32_t>(e) * 2u + 16u);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) rf.inv[q] = ip[q];
-    }
-  }
+  for (int q = 0; q < 4; ++q)
+    rf.inv[q] = __builtin_bit_cast(float4, buf_load16(inv_rsrc, static_cast<uint32_t>(e) * 4u + 16u * q));
   uint4 lt[CH / 8];
 #pragma unroll
   for (int k = 0; k < CH / 8; ++k) {
-    lt[k] = make_uint4(0, 0, 0, 0);
-    if (c0 + 8 * k < K) lt[k] = *reinterpret_cast<const uint4*>(L1t + static_cast<int64_t>(tj) * K + c0 + 8 * k);
+    // a segment past K would read the next row: zero it (its terms are skipped too)
+    const uint4 w = buf_load16(lt_rsrc, static_cast<uint32_t>(tj * K + c0 + 8 * k) * 2u);
+    lt[k] = c0 + 8 * k < K ? w : make_uint4(0, 0, 0, 0);
   }
   uint32_t l1w[DEFLATE ? CPT : 1][RANK / 2];
   if constexpr (DEFLATE) {
+    const buf_rsrc l1_rsrc = make_rsrc(L1, static_cast<uint32_t>(K * RANK) * 2u);
 #pragma unroll
-    for (int i = 0; i < CPT; ++i)
-      if (tid + 256 * i < K) load_l1_row<RANK>(L1, tid + 256 * i, l1w[i]);
+    for (int i = 0; i < CPT; ++i) {
+#pragma unroll
+      for (int q = 0; q < RANK / 8; ++q) {
+        const uint4 w = buf_load16(l1_rsrc, static_cast<uint32_t>((tid + 256 * i) * RANK + 8 * q) * 2u);
+        l1w[i][4 * q] = w.x;
+        l1w[i][4 * q + 1] = w.y;
+        l1w[i][4 * q + 2] = w.z;
+        l1w[i][4 * q + 3] = w.w;
+      }
+    }
   }
 
-  // rotate into the LDS rows (lanes past K stay out of every block: B divides K)
-  if (rot_wave) {
+  // rotate into the LDS rows (lanes past K stay out of every block: B divides K);
+  // the other waves rotate zeros and store nothing (a branch around the
+  // rotation would let the compiler move the x and 1/lambda requests into it,
+  // behind the L1t and L1 ones, and the rotation would wait for all of them)
+  {
     float v[16];
     smooth16_regs(rf.xa, rf.xb, rf.inv, v);
     fwht16(v, lane, logB);
@@ -356,7 +369,10 @@ __global__ __launch_bounds__(256) void quantize_act_rotated_few_kernel(
 
   // column tj of t over the thread's channel range, in double
   {
-    double s = 0.0;
+    // four interleaved partial sums (a quarter of the dependent chain each):
+    // the products are exact in double and each sum is within ~1e-14 of the
+    // exact one, so the order does not reach the single rounding to bf16
+    double s[4] = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
     for (int k = 0; k < CH / 8; ++k) {
       if (c0 + 8 * k < K) {
@@ -365,12 +381,12 @@ __global__ __launch_bounds__(256) void quantize_act_rotated_few_kernel(
 #pragma unroll
         for (int h = 0; h < 4; ++h) {
           const double2 a = xp[h];
-          s = __builtin_fma(a.x, static_cast<double>(__uint_as_float(w[h] << 16)), s);
-          s = __builtin_fma(a.y, static_cast<double>(__uint_as_float(w[h] & 0xFFFF0000u)), s);
+          s[h] = __builtin_fma(a.x, static_cast<double>(__uint_as_float(w[h] << 16)), s[h]);
+          s[h] = __builtin_fma(a.y, static_cast<double>(__uint_as_float(w[h] & 0xFFFF0000u)), s[h]);
         }
       }
     }
-    sums[(tid / RANK) * RANK + tj] = s;
+    sums[(tid / RANK) * RANK + tj] = (s[0] + s[1]) + (s[2] + s[3]);
   }
   __syncthreads();
   if (tid < RANK) {
@@ -383,20 +399,26 @@ __global__ __launch_bounds__(256) void quantize_act_rotated_few_kernel(
 
   if constexpr (DEFLATE) {
     __syncthreads();
+    // -t and the thread's channels into registers first (the stores into xt
+    // would otherwise make every read of tn wait for them); each channel
+    // still takes its r updates one after another, j ascending
+    float tr[RANK], v[CPT];
 #pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      const int c = tid + 256 * i;
-      if (c < K) {
-        float v = xt[c];
+    for (int j = 0; j < RANK; ++j) tr[j] = tn[j];
 #pragma unroll
-        for (int j = 0; j < RANK; j += 2) {
-          const uint32_t w = l1w[i][j / 2];
-          v = __builtin_fmaf(__uint_as_float(w << 16), tn[j], v);
-          v = __builtin_fmaf(__uint_as_float(w & 0xFFFF0000u), tn[j + 1], v);
-        }
-        xt[c] = v;
+    for (int i = 0; i < CPT; ++i) v[i] = tid + 256 * i < K ? xt[tid + 256 * i] : 0.0f;
+#pragma unroll
+    for (int j = 0; j < RANK; j += 2) {
+#pragma unroll
+      for (int i = 0; i < CPT; ++i) {
+        const uint32_t w = l1w[i][j / 2];
+        v[i] = __builtin_fmaf(__uint_as_float(w << 16), tr[j], v[i]);
+        v[i] = __builtin_fmaf(__uint_as_float(w & 0xFFFF0000u), tr[j + 1], v[i]);
       }
     }
+#pragma unroll
+    for (int i = 0; i < CPT; ++i)
+      if (tid + 256 * i < K) xt[tid + 256 * i] = v[i];
     __syncthreads();
   }
 
