@@ -195,11 +195,19 @@ __global__ __launch_bounds__(64 * LW) void asp_layer_small_kernel(
 
   // the wave's spans, one fetched ahead
   if (g_lo < g_hi) {
+    // a fetch is 4 requests of x, then 6 (weights, scale, L1t); the 1/lambda
+    // copies were issued before both fetches and requests complete in issue
+    // order, so waiting until only the later requests are outstanding lets
+    // the first span's quantization overlap the weights' arrival
     Fetch fa, fb;
     fetch(g_lo, fa);
     int g = g_lo;
-    if (g + 1 < g_hi) fetch(g + 1, fb);
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the 1/lambda copies have landed
+    if (g + 1 < g_hi) {
+      fetch(g + 1, fb);
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(6 + 10) : "memory");
+    } else {
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(6) : "memory");
+    }
     for (; g + 1 < g_hi; g += 2) {
       work(g, fa);
       if (g + 2 < g_hi) fetch(g + 2, fa);
@@ -470,20 +478,29 @@ __global__ __launch_bounds__(64 * LW) void asp_layer_tiny_kernel(
       if (c + 4 * lane < nfl)
         buf_load16_lds(i_rsrc, static_cast<uint32_t>(g_lo * kGroup + c + 4 * lane) * 4u, inv_l + g_lo * kGroup + c);
   }
+  // a fetch is 4 requests of x, then kLater (weights, their scales, L1t);
+  // the 1/lambda copies were issued before it and requests complete in issue
+  // order, so waiting until only the later requests are outstanding lets the
+  // quantization of the first step overlap the weights' arrival
+  constexpr int kLater = 3 * NB + 4 * RB;
   if constexpr (NB == 4) {
     // one step per wave (K <= 1024, chosen by the launcher): no prefetch buffer
     if (g_lo < g_hi) {
       Fetch fa;
       fetch(g_lo, fa);
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the 1/lambda copies have landed
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kLater) : "memory");
       work(g_lo, fa);
     }
   } else if (g_lo < g_hi) {
     Fetch fa, fb;
     fetch(g_lo, fa);
     int g = g_lo;
-    if (g + 2 < g_hi) fetch(g + 2, fb);
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the 1/lambda copies have landed
+    if (g + 2 < g_hi) {
+      fetch(g + 2, fb);
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kLater + 4 + kLater) : "memory");
+    } else {
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kLater) : "memory");
+    }
     for (; g + 2 < g_hi; g += 4) {
       work(g, fa);
       if (g + 4 < g_hi) fetch(g + 4, fa);
